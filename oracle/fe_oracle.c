@@ -1,0 +1,343 @@
+/*
+ * fe_oracle.c -- CPU oracle of the FastEagle drafting pass and tree.
+ *
+ * TEST INFRASTRUCTURE ONLY (tests, smoke check, bench CPU-baseline leg).  It
+ * is deliberately plain: double precision, one sequence at a time, straight
+ * loops over rows, no blocking or fusion, steps in the paper's order.  It
+ * shares no code with the GPU library.
+ *
+ * Paper passages followed (FastEagle):
+ *   Section 2.1, first paragraph: multi-level features l_t, m_t, h_t of the
+ *     target are concatenated and fused by an FC layer into g_t; g_t is
+ *     concatenated with the embedding e_{t+1} of the next token.
+ *   Section 2.1, Eq. 1: h_1 = L_1(FC(concat(g_t, e_{t+1}))).
+ *   Section 2.1, Eq. 2: h_i = L_i(h_{i-1}) for i = 2..N, each L_i with its own
+ *     parameters; every h_i goes through the target's frozen LM head to give
+ *     the distribution for position t+i.
+ *   Section 2.1 (EAGLE-style drafter): each L_i is one lightweight decoder
+ *     layer; its internals are a pre-norm LLaMA layer (RMSNorm, rotary GQA
+ *     attention over the prefix KV cache plus the cascade entries, SwiGLU).
+ *   Section 2.2: Backbone Expansion tree.
+ *   Section 2.4: one pass yields all N distributions, then the tree is built.
+ *
+ * Readings where the paper is silent (they are listed with reasons in the
+ * design notes of the repository):
+ *   - cascade context: layer i's query is x_{i-1} at position P+i-1 and its
+ *     keys/values are its own prefix cache plus its own projections of
+ *     x_0..x_{i-1} at positions P..P+i-1 (FEO_CTX_CASCADE); FEO_CTX_SELF lets
+ *     layer i see the prefix plus its own input only, at position P;
+ *   - two FC layers (3d->d fusion, then 2d->d input), no biases;
+ *   - one shared final RMSNorm before the LM head;
+ *   - k candidates per level are the k largest logits, ties to the lower
+ *     draft id;  probabilities are the temperature-1 softmax over the draft
+ *     vocabulary;
+ *   - rotary embedding in rotate-half form, frequencies theta^(-2m/D);
+ *   - q head h reads KV head floor(h / (H_q/H_kv)).
+ */
+#include "fe_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+static int g_threads = 1;
+
+void feo_set_threads(int n) { g_threads = n < 1 ? 1 : n; }
+int feo_get_threads(void) { return g_threads; }
+
+/* Exact widening of one stored element. */
+static double widen(const void *p, int32_t dtype, size_t i) {
+  if (dtype == FEO_BF16) {
+    uint32_t bits = (uint32_t)((const uint16_t *)p)[i] << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+  }
+  return (double)((const float *)p)[i];
+}
+
+/* y[o] = sum_k W[o][k] * x[k] with W stored row-major [rows][cols]
+ * (an FC layer without bias, nn.Linear convention). */
+static void matvec(const void *W, int32_t dtype, int64_t rows, int64_t cols, const double *x,
+                   double *y) {
+  if (dtype == FEO_BF16) {
+    const uint16_t *w = (const uint16_t *)W;
+#pragma omp parallel for num_threads(g_threads) schedule(static)
+    for (int64_t o = 0; o < rows; ++o) {
+      const uint16_t *row = w + (size_t)o * (size_t)cols;
+      double acc = 0.0;
+      for (int64_t k = 0; k < cols; ++k) {
+        uint32_t bits = (uint32_t)row[k] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        acc += (double)f * x[k];
+      }
+      y[o] = acc;
+    }
+  } else {
+    const float *w = (const float *)W;
+#pragma omp parallel for num_threads(g_threads) schedule(static)
+    for (int64_t o = 0; o < rows; ++o) {
+      const float *row = w + (size_t)o * (size_t)cols;
+      double acc = 0.0;
+      for (int64_t k = 0; k < cols; ++k) acc += (double)row[k] * x[k];
+      y[o] = acc;
+    }
+  }
+}
+
+void feo_rmsnorm(const double *x, const void *gamma, int32_t dtype, int32_t n, double eps,
+                 double *y) {
+  double ss = 0.0;
+  for (int32_t i = 0; i < n; ++i) ss += x[i] * x[i];
+  const double inv = 1.0 / sqrt(ss / (double)n + eps);
+  for (int32_t i = 0; i < n; ++i) y[i] = widen(gamma, dtype, (size_t)i) * (x[i] * inv);
+}
+
+void feo_rope(double *v, int32_t D, int64_t pos, double theta) {
+  const int32_t half = D / 2;
+  for (int32_t m = 0; m < half; ++m) {
+    const double freq = pow(theta, -2.0 * (double)m / (double)D);
+    const double ang = (double)pos * freq;
+    const double c = cos(ang), s = sin(ang);
+    const double a = v[m], b = v[m + half];
+    v[m] = a * c - b * s;
+    v[m + half] = b * c + a * s;
+  }
+}
+
+void feo_attend(const double *q, const double *keys, const double *vals, int32_t L, int32_t D,
+                int64_t stride, double *out) {
+  for (int32_t d = 0; d < D; ++d) out[d] = 0.0;
+  if (L <= 0) return;
+  double *s = (double *)malloc(sizeof(double) * (size_t)L);
+  const double scale = 1.0 / sqrt((double)D);
+  double mx = -INFINITY;
+  for (int32_t j = 0; j < L; ++j) {
+    double dot = 0.0;
+    for (int32_t d = 0; d < D; ++d) dot += q[d] * keys[(size_t)j * stride + d];
+    s[j] = dot * scale;
+    if (s[j] > mx) mx = s[j];
+  }
+  double den = 0.0;
+  for (int32_t j = 0; j < L; ++j) {
+    s[j] = exp(s[j] - mx);
+    den += s[j];
+  }
+  for (int32_t j = 0; j < L; ++j)
+    for (int32_t d = 0; d < D; ++d) out[d] += s[j] * vals[(size_t)j * stride + d];
+  for (int32_t d = 0; d < D; ++d) out[d] /= den;
+  free(s);
+}
+
+typedef struct {
+  double z;
+  int32_t id;
+} scored;
+
+/* Order: larger logit first, equal logits by lower draft id. */
+static int by_logit_desc(const void *pa, const void *pb) {
+  const scored *a = (const scored *)pa, *b = (const scored *)pb;
+  if (a->z > b->z) return -1;
+  if (a->z < b->z) return 1;
+  return (a->id > b->id) - (a->id < b->id);
+}
+
+static double silu(double u) { return u / (1.0 + exp(-u)); }
+
+/* One decoder layer L_i of the cascade for one sequence (Section 2.1, Eq. 1-2).
+ * xs[0..i-1] are the cascade states produced so far (x_0 = fused input);
+ * writes x_i into xs[i]. */
+static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, double *xs,
+                          const void *kc, const void *vc, int64_t prefix_off, int32_t P) {
+  const int32_t d = c->hidden, D = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads;
+  const int32_t G = Hq / Hkv, I = c->intermediate;
+  const int32_t qd = Hq * D, kvd = Hkv * D;
+  const int32_t j0 = (c->cascade_ctx == FEO_CTX_CASCADE) ? 0 : i - 1;
+  const int32_t nctx = i - j0;
+
+  /* Pre-attention RMSNorm and projections of every context row. */
+  double *a = (double *)malloc(sizeof(double) * (size_t)d);
+  double *kn = (double *)malloc(sizeof(double) * (size_t)nctx * kvd);
+  double *vn = (double *)malloc(sizeof(double) * (size_t)nctx * kvd);
+  double *q = (double *)malloc(sizeof(double) * (size_t)qd);
+  for (int32_t t = 0; t < nctx; ++t) {
+    const int32_t j = j0 + t;
+    const int64_t pos = (c->cascade_ctx == FEO_CTX_CASCADE) ? (int64_t)P + j : (int64_t)P;
+    feo_rmsnorm(xs + (size_t)j * d, L->attn_norm, c->dtype, d, c->rms_eps, a);
+    matvec(L->wk, c->dtype, kvd, d, a, kn + (size_t)t * kvd);
+    matvec(L->wv, c->dtype, kvd, d, a, vn + (size_t)t * kvd);
+    for (int32_t h = 0; h < Hkv; ++h) feo_rope(kn + (size_t)t * kvd + (size_t)h * D, D, pos, c->rope_theta);
+    if (j == i - 1) {
+      matvec(L->wq, c->dtype, qd, d, a, q);
+      for (int32_t h = 0; h < Hq; ++h) feo_rope(q + (size_t)h * D, D, pos, c->rope_theta);
+    }
+  }
+
+  /* GQA attention: q head h reads KV head h / G over [prefix ; context rows]. */
+  const int32_t Lk = P + nctx;
+  double *o = (double *)malloc(sizeof(double) * (size_t)qd);
+#pragma omp parallel for num_threads(g_threads) schedule(static)
+  for (int32_t ch = 0; ch < Hkv; ++ch) {
+    double *K = (double *)malloc(sizeof(double) * ((size_t)Lk * D + 1));
+    double *V = (double *)malloc(sizeof(double) * ((size_t)Lk * D + 1));
+    for (int32_t t = 0; t < P; ++t)
+      for (int32_t e = 0; e < D; ++e) {
+        const size_t src = ((size_t)(prefix_off + t) * Hkv + ch) * D + e;
+        K[(size_t)t * D + e] = widen(kc, c->dtype, src);
+        V[(size_t)t * D + e] = widen(vc, c->dtype, src);
+      }
+    for (int32_t t = 0; t < nctx; ++t)
+      for (int32_t e = 0; e < D; ++e) {
+        K[(size_t)(P + t) * D + e] = kn[(size_t)t * kvd + (size_t)ch * D + e];
+        V[(size_t)(P + t) * D + e] = vn[(size_t)t * kvd + (size_t)ch * D + e];
+      }
+    for (int32_t g = 0; g < G; ++g) {
+      const int32_t h = ch * G + g;
+      feo_attend(q + (size_t)h * D, K, V, Lk, D, D, o + (size_t)h * D);
+    }
+    free(K);
+    free(V);
+  }
+
+  /* Output projection and residual. */
+  double *xp = (double *)malloc(sizeof(double) * (size_t)d);
+  matvec(L->wo, c->dtype, d, qd, o, xp);
+  for (int32_t e = 0; e < d; ++e) xp[e] += xs[(size_t)(i - 1) * d + e];
+
+  /* Post-attention RMSNorm, SwiGLU MLP and residual. */
+  double *bn = (double *)malloc(sizeof(double) * (size_t)d);
+  double *gt = (double *)malloc(sizeof(double) * (size_t)I);
+  double *up = (double *)malloc(sizeof(double) * (size_t)I);
+  double *dn = (double *)malloc(sizeof(double) * (size_t)d);
+  feo_rmsnorm(xp, L->mlp_norm, c->dtype, d, c->rms_eps, bn);
+  matvec(L->w_gate, c->dtype, I, d, bn, gt);
+  matvec(L->w_up, c->dtype, I, d, bn, up);
+  for (int32_t e = 0; e < I; ++e) gt[e] = silu(gt[e]) * up[e];
+  matvec(L->w_down, c->dtype, d, I, gt, dn);
+  for (int32_t e = 0; e < d; ++e) xs[(size_t)i * d + e] = xp[e] + dn[e];
+
+  free(a); free(kn); free(vn); free(q); free(o); free(xp);
+  free(bn); free(gt); free(up); free(dn);
+}
+
+int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
+                      const void *features, const int32_t *next_tok,
+                      const void *const *kcache, const void *const *vcache,
+                      const int32_t *prefix_lens, int32_t topk, double *hidden, double *logits,
+                      int32_t *topk_draft, int32_t *topk_ids, double *topk_probs) {
+  if (!c || !w || batch < 0 || topk < 1 || topk > c->draft_vocab || c->n_layers < 1) return -1;
+  if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0) return -1;
+  const int32_t d = c->hidden, N = c->n_layers, V = c->draft_vocab, F = c->n_feat_levels;
+  int64_t prefix_off = 0;
+  double *xs = (double *)malloc(sizeof(double) * (size_t)(N + 1) * d);
+  double *f = (double *)malloc(sizeof(double) * (size_t)F * d);
+  double *ge = (double *)malloc(sizeof(double) * (size_t)2 * d);
+  double *hn = (double *)malloc(sizeof(double) * (size_t)d);
+  double *z = (double *)malloc(sizeof(double) * (size_t)V);
+  scored *ord = (scored *)malloc(sizeof(scored) * (size_t)V);
+
+  for (int32_t b = 0; b < batch; ++b) {
+    const int32_t P = prefix_lens[b];
+    if (P < 0 || next_tok[b] < 0 || next_tok[b] >= c->target_vocab) {
+      free(xs); free(f); free(ge); free(hn); free(z); free(ord);
+      return -1;
+    }
+    /* g_t = FC(concat(l_t, m_t, h_t)) */
+    for (int64_t e = 0; e < (int64_t)F * d; ++e)
+      f[e] = widen(features, c->dtype, (size_t)b * F * d + (size_t)e);
+    matvec(w->w_fuse, c->dtype, d, (int64_t)F * d, f, ge);
+    /* e_{t+1}: row of the target's embedding table */
+    for (int32_t e = 0; e < d; ++e)
+      ge[d + e] = widen(w->embed, c->dtype, (size_t)next_tok[b] * d + e);
+    /* x_0 = FC(concat(g_t, e_{t+1})), the input of L_1 (Eq. 1) */
+    matvec(w->w_in, c->dtype, d, 2 * d, ge, xs);
+    /* h_i = L_i(h_{i-1}) (Eq. 1-2) */
+    for (int32_t i = 1; i <= N; ++i)
+      cascade_layer(c, &w->layers[i - 1], i, xs, kcache[i - 1], vcache[i - 1], prefix_off, P);
+    if (hidden) memcpy(hidden + (size_t)b * (N + 1) * d, xs, sizeof(double) * (size_t)(N + 1) * d);
+
+    /* q_{t+i} = softmax(LMHead(RMSNorm(h_i))) and its k most probable tokens */
+    for (int32_t i = 1; i <= N; ++i) {
+      feo_rmsnorm(xs + (size_t)i * d, w->final_norm, c->dtype, d, c->rms_eps, hn);
+      matvec(w->lm_head, c->dtype, V, d, hn, z);
+      const size_t row = (size_t)b * N + (size_t)(i - 1);
+      if (logits) memcpy(logits + row * V, z, sizeof(double) * (size_t)V);
+      double mx = -INFINITY;
+      for (int32_t v = 0; v < V; ++v) mx = z[v] > mx ? z[v] : mx;
+      double den = 0.0;
+      for (int32_t v = 0; v < V; ++v) den += exp(z[v] - mx);
+      for (int32_t v = 0; v < V; ++v) { ord[v].z = z[v]; ord[v].id = v; }
+      qsort(ord, (size_t)V, sizeof(scored), by_logit_desc);
+      for (int32_t r = 0; r < topk; ++r) {
+        const int32_t id = ord[r].id;
+        if (topk_draft) topk_draft[row * topk + r] = id;
+        if (topk_ids) topk_ids[row * topk + r] = w->d2t ? w->d2t[id] : id;
+        if (topk_probs) topk_probs[row * topk + r] = exp(ord[r].z - mx) / den;
+      }
+    }
+    prefix_off += P;
+  }
+  free(xs); free(f); free(ge); free(hn); free(z); free(ord);
+  return 0;
+}
+
+/* Backbone Expansion (Section 2.2): level 1 takes the k candidates of
+ * q_{t+1} as children of the root; the most probable one becomes the
+ * backbone node and the other k-1 are side branches.  Every later level takes
+ * its k candidates as children of the previous backbone node and again extends
+ * the backbone with the most probable one.  Nodes are numbered level by level,
+ * rank by rank, after the root. */
+int feo_build_tree(int32_t batch, int32_t n_layers, int32_t topk, const int32_t *root_tokens,
+                   const int32_t *topk_ids, const int32_t *prefix_lens, int32_t *tokens,
+                   int32_t *parents, int32_t *depth, int32_t *positions, uint8_t *mask,
+                   int32_t *retrieve) {
+  if (batch < 0 || n_layers < 1 || topk < 1) return -1;
+  const int32_t N = n_layers, k = topk, T = 1 + N * k, NL = N * (k - 1) + 1;
+  int32_t *path = (int32_t *)malloc(sizeof(int32_t) * (size_t)(N + 1));
+  for (int32_t b = 0; b < batch; ++b) {
+    int32_t *tok = tokens + (size_t)b * T, *par = parents + (size_t)b * T;
+    int32_t *dep = depth + (size_t)b * T, *pos = positions + (size_t)b * T;
+    uint8_t *msk = mask + (size_t)b * T * T;
+    int32_t *ret = retrieve + (size_t)b * NL * (N + 1);
+    tok[0] = root_tokens[b];
+    par[0] = -1;
+    dep[0] = 0;
+    int32_t backbone = 0, next = 1;
+    for (int32_t lvl = 1; lvl <= N; ++lvl) {
+      const int32_t *cand = topk_ids + ((size_t)b * N + (size_t)(lvl - 1)) * k;
+      int32_t new_backbone = -1;
+      for (int32_t r = 0; r < k; ++r) {
+        tok[next] = cand[r];
+        par[next] = backbone;
+        dep[next] = dep[backbone] + 1;
+        if (r == 0) new_backbone = next;
+        ++next;
+      }
+      backbone = new_backbone;
+    }
+    for (int32_t n = 0; n < T; ++n) pos[n] = prefix_lens[b] + dep[n];
+    /* ancestor-or-self mask: walk each node's parent chain */
+    memset(msk, 0, (size_t)T * T);
+    for (int32_t a = 0; a < T; ++a)
+      for (int32_t cur = a; cur >= 0; cur = par[cur]) msk[(size_t)a * T + cur] = 1;
+    /* leaves (nodes with no children) in node order, with their root paths */
+    int32_t leaf = 0;
+    for (int32_t n = 0; n < T; ++n) {
+      int has_child = 0;
+      for (int32_t m = 0; m < T; ++m) has_child |= (par[m] == n);
+      if (has_child) continue;
+      int32_t len = 0;
+      for (int32_t cur = n; cur >= 0; cur = par[cur]) path[len++] = cur;
+      int32_t *row = ret + (size_t)leaf * (N + 1);
+      for (int32_t t = 0; t < N + 1; ++t) row[t] = t < len ? path[len - 1 - t] : -1;
+      ++leaf;
+    }
+    if (leaf != NL) {
+      free(path);
+      return -1;
+    }
+  }
+  free(path);
+  return 0;
+}

@@ -1,0 +1,93 @@
+/*
+ * fe_oracle.h -- CPU oracle of the FastEagle cascaded drafter and its
+ * Backbone Expansion tree (FastEagle, Sections 2.1, 2.2 and 2.4).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the bench's
+ * CPU-baseline leg may load this library.  It shares no code, header, table or
+ * helper with the GPU library and must never be on the product path.
+ *
+ * Everything is computed in double precision on the host, one sequence at a
+ * time, in the order the paper states the steps.  Stored inputs (fp32 or bf16
+ * bit patterns) are widened exactly to double.
+ */
+#ifndef FE_ORACLE_H
+#define FE_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { FEO_F32 = 0, FEO_BF16 = 1 };
+enum { FEO_CTX_CASCADE = 0, FEO_CTX_SELF = 1 };
+
+typedef struct {
+  int32_t hidden, n_q_heads, n_kv_heads, head_dim, intermediate, n_layers;
+  int32_t draft_vocab, target_vocab, n_feat_levels;
+  int32_t dtype;        /* storage of weights, features and prefix KV: FEO_F32 / FEO_BF16 */
+  int32_t cascade_ctx;  /* FEO_CTX_CASCADE / FEO_CTX_SELF */
+  double rope_theta, rms_eps;
+} feo_config;
+
+typedef struct {
+  const void *attn_norm, *wq, *wk, *wv, *wo, *mlp_norm, *w_gate, *w_up, *w_down;
+} feo_layer;
+
+typedef struct {
+  const void *w_fuse, *w_in, *embed, *final_norm, *lm_head;
+  const int32_t *d2t;       /* [V] draft id -> target id; NULL = identity */
+  const feo_layer *layers;  /* [n_layers] */
+} feo_weights;
+
+/* Threads used by the matrix-vector loops (OpenMP over output rows). */
+void feo_set_threads(int n);
+int feo_get_threads(void);
+
+/* y = gamma * x / sqrt(mean(x^2) + eps), n elements. */
+void feo_rmsnorm(const double *x, const void *gamma, int32_t dtype, int32_t n, double eps,
+                 double *y);
+
+/* Rotate-half rotary embedding of one head vector v[D] in place at position pos:
+ * pairs (m, m + D/2), angle pos * theta^(-2m/D). */
+void feo_rope(double *v, int32_t D, int64_t pos, double theta);
+
+/* One query head against L key/value rows (row stride `stride` doubles):
+ * out[D] = sum_j softmax_j(q.k_j / sqrt(D)) v_j.  L == 0 writes zeros. */
+void feo_attend(const double *q, const double *keys, const double *vals, int32_t L,
+                int32_t D, int64_t stride, double *out);
+
+/*
+ * The drafting pass for `batch` sequences.
+ *  features  [B, n_feat_levels*d]  (dtype)   l_t, m_t, h_t concatenated
+ *  next_tok  [B] int32                       token t+1 (target vocabulary)
+ *  kcache/vcache  [n_layers] pointers, each [sum P_b, H_kv, D] (dtype), K already rotated
+ *  prefix_lens [B] int32
+ * Outputs (any may be NULL):
+ *  hidden [B, N+1, d]  x_0 .. x_N;   logits [B, N, V]
+ *  topk_draft [B, N, k] int32 draft ids;  topk_ids [B, N, k] int32 target ids;
+ *  topk_probs [B, N, k] double.
+ * Returns 0, or -1 on invalid arguments.
+ */
+int feo_draft_forward(const feo_config *cfg, const feo_weights *w, int32_t batch,
+                      const void *features, const int32_t *next_tok,
+                      const void *const *kcache, const void *const *vcache,
+                      const int32_t *prefix_lens, int32_t topk, double *hidden, double *logits,
+                      int32_t *topk_draft, int32_t *topk_ids, double *topk_probs);
+
+/*
+ * Backbone Expansion tree for `batch` sequences, T = 1 + N*k nodes each.
+ *  root_tokens [B], topk_ids [B, N, k] (rank order), prefix_lens [B]
+ * Outputs: tokens/parents/depth/positions [B, T] int32, mask [B, T, T] uint8
+ * (mask[a][c] = 1 iff c is on the root->a path), retrieve [B, N*(k-1)+1, N+1]
+ * (root->leaf node paths, -1 padded).  Returns 0, or -1 on invalid arguments.
+ */
+int feo_build_tree(int32_t batch, int32_t n_layers, int32_t topk, const int32_t *root_tokens,
+                   const int32_t *topk_ids, const int32_t *prefix_lens, int32_t *tokens,
+                   int32_t *parents, int32_t *depth, int32_t *positions, uint8_t *mask,
+                   int32_t *retrieve);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,169 @@
+"""ctypes wrapper of the C oracle (test infrastructure only).
+
+Marshals numpy arrays (as made by fe_synth) into the oracle's C calls.  No
+arithmetic of the drafter is done here.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+
+class FeoConfig(C.Structure):
+    _fields_ = [("hidden", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("intermediate", C.c_int32), ("n_layers", C.c_int32),
+                ("draft_vocab", C.c_int32), ("target_vocab", C.c_int32),
+                ("n_feat_levels", C.c_int32), ("dtype", C.c_int32), ("cascade_ctx", C.c_int32),
+                ("rope_theta", C.c_double), ("rms_eps", C.c_double)]
+
+
+class FeoLayer(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm",
+                                          "w_gate", "w_up", "w_down")]
+
+
+class FeoWeights(C.Structure):
+    _fields_ = [("w_fuse", C.c_void_p), ("w_in", C.c_void_p), ("embed", C.c_void_p),
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
+                ("d2t", C.POINTER(C.c_int32)), ("layers", C.POINTER(FeoLayer))]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = C.CDLL(_build.LIB)
+        L.feo_draft_forward.restype = C.c_int
+        L.feo_build_tree.restype = C.c_int
+        L.feo_get_threads.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def set_threads(n: int) -> None:
+    lib().feo_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().feo_get_threads())
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def _pd(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"] and a.dtype == np.float64
+    return a.ctypes.data_as(C.POINTER(C.c_double))
+
+
+def _pi(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"] and a.dtype == np.int32
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def make_config(cfg) -> FeoConfig:
+    return FeoConfig(cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.intermediate,
+                     cfg.n_layers, cfg.draft_vocab, cfg.target_vocab, cfg.n_feat_levels,
+                     1 if cfg.dtype == "bf16" else 0,
+                     0 if cfg.cascade_ctx == "cascade" else 1,
+                     float(cfg.rope_theta), float(cfg.rms_eps))
+
+
+def rmsnorm(x: np.ndarray, gamma: np.ndarray, dtype: str, eps: float) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty_like(x)
+    lib().feo_rmsnorm(_pd(x), _p(np.ascontiguousarray(gamma)), C.c_int32(1 if dtype == "bf16" else 0),
+                      C.c_int32(x.size), C.c_double(eps), _pd(y))
+    return y
+
+
+def rope(v: np.ndarray, pos: int, theta: float) -> np.ndarray:
+    y = np.array(v, dtype=np.float64, copy=True)
+    lib().feo_rope(_pd(y), C.c_int32(y.size), C.c_int64(pos), C.c_double(theta))
+    return y
+
+
+def attend(q: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    keys = np.ascontiguousarray(keys, dtype=np.float64)
+    vals = np.ascontiguousarray(vals, dtype=np.float64)
+    L, D = keys.shape if keys.ndim == 2 else (0, q.size)
+    out = np.empty(q.size, dtype=np.float64)
+    lib().feo_attend(_pd(q), _pd(keys), _pd(vals), C.c_int32(L), C.c_int32(D), C.c_int64(D),
+                     _pd(out))
+    return out
+
+
+def draft_forward(cfg, w, inp, topk: Optional[int] = None, want_logits: bool = True,
+                  batch_index: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+    """Run the oracle pass.  `batch_index` restricts it to some sequences of the
+    batch (sequences are independent), keeping the given order."""
+    k = cfg.topk if topk is None else int(topk)
+    B_all = len(inp.prefix_lens)
+    idx = list(range(B_all)) if batch_index is None else [int(i) for i in batch_index]
+    cu = inp.cu_prefix
+    feats = np.ascontiguousarray(inp.features[idx])
+    toks = np.ascontiguousarray(inp.next_tokens[idx], dtype=np.int32)
+    plens = np.ascontiguousarray(inp.prefix_lens[idx], dtype=np.int32)
+    # gather the selected sequences' caches into packed arrays
+    if idx == list(range(B_all)):
+        kc = [np.ascontiguousarray(a) for a in inp.kcache]
+        vc = [np.ascontiguousarray(a) for a in inp.vcache]
+    else:
+        kc = [np.ascontiguousarray(np.concatenate([a[cu[i]:cu[i + 1]] for i in idx])) for a in inp.kcache]
+        vc = [np.ascontiguousarray(np.concatenate([a[cu[i]:cu[i + 1]] for i in idx])) for a in inp.vcache]
+    B, N, d, V = len(idx), cfg.n_layers, cfg.hidden, cfg.draft_vocab
+    layers = (FeoLayer * N)()
+    for i, lw in enumerate(w.layers):
+        for f in FeoLayer._fields_:
+            setattr(layers[i], f[0], _p(getattr(lw, f[0])))
+    d2t = np.ascontiguousarray(w.d2t, dtype=np.int32)
+    W = FeoWeights(_p(w.w_fuse), _p(w.w_in), _p(w.embed), _p(w.final_norm), _p(w.lm_head),
+                   _pi(d2t), C.cast(layers, C.POINTER(FeoLayer)))
+    kp = (C.c_void_p * N)(*[a.ctypes.data for a in kc])
+    vp = (C.c_void_p * N)(*[a.ctypes.data for a in vc])
+    hidden = np.zeros((B, N + 1, d), dtype=np.float64)
+    logits = np.zeros((B, N, V), dtype=np.float64) if want_logits else None
+    tdraft = np.zeros((B, N, k), dtype=np.int32)
+    tids = np.zeros((B, N, k), dtype=np.int32)
+    tprob = np.zeros((B, N, k), dtype=np.float64)
+    cfgc = make_config(cfg)
+    rc = lib().feo_draft_forward(C.byref(cfgc), C.byref(W), C.c_int32(B), _p(feats), _pi(toks),
+                                 kp, vp, _pi(plens), C.c_int32(k), _pd(hidden),
+                                 _pd(logits) if logits is not None else None,
+                                 _pi(tdraft), _pi(tids), _pd(tprob))
+    if rc != 0:
+        raise ValueError("oracle draft_forward rejected its arguments")
+    out = dict(hidden=hidden, topk_draft=tdraft, topk_ids=tids, topk_probs=tprob)
+    if logits is not None:
+        out["logits"] = logits
+    return out
+
+
+def build_tree(n_layers: int, topk: int, root_tokens: np.ndarray, topk_ids: np.ndarray,
+               prefix_lens: np.ndarray) -> Dict[str, np.ndarray]:
+    root_tokens = np.ascontiguousarray(root_tokens, dtype=np.int32)
+    topk_ids = np.ascontiguousarray(topk_ids, dtype=np.int32)
+    prefix_lens = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+    B, N, k = len(root_tokens), int(n_layers), int(topk)
+    T, NL = 1 + N * k, N * (k - 1) + 1
+    out = dict(tokens=np.zeros((B, T), np.int32), parents=np.zeros((B, T), np.int32),
+               depth=np.zeros((B, T), np.int32), positions=np.zeros((B, T), np.int32),
+               mask=np.zeros((B, T, T), np.uint8), retrieve=np.zeros((B, NL, N + 1), np.int32))
+    rc = lib().feo_build_tree(C.c_int32(B), C.c_int32(N), C.c_int32(k), _pi(root_tokens),
+                              _pi(topk_ids), _pi(prefix_lens), _pi(out["tokens"]),
+                              _pi(out["parents"]), _pi(out["depth"]), _pi(out["positions"]),
+                              _p(out["mask"]), _pi(out["retrieve"]))
+    if rc != 0:
+        raise ValueError("oracle build_tree rejected its arguments")
+    return out
