@@ -1,0 +1,203 @@
+/*
+ * fe.h -- C ABI of the MI355X (gfx950) FastEagle drafting library, libfe.so.
+ *
+ * FastEagle (arXiv 2509.20416) replaces N sequential EAGLE drafting passes by
+ * ONE pass through N lightweight decoder layers in series (Section 2.1,
+ * Eq. 1-2), reads a distribution for position t+i off every layer through the
+ * target's shared LM head, and turns the N distributions into a linear-size
+ * "Backbone Expansion" draft tree for tree-attention verification
+ * (Sections 2.2 and 2.4).  This library computes exactly that pass and that
+ * tree on one GPU.
+ *
+ * Conventions for every call
+ *  - Pointers are DEVICE pointers unless a field says HOST.
+ *  - Every tensor (weights, KV caches, inputs, outputs, workspace) is allocated
+ *    by the caller and BORROWED.  The library frees nothing it did not
+ *    allocate; the only library-owned allocations are the handle (host memory)
+ *    and, if graph replay is on, the HIP graphs it captures.  Weights and the
+ *    workspace must outlive the handle.
+ *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *    Calls are asynchronous on `stream`; device-side faults surface at the
+ *    caller's next synchronisation.
+ *  - Every call validates its arguments on the host BEFORE enqueueing
+ *    anything: a non-OK status has no device side effect.  No C++ exception
+ *    crosses the ABI.  fe_last_error() gives a message for the last non-OK
+ *    status of the calling thread.
+ *  - Calls on one handle must be serialised by the caller.  Outputs are
+ *    bitwise deterministic for identical inputs (fixed reduction order, no
+ *    floating-point atomics).
+ *  - Matrices are row-major [out, in] (nn.Linear convention), no biases.
+ *    Weight, feature and KV storage is FE_BF16 (bf16 bit patterns) or FE_F32
+ *    for all of them; every pointer must be 16-byte aligned.
+ */
+#ifndef FE_H
+#define FE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FE_OK = 0,
+  FE_E_INVALID = 1,     /* bad pointer, size or enum value */
+  FE_E_UNSUPPORTED = 2, /* shape the kernels do not implement (see fe_drafter_create) */
+  FE_E_ALIGN = 3,       /* a pointer is not 16-byte aligned */
+  FE_E_WORKSPACE = 4,   /* workspace missing or smaller than fe_workspace_bytes() */
+  FE_E_HIP = 5          /* a HIP runtime call failed */
+} fe_status;
+
+typedef enum { FE_F32 = 0, FE_BF16 = 1 } fe_dtype;
+
+/* What cascade layer i attends to, besides its prefix KV cache (the paper's
+ * architecture figure is not available; Eq. 2 and Section 2.1 are read as):
+ *  FE_CTX_CASCADE: the query is x_{i-1} at position P+i-1; keys/values are
+ *    layer i's own projections of x_0..x_{i-1} at positions P..P+i-1;
+ *  FE_CTX_SELF: query, key and value come from x_{i-1} alone, at position P. */
+typedef enum { FE_CTX_CASCADE = 0, FE_CTX_SELF = 1 } fe_cascade_ctx;
+
+typedef struct {
+  int32_t hidden;        /* d */
+  int32_t n_q_heads;     /* H_q */
+  int32_t n_kv_heads;    /* H_kv, divides H_q (q head h reads KV head h / (H_q/H_kv)) */
+  int32_t head_dim;      /* D: 64 or 128 */
+  int32_t intermediate;  /* SwiGLU width I */
+  int32_t n_layers;      /* N cascade layers (1..16) */
+  int32_t draft_vocab;   /* V: rows of the LM head */
+  int32_t target_vocab;  /* V_t: rows of the embedding table, range of d2t */
+  int32_t n_feat_levels; /* number of target features fused (3: low, mid, high) */
+  int32_t max_batch;     /* largest batch any call will pass */
+  int32_t max_topk;      /* largest k any call will pass (1..16) */
+  int32_t max_prefix;    /* largest prefix length P_b any call will pass */
+  float rope_theta;      /* rotary base: angle of pair m at position p is p*theta^(-2m/D) */
+  float rms_eps;         /* RMSNorm epsilon */
+  int32_t dtype;         /* fe_dtype of weights, features and KV caches */
+  int32_t cascade_ctx;   /* fe_cascade_ctx */
+} fe_config;
+
+/* One cascade layer L_i (Section 2.1: every layer has its own parameters). */
+typedef struct {
+  const void *attn_norm; /* [d] */
+  const void *wq;        /* [H_q*D, d] */
+  const void *wk;        /* [H_kv*D, d] */
+  const void *wv;        /* [H_kv*D, d] */
+  const void *wo;        /* [d, H_q*D] */
+  const void *mlp_norm;  /* [d] */
+  const void *w_gate;    /* [I, d] */
+  const void *w_up;      /* [I, d] */
+  const void *w_down;    /* [d, I] */
+} fe_layer_weights;
+
+typedef struct {
+  const void *w_fuse;     /* [d, n_feat_levels*d]: g_t = FC(concat(l_t, m_t, h_t)) */
+  const void *w_in;       /* [d, 2d]: x_0 = FC(concat(g_t, e_{t+1})) (Eq. 1) */
+  const void *embed;      /* [V_t, d]: the target's (frozen) embedding table */
+  const void *final_norm; /* [d]: RMSNorm applied before the LM head */
+  const void *lm_head;    /* [V, d]: the target's frozen LM head (draft vocabulary rows) */
+  const int32_t *d2t;     /* [V] draft id -> target id, or NULL for the identity */
+  const fe_layer_weights *layers; /* HOST array [n_layers] */
+} fe_weights;
+
+/* Prefix KV caches of the N cascade layers for a batch (packed, ragged). */
+typedef struct {
+  const void *const *k;      /* HOST array [n_layers] of device pointers, each
+                                [sum_b P_b, H_kv, D], keys ALREADY rotary-embedded */
+  const void *const *v;      /* HOST array [n_layers], each [sum_b P_b, H_kv, D] */
+  const int32_t *cu_prefix;  /* device [B+1]: sequence b owns rows cu[b]..cu[b+1]-1 */
+  int32_t max_prefix;        /* HOST bound: every P_b <= max_prefix <= cfg.max_prefix */
+} fe_kv_view;
+
+typedef struct {
+  int32_t *topk_ids;  /* [B, N, k]: target-vocabulary ids, rank order (largest logit
+                         first; equal logits -> lower draft id first) */
+  float *topk_probs;  /* [B, N, k]: temperature-1 softmax probability over the draft vocab */
+  int32_t *topk_draft;/* optional [B, N, k] draft-vocabulary ids; NULL = not written */
+  float *logits;      /* optional [B, N, V] fp32; NULL = never materialised */
+  float *hidden;      /* optional [B, N+1, d] fp32 cascade states x_0..x_N; NULL = not written */
+} fe_draft_out;
+
+typedef struct {
+  int32_t *tokens;    /* [B, T], T = 1 + N*k: root token, then level by level in rank order */
+  int32_t *parents;   /* [B, T]: parent node index, -1 for the root */
+  int32_t *depth;     /* [B, T]: 0 for the root, level l for level-l nodes */
+  int32_t *positions; /* [B, T]: P_b + depth */
+  uint8_t *mask;      /* [B, T, T]: mask[a][c] = 1 iff c is on the root->a path (inclusive) */
+  int32_t *retrieve;  /* [B, N*(k-1)+1, N+1]: root->leaf node paths of the leaves in node
+                         order, -1 padded */
+} fe_tree_out;
+
+typedef struct fe_drafter fe_drafter;
+
+/* Device workspace the handle needs for `cfg` (bytes; 0 if cfg is invalid). */
+size_t fe_workspace_bytes(const fe_config *cfg);
+
+/* Creates a drafter over borrowed weights and workspace (Section 2.1).
+ * Supported shapes: head_dim 64 or 128; d, I, H_q*D, V multiples of 32 (bf16)
+ * or 16 (fp32); 1 <= n_layers <= 16; 1 <= max_topk <= 16; H_q % H_kv == 0.
+ * `workspace` must hold fe_workspace_bytes(cfg) bytes.  `stream` is used for
+ * set-up work only.  On success *out receives the handle. */
+fe_status fe_drafter_create(const fe_config *cfg, const fe_weights *w, void *workspace,
+                            size_t workspace_bytes, void *stream, fe_drafter **out);
+
+/* One drafting pass (Section 2.4, "Non-Autoregressive Drafting"): from the
+ * target features of the last verified token and the next token t+1, produce
+ * the N distributions q_{t+1..t+N} in a single pass and write their top-k.
+ *  features    [B, n_feat_levels*d] (dtype): l_t, m_t, h_t concatenated
+ *  next_tokens [B] int32: token t+1 in the target vocabulary (its embedding row is read)
+ *  kv          prefix caches of the N layers
+ *  topk        1..cfg.max_topk, <= V
+ * The KV caches are read only. */
+fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *features,
+                           const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
+                           const fe_draft_out *out, void *stream);
+
+/* Backbone Expansion tree (Section 2.2) of every sequence in one launch:
+ * level 1 hangs the k candidates of q_{t+1} under the root; the most probable
+ * extends the backbone, the other k-1 are side branches; every later level hangs
+ * its k candidates under the previous backbone node.
+ *  root_tokens [B] (the root is token t+1), topk_ids [B, N, k] (rank order, as
+ *  written by fe_draft_forward), prefix_lens [B] (node positions are P_b + depth). */
+fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk, const int32_t *root_tokens,
+                        const int32_t *topk_ids, const int32_t *prefix_lens,
+                        const fe_tree_out *out, void *stream);
+
+/* Replays fe_draft_forward through a captured HIP graph when on != 0 (the
+ * default is off).  A graph is captured on the first call with a given set of
+ * arguments and replayed while they stay the same. */
+fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
+
+/* Stages of the pass whose kernel launches can be timed with HIP events. */
+typedef enum {
+  FE_STAGE_NONE = -1,
+  FE_STAGE_FUSE = 0,     /* g_t = FC(l, m, h) and the embedding gather (one launch) */
+  FE_STAGE_INPUT = 1,    /* x_0 = FC(g_t, e_{t+1}) (one launch) */
+  FE_STAGE_QKV = 2,      /* per layer: Q/K/V projections + rotary embedding */
+  FE_STAGE_ATTN = 3,     /* per layer: prefix attention partials */
+  FE_STAGE_OPROJ = 4,    /* per layer: output projection + residual */
+  FE_STAGE_GATEUP = 5,   /* per layer: gate/up projections + SwiGLU */
+  FE_STAGE_DOWN = 6,     /* per layer: down projection + residual */
+  FE_STAGE_LMHEAD = 7    /* LM head on all N states + tile softmax statistics and top-k */
+} fe_stage;
+
+/* Times every launch of `stage` (FE_STAGE_NONE turns timing off): from the
+ * next fe_draft_forward on, a pair of HIP events owned by the handle is
+ * recorded on the launch stream around each launch of that stage (also
+ * inside a captured graph).  Changing the stage forces a new graph capture. */
+fe_status fe_profile_stage(fe_drafter *h, int32_t stage);
+
+/* Waits for the events of the most recent pass and writes the duration in
+ * milliseconds of each timed launch, in launch order, to ms[0..cap-1];
+ * *count receives the number of timed launches of that pass. */
+fe_status fe_profile_read(fe_drafter *h, float *ms, int32_t cap, int32_t *count);
+
+void fe_drafter_destroy(fe_drafter *h);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char *fe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FE_H */

@@ -1,0 +1,442 @@
+// fe_gemm.hip -- weight-streaming MFMA GEMM for gfx950 with fused epilogues.
+//
+// Every FC of the drafter (feature fusion and input FC of Eq. 1; Q/K/V, O,
+// gate/up and down projections of each cascade layer; the shared LM head) is
+// Y[M, C] = A[M, K] * W[C, K]^T with a weight matrix that is read exactly once
+// per pass and a handful of activation rows (M = batch, or batch x cascade
+// rows).  The kernel is built around streaming W from HBM:
+//
+//  * A wave owns NT tiles of 16 output columns and a K slice.  Lane (r, g)
+//    (r = lane % 16, g = lane / 16) loads 16 contiguous bytes of weight row
+//    r at K offset g*E of every K step (E = 8 bf16 or 4 fp32 elements), which
+//    is exactly the B operand of v_mfma_f32_16x16x32_bf16 (one MFMA per step)
+//    or of four v_mfma_f32_16x16x4_f32.  No LDS staging for weights, no
+//    re-reads: each weight byte is loaded by one lane once.
+//  * Activation rows are the A operand, loaded with the same (g, element) ->
+//    k mapping, so the products pair up correctly whatever order the matrix
+//    core sums the K elements in.  Rows beyond M are fed as zeros.
+//  * Loads are double-buffered in registers: the next U steps of weights and
+//    activations are in flight while the current U steps run on the MFMA.
+//  * WK waves of a workgroup split K; their partial tiles are summed in LDS in
+//    a fixed order (deterministic, no atomics), then an epilogue functor
+//    consumes the [M, span] fp32 tile.
+//  * Which weight row feeds a "virtual column" is the epilogue's choice:
+//    Q/K tiles pair rotary halves (dims m and m + D/2) inside one 16-column
+//    tile; gate/up tiles pair gate row c with up row c.
+#include "fe_internal.h"
+
+namespace fe {
+
+template <typename T> __device__ __forceinline__ void mma16(f32x4 &acc, u32x4 a, u32x4 b);
+
+template <> __device__ __forceinline__ void mma16<uint16_t>(f32x4 &acc, u32x4 a, u32x4 b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+
+template <> __device__ __forceinline__ void mma16<float>(f32x4 &acc, u32x4 a, u32x4 b) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a[e]),
+                                               __builtin_bit_cast(float, b[e]), acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ u32x4 ldg_stream(const u32x4 *p) { return __builtin_nontemporal_load(p); }
+
+// ---------------------------------------------------------------------------
+// The GEMM body.
+// ---------------------------------------------------------------------------
+template <typename T, int MT, int NT, int WK, int WN, int U, class Epi>
+__global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, int lda, int M,
+                                                       int K, Epi epi) {
+  constexpr int E = Elt<T>::kPer16B;
+  constexpr int KS = 4 * E;  // K elements per MFMA step
+  constexpr int SPAN = WN * NT * 16;
+  constexpr int LDT = SPAN + 1;
+  __shared__ float red[WK][MT * 16][LDT];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave % WN, wk = wave / WN;
+  const int r = lane & 15, g = lane >> 4;
+  const int c0_wg = blockIdx.x * SPAN;
+  const int c0 = c0_wg + wn * NT * 16;
+  const bool active = c0 < epi.nvcols;
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < NT; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (active) {
+    const int nsteps = K / KS;
+    const int s0 = (int)(((long)nsteps * wk) / WK);
+    const int s1 = (int)(((long)nsteps * (wk + 1)) / WK);
+    const u32x4 *wp[NT];
+#pragma unroll
+    for (int f = 0; f < NT; ++f)
+      wp[f] = reinterpret_cast<const u32x4 *>(epi.wrow(c0 + f * 16 + r)) + g;
+    const u32x4 *ap[MT];
+    bool am[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int m = i * 16 + r;
+      am[i] = m < M;
+      ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
+    }
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 wc[U][NT], ac[U][MT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + u;
+      const bool ok = s < s1;
+#pragma unroll
+      for (int f = 0; f < NT; ++f) wc[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) ac[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
+    }
+    for (int sb = s0; sb < s1; sb += U) {
+      u32x4 wn_[U][NT], an_[U][MT];
+      const int sn = sb + U;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int s = sn + u;
+        const bool ok = s < s1;
+#pragma unroll
+        for (int f = 0; f < NT; ++f) wn_[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
+#pragma unroll
+        for (int i = 0; i < MT; ++i) an_[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int f = 0; f < NT; ++f) mma16<T>(acc[i][f], ac[u][i], wc[u][f]);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int f = 0; f < NT; ++f) wc[u][f] = wn_[u][f];
+#pragma unroll
+        for (int i = 0; i < MT; ++i) ac[u][i] = an_[u][i];
+      }
+    }
+  }
+
+  // Lane (r, g) holds C[row 4g+v][col r] of each 16x16 tile.
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < NT; ++f)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[wk][i * 16 + 4 * g + v][wn * NT * 16 + f * 16 + r] = acc[i][f][v];
+  __syncthreads();
+  if (WK > 1) {
+    for (int idx = threadIdx.x; idx < MT * 16 * SPAN; idx += 64 * WK * WN) {
+      const int m = idx / SPAN, c = idx % SPAN;
+      float sum = red[0][m][c];
+#pragma unroll
+      for (int w = 1; w < WK; ++w) sum += red[w][m][c];
+      red[0][m][c] = sum;
+    }
+    __syncthreads();
+  }
+  epi.finish(&red[0][0][0], LDT, M, c0_wg, SPAN);
+}
+
+// ---------------------------------------------------------------------------
+// Epilogues.
+// ---------------------------------------------------------------------------
+template <typename T> struct EpiStore {
+  const T *w;
+  int ldw, nvcols;
+  T *out;
+  int ldo;
+  const T *embed;
+  const int32_t *tokens;
+  int vocab;
+  T *gather_out;
+  int ld_gather, d, B;
+  __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
+  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
+      const int m = idx / span, c = idx % span;
+      if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = Elt<T>::from_f(tile[m * ldt + c]);
+    }
+    if (embed) {  // the embedding row e_{t+1} of every sequence, copied next to g_t
+      constexpr int E = Elt<T>::kPer16B;
+      for (int b = blockIdx.x; b < B; b += gridDim.x) {
+        const int tok = tokens[b];
+        T *dst = gather_out + (size_t)b * ld_gather;
+        if (tok < 0 || tok >= vocab) {
+          for (int e = threadIdx.x; e < d; e += blockDim.x) dst[e] = Elt<T>::from_f(__int_as_float(0x7fc00000));
+          continue;
+        }
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(embed + (size_t)tok * d);
+        u32x4 *dv = reinterpret_cast<u32x4 *>(dst);
+        for (int e = threadIdx.x; e < d / E; e += blockDim.x) dv[e] = src[e];
+      }
+    }
+  }
+};
+
+template <typename T> struct EpiResid {
+  const T *w;
+  int ldw, nvcols;
+  float *out;
+  long ldo;
+  const float *resid;
+  long ldr;
+  __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
+  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
+      const int m = idx / span, c = idx % span;
+      if (c0 + c >= nvcols) continue;
+      float v = tile[m * ldt + c];
+      if (resid) v = resid[(size_t)m * ldr + c0 + c] + v;
+      out[(size_t)m * ldo + c0 + c] = v;
+    }
+  }
+};
+
+// Within a head, 16-column tile t holds rotary pairs 8t..8t+7: column n < 8 is
+// dim 8t+n, column n >= 8 is its partner dim D/2 + 8t + (n-8).
+__device__ __forceinline__ int rope_dim(int cc, int D) {
+  const int t = cc >> 4, n = cc & 15;
+  return ((n & 8) ? (D >> 1) : 0) + 8 * t + (n & 7);
+}
+
+template <typename T> struct EpiQkv {
+  QkvArgs a;
+  int nvcols;
+  __device__ const T *wrow(int c) const {
+    const int qd = a.Hq * a.D, kvd = a.Hkv * a.D;
+    const T *base;
+    int row;
+    if (c < qd) {
+      base = (const T *)a.wq;
+      row = (c / a.D) * a.D + rope_dim(c % a.D, a.D);
+    } else if (c < qd + kvd) {
+      c -= qd;
+      base = (const T *)a.wk;
+      row = (c / a.D) * a.D + rope_dim(c % a.D, a.D);
+    } else {
+      base = (const T *)a.wv;
+      row = c - qd - kvd;
+    }
+    return base + (size_t)row * a.d;
+  }
+  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+    const int qd = a.Hq * a.D, kvd = a.Hkv * a.D, D = a.D;
+    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
+      const int m = idx / span, c = idx % span;
+      int vc = c0 + c;
+      if (vc >= nvcols) continue;
+      const int b = m / a.nctx, t = m % a.nctx, j = a.j0 + t;
+      const float val = tile[m * ldt + c];
+      if (vc < qd + kvd) {
+        const bool isq = vc < qd;
+        if (isq && t != a.nctx - 1) continue;
+        const int lc = isq ? vc : vc - qd;
+        const int h = lc / D, cc = lc % D, dd = rope_dim(cc, D);
+        const float pv = tile[m * ldt + (c ^ 8)];
+        const int P = a.cu_prefix[b + 1] - a.cu_prefix[b];
+        const long pos = a.cascade ? (long)P + j : (long)P;
+        const int pm = 8 * (cc >> 4) + (cc & 7);
+        const double ang = (double)pos * pow(a.theta, -2.0 * (double)pm / (double)D);
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        const float c_ = (float)cs, s_ = (float)sn;
+        const float o = (cc & 8) ? (val * c_ + pv * s_) : (val * c_ - pv * s_);
+        if (isq)
+          a.q_out[((size_t)b * a.Hq + h) * D + dd] = o;
+        else
+          a.k_out[(((size_t)b * a.nctx + t) * a.Hkv + h) * D + dd] = o;
+      } else {
+        vc -= qd + kvd;
+        a.v_out[((size_t)b * a.nctx + t) * kvd + vc] = val;
+      }
+    }
+  }
+};
+
+template <typename T> struct EpiSwiglu {
+  const T *wg, *wu;
+  int ldw, I, nvcols;  // nvcols = 2*I
+  T *out;
+  int ldo;
+  // virtual tile pair (2p, 2p+1) = gate rows and up rows 16p..16p+15
+  __device__ const T *wrow(int c) const {
+    const int p = c >> 5, f = (c >> 4) & 1, n = c & 15;
+    return (f ? wu : wg) + (size_t)(p * 16 + n) * ldw;
+  }
+  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+    const int half = span >> 1;
+    for (int idx = threadIdx.x; idx < M * half; idx += blockDim.x) {
+      const int m = idx / half, q = idx % half;
+      const int c = (q >> 4) * 32 + (q & 15);  // gate column inside the tile
+      const int vc = c0 + c;
+      if (vc >= nvcols) continue;
+      const float gt = tile[m * ldt + c], up = tile[m * ldt + c + 16];
+      const float s = gt / (1.f + expf(-gt)) * up;
+      const int col = (vc >> 5) * 16 + (vc & 15);
+      out[(size_t)m * ldo + col] = Elt<T>::from_f(s);
+    }
+  }
+};
+
+// Shared LM head: per (row, column tile) max, sum of exp(z - max) and the top-k
+// (largest logit first, equal logits by lower draft id); logits optionally kept.
+template <typename T> struct EpiLm {
+  LmArgs a;
+  int ldw, nvcols;
+  __device__ const T *wrow(int c) const { return (const T *)a.w + (size_t)c * ldw; }
+  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int nvalid = min(span, nvcols - c0);
+    const int nwg = gridDim.x, tileid = blockIdx.x;
+    for (int m = wave; m < M; m += nw) {
+      const float *row = tile + m * ldt;
+      constexpr int PER = 4;  // span <= 256
+      float v[PER];
+      int id[PER];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int p = 0; p < PER; ++p) {
+        const int c = lane + 64 * p;
+        const bool ok = c < nvalid;
+        v[p] = ok ? row[c] : -INFINITY;
+        id[p] = ok ? c0 + c : 0x7fffffff;
+        mx = fmaxf(mx, v[p]);
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      float se = 0.f;
+#pragma unroll
+      for (int p = 0; p < PER; ++p) se += (id[p] != 0x7fffffff) ? expf(v[p] - mx) : 0.f;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) se += __shfl_xor(se, o);
+      if (a.logits) {
+#pragma unroll
+        for (int p = 0; p < PER; ++p)
+          if (id[p] != 0x7fffffff) a.logits[(size_t)m * nvcols + id[p]] = v[p];
+      }
+      const size_t pb = (size_t)m * nwg + tileid;
+      if (lane == 0) {
+        a.part_max[pb] = mx;
+        a.part_sum[pb] = se;
+      }
+      for (int r = 0; r < a.topk; ++r) {
+        // lane-local best, then wave argmax with the lower-id tie-break
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int p = 0; p < PER; ++p)
+          if (v[p] > bv || (v[p] == bv && id[p] < bi)) { bv = v[p]; bi = id[p]; }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+          const float ov = __shfl_xor(bv, o);
+          const int oi = __shfl_xor(bi, o);
+          if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+        }
+#pragma unroll
+        for (int p = 0; p < PER; ++p)
+          if (id[p] == bi) { v[p] = -INFINITY; id[p] = 0x7fffffff; }
+        if (lane == 0) {
+          a.cand_val[pb * kMaxTopk + r] = bv;
+          a.cand_idx[pb * kMaxTopk + r] = bi;
+        }
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Dispatch.
+// ---------------------------------------------------------------------------
+// Unroll depth of the load pipeline and split-K width shrink as the number of
+// 16-row tiles grows, to bound registers and the LDS reduction buffer.
+template <int MT> struct Unroll {
+  static constexpr int value = MT <= 2 ? 8 : (MT <= 4 ? 4 : (MT <= 8 ? 2 : 1));
+};
+template <int WKmax, int MT> struct SplitK {
+  static constexpr int cap = MT <= 1 ? 8 : (MT <= 2 ? 4 : (MT <= 4 ? 2 : 1));
+  static constexpr int value = WKmax < cap ? WKmax : cap;
+};
+
+template <typename T, int NT, int WKmax, int WN, class Epi>
+static hipError_t run_gemm(const T *A, int lda, int M, int K, const Epi &epi, hipStream_t s) {
+  constexpr int SPAN = WN * NT * 16;
+  const int grid = (epi.nvcols + SPAN - 1) / SPAN;
+  const int mt = (M + 15) / 16;
+#define FE_GEMM_CASE(MTV)                                                              \
+  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, Unroll<MTV>::value, Epi>), \
+                     dim3(grid), dim3(64 * SplitK<WKmax, MTV>::value * WN), 0, s, A, lda, M, K, epi)
+  if (mt <= 1) FE_GEMM_CASE(1);
+  else if (mt <= 2) FE_GEMM_CASE(2);
+  else if (mt <= 4) FE_GEMM_CASE(4);
+  else if (mt <= 8) FE_GEMM_CASE(8);
+  else FE_GEMM_CASE(16);
+#undef FE_GEMM_CASE
+  return hipGetLastError();
+}
+
+hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
+                      void *out, int ldo, const void *embed, const int32_t *tokens, int vocab,
+                      void *gather_out, int ld_gather, int d, int B, hipStream_t s) {
+  if (dt) {
+    EpiStore<bf16_t> e{(const bf16_t *)W, K, ncols, (bf16_t *)out, ldo, (const bf16_t *)embed,
+                       tokens, vocab, (bf16_t *)gather_out, ld_gather, d, B};
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, K, e, s);
+  }
+  EpiStore<float> e{(const float *)W, K, ncols, (float *)out, ldo, (const float *)embed,
+                    tokens, vocab, (float *)gather_out, ld_gather, d, B};
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, K, e, s);
+}
+
+hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
+                      float *out, long ldo, const float *resid, long ldr, hipStream_t s) {
+  if (dt) {
+    EpiResid<bf16_t> e{(const bf16_t *)W, K, ncols, out, ldo, resid, ldr};
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, K, e, s);
+  }
+  EpiResid<float> e{(const float *)W, K, ncols, out, ldo, resid, ldr};
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, K, e, s);
+}
+
+hipError_t gemm_qkv(int dt, const void *A, int lda, int M, const QkvArgs &a, hipStream_t s) {
+  const int nv = (a.Hq + 2 * a.Hkv) * a.D;
+  if (dt) {
+    EpiQkv<bf16_t> e{a, nv};
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, a.d, e, s);
+  }
+  EpiQkv<float> e{a, nv};
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, a.d, e, s);
+}
+
+hipError_t gemm_swiglu(int dt, const void *A, int lda, int M, int K, const void *w_gate,
+                       const void *w_up, int I, void *s_out, int lds, hipStream_t s) {
+  if (dt) {
+    EpiSwiglu<bf16_t> e{(const bf16_t *)w_gate, (const bf16_t *)w_up, K, I, 2 * I,
+                        (bf16_t *)s_out, lds};
+    return run_gemm<bf16_t, 2, 4, 1>((const bf16_t *)A, lda, M, K, e, s);
+  }
+  EpiSwiglu<float> e{(const float *)w_gate, (const float *)w_up, K, I, 2 * I, (float *)s_out, lds};
+  return run_gemm<float, 2, 4, 1>((const float *)A, lda, M, K, e, s);
+}
+
+constexpr int kLmWN = 4;
+int lmhead_tiles(int V) { return (V + kLmWN * 16 - 1) / (kLmWN * 16); }
+
+hipError_t gemm_lmhead(int dt, const void *A, int lda, int M, int K, const LmArgs &a,
+                       int *nwg_out, hipStream_t s) {
+  *nwg_out = lmhead_tiles(a.V);
+  if (dt) {
+    EpiLm<bf16_t> e{a, K, a.V};
+    return run_gemm<bf16_t, 1, 2, kLmWN>((const bf16_t *)A, lda, M, K, e, s);
+  }
+  EpiLm<float> e{a, K, a.V};
+  return run_gemm<float, 1, 2, kLmWN>((const float *)A, lda, M, K, e, s);
+}
+
+}  // namespace fe

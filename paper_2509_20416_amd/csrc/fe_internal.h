@@ -1,0 +1,125 @@
+// fe_internal.h -- shared device helpers and kernel launchers of libfe.so
+// (gfx950 / CDNA4 only).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Storage types: bf16 is carried as its 16-bit pattern.
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct Elt;
+template <> struct Elt<uint16_t> {
+  static constexpr int kPer16B = 8;
+  __device__ static __forceinline__ float to_f(uint16_t v) { return bf2f(v); }
+  __device__ static __forceinline__ uint16_t from_f(float f) { return f2bf(f); }
+};
+template <> struct Elt<float> {
+  static constexpr int kPer16B = 4;
+  __device__ static __forceinline__ float to_f(float v) { return v; }
+  __device__ static __forceinline__ float from_f(float f) { return f; }
+};
+
+// Keys per attention chunk (one wave per chunk and KV-head group).
+constexpr int kAttnChunk = 64;
+// Largest M (rows) one GEMM launch handles; larger M is split on the host.
+constexpr int kGemmMaxRows = 256;
+constexpr int kMaxTopk = 16;
+constexpr int kMaxLayers = 16;
+
+// ---------------------------------------------------------------------------
+// Launchers.  `dt` is 0 for fp32 storage, 1 for bf16.  All return the status
+// of hipGetLastError() after the launch.
+// ---------------------------------------------------------------------------
+
+// out[m, c] = round_T(sum_k A[m,k] W[c,k]) for c < ncols; when `embed` is not
+// null, also copies embed[tokens[b]] (d elements) to gather_out + b*ld_gather.
+// Token ids outside [0, vocab) get a NaN row, so a bad id poisons that sequence's
+// outputs instead of reading outside the table.
+hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
+                      void *out, int ldo, const void *embed, const int32_t *tokens, int vocab,
+                      void *gather_out, int ld_gather, int d, int B, hipStream_t s);
+
+// out[m, c] = (resid ? resid[m, c] : 0) + sum_k A[m,k] W[c,k]   (fp32 out/resid)
+hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
+                      float *out, long ldo, const float *resid, long ldr, hipStream_t s);
+
+struct QkvArgs {
+  const void *wq, *wk, *wv;
+  int d, D, Hq, Hkv;
+  int nctx, j0, cascade;     // rows are (b, t) with t < nctx, cascade state j = j0 + t
+  const int32_t *cu_prefix;  // [B+1]
+  double theta;
+  float *q_out;              // [B, Hq, D]       (row t == nctx-1 only)
+  float *k_out, *v_out;      // [B, nctx, Hkv, D]
+};
+// Q/K/V projections of the RMS-normed context rows with rotary embedding of Q and K.
+hipError_t gemm_qkv(int dt, const void *A, int lda, int M, const QkvArgs &a, hipStream_t s);
+
+// s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
+hipError_t gemm_swiglu(int dt, const void *A, int lda, int M, int K, const void *w_gate,
+                       const void *w_up, int I, void *s_out, int lds, hipStream_t s);
+
+struct LmArgs {
+  const void *w;             // [V, d]
+  int V;
+  int topk;
+  float *logits;             // optional [M, V]
+  float *part_max, *part_sum;// [M, nwg]
+  float *cand_val;           // [M, nwg, kMaxTopk]
+  int32_t *cand_idx;         // [M, nwg, kMaxTopk]
+};
+// LM head tiles with per-tile max, sum of exponentials and top-k candidates.
+// Returns the number of column tiles (nwg) through *nwg_out.
+hipError_t gemm_lmhead(int dt, const void *A, int lda, int M, int K, const LmArgs &a,
+                       int *nwg_out, hipStream_t s);
+int lmhead_tiles(int V);
+
+// RMSNorm of rows r < rows: source row = X + (r / per)*outer + (j0 + r % per)*inner.
+hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long outer,
+                        long inner, const void *gamma, void *out, int d, float eps,
+                        hipStream_t s);
+
+// Flash-decoding partials over the prefix cache of one layer: chunks
+// 0..nch-1 of every sequence (keys beyond nch*kAttnChunk are not read);
+// partials are laid out [B, Hq, nch_ld, D+2].
+hipError_t attn_prefix(int dt, const void *K, const void *V, const int32_t *cu_prefix,
+                       const float *q, float *part, int B, int Hq, int Hkv, int D, int nch,
+                       int nch_ld, hipStream_t s);
+
+// Merge of the prefix partials (at most nch chunks per sequence) with the nctx
+// cascade keys -> out [B, Hq*D] (storage type).
+hipError_t attn_combine(int dt, const float *part, int nch, int nch_ld, const int32_t *cu_prefix,
+                        const float *q, const float *knew, const float *vnew, int nctx,
+                        void *out, int B, int Hq, int Hkv, int D, hipStream_t s);
+
+// Global top-k of every row from the tile candidates; softmax statistics merge.
+hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
+                      const int32_t *cand_idx, int rows, int nwg, int topk, int V,
+                      const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
+                      hipStream_t s);
+
+// Backbone Expansion tree of every sequence.
+hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int32_t *topk_ids,
+                      const int32_t *prefix_lens, int32_t *tokens, int32_t *parents,
+                      int32_t *depth, int32_t *positions, uint8_t *mask, int32_t *retrieve,
+                      hipStream_t s);
+
+}  // namespace fe

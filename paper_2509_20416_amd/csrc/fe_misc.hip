@@ -1,0 +1,207 @@
+// fe_misc.hip -- RMSNorm rows, LM-head top-k merge and the Backbone Expansion
+// tree (gfx950).
+#include "fe_internal.h"
+
+namespace fe {
+
+// ---------------------------------------------------------------------------
+// RMSNorm (pre-attention, pre-MLP and final norm of the LLaMA-style layer):
+// y = gamma * x / sqrt(mean(x^2) + eps), fp32 statistics, storage-type output.
+// One workgroup per row; fixed-order reductions.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *__restrict__ X, int per, int j0,
+                                                 long outer, long inner,
+                                                 const T *__restrict__ gamma, T *__restrict__ out,
+                                                 int d, float eps) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const float *x = X + (long)(r / per) * outer + (long)(j0 + r % per) * inner;
+  float ss = 0.f;
+  for (int e = threadIdx.x; e < d; e += 256) ss += x[e] * x[e];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  T *y = out + (long)r * d;
+  for (int e = threadIdx.x; e < d; e += 256)
+    y[e] = Elt<T>::from_f(Elt<T>::to_f(gamma[e]) * (x[e] * inv));
+}
+
+hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long outer, long inner,
+                        const void *gamma, void *out, int d, float eps, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (dt)
+    hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(rows), dim3(256), 0, s, X, per, j0, outer, inner,
+                       (const bf16_t *)gamma, (bf16_t *)out, d, eps);
+  else
+    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, X, per, j0, outer, inner,
+                       (const float *)gamma, (float *)out, d, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Top-k merge: the LM-head tiles left, per row, a (max, sum exp) pair and k
+// candidates each.  The row's softmax statistics are mu = max_t m_t and
+// S = sum_t s_t exp(m_t - mu); the global top-k is the best k of all tile
+// candidates (larger logit first, lower draft id on ties); p = exp(z - mu)/S.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+__global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
+                                                    const float *__restrict__ psum,
+                                                    const float *__restrict__ cval,
+                                                    const int32_t *__restrict__ cidx, int nwg,
+                                                    int topk, int V, const int32_t *__restrict__ d2t,
+                                                    int32_t *ids, int32_t *draft_ids,
+                                                    float *probs) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  __shared__ float s_mu, s_S;
+  __shared__ int taken[kMaxTopk];
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float *pm = pmax + (size_t)row * nwg;
+  const float *ps = psum + (size_t)row * nwg;
+  // mu
+  float m = -INFINITY;
+  for (int t = tid; t < nwg; t += 256) m = fmaxf(m, pm[t]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  if (lane == 0) sv[wave] = m;
+  __syncthreads();
+  const float mu = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+  __syncthreads();
+  // S, fixed order: per-thread strided partial sums, then a fixed tree
+  float S = 0.f;
+  for (int t = tid; t < nwg; t += 256) S += ps[t] * expf(pm[t] - mu);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) S += __shfl_xor(S, o);
+  if (lane == 0) sv[wave] = S;
+  __syncthreads();
+  if (tid == 0) {
+    s_mu = mu;
+    s_S = (sv[0] + sv[1]) + (sv[2] + sv[3]);
+  }
+  __syncthreads();
+  // k rounds of block argmax over nwg*topk candidates
+  const int ncand = nwg * topk;
+  for (int r = 0; r < topk; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int c = tid; c < ncand; c += 256) {
+      const int t = c / topk, j = c % topk;
+      const float v = cval[((size_t)row * nwg + t) * kMaxTopk + j];
+      const int i = cidx[((size_t)row * nwg + t) * kMaxTopk + j];
+      bool used = false;
+      for (int q = 0; q < r; ++q) used |= (taken[q] == i);
+      if (!used && better(v, i, bv, bi)) { bv = v; bi = i; }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o);
+      const int oi = __shfl_xor(bi, o);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) { sv[wave] = bv; si[wave] = bi; }
+    __syncthreads();
+    if (tid == 0) {
+      float v = sv[0];
+      int i = si[0];
+      for (int w = 1; w < 4; ++w)
+        if (better(sv[w], si[w], v, i)) { v = sv[w]; i = si[w]; }
+      taken[r] = i;
+      const size_t o = (size_t)row * topk + r;
+      const bool valid = i >= 0 && i < V;  // no valid candidate left (NaN row): -1
+      ids[o] = valid ? (d2t ? d2t[i] : i) : -1;
+      if (draft_ids) draft_ids[o] = valid ? i : -1;
+      probs[o] = valid ? expf(v - s_mu) / s_S : __int_as_float(0x7fc00000);
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
+                      const int32_t *cand_idx, int rows, int nwg, int topk, int V,
+                      const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
+                      hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, s, part_max, part_sum, cand_val,
+                     cand_idx, nwg, topk, V, d2t, ids, draft_ids, probs);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Backbone Expansion tree (Section 2.2), one workgroup per sequence.  With
+// nodes numbered root first and then level by level in rank order, node
+// n >= 1 sits at level l = 1 + (n-1)/k with rank rho = (n-1)%k; its parent is
+// the root for l = 1 and the level-(l-1) backbone node 1 + (l-2)k otherwise.
+// Its ancestors are the root, the backbone nodes of the levels above it, and
+// itself.  Leaves are the side branches (rho != 0) and the level-N backbone
+// node.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_build_tree(int N, int k,
+                                                    const int32_t *__restrict__ root_tokens,
+                                                    const int32_t *__restrict__ topk_ids,
+                                                    const int32_t *__restrict__ prefix_lens,
+                                                    int32_t *tokens, int32_t *parents,
+                                                    int32_t *depth, int32_t *positions,
+                                                    uint8_t *mask, int32_t *retrieve) {
+  const int b = blockIdx.x, T = 1 + N * k, NL = N * (k - 1) + 1;
+  const int P = prefix_lens[b];
+  for (int n = threadIdx.x; n < T; n += blockDim.x) {
+    int lvl = 0, tok = root_tokens[b], par = -1;
+    if (n > 0) {
+      lvl = 1 + (n - 1) / k;
+      const int rho = (n - 1) % k;
+      tok = topk_ids[((size_t)b * N + (lvl - 1)) * k + rho];
+      par = (lvl == 1) ? 0 : 1 + (lvl - 2) * k;
+    }
+    const size_t o = (size_t)b * T + n;
+    tokens[o] = tok;
+    parents[o] = par;
+    depth[o] = lvl;
+    positions[o] = P + lvl;
+  }
+  uint8_t *mb = mask + (size_t)b * T * T;
+  for (int idx = threadIdx.x; idx < T * T; idx += blockDim.x) {
+    const int a = idx / T, c = idx % T;
+    const int la = a == 0 ? 0 : 1 + (a - 1) / k;
+    const int lc = c == 0 ? 0 : 1 + (c - 1) / k;
+    const bool backbone_c = c > 0 && (c - 1) % k == 0;
+    mb[idx] = (c == a) || (c == 0) || (backbone_c && lc < la);
+  }
+  int32_t *rb = retrieve + (size_t)b * NL * (N + 1);
+  for (int leaf = threadIdx.x; leaf < NL; leaf += blockDim.x) {
+    // leaves in node order: levels 1..N-1 contribute ranks 1..k-1; level N
+    // contributes its backbone node and then ranks 1..k-1
+    int lvl, rho;
+    if (leaf < (N - 1) * (k - 1)) {
+      lvl = 1 + leaf / (k - 1);
+      rho = 1 + leaf % (k - 1);
+    } else {
+      lvl = N;
+      rho = leaf - (N - 1) * (k - 1);
+    }
+    int32_t *row = rb + (size_t)leaf * (N + 1);
+    row[0] = 0;
+    for (int l = 1; l < lvl; ++l) row[l] = 1 + (l - 1) * k;
+    row[lvl] = 1 + (lvl - 1) * k + rho;
+    for (int t = lvl + 1; t <= N; ++t) row[t] = -1;
+  }
+}
+
+hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int32_t *topk_ids,
+                      const int32_t *prefix_lens, int32_t *tokens, int32_t *parents,
+                      int32_t *depth, int32_t *positions, uint8_t *mask, int32_t *retrieve,
+                      hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_build_tree, dim3(B), dim3(256), 0, s, N, k, root_tokens, topk_ids,
+                     prefix_lens, tokens, parents, depth, positions, mask, retrieve);
+  return hipGetLastError();
+}
+
+}  // namespace fe

@@ -1,0 +1,370 @@
+// fe_runtime.hip -- host side of libfe.so: the C ABI of include/fe.h,
+// argument validation, workspace layout, the launch sequence of one drafting
+// pass and HIP graph capture/replay.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "../../include/fe.h"
+#include "fe_internal.h"
+
+using namespace fe;
+
+namespace {
+
+thread_local char g_err[512];
+
+fe_status fail(fe_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t cat, X, Xp, an, bn, q, knew, vnew, part, ao, s, pmax, psum, cval, cidx, total;
+  int nchmax, nwg;
+};
+
+int es_of(const fe_config &c) { return c.dtype == FE_BF16 ? 2 : 4; }
+
+Layout layout_of(const fe_config &c) {
+  Layout L{};
+  const size_t B = c.max_batch, N = c.n_layers, d = c.hidden, es = es_of(c);
+  const size_t Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, I = c.intermediate;
+  L.nchmax = c.max_prefix > 0 ? (c.max_prefix + kAttnChunk - 1) / kAttnChunk : 1;
+  L.nwg = lmhead_tiles(c.draft_vocab);
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
+  L.cat = take(B * 2 * d * es);
+  L.X = take(B * (N + 1) * d * 4);
+  L.Xp = take(B * d * 4);
+  L.an = take(B * N * d * es);
+  L.bn = take(B * d * es);
+  L.q = take(B * Hq * D * 4);
+  L.knew = take(B * N * Hkv * D * 4);
+  L.vnew = take(B * N * Hkv * D * 4);
+  L.part = take(B * Hq * (size_t)L.nchmax * (D + 2) * 4);
+  L.ao = take(B * Hq * D * es);
+  L.s = take(B * I * es);
+  L.pmax = take(B * N * (size_t)L.nwg * 4);
+  L.psum = take(B * N * (size_t)L.nwg * 4);
+  L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
+  L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
+  L.total = o;
+  return L;
+}
+
+fe_status check_config(const fe_config *c) {
+  if (!c) return fail(FE_E_INVALID, "config is NULL");
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->intermediate <= 0 || c->n_layers <= 0 || c->draft_vocab <= 0 || c->target_vocab <= 0 ||
+      c->n_feat_levels <= 0 || c->max_batch <= 0 || c->max_topk <= 0 || c->max_prefix < 0)
+    return fail(FE_E_INVALID, "config has a non-positive size");
+  if (c->dtype != FE_F32 && c->dtype != FE_BF16) return fail(FE_E_INVALID, "unknown dtype %d", c->dtype);
+  if (c->cascade_ctx != FE_CTX_CASCADE && c->cascade_ctx != FE_CTX_SELF)
+    return fail(FE_E_INVALID, "unknown cascade_ctx %d", c->cascade_ctx);
+  if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(FE_E_INVALID, "bad rope_theta or rms_eps");
+  if (c->n_q_heads % c->n_kv_heads) return fail(FE_E_INVALID, "n_q_heads must be a multiple of n_kv_heads");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(FE_E_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->n_layers > kMaxLayers) return fail(FE_E_UNSUPPORTED, "n_layers > %d", kMaxLayers);
+  if (c->max_topk > kMaxTopk) return fail(FE_E_UNSUPPORTED, "max_topk > %d", kMaxTopk);
+  if (c->max_topk > c->draft_vocab) return fail(FE_E_INVALID, "max_topk > draft_vocab");
+  if ((long)c->max_batch * c->n_layers > kGemmMaxRows)
+    return fail(FE_E_UNSUPPORTED, "max_batch * n_layers > %d", kGemmMaxRows);
+  const int kstep = c->dtype == FE_BF16 ? 32 : 16;
+  const long qd = (long)c->n_q_heads * c->head_dim;
+  if (c->hidden % kstep || c->intermediate % kstep || qd % kstep)
+    return fail(FE_E_UNSUPPORTED, "hidden, intermediate and n_q_heads*head_dim must be multiples of %d", kstep);
+  if (c->draft_vocab % 16) return fail(FE_E_UNSUPPORTED, "draft_vocab must be a multiple of 16");
+  if ((long)c->n_feat_levels * c->hidden > (1L << 30)) return fail(FE_E_UNSUPPORTED, "feature width too large");
+  return FE_OK;
+}
+
+}  // namespace
+
+struct fe_drafter {
+  fe_config cfg;
+  fe_weights w;
+  std::vector<fe_layer_weights> layers;
+  char *ws;
+  Layout L;
+  hipStream_t cap_stream = nullptr;
+  bool graph_mode = false;
+  // graph cache: key = every argument of the last captured call
+  std::vector<uintptr_t> key;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  // launch timing of one stage
+  int prof_stage = FE_STAGE_NONE;
+  int prof_count = 0;  // launches timed in the last enqueued pass
+  hipEvent_t ev_start[kMaxLayers] = {}, ev_stop[kMaxLayers] = {};
+};
+
+extern "C" {
+
+const char *fe_last_error(void) { return g_err; }
+
+size_t fe_workspace_bytes(const fe_config *cfg) {
+  if (check_config(cfg) != FE_OK) return 0;
+  return layout_of(*cfg).total;
+}
+
+fe_status fe_drafter_create(const fe_config *cfg, const fe_weights *w, void *workspace,
+                            size_t workspace_bytes, void *stream, fe_drafter **out) {
+  (void)stream;
+  if (!out) return fail(FE_E_INVALID, "out is NULL");
+  *out = nullptr;
+  fe_status st = check_config(cfg);
+  if (st != FE_OK) return st;
+  if (!w || !w->layers) return fail(FE_E_INVALID, "weights or weights->layers is NULL");
+  const void *top[] = {w->w_fuse, w->w_in, w->embed, w->final_norm, w->lm_head};
+  const char *topn[] = {"w_fuse", "w_in", "embed", "final_norm", "lm_head"};
+  for (int i = 0; i < 5; ++i) {
+    if (!top[i]) return fail(FE_E_INVALID, "weight %s is NULL", topn[i]);
+    if (!aligned16(top[i])) return fail(FE_E_ALIGN, "weight %s is not 16-byte aligned", topn[i]);
+  }
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const fe_layer_weights &lw = w->layers[l];
+    const void *p[] = {lw.attn_norm, lw.wq, lw.wk, lw.wv, lw.wo, lw.mlp_norm, lw.w_gate, lw.w_up, lw.w_down};
+    for (int i = 0; i < 9; ++i) {
+      if (!p[i]) return fail(FE_E_INVALID, "layer %d weight %d is NULL", l, i);
+      if (!aligned16(p[i])) return fail(FE_E_ALIGN, "layer %d weight %d is not 16-byte aligned", l, i);
+    }
+  }
+  const Layout L = layout_of(*cfg);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(FE_E_WORKSPACE, "workspace needs %zu bytes, got %zu", L.total, workspace ? workspace_bytes : 0);
+  if (((uintptr_t)workspace & 255u) != 0) return fail(FE_E_ALIGN, "workspace must be 256-byte aligned");
+  fe_drafter *h = new (std::nothrow) fe_drafter();
+  if (!h) return fail(FE_E_INVALID, "out of host memory");
+  h->cfg = *cfg;
+  h->w = *w;
+  h->layers.assign(w->layers, w->layers + cfg->n_layers);
+  h->w.layers = h->layers.data();
+  h->ws = (char *)workspace;
+  h->L = L;
+  *out = h;
+  return FE_OK;
+}
+
+fe_status fe_set_graph_mode(fe_drafter *h, int32_t on) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  h->graph_mode = on != 0;
+  return FE_OK;
+}
+
+fe_status fe_profile_stage(fe_drafter *h, int32_t stage) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  if (stage < FE_STAGE_NONE || stage > FE_STAGE_LMHEAD) return fail(FE_E_INVALID, "unknown stage %d", stage);
+  if (stage != FE_STAGE_NONE && !h->ev_start[0]) {
+    for (int i = 0; i < kMaxLayers; ++i) {
+      if (hipEventCreate(&h->ev_start[i]) != hipSuccess || hipEventCreate(&h->ev_stop[i]) != hipSuccess)
+        return fail(FE_E_HIP, "hipEventCreate failed");
+    }
+  }
+  h->prof_stage = stage;
+  h->prof_count = 0;
+  return FE_OK;
+}
+
+fe_status fe_profile_read(fe_drafter *h, float *ms, int32_t cap, int32_t *count) {
+  if (!h || !count || (cap > 0 && !ms)) return fail(FE_E_INVALID, "bad arguments");
+  *count = h->prof_stage == FE_STAGE_NONE ? 0 : h->prof_count;
+  for (int i = 0; i < *count && i < cap; ++i) {
+    hipError_t e = hipEventSynchronize(h->ev_stop[i]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms[i], h->ev_start[i], h->ev_stop[i]);
+    if (e != hipSuccess) return fail(FE_E_HIP, "event timing: %s", hipGetErrorString(e));
+  }
+  return FE_OK;
+}
+
+void fe_drafter_destroy(fe_drafter *h) {
+  if (!h) return;
+  for (int i = 0; i < kMaxLayers; ++i) {
+    if (h->ev_start[i]) (void)hipEventDestroy(h->ev_start[i]);
+    if (h->ev_stop[i]) (void)hipEventDestroy(h->ev_stop[i]);
+  }
+  if (h->exec) (void)hipGraphExecDestroy(h->exec);
+  if (h->graph) (void)hipGraphDestroy(h->graph);
+  if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
+  delete h;
+}
+
+}  // extern "C"
+
+namespace {
+
+#define FE_TRY(x)                                                           \
+  do {                                                                      \
+    hipError_t e_ = (x);                                                    \
+    if (e_ != hipSuccess) return fail(FE_E_HIP, "%s: %s", #x, hipGetErrorString(e_)); \
+  } while (0)
+
+// Brackets one launch with the handle's timing events when its stage is timed.
+struct StageTimer {
+  fe_drafter *h;
+  hipStream_t s;
+  int stage, idx = -1;
+  StageTimer(fe_drafter *h_, int stage_, hipStream_t s_) : h(h_), s(s_), stage(stage_) {
+    if (h->prof_stage == stage && h->prof_count < kMaxLayers) {
+      idx = h->prof_count++;
+      (void)hipEventRecord(h->ev_start[idx], s);
+    }
+  }
+  ~StageTimer() {
+    if (idx >= 0) (void)hipEventRecord(h->ev_stop[idx], s);
+  }
+};
+#define FE_TIMED(stage, x) \
+  do {                     \
+    StageTimer t_(h, stage, s); \
+    FE_TRY(x);             \
+  } while (0)
+
+// The whole pass: FCs of Eq. 1, N cascade layers (Eq. 2), LM head + top-k.
+fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int32_t *next_tokens,
+                          const fe_kv_view *kv, int topk, const fe_draft_out *out,
+                          hipStream_t s) {
+  const fe_config &c = h->cfg;
+  const Layout &L = h->L;
+  const int dt = c.dtype == FE_BF16 ? 1 : 0;
+  const int d = c.hidden, N = c.n_layers, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
+  const int I = c.intermediate, qd = Hq * D, F = c.n_feat_levels;
+  char *ws = h->ws;
+  void *cat = ws + L.cat;
+  float *X = (float *)(ws + L.X), *Xp = (float *)(ws + L.Xp);
+  void *an = ws + L.an, *bn = ws + L.bn, *ao = ws + L.ao, *sbuf = ws + L.s;
+  float *q = (float *)(ws + L.q), *knew = (float *)(ws + L.knew), *vnew = (float *)(ws + L.vnew);
+  float *part = (float *)(ws + L.part);
+  const long xrow = (long)(N + 1) * d;  // stride between sequences in X
+  const int esz = dt ? 2 : 4;
+  const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
+  const int nch_ld = L.nchmax;
+  h->prof_count = 0;
+
+  // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
+  FE_TIMED(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
+                    next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s));
+  // x_0 = FC(concat(g_t, e_{t+1}))  (Eq. 1)
+  FE_TIMED(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr, 0, s));
+
+  for (int i = 1; i <= N; ++i) {
+    const fe_layer_weights &lw = h->layers[i - 1];
+    const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
+    const int nctx = cascade ? i : 1, j0 = cascade ? 0 : i - 1;
+    // pre-attention RMSNorm of the context rows
+    FE_TRY(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
+    QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
+               (double)c.rope_theta, q, knew, vnew};
+    FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, an, d, B * nctx, qa, s));
+    // attention over the layer's prefix cache plus the cascade keys
+    FE_TIMED(FE_STAGE_ATTN, attn_prefix(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, part, B, Hq, Hkv, D,
+                       nch, nch_ld, s));
+    FE_TRY(attn_combine(dt, part, nch, nch_ld, kv->cu_prefix, q, knew, vnew, nctx, ao, B, Hq,
+                        Hkv, D, s));
+    // x' = x_{i-1} + W_o o
+    FE_TIMED(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d, X + (size_t)(i - 1) * d, xrow, s));
+    // SwiGLU MLP on RMSNorm(x'), residual into x_i
+    FE_TRY(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
+    FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, B, d, lw.w_gate, lw.w_up, I, sbuf, I, s));
+    FE_TIMED(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow, Xp, d, s));
+  }
+
+  // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
+  FE_TRY(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
+  LmArgs la{h->w.lm_head, c.draft_vocab, topk, out->logits, (float *)(ws + L.pmax),
+            (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx)};
+  int nwg = 0;
+  FE_TIMED(FE_STAGE_LMHEAD, gemm_lmhead(dt, an, d, B * N, d, la, &nwg, s));
+  FE_TRY(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx, B * N, nwg, topk,
+                    c.draft_vocab, h->w.d2t, out->topk_ids, out->topk_draft, out->topk_probs, s));
+  if (out->hidden)
+    FE_TRY(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
+                          hipMemcpyDeviceToDevice, s));
+  return FE_OK;
+}
+
+}  // namespace
+
+extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *features,
+                                      const int32_t *next_tokens, const fe_kv_view *kv,
+                                      int32_t topk, const fe_draft_out *out, void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const fe_config &c = h->cfg;
+  if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
+  if (topk < 1 || topk > c.max_topk || topk > c.draft_vocab)
+    return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
+  if (!out || !out->topk_ids || !out->topk_probs) return fail(FE_E_INVALID, "out, out->topk_ids and out->topk_probs are required");
+  if (!kv || !kv->k || !kv->v || !kv->cu_prefix) return fail(FE_E_INVALID, "kv view is incomplete");
+  if (kv->max_prefix < 0 || kv->max_prefix > c.max_prefix)
+    return fail(FE_E_INVALID, "kv->max_prefix %d outside [0, %d]", kv->max_prefix, c.max_prefix);
+  if (batch == 0) return FE_OK;
+  if (!features || !next_tokens) return fail(FE_E_INVALID, "features and next_tokens are required");
+  if (!aligned16(features)) return fail(FE_E_ALIGN, "features must be 16-byte aligned");
+  for (int l = 0; l < c.n_layers; ++l) {
+    if (kv->max_prefix > 0 && (!kv->k[l] || !kv->v[l]))
+      return fail(FE_E_INVALID, "kv cache pointer of layer %d is NULL", l);
+    if (!aligned16(kv->k[l]) || !aligned16(kv->v[l]))
+      return fail(FE_E_ALIGN, "kv cache of layer %d is not 16-byte aligned", l);
+  }
+  if (out->logits && ((uintptr_t)out->logits & 3u)) return fail(FE_E_ALIGN, "logits misaligned");
+  hipStream_t s = (hipStream_t)stream;
+
+  if (!h->graph_mode) return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
+
+  std::vector<uintptr_t> key = {(uintptr_t)batch, (uintptr_t)features, (uintptr_t)next_tokens,
+                                (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
+                                (uintptr_t)topk, (uintptr_t)out->topk_ids,
+                                (uintptr_t)out->topk_probs, (uintptr_t)out->topk_draft,
+                                (uintptr_t)out->logits, (uintptr_t)out->hidden,
+                                (uintptr_t)(intptr_t)h->prof_stage};
+  for (int l = 0; l < c.n_layers; ++l) {
+    key.push_back((uintptr_t)kv->k[l]);
+    key.push_back((uintptr_t)kv->v[l]);
+  }
+  if (!h->exec || key != h->key) {
+    if (!h->cap_stream) FE_TRY(hipStreamCreateWithFlags(&h->cap_stream, hipStreamNonBlocking));
+    if (h->exec) { (void)hipGraphExecDestroy(h->exec); h->exec = nullptr; }
+    if (h->graph) { (void)hipGraphDestroy(h->graph); h->graph = nullptr; }
+    h->key.clear();
+    FE_TRY(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
+    fe_status st = enqueue_forward(h, batch, features, next_tokens, kv, topk, out, h->cap_stream);
+    hipGraph_t g = nullptr;
+    hipError_t ec = hipStreamEndCapture(h->cap_stream, &g);
+    if (st != FE_OK) { if (g) (void)hipGraphDestroy(g); return st; }
+    if (ec != hipSuccess) return fail(FE_E_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ec));
+    h->graph = g;
+    FE_TRY(hipGraphInstantiate(&h->exec, g, nullptr, nullptr, 0));
+    h->key = key;
+  }
+  FE_TRY(hipGraphLaunch(h->exec, s));
+  return FE_OK;
+}
+
+extern "C" fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk,
+                                   const int32_t *root_tokens, const int32_t *topk_ids,
+                                   const int32_t *prefix_lens, const fe_tree_out *out,
+                                   void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const fe_config &c = h->cfg;
+  if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
+  if (topk < 1 || topk > c.max_topk) return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
+  if (batch == 0) return FE_OK;
+  if (!root_tokens || !topk_ids || !prefix_lens) return fail(FE_E_INVALID, "tree inputs are required");
+  if (!out || !out->tokens || !out->parents || !out->depth || !out->positions || !out->mask ||
+      !out->retrieve)
+    return fail(FE_E_INVALID, "every tree output is required");
+  FE_TRY(build_tree(batch, c.n_layers, topk, root_tokens, topk_ids, prefix_lens, out->tokens,
+                    out->parents, out->depth, out->positions, out->mask, out->retrieve,
+                    (hipStream_t)stream));
+  return FE_OK;
+}

@@ -1,0 +1,158 @@
+"""ctypes binding of libfe.so (include/fe.h): argument marshalling only.
+
+Every computation happens in the HIP kernels of the library; this module
+mirrors the C structs and calls the C entry points by the same names.  It
+raises if the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfe.so")
+
+FE_OK, FE_E_INVALID, FE_E_UNSUPPORTED, FE_E_ALIGN, FE_E_WORKSPACE, FE_E_HIP = range(6)
+FE_F32, FE_BF16 = 0, 1
+FE_CTX_CASCADE, FE_CTX_SELF = 0, 1
+STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_ALIGN",
+                4: "FE_E_WORKSPACE", 5: "FE_E_HIP"}
+
+# Every function include/fe.h declares.
+EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
+           "fe_set_graph_mode", "fe_profile_stage", "fe_profile_read", "fe_drafter_destroy",
+           "fe_last_error")
+FE_STAGE = dict(none=-1, fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
+
+
+class fe_config(C.Structure):
+    _fields_ = [("hidden", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("intermediate", C.c_int32), ("n_layers", C.c_int32),
+                ("draft_vocab", C.c_int32), ("target_vocab", C.c_int32),
+                ("n_feat_levels", C.c_int32), ("max_batch", C.c_int32), ("max_topk", C.c_int32),
+                ("max_prefix", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float),
+                ("dtype", C.c_int32), ("cascade_ctx", C.c_int32)]
+
+
+class fe_layer_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm",
+                                          "w_gate", "w_up", "w_down")]
+
+
+class fe_weights(C.Structure):
+    _fields_ = [("w_fuse", C.c_void_p), ("w_in", C.c_void_p), ("embed", C.c_void_p),
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p), ("d2t", C.c_void_p),
+                ("layers", C.POINTER(fe_layer_weights))]
+
+
+class fe_kv_view(C.Structure):
+    _fields_ = [("k", C.POINTER(C.c_void_p)), ("v", C.POINTER(C.c_void_p)),
+                ("cu_prefix", C.c_void_p), ("max_prefix", C.c_int32)]
+
+
+class fe_draft_out(C.Structure):
+    _fields_ = [("topk_ids", C.c_void_p), ("topk_probs", C.c_void_p), ("topk_draft", C.c_void_p),
+                ("logits", C.c_void_p), ("hidden", C.c_void_p)]
+
+
+class fe_tree_out(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("tokens", "parents", "depth", "positions", "mask",
+                                          "retrieve")]
+
+
+_lib = None
+
+
+class FeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib() -> C.CDLL:
+    """Load libfe.so; raise if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2509_20416_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        L.fe_workspace_bytes.restype = C.c_size_t
+        L.fe_workspace_bytes.argtypes = [C.POINTER(fe_config)]
+        L.fe_drafter_create.restype = C.c_int
+        L.fe_drafter_create.argtypes = [C.POINTER(fe_config), C.POINTER(fe_weights), C.c_void_p,
+                                        C.c_size_t, C.c_void_p, C.POINTER(C.c_void_p)]
+        L.fe_draft_forward.restype = C.c_int
+        L.fe_draft_forward.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                       C.POINTER(fe_kv_view), C.c_int32,
+                                       C.POINTER(fe_draft_out), C.c_void_p]
+        L.fe_build_tree.restype = C.c_int
+        L.fe_build_tree.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                    C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
+        L.fe_set_graph_mode.restype = C.c_int
+        L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
+        L.fe_profile_stage.restype = C.c_int
+        L.fe_profile_stage.argtypes = [C.c_void_p, C.c_int32]
+        L.fe_profile_read.restype = C.c_int
+        L.fe_profile_read.argtypes = [C.c_void_p, C.POINTER(C.c_float), C.c_int32,
+                                      C.POINTER(C.c_int32)]
+        L.fe_drafter_destroy.restype = None
+        L.fe_drafter_destroy.argtypes = [C.c_void_p]
+        L.fe_last_error.restype = C.c_char_p
+        L.fe_last_error.argtypes = []
+        _lib = L
+    return _lib
+
+
+def fe_last_error() -> str:
+    return lib().fe_last_error().decode(errors="replace")
+
+
+def check(status: int) -> None:
+    if status != FE_OK:
+        raise FeError(status, fe_last_error())
+
+
+def fe_workspace_bytes(cfg: fe_config) -> int:
+    return int(lib().fe_workspace_bytes(C.byref(cfg)))
+
+
+def fe_drafter_create(cfg: fe_config, w: fe_weights, workspace: int, ws_bytes: int,
+                      stream: int = 0) -> int:
+    h = C.c_void_p()
+    check(lib().fe_drafter_create(C.byref(cfg), C.byref(w), C.c_void_p(workspace),
+                                  C.c_size_t(ws_bytes), C.c_void_p(stream), C.byref(h)))
+    return h.value
+
+
+def fe_draft_forward(h: int, batch: int, features: int, next_tokens: int, kv: fe_kv_view,
+                     topk: int, out: fe_draft_out, stream: int) -> None:
+    check(lib().fe_draft_forward(C.c_void_p(h), batch, C.c_void_p(features),
+                                 C.c_void_p(next_tokens), C.byref(kv), topk, C.byref(out),
+                                 C.c_void_p(stream)))
+
+
+def fe_build_tree(h: int, batch: int, topk: int, root_tokens: int, topk_ids: int,
+                  prefix_lens: int, out: fe_tree_out, stream: int) -> None:
+    check(lib().fe_build_tree(C.c_void_p(h), batch, topk, C.c_void_p(root_tokens),
+                              C.c_void_p(topk_ids), C.c_void_p(prefix_lens), C.byref(out),
+                              C.c_void_p(stream)))
+
+
+def fe_set_graph_mode(h: int, on: bool) -> None:
+    check(lib().fe_set_graph_mode(C.c_void_p(h), 1 if on else 0))
+
+
+def fe_profile_stage(h: int, stage: int) -> None:
+    check(lib().fe_profile_stage(C.c_void_p(h), int(stage)))
+
+
+def fe_profile_read(h: int, cap: int = 16):
+    ms = (C.c_float * cap)()
+    n = C.c_int32()
+    check(lib().fe_profile_read(C.c_void_p(h), ms, cap, C.byref(n)))
+    return [float(ms[i]) for i in range(min(cap, n.value))]
+
+
+def fe_drafter_destroy(h: int) -> None:
+    lib().fe_drafter_destroy(C.c_void_p(h))

@@ -1,0 +1,78 @@
+"""Comparison rules between the GPU path and the CPU oracle.
+
+* Cascade states x_0..x_N and logits: per row, max|gpu - ref| / max|ref| <= tol,
+  tol = 1e-4 for fp32 storage and 2e-2 for bf16 storage.
+* Top-k: a rank is decided by the oracle when both of its neighbouring oracle
+  gaps exceed thr = 2 * tol * max|z_row| (twice the worst per-logit error the
+  tolerance allows); a decided rank must hold exactly the oracle's id.  An
+  undecided rank must hold an id whose oracle logit lies within thr of the
+  oracle's value at that rank (several answers are correct there).
+* Probabilities: |log p_gpu - log p_ref(id)| <= 2 * thr.
+* Tree structure (parents, depth, positions, mask, retrieve) is value
+  independent and must be bit-exact; tree tokens follow the top-k rule.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_row_err(gpu: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    g = gpu.reshape(-1, gpu.shape[-1]).astype(np.float64)
+    r = ref.reshape(-1, ref.shape[-1]).astype(np.float64)
+    return np.abs(g - r).max(-1) / np.maximum(np.abs(r).max(-1), 1e-30)
+
+
+def assert_rows_close(name, gpu, ref, tol):
+    err = rel_row_err(gpu, ref)
+    worst = float(err.max()) if err.size else 0.0
+    assert np.isfinite(gpu).all(), f"{name}: non-finite GPU values"
+    assert worst <= tol, f"{name}: worst per-row relative error {worst:.3e} > {tol:.1e}"
+    return worst
+
+
+def check_topk(gpu_draft: np.ndarray, gpu_probs: np.ndarray, ref_logits: np.ndarray,
+               ref_draft: np.ndarray, tol: float):
+    """gpu_draft/ref_draft [rows, k] draft ids; ref_logits [rows, V].
+    Returns (n_decided, n_ranks)."""
+    rows, k = gpu_draft.shape
+    z = ref_logits.reshape(rows, -1)
+    decided = 0
+    for r in range(rows):
+        zr = z[r]
+        thr = 2.0 * tol * np.abs(zr).max()
+        order = ref_draft[r]
+        assert len(set(gpu_draft[r].tolist())) == k, f"row {r}: duplicate ids {gpu_draft[r]}"
+        zs = zr[order]                           # oracle values at ranks 0..k-1
+        znext = np.partition(zr, -(k + 1))[-(k + 1)] if zr.size > k else -np.inf
+        for rho in range(k):
+            up = np.inf if rho == 0 else zs[rho - 1] - zs[rho]
+            down = (zs[rho] - zs[rho + 1]) if rho + 1 < k else (zs[rho] - znext)
+            gid = int(gpu_draft[r, rho])
+            if up > thr and down > thr:
+                decided += 1
+                assert gid == order[rho], (f"row {r} rank {rho}: gpu id {gid} != oracle "
+                                           f"{order[rho]} (gaps {up:.3g}/{down:.3g} > {thr:.3g})")
+            else:
+                assert abs(zr[gid] - zs[rho]) <= thr, (
+                    f"row {r} rank {rho}: gpu id {gid} has oracle logit {zr[gid]:.6g}, "
+                    f"rank value {zs[rho]:.6g}, allowed {thr:.3g}")
+        # probabilities of what the GPU chose
+        mx = zr.max()
+        lse = mx + np.log(np.exp(zr - mx).sum())
+        lp_ref = zr[gpu_draft[r]] - lse
+        lp_gpu = np.log(np.maximum(gpu_probs[r].astype(np.float64), 1e-300))
+        assert np.abs(lp_gpu - lp_ref).max() <= 2 * thr + 1e-6, (
+            f"row {r}: log-prob error {np.abs(lp_gpu - lp_ref).max():.3e} > {2 * thr:.3e}")
+    return decided, rows * k
+
+
+def check_topk_self_consistent(gpu_draft: np.ndarray, gpu_logits: np.ndarray):
+    """The fused top-k must be exactly the (z desc, id asc) order of the GPU's own
+    fp32 logits: the selection is taken in the kernel's precision."""
+    rows, k = gpu_draft.shape
+    z = gpu_logits.reshape(rows, -1)
+    for r in range(rows):
+        idx = np.lexsort((np.arange(z.shape[1]), -z[r].astype(np.float64)))[:k]
+        np.testing.assert_array_equal(gpu_draft[r], idx, err_msg=f"row {r}")

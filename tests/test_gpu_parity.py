@@ -1,0 +1,170 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Rules in tests/parity.py."""
+import os
+
+import numpy as np
+import pytest
+
+from fe_synth import configs as C
+from fe_synth import make_inputs, make_weights
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2509_20416_amd import fe
+    fe.lib()   # loud failure if the library is missing
+    from oracle import feo
+    feo.set_threads(min(16, len(os.sched_getaffinity(0))))
+
+
+def _run(*a, **kw):
+    from tests.gpu_case import run_case
+    return run_case(*a, **kw)
+
+
+# --- tree kernel alone: bit-exact on every array -------------------------------------------
+@pytest.mark.parametrize("N,k,B", [(1, 1, 1), (3, 1, 2), (5, 8, 1), (7, 8, 32), (5, 10, 3),
+                                   (16, 16, 2), (2, 3, 5)])
+def test_tree_kernel_bit_exact(N, k, B):
+    import torch
+    from oracle import feo
+    from paper_2509_20416_amd import Drafter
+    cfg = C.TINY_F32_B1.with_(n_layers=N, topk=k, batch=B, draft_vocab=max(1024, 16 * k))
+    rng = np.random.default_rng(N * 1000 + k * 10 + B)
+    ids = np.stack([np.stack([rng.choice(128256, k, replace=False) for _ in range(N)])
+                    for _ in range(B)]).astype(np.int32)
+    roots = rng.integers(0, 128256, B).astype(np.int32)
+    plens = rng.integers(0, 9000, B).astype(np.int32)
+    w = make_weights(cfg.with_(n_layers=1), 0)
+    w.layers = w.layers * N
+    dr = Drafter(cfg, w, max_batch=B, max_prefix=0, max_topk=k)
+    inp = make_inputs(cfg.with_(n_layers=N, prefix=0), 0)
+    inp.next_tokens = roots
+    inp.prefix_lens = plens
+    inp.kcache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim), np.float32)] * N
+    inp.vcache = inp.kcache
+    di = dr.upload_inputs(inp, max_prefix=0)
+    di.next_tokens = torch.from_numpy(roots).cuda()
+    tree = dr.build_tree(di, torch.from_numpy(ids).cuda(), k)
+    torch.cuda.synchronize()
+    ref = feo.build_tree(N, k, roots, ids, plens)
+    for n in ref:
+        np.testing.assert_array_equal(tree[n].cpu().numpy(), ref[n], err_msg=n)
+    dr.close()
+
+
+# --- small shapes: several tiles, ragged chunks, ragged batch, P = 0 -----------------------
+SMALL = [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128, C.TINY_F32_B1]
+
+
+@pytest.mark.parametrize("ctx", ["cascade", "self"])
+@pytest.mark.parametrize("cfg", SMALL, ids=lambda c: c.name)
+def test_small_parity(cfg, ctx):
+    cfg = cfg.with_(cascade_ctx=ctx)
+    plens = None
+    if cfg.batch == 3:
+        plens = np.array([0, 700, 65], np.int32)   # empty prefix, several chunks, ragged tail
+    rep, _, _ = _run(cfg, seed=1, prefix_lens=plens)
+    if cfg.dtype == "f32":
+        assert rep["decided"] >= rep["ranks"] // 2, rep
+
+
+def test_topk_edge_values():
+    """k = 1 (chain tree) and k = max (16)."""
+    for k in (1, 16):
+        _run(C.SMALL_GQA_BF16.with_(topk=k), seed=2, topk=k,
+             prefix_lens=np.array([3, 129, 64], np.int32))
+
+
+def test_planted_topk_is_exact():
+    """LM-head rows planted so that one row's top-k has wide, known gaps: every
+    rank of that row must be decided and match."""
+    from oracle import feo
+    from fe_synth import to_f64
+    cfg = C.SMALL_GQA_BF16
+    w = make_weights(cfg, 3)
+    inp = make_inputs(cfg, 3, np.array([10, 0, 300], np.int32))
+    ref = feo.draft_forward(cfg, w, inp)
+    h = ref["hidden"][0, 1]                                   # x_1 of sequence 0
+    g = to_f64(w.final_norm, "bf16")
+    hn = g * h / np.sqrt(np.mean(h * h) + cfg.rms_eps)
+    ids = np.array([17, 1999, 3, 640, 1024])
+    scale = np.array([13.0, 11.0, 9.0, 7.0, 5.0])
+    rows = (scale[:, None] * hn[None] / (hn @ hn)).astype(np.float32)
+    b = rows.view(np.uint32)
+    w.lm_head[ids] = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+    rep, res, _ = _run(cfg, seed=3, weights=w, inputs=inp)
+    np.testing.assert_array_equal(res["topk_draft"][0, 0], ids)
+
+
+def test_deterministic_and_graph_replay_bitwise():
+    import torch
+    from paper_2509_20416_amd import Drafter
+    cfg = C.SMALL_GQA_BF16
+    w = make_weights(cfg, 4)
+    inp = make_inputs(cfg, 4)
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(inp.prefix_lens.max()))
+    di = dr.upload_inputs(inp)
+    a = {n: t.cpu().numpy() for n, t in dr.forward(di, logits=True, hidden=True).items()}
+    b = {n: t.cpu().numpy() for n, t in dr.forward(di, logits=True, hidden=True).items()}
+    for n in a:
+        np.testing.assert_array_equal(a[n], b[n], err_msg=n)
+    dr.set_graph_mode(True)
+    out = dr.alloc_outputs(cfg.batch, cfg.topk, logits=True, hidden=True)
+    for rep in range(4):                     # replays with eager work in between
+        for t in out.values():
+            t.zero_()
+        dr.forward(di, out=out)
+        torch.cuda.synchronize()
+        _ = torch.ones(1000, device="cuda").sum().item()
+        for n in a:
+            np.testing.assert_array_equal(out[n].cpu().numpy(), a[n], err_msg=f"replay {rep} {n}")
+    dr.close()
+
+
+def test_invalid_token_poisons_only_its_sequence():
+    import torch
+    from paper_2509_20416_amd import Drafter
+    cfg = C.SMALL_GQA_BF16
+    w = make_weights(cfg, 5)
+    inp = make_inputs(cfg, 5)
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(inp.prefix_lens.max()))
+    inp.next_tokens = np.array([inp.next_tokens[0], cfg.target_vocab + 7, inp.next_tokens[2]],
+                               np.int32)
+    di = dr.upload_inputs(inp)
+    out = dr.forward(di, hidden=True)
+    torch.cuda.synchronize()
+    hid = out["hidden"].cpu().numpy()
+    assert np.isnan(hid[1]).all() and np.isfinite(hid[[0, 2]]).all()
+    dr.close()
+
+
+# --- paper-shaped workloads at full size, in the configuration the bench times -----------
+@pytest.mark.timeout(900)
+def test_llama8b_b1_full():
+    _run(C.LLAMA8B_BF16_B1, seed=0, graph=True)
+
+
+@pytest.mark.timeout(900)
+def test_vicuna13b_b1_full():
+    _run(C.VICUNA13B_BF16_B1, seed=0, graph=True)
+
+
+@pytest.mark.timeout(1200)
+def test_llama70b_b1_full():
+    _run(C.LLAMA70B_BF16_B1, seed=0, graph=True, with_debug=False)
+
+
+@pytest.mark.timeout(1200)
+def test_llama8b_b32_ragged_sampled():
+    """Batch 32, P_b ~ U[256, 8192]: oracle on the shortest and the longest sequence."""
+    from fe_synth import make_prefix_lens
+    cfg = C.LLAMA8B_BF16_B32
+    plens = make_prefix_lens(cfg, 0)
+    sample = [int(np.argmin(plens)), int(np.argmax(plens))]
+    _run(cfg, seed=0, graph=True, sample=sample)
