@@ -183,8 +183,9 @@ typedef enum {
 
 /* Times every launch of `stage` (FE_STAGE_NONE turns timing off): from the
  * next fe_draft_forward on, a pair of HIP events owned by the handle is
- * recorded on the launch stream around each launch of that stage (also
- * inside a captured graph).  Changing the stage forces a new graph capture. */
+ * recorded on the launch stream around each launch of that stage.  While a
+ * stage is timed, fe_draft_forward launches its kernels one by one (no graph
+ * replay) so that every launch can be bracketed. */
 fe_status fe_profile_stage(fe_drafter *h, int32_t stage);
 
 /* Waits for the events of the most recent pass and writes the duration in

@@ -25,18 +25,24 @@ namespace fe {
 template <typename T, int D> struct KvRow {
   static constexpr int DL = D / 8;                      // dims per lane
   static constexpr int NV = DL * sizeof(T) / 16;        // 16-byte loads per lane
-  u32x4 raw[NV];
+  uint32_t w[NV * 4];  // plain words: element access by index never touches a vector
   __device__ __forceinline__ void load(const T *p) {
     const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) raw[i] = q[i];
+    for (int i = 0; i < NV; ++i) {
+      const u32x4 v = q[i];
+      w[4 * i + 0] = v.x;
+      w[4 * i + 1] = v.y;
+      w[4 * i + 2] = v.z;
+      w[4 * i + 3] = v.w;
+    }
   }
   __device__ __forceinline__ float at(int e) const {
     if constexpr (sizeof(T) == 2) {
-      const uint32_t w = raw[e / 8][(e % 8) / 2];
-      return (e & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
+      const uint32_t u = w[e / 2];
+      return (e & 1) ? __uint_as_float(u & 0xffff0000u) : __uint_as_float(u << 16);
     } else {
-      return __uint_as_float(raw[e / 4][e % 4]);
+      return __uint_as_float(w[e]);
     }
   }
 };

@@ -34,11 +34,15 @@ template <> __device__ __forceinline__ void mma16<uint16_t>(f32x4 &acc, u32x4 a,
                                                 __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
 }
 
+// Four K=4 fp32 MFMAs, one per element of the lanes' 16-byte fragments.  The
+// elements are named explicitly: a loop over a vector element index here was
+// compiled to four uses of element 0.
 template <> __device__ __forceinline__ void mma16<float>(f32x4 &acc, u32x4 a, u32x4 b) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a[e]),
-                                               __builtin_bit_cast(float, b[e]), acc, 0, 0, 0);
+  const f32x4 af = __builtin_bit_cast(f32x4, a), bf = __builtin_bit_cast(f32x4, b);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af.x, bf.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af.y, bf.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af.z, bf.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af.w, bf.w, acc, 0, 0, 0);
 }
 
 __device__ __forceinline__ u32x4 ldg_stream(const u32x4 *p) { return __builtin_nontemporal_load(p); }

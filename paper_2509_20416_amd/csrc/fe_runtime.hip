@@ -319,14 +319,14 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   if (out->logits && ((uintptr_t)out->logits & 3u)) return fail(FE_E_ALIGN, "logits misaligned");
   hipStream_t s = (hipStream_t)stream;
 
-  if (!h->graph_mode) return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
+  if (!h->graph_mode || h->prof_stage != FE_STAGE_NONE)
+    return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
 
   std::vector<uintptr_t> key = {(uintptr_t)batch, (uintptr_t)features, (uintptr_t)next_tokens,
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
                                 (uintptr_t)topk, (uintptr_t)out->topk_ids,
                                 (uintptr_t)out->topk_probs, (uintptr_t)out->topk_draft,
-                                (uintptr_t)out->logits, (uintptr_t)out->hidden,
-                                (uintptr_t)(intptr_t)h->prof_stage};
+                                (uintptr_t)out->logits, (uintptr_t)out->hidden};
   for (int l = 0; l < c.n_layers; ++l) {
     key.push_back((uintptr_t)kv->k[l]);
     key.push_back((uintptr_t)kv->v[l]);
