@@ -134,10 +134,13 @@ typedef struct fe_drafter fe_drafter;
 size_t fe_workspace_bytes(const fe_config *cfg);
 
 /* Creates a drafter over borrowed weights and workspace (Section 2.1).
- * Supported shapes: head_dim 64 or 128; d, I, H_q*D, V multiples of 32 (bf16)
- * or 16 (fp32); 1 <= n_layers <= 16; 1 <= max_topk <= 16; H_q % H_kv == 0.
- * `workspace` must hold fe_workspace_bytes(cfg) bytes.  `stream` is used for
- * set-up work only.  On success *out receives the handle. */
+ * Supported shapes: head_dim 64 or 128; d, I, H_q*D multiples of 32 (bf16) or
+ * 16 (fp32); V a multiple of 16 with ceil(V/64)*max_topk <= 8192;
+ * 1 <= n_layers <= 16; 1 <= max_topk <= 16; H_q % H_kv == 0;
+ * max_batch*n_layers <= 256.  `workspace` (256-byte aligned) must hold
+ * fe_workspace_bytes(cfg) bytes; the first fe_draft_forward initialises the
+ * small part of it that persists between calls.  Creation makes no HIP call;
+ * `stream` is unused.  On success *out receives the handle. */
 fe_status fe_drafter_create(const fe_config *cfg, const fe_weights *w, void *workspace,
                             size_t workspace_bytes, void *stream, fe_drafter **out);
 
@@ -174,7 +177,7 @@ typedef enum {
   FE_STAGE_FUSE = 0,     /* g_t = FC(l, m, h) and the embedding gather (one launch) */
   FE_STAGE_INPUT = 1,    /* x_0 = FC(g_t, e_{t+1}) (one launch) */
   FE_STAGE_QKV = 2,      /* per layer: Q/K/V projections + rotary embedding */
-  FE_STAGE_ATTN = 3,     /* per layer: prefix attention partials */
+  FE_STAGE_ATTN = 3,     /* per layer: attention over the prefix cache and cascade keys */
   FE_STAGE_OPROJ = 4,    /* per layer: output projection + residual */
   FE_STAGE_GATEUP = 5,   /* per layer: gate/up projections + SwiGLU */
   FE_STAGE_DOWN = 6,     /* per layer: down projection + residual */

@@ -1,23 +1,25 @@
 // fe_attn.hip -- GQA decode attention of a cascade layer over its prefix KV
-// cache plus the cascade entries (gfx950).
+// cache plus the cascade entries, in one launch (gfx950).
 //
 // Layer i's query (one row per sequence, H_q heads) attends to the P_b cached
 // prefix keys of its own cache and to the nctx keys it projected from the
 // cascade states (Section 2.1; the cache is per layer because every L_i has
-// its own parameters).  The prefix part is flash-decoding:
+// its own parameters).
 //
-//  * one wave per (sequence, KV head, head group, chunk of 64 keys); the GH
-//    query heads that share a KV head are processed together, so every K/V
-//    byte is loaded once per chunk;
-//  * 8 lanes cover one key row (D/8 dims each, 16-byte vector loads, a whole
-//    row contiguous), 8 keys per load step;
-//  * dot products are reduced over the 8 lanes of a key with xor-shuffles,
-//    the softmax max/sum over the chunk with xor-shuffles across key slots,
-//    and the value accumulation likewise; the chunk leaves (max, sum, o[D])
-//    per head.
-//
-// The combine kernel merges the chunk partials and the nctx cascade keys (held
-// in fp32) with the usual max-rescaling, in a fixed order.
+//  * One workgroup (4 waves) per (sequence, KV head, head group, chunk of
+//    kAttnChunk prefix keys); the GH query heads sharing a KV head are done
+//    together so every K/V byte is read once.  Each wave takes 32 keys: 8 lanes
+//    per key row (D/8 dims each, 16-byte loads, the row contiguous), 8 keys
+//    per load step, K and V loads issued together.
+//  * Dot products reduce over the 8 lanes of a key with xor-shuffles; the
+//    softmax max/sum and the value sums reduce across key slots with
+//    xor-shuffles, then across the 4 waves in LDS.  Each chunk leaves
+//    (sum, max, o[D]) per head in the workspace.
+//  * Split-K completion: every chunk workgroup bumps a counter after a
+//    release fence; the last one (acquire fence) merges all chunk partials and
+//    the nctx cascade keys, held in fp32, in a fixed order, writes the output
+//    row and resets the counter for the next launch.  A sequence with an empty
+//    prefix still runs chunk 0, which carries no keys.
 #include "fe_internal.h"
 
 namespace fe {
@@ -47,76 +49,86 @@ template <typename T, int D> struct KvRow {
   }
 };
 
+constexpr int kWaveKeys = kAttnChunk / 4;   // keys per wave
+constexpr int kSteps = kWaveKeys / 8;       // load steps per wave
+
+__device__ __forceinline__ float scaled_exp(float m, float M) {
+  return m == -INFINITY ? 0.f : expf(m - M);
+}
+
 template <typename T, int D, int GH>
-__global__ __launch_bounds__(64) void k_attn_prefix(const T *__restrict__ Kc,
-                                                    const T *__restrict__ Vc,
-                                                    const int32_t *__restrict__ cu,
-                                                    const float *__restrict__ q,
-                                                    float *__restrict__ part, int Hq, int Hkv,
-                                                    int nch_ld) {
+__global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T *__restrict__ Vc,
+                                              const int32_t *__restrict__ cu,
+                                              const float *__restrict__ q,
+                                              const float *__restrict__ knew,
+                                              const float *__restrict__ vnew, int nctx,
+                                              float *__restrict__ part, int nch, int nch_ld,
+                                              int *__restrict__ counters, T *__restrict__ out,
+                                              int Hq, int Hkv) {
   constexpr int DL = D / 8;
-  constexpr int STEPS = kAttnChunk / 8;
+  __shared__ float s_m[4][GH], s_l[4][GH];
+  __shared__ float s_o[4][GH][D];
+  __shared__ float s_sc[GH][kMaxLayers];
+  __shared__ float s_M[GH], s_L[GH];
+  __shared__ int s_last;
+
   const int G = Hq / Hkv, ngrp = G / GH;
   const int ch = blockIdx.x, c = blockIdx.y / ngrp, hg = blockIdx.y % ngrp, b = blockIdx.z;
   const int start = cu[b], P = cu[b + 1] - start;
-  const int key0 = ch * kAttnChunk;
-  if (key0 >= P) return;  // chunk beyond this sequence's prefix: nothing to write
-  const int lane = threadIdx.x, slot = lane >> 3, dp = lane & 7;
+  const int nv = max(1, min((P + kAttnChunk - 1) / kAttnChunk, nch));
+  if (ch >= nv) return;  // chunk beyond this sequence's prefix
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, slot = lane >> 3, dp = lane & 7;
   const int h0 = c * G + hg * GH;
   const float scale = rsqrtf((float)D);
+  const int key0 = ch * kAttnChunk + wave * kWaveKeys;
 
+  // ---- this wave's 32 keys -------------------------------------------------
+  const size_t rowstride = (size_t)Hkv * D;
+  const T *kbase = Kc + ((size_t)start * Hkv + c) * D + dp * DL;
+  const T *vbase = Vc + ((size_t)start * Hkv + c) * D + dp * DL;
+  KvRow<T, D> kr[kSteps], vr[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int key = key0 + st * 8 + slot;
+    if (key < P) {
+      kr[st].load(kbase + (size_t)key * rowstride);
+      vr[st].load(vbase + (size_t)key * rowstride);
+    }
+  }
   float qv[GH][DL];
 #pragma unroll
   for (int gh = 0; gh < GH; ++gh)
 #pragma unroll
     for (int e = 0; e < DL; ++e) qv[gh][e] = q[((size_t)b * Hq + h0 + gh) * D + dp * DL + e];
 
-  const size_t rowstride = (size_t)Hkv * D;
-  const T *kbase = Kc + ((size_t)start * Hkv + c) * D + dp * DL;
-  const T *vbase = Vc + ((size_t)start * Hkv + c) * D + dp * DL;
-
-  KvRow<T, D> kr[STEPS];
+  float s[kSteps][GH];
 #pragma unroll
-  for (int st = 0; st < STEPS; ++st) {
-    const int key = key0 + st * 8 + slot;
-    if (key < P) kr[st].load(kbase + (size_t)key * rowstride);
-  }
-  float s[STEPS][GH];
-#pragma unroll
-  for (int st = 0; st < STEPS; ++st) {
+  for (int st = 0; st < kSteps; ++st)
 #pragma unroll
     for (int gh = 0; gh < GH; ++gh) {
       float acc = 0.f;
 #pragma unroll
       for (int e = 0; e < DL; ++e) acc += qv[gh][e] * kr[st].at(e);
-      s[st][gh] = acc;
-    }
-  }
-#pragma unroll
-  for (int st = 0; st < STEPS; ++st)
-#pragma unroll
-    for (int gh = 0; gh < GH; ++gh) {
-      float v = s[st][gh];
-      v += __shfl_xor(v, 1);
-      v += __shfl_xor(v, 2);
-      v += __shfl_xor(v, 4);
+      acc += __shfl_xor(acc, 1);
+      acc += __shfl_xor(acc, 2);
+      acc += __shfl_xor(acc, 4);
       const int key = key0 + st * 8 + slot;
-      s[st][gh] = key < P ? v * scale : -INFINITY;
+      s[st][gh] = key < P ? acc * scale : -INFINITY;
     }
-  float mx[GH], l[GH];
+  float mx[GH], l[GH], o[GH][DL];
 #pragma unroll
   for (int gh = 0; gh < GH; ++gh) {
     float m = -INFINITY;
 #pragma unroll
-    for (int st = 0; st < STEPS; ++st) m = fmaxf(m, s[st][gh]);
+    for (int st = 0; st < kSteps; ++st) m = fmaxf(m, s[st][gh]);
     m = fmaxf(m, __shfl_xor(m, 8));
     m = fmaxf(m, __shfl_xor(m, 16));
     m = fmaxf(m, __shfl_xor(m, 32));
     mx[gh] = m;
     float sum = 0.f;
 #pragma unroll
-    for (int st = 0; st < STEPS; ++st) {
-      const float p = expf(s[st][gh] - m);  // exp(-inf) = 0 for missing keys
+    for (int st = 0; st < kSteps; ++st) {
+      const float p = scaled_exp(s[st][gh], m);
       s[st][gh] = p;
       sum += p;
     }
@@ -124,21 +136,16 @@ __global__ __launch_bounds__(64) void k_attn_prefix(const T *__restrict__ Kc,
     sum += __shfl_xor(sum, 16);
     sum += __shfl_xor(sum, 32);
     l[gh] = sum;
-  }
-  float o[GH][DL];
-#pragma unroll
-  for (int gh = 0; gh < GH; ++gh)
 #pragma unroll
     for (int e = 0; e < DL; ++e) o[gh][e] = 0.f;
+  }
 #pragma unroll
-  for (int st = 0; st < STEPS; ++st) {
+  for (int st = 0; st < kSteps; ++st) {
     const int key = key0 + st * 8 + slot;
     if (key < P) {
-      KvRow<T, D> vr;
-      vr.load(vbase + (size_t)key * rowstride);
 #pragma unroll
       for (int e = 0; e < DL; ++e) {
-        const float ve = vr.at(e);
+        const float ve = vr[st].at(e);
 #pragma unroll
         for (int gh = 0; gh < GH; ++gh) o[gh][e] += s[st][gh] * ve;
       }
@@ -157,118 +164,134 @@ __global__ __launch_bounds__(64) void k_attn_prefix(const T *__restrict__ Kc,
   if (slot == 0) {
 #pragma unroll
     for (int gh = 0; gh < GH; ++gh) {
-      float *dst = part + (((size_t)b * Hq + h0 + gh) * nch_ld + ch) * (D + 2);
 #pragma unroll
-      for (int e = 0; e < DL; ++e) dst[dp * DL + e] = o[gh][e];
+      for (int e = 0; e < DL; ++e) s_o[wave][gh][dp * DL + e] = o[gh][e];
       if (dp == 0) {
-        dst[D] = mx[gh];
-        dst[D + 1] = l[gh];
+        s_m[wave][gh] = mx[gh];
+        s_l[wave][gh] = l[gh];
       }
     }
   }
-}
+  __syncthreads();
 
-// One workgroup of D threads per (query head, sequence); thread e owns dim e.
-template <typename T, int D>
-__global__ __launch_bounds__(D) void k_attn_combine(const float *__restrict__ part, int nch,
-                                                    int nch_ld,
-                                                    const int32_t *__restrict__ cu,
-                                                    const float *__restrict__ q,
-                                                    const float *__restrict__ knew,
-                                                    const float *__restrict__ vnew, int nctx,
-                                                    T *__restrict__ out, int Hq, int Hkv) {
-  __shared__ float red[D / 64][kMaxLayers];
-  __shared__ float sc[kMaxLayers];
-  const int h = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
-  const int G = Hq / Hkv, c = h / G;
-  const int P = cu[b + 1] - cu[b];
-  const int nv = min((P + kAttnChunk - 1) / kAttnChunk, nch);
-  const float scale = rsqrtf((float)D);
-  const float qe = q[((size_t)b * Hq + h) * D + e];
-  // scores of the cascade keys
-  for (int j = 0; j < nctx; ++j) {
-    float v = qe * knew[(((size_t)b * nctx + j) * Hkv + c) * D + e];
+  // ---- merge the 4 waves into this chunk's partial: [o[D], max, sum] --------
+  for (int idx = tid; idx < GH * (D + 2); idx += 256) {
+    const int gh = idx / (D + 2), e = idx % (D + 2);
+    float M = -INFINITY;
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    if ((e & 63) == 0) red[e >> 6][j] = v;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][gh]);
+    float acc = 0.f;
+    if (e == D) {
+      acc = M;
+    } else {
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        acc += scaled_exp(s_m[w][gh], M) * (e < D ? s_o[w][gh][e] : s_l[w][gh]);
+    }
+    part[(((size_t)b * Hq + h0 + gh) * nch_ld + ch) * (D + 2) + e] = acc;
+  }
+
+  // ---- split-K completion ---------------------------------------------------
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const int old = atomicAdd(&counters[((size_t)b * Hkv + c) * ngrp + hg], 1);
+    s_last = (old == nv - 1);
   }
   __syncthreads();
-  if (e < nctx) {
-    float v = 0.f;
+  if (!s_last) return;
+  __threadfence();
+
+  // ---- last chunk workgroup: merge every chunk and the cascade keys ---------
+  constexpr int DPL = D / 64;
+  if (wave < GH) {
+    const int gh = wave, h = h0 + gh;
+    float qd[DPL];
 #pragma unroll
-    for (int w = 0; w < D / 64; ++w) v += red[w][e];
-    sc[e] = v * scale;
+    for (int t = 0; t < DPL; ++t) qd[t] = q[((size_t)b * Hq + h) * D + lane * DPL + t];
+    float sj[kMaxLayers];
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) {
+      sj[j] = -INFINITY;
+      if (j < nctx) {
+        float v = 0.f;
+#pragma unroll
+        for (int t = 0; t < DPL; ++t)
+          v += qd[t] * knew[(((size_t)b * nctx + j) * Hkv + c) * D + lane * DPL + t];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+        sj[j] = v * scale;
+      }
+    }
+    const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
+    float M = -INFINITY;
+    for (int k = lane; k < nv; k += 64) M = fmaxf(M, pp[(size_t)k * (D + 2) + D]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) M = fmaxf(M, sj[j]);
+    float L = 0.f;
+    for (int k = lane; k < nv; k += 64)
+      L += pp[(size_t)k * (D + 2) + D + 1] * scaled_exp(pp[(size_t)k * (D + 2) + D], M);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) L += scaled_exp(sj[j], M);
+    if (lane == 0) {
+      s_M[gh] = M;
+      s_L[gh] = L;
+#pragma unroll
+      for (int j = 0; j < kMaxLayers; ++j) s_sc[gh][j] = sj[j];
+    }
   }
   __syncthreads();
-  const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
-  float M = -INFINITY;
-  for (int ch = 0; ch < nv; ++ch) M = fmaxf(M, pp[(size_t)ch * (D + 2) + D]);
-  for (int j = 0; j < nctx; ++j) M = fmaxf(M, sc[j]);
-  float L = 0.f, acc = 0.f;
-  for (int ch = 0; ch < nv; ++ch) {
-    const float *p = pp + (size_t)ch * (D + 2);
-    const float w = expf(p[D] - M);
-    L += p[D + 1] * w;
-    acc += p[e] * w;
+  for (int idx = tid; idx < GH * D; idx += 256) {
+    const int gh = idx / D, e = idx % D, h = h0 + gh;
+    const float M = s_M[gh];
+    const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
+    float acc = 0.f;
+    for (int k = 0; k < nv; ++k)
+      acc += pp[(size_t)k * (D + 2) + e] * scaled_exp(pp[(size_t)k * (D + 2) + D], M);
+    for (int j = 0; j < nctx; ++j)
+      acc += scaled_exp(s_sc[gh][j], M) * vnew[(((size_t)b * nctx + j) * Hkv + c) * D + e];
+    out[(size_t)b * Hq * D + (size_t)h * D + e] = Elt<T>::from_f(acc / s_L[gh]);
   }
-  for (int j = 0; j < nctx; ++j) {
-    const float w = expf(sc[j] - M);
-    L += w;
-    acc += w * vnew[(((size_t)b * nctx + j) * Hkv + c) * D + e];
-  }
-  out[(size_t)b * Hq * D + (size_t)h * D + e] = Elt<T>::from_f(acc / L);
+  if (tid == 0) counters[((size_t)b * Hkv + c) * ngrp + hg] = 0;
 }
 
 template <typename T, int D>
-static hipError_t attn_prefix_t(const void *K, const void *V, const int32_t *cu, const float *q,
-                                float *part, int B, int Hq, int Hkv, int nch, int nch_ld,
-                                hipStream_t s) {
+static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const float *q,
+                         const float *knew, const float *vnew, int nctx, float *part, int nch,
+                         int nch_ld, int *counters, void *out, int B, int Hq, int Hkv,
+                         hipStream_t s) {
   const int G = Hq / Hkv;
   const int GH = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
-  const dim3 grid(nch, Hkv * (G / GH), B);
-  if (GH == 4)
-    hipLaunchKernelGGL((k_attn_prefix<T, D, 4>), grid, dim3(64), 0, s, (const T *)K, (const T *)V,
-                       cu, q, part, Hq, Hkv, nch_ld);
-  else if (GH == 2)
-    hipLaunchKernelGGL((k_attn_prefix<T, D, 2>), grid, dim3(64), 0, s, (const T *)K, (const T *)V,
-                       cu, q, part, Hq, Hkv, nch_ld);
-  else
-    hipLaunchKernelGGL((k_attn_prefix<T, D, 1>), grid, dim3(64), 0, s, (const T *)K, (const T *)V,
-                       cu, q, part, Hq, Hkv, nch_ld);
+  const int nchl = nch < 1 ? 1 : nch;
+  const dim3 grid(nchl, Hkv * (G / GH), B);
+#define FE_ATTN(GHV)                                                                            \
+  hipLaunchKernelGGL((k_attn<T, D, GHV>), grid, dim3(256), 0, s, (const T *)K, (const T *)V, cu, \
+                     q, knew, vnew, nctx, part, nchl, nch_ld, counters, (T *)out, Hq, Hkv)
+  if (GH == 4) FE_ATTN(4);
+  else if (GH == 2) FE_ATTN(2);
+  else FE_ATTN(1);
+#undef FE_ATTN
   return hipGetLastError();
 }
 
-hipError_t attn_prefix(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
-                       float *part, int B, int Hq, int Hkv, int D, int nch, int nch_ld,
-                       hipStream_t s) {
-  if (nch <= 0 || B <= 0) return hipSuccess;
-  if (dt) return D == 128 ? attn_prefix_t<bf16_t, 128>(K, V, cu, q, part, B, Hq, Hkv, nch, nch_ld, s)
-                          : attn_prefix_t<bf16_t, 64>(K, V, cu, q, part, B, Hq, Hkv, nch, nch_ld, s);
-  return D == 128 ? attn_prefix_t<float, 128>(K, V, cu, q, part, B, Hq, Hkv, nch, nch_ld, s)
-                  : attn_prefix_t<float, 64>(K, V, cu, q, part, B, Hq, Hkv, nch, nch_ld, s);
-}
-
-hipError_t attn_combine(int dt, const float *part, int nch, int nch_ld, const int32_t *cu,
-                        const float *q,
-                        const float *knew, const float *vnew, int nctx, void *out, int B, int Hq,
-                        int Hkv, int D, hipStream_t s) {
-  const dim3 grid(Hq, B);
-  if (dt) {
-    if (D == 128)
-      hipLaunchKernelGGL((k_attn_combine<bf16_t, 128>), grid, dim3(128), 0, s, part, nch, nch_ld, cu, q,
-                         knew, vnew, nctx, (bf16_t *)out, Hq, Hkv);
-    else
-      hipLaunchKernelGGL((k_attn_combine<bf16_t, 64>), grid, dim3(64), 0, s, part, nch, nch_ld, cu, q,
-                         knew, vnew, nctx, (bf16_t *)out, Hq, Hkv);
-  } else {
-    if (D == 128)
-      hipLaunchKernelGGL((k_attn_combine<float, 128>), grid, dim3(128), 0, s, part, nch, nch_ld, cu, q,
-                         knew, vnew, nctx, (float *)out, Hq, Hkv);
-    else
-      hipLaunchKernelGGL((k_attn_combine<float, 64>), grid, dim3(64), 0, s, part, nch, nch_ld, cu, q,
-                         knew, vnew, nctx, (float *)out, Hq, Hkv);
-  }
-  return hipGetLastError();
+hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
+                     const float *knew, const float *vnew, int nctx, float *part, int nch,
+                     int nch_ld, int *counters, void *out, int B, int Hq, int Hkv, int D,
+                     hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (dt)
+    return D == 128 ? attn_t<bf16_t, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
+                                          counters, out, B, Hq, Hkv, s)
+                    : attn_t<bf16_t, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
+                                         counters, out, B, Hq, Hkv, s);
+  return D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
+                                       counters, out, B, Hq, Hkv, s)
+                  : attn_t<float, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, counters,
+                                      out, B, Hq, Hkv, s);
 }
 
 }  // namespace fe

@@ -48,23 +48,177 @@ template <> __device__ __forceinline__ void mma16<float>(f32x4 &acc, u32x4 a, u3
 __device__ __forceinline__ u32x4 ldg_stream(const u32x4 *p) { return __builtin_nontemporal_load(p); }
 
 // ---------------------------------------------------------------------------
-// The GEMM body.
+// Accumulation paths.  Both leave, in lane (r, g) of a wave, the 16x16 tiles
+// acc[i][f] = rows 16i.. of A times weight rows of virtual columns c0+16f..,
+// summed over this wave's share of K.
 // ---------------------------------------------------------------------------
-template <typename T, int MT, int NT, int WK, int WN, int U, class Epi>
+
+// Staged path (M <= 32): weights are read as 512-byte contiguous pieces of
+// two rows per load instruction (the access pattern HBM streams best), parked
+// in the wave's own padded LDS tile, and read back as MFMA B fragments; the
+// next 512-byte chunk of every row is in flight while the current one is
+// multiplied.  K is walked in chunks of KC elements, split over WK waves.
+constexpr int kStageRowBytes = 512 + 16;  // padded LDS row: 16 rows hit distinct banks
+
+template <typename T, int MT, int NT, class Epi>
+__device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, int M, int K,
+                                             const Epi &epi, int c0, int wk, int WKn,
+                                             char *stage, f32x4 (&acc)[MT][NT]) {
+  constexpr int E = Elt<T>::kPer16B;
+  constexpr int KC = 32 * E;       // elements per chunk: 512 bytes of a row
+  constexpr int KS = 4 * E;        // elements per MFMA step
+  constexpr int STEPS = KC / KS;   // 8
+  constexpr int NLD = NT * 8;      // load instructions per chunk (2 rows each)
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int nchunk = (K + KC - 1) / KC;
+  const int ch0 = (int)(((long)nchunk * wk) / WKn), ch1 = (int)(((long)nchunk * (wk + 1)) / WKn);
+  if (ch0 >= ch1) return;
+  const u32x4 *src[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j)
+    src[j] = reinterpret_cast<const u32x4 *>(epi.wrow(c0 + 2 * j + half)) + l32;
+  const u32x4 *ap[MT];
+  bool am[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int m = i * 16 + r;
+    am[i] = m < M;
+    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
+  }
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  u32x4 wr[NLD], ar[STEPS][MT];
+  auto load = [&](int ch) {
+    const int kb = ch * KC;
+    const bool wok = kb + l32 * E < K;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) wr[j] = wok ? ldg_stream(src[j] + ch * 32) : zero;
+#pragma unroll
+    for (int st = 0; st < STEPS; ++st)
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+        ar[st][i] = (am[i] && kb + st * KS + g * E < K) ? ap[i][ch * 32 + st * 4] : zero;
+  };
+  load(ch0);
+  for (int ch = ch0; ch < ch1; ++ch) {
+    // the previous chunk's LDS reads are complete before its rows are overwritten
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      *reinterpret_cast<u32x4 *>(stage + (2 * j + half) * kStageRowBytes + l32 * 16) = wr[j];
+    u32x4 ac[STEPS][MT];
+#pragma unroll
+    for (int st = 0; st < STEPS; ++st)
+#pragma unroll
+      for (int i = 0; i < MT; ++i) ac[st][i] = ar[st][i];
+    // this chunk's rows are in LDS before any lane reads them
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (ch + 1 < ch1) load(ch + 1);
+    const int nst = min(STEPS, (K - ch * KC) / KS);
+#pragma unroll
+    for (int st = 0; st < STEPS; ++st) {
+      if (st < nst) {
+#pragma unroll
+        for (int f = 0; f < NT; ++f) {
+          const u32x4 bfr = *reinterpret_cast<const u32x4 *>(
+              stage + (f * 16 + r) * kStageRowBytes + st * 64 + g * 16);
+#pragma unroll
+          for (int i = 0; i < MT; ++i) mma16<T>(acc[i][f], ac[st][i], bfr);
+        }
+      }
+    }
+  }
+}
+
+// Direct path (larger M): lane (r, g) loads 16 bytes of weight row r per
+// K step straight into the B operand; U steps double-buffered in registers.
+template <typename T, int MT, int NT, int U, class Epi>
+__device__ __forceinline__ void accum_direct(const T *__restrict__ A, int lda, int M, int K,
+                                             const Epi &epi, int c0, int wk, int WKn,
+                                             f32x4 (&acc)[MT][NT]) {
+  constexpr int E = Elt<T>::kPer16B;
+  constexpr int KS = 4 * E;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int nsteps = K / KS;
+  const int s0 = (int)(((long)nsteps * wk) / WKn);
+  const int s1 = (int)(((long)nsteps * (wk + 1)) / WKn);
+  const u32x4 *wp[NT];
+#pragma unroll
+  for (int f = 0; f < NT; ++f)
+    wp[f] = reinterpret_cast<const u32x4 *>(epi.wrow(c0 + f * 16 + r)) + g;
+  const u32x4 *ap[MT];
+  bool am[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int m = i * 16 + r;
+    am[i] = m < M;
+    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
+  }
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  u32x4 wc[U][NT], ac[U][MT];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int s = s0 + u;
+    const bool ok = s < s1;
+#pragma unroll
+    for (int f = 0; f < NT; ++f) wc[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) ac[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
+  }
+  for (int sb = s0; sb < s1; sb += U) {
+    u32x4 wn_[U][NT], an_[U][MT];
+    const int sn = sb + U;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = sn + u;
+      const bool ok = s < s1;
+#pragma unroll
+      for (int f = 0; f < NT; ++f) wn_[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) an_[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int f = 0; f < NT; ++f) mma16<T>(acc[i][f], ac[u][i], wc[u][f]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int f = 0; f < NT; ++f) wc[u][f] = wn_[u][f];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) ac[u][i] = an_[u][i];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The GEMM body: WN x WK waves; wave (wn, wk) owns NT 16-column tiles and the
+// wk-th share of K.  Partial tiles are summed over wk in LDS in a fixed order
+// (deterministic, no atomics), then the epilogue consumes the [M, span] tile.
+// ---------------------------------------------------------------------------
+template <int MT> struct Unroll {
+  static constexpr int value = MT <= 2 ? 8 : (MT <= 4 ? 4 : (MT <= 8 ? 2 : 1));
+};
+
+template <typename T, int MT, int NT, int WK, int WN, class Epi>
 __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, int lda, int M,
                                                        int K, Epi epi) {
-  constexpr int E = Elt<T>::kPer16B;
-  constexpr int KS = 4 * E;  // K elements per MFMA step
+  constexpr bool kStaged = MT <= 2;
   constexpr int SPAN = WN * NT * 16;
   constexpr int LDT = SPAN + 1;
-  __shared__ float red[WK][MT * 16][LDT];
+  constexpr int kStageBytes = kStaged ? WK * WN * NT * 16 * kStageRowBytes : 0;
+  constexpr int kRedBytes = WK * MT * 16 * LDT * 4;
+  constexpr int kSmem = kStageBytes > kRedBytes ? kStageBytes : kRedBytes;
+  __shared__ __attribute__((aligned(16))) char smem[kSmem];
+  float(*red)[MT * 16][LDT] = reinterpret_cast<float(*)[MT * 16][LDT]>(smem);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wn = wave % WN, wk = wave / WN;
   const int r = lane & 15, g = lane >> 4;
   const int c0_wg = blockIdx.x * SPAN;
   const int c0 = c0_wg + wn * NT * 16;
-  const bool active = c0 < epi.nvcols;
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -72,60 +226,14 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
 #pragma unroll
     for (int f = 0; f < NT; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (active) {
-    const int nsteps = K / KS;
-    const int s0 = (int)(((long)nsteps * wk) / WK);
-    const int s1 = (int)(((long)nsteps * (wk + 1)) / WK);
-    const u32x4 *wp[NT];
-#pragma unroll
-    for (int f = 0; f < NT; ++f)
-      wp[f] = reinterpret_cast<const u32x4 *>(epi.wrow(c0 + f * 16 + r)) + g;
-    const u32x4 *ap[MT];
-    bool am[MT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int m = i * 16 + r;
-      am[i] = m < M;
-      ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
-    }
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    u32x4 wc[U][NT], ac[U][MT];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int s = s0 + u;
-      const bool ok = s < s1;
-#pragma unroll
-      for (int f = 0; f < NT; ++f) wc[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
-#pragma unroll
-      for (int i = 0; i < MT; ++i) ac[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
-    }
-    for (int sb = s0; sb < s1; sb += U) {
-      u32x4 wn_[U][NT], an_[U][MT];
-      const int sn = sb + U;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int s = sn + u;
-        const bool ok = s < s1;
-#pragma unroll
-        for (int f = 0; f < NT; ++f) wn_[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
-#pragma unroll
-        for (int i = 0; i < MT; ++i) an_[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int i = 0; i < MT; ++i)
-#pragma unroll
-          for (int f = 0; f < NT; ++f) mma16<T>(acc[i][f], ac[u][i], wc[u][f]);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-#pragma unroll
-        for (int f = 0; f < NT; ++f) wc[u][f] = wn_[u][f];
-#pragma unroll
-        for (int i = 0; i < MT; ++i) ac[u][i] = an_[u][i];
-      }
-    }
+  if (c0 < epi.nvcols) {
+    if constexpr (kStaged)
+      accum_staged<T, MT, NT>(A, lda, M, K, epi, c0, wk, WK,
+                              smem + wave * NT * 16 * kStageRowBytes, acc);
+    else
+      accum_direct<T, MT, NT, Unroll<MT>::value>(A, lda, M, K, epi, c0, wk, WK, acc);
   }
+  __syncthreads();  // staging tiles are dead; the buffer becomes the reduction tile
 
   // Lane (r, g) holds C[row 4g+v][col r] of each 16x16 tile.
 #pragma unroll
@@ -360,11 +468,8 @@ template <typename T> struct EpiLm {
 // ---------------------------------------------------------------------------
 // Unroll depth of the load pipeline and split-K width shrink as the number of
 // 16-row tiles grows, to bound registers and the LDS reduction buffer.
-template <int MT> struct Unroll {
-  static constexpr int value = MT <= 2 ? 8 : (MT <= 4 ? 4 : (MT <= 8 ? 2 : 1));
-};
 template <int WKmax, int MT> struct SplitK {
-  static constexpr int cap = MT <= 1 ? 8 : (MT <= 2 ? 4 : (MT <= 4 ? 2 : 1));
+  static constexpr int cap = MT <= 2 ? 8 : (MT <= 4 ? 2 : 1);
   static constexpr int value = WKmax < cap ? WKmax : cap;
 };
 
@@ -374,7 +479,7 @@ static hipError_t run_gemm(const T *A, int lda, int M, int K, const Epi &epi, hi
   const int grid = (epi.nvcols + SPAN - 1) / SPAN;
   const int mt = (M + 15) / 16;
 #define FE_GEMM_CASE(MTV)                                                              \
-  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, Unroll<MTV>::value, Epi>), \
+  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, Epi>), \
                      dim3(grid), dim3(64 * SplitK<WKmax, MTV>::value * WN), 0, s, A, lda, M, K, epi)
   if (mt <= 1) FE_GEMM_CASE(1);
   else if (mt <= 2) FE_GEMM_CASE(2);

@@ -37,8 +37,10 @@ template <> struct Elt<float> {
   __device__ static __forceinline__ float from_f(float f) { return f; }
 };
 
-// Keys per attention chunk (one wave per chunk and KV-head group).
-constexpr int kAttnChunk = 64;
+// Prefix keys per attention workgroup (4 waves of 32 keys).
+constexpr int kAttnChunk = 128;
+// Tile candidates the top-k merge holds in registers: 256 threads x 32.
+constexpr int kMergeMaxCand = 256 * 32;
 // Largest M (rows) one GEMM launch handles; larger M is split on the host.
 constexpr int kGemmMaxRows = 256;
 constexpr int kMaxTopk = 16;
@@ -97,18 +99,18 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
                         long inner, const void *gamma, void *out, int d, float eps,
                         hipStream_t s);
 
-// Flash-decoding partials over the prefix cache of one layer: chunks
-// 0..nch-1 of every sequence (keys beyond nch*kAttnChunk are not read);
-// partials are laid out [B, Hq, nch_ld, D+2].
-hipError_t attn_prefix(int dt, const void *K, const void *V, const int32_t *cu_prefix,
-                       const float *q, float *part, int B, int Hq, int Hkv, int D, int nch,
-                       int nch_ld, hipStream_t s);
+// Attention of the query rows q [B, Hq, D] over the prefix cache (chunks
+// 0..nch-1 of kAttnChunk keys; keys beyond are not read) and the nctx cascade
+// keys/values knew/vnew [B, nctx, Hkv, D] -> out [B, Hq*D] (storage type).
+// part [B, Hq, nch_ld, D+2] holds chunk partials; counters [B*Hq] must be zero
+// before the first launch and are left zero after each launch.
+hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
+                     const float *q, const float *knew, const float *vnew, int nctx,
+                     float *part, int nch, int nch_ld, int *counters, void *out, int B, int Hq,
+                     int Hkv, int D, hipStream_t s);
 
-// Merge of the prefix partials (at most nch chunks per sequence) with the nctx
-// cascade keys -> out [B, Hq*D] (storage type).
-hipError_t attn_combine(int dt, const float *part, int nch, int nch_ld, const int32_t *cu_prefix,
-                        const float *q, const float *knew, const float *vnew, int nctx,
-                        void *out, int B, int Hq, int Hkv, int D, hipStream_t s);
+// Sets n 32-bit words to zero (a kernel, so it is safe inside graph capture).
+hipError_t zero_words(uint32_t *p, size_t n, hipStream_t s);
 
 // Global top-k of every row from the tile candidates; softmax statistics merge.
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,

@@ -59,13 +59,29 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
                                                     int topk, int V, const int32_t *__restrict__ d2t,
                                                     int32_t *ids, int32_t *draft_ids,
                                                     float *probs) {
+  constexpr int CAP = kMergeMaxCand / 256;
   __shared__ float sv[4];
   __shared__ int si[4];
   __shared__ float s_mu, s_S;
-  __shared__ int taken[kMaxTopk];
+  __shared__ int s_win;
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *pm = pmax + (size_t)row * nwg;
   const float *ps = psum + (size_t)row * nwg;
+  // every candidate of the row into registers (thread t holds t, t+256, ...)
+  const int ncand = nwg * topk;
+  float cv[CAP];
+  int ci[CAP];
+#pragma unroll
+  for (int j = 0; j < CAP; ++j) {
+    const int c = tid + 256 * j;
+    cv[j] = -INFINITY;
+    ci[j] = 0x7fffffff;
+    if (c < ncand) {
+      const size_t o = ((size_t)row * nwg + c / topk) * kMaxTopk + c % topk;
+      cv[j] = cval[o];
+      ci[j] = cidx[o];
+    }
+  }
   // mu
   float m = -INFINITY;
   for (int t = tid; t < nwg; t += 256) m = fmaxf(m, pm[t]);
@@ -87,19 +103,13 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
     s_S = (sv[0] + sv[1]) + (sv[2] + sv[3]);
   }
   __syncthreads();
-  // k rounds of block argmax over nwg*topk candidates
-  const int ncand = nwg * topk;
+  // k rounds of block argmax over the register-held candidates
   for (int r = 0; r < topk; ++r) {
     float bv = -INFINITY;
     int bi = 0x7fffffff;
-    for (int c = tid; c < ncand; c += 256) {
-      const int t = c / topk, j = c % topk;
-      const float v = cval[((size_t)row * nwg + t) * kMaxTopk + j];
-      const int i = cidx[((size_t)row * nwg + t) * kMaxTopk + j];
-      bool used = false;
-      for (int q = 0; q < r; ++q) used |= (taken[q] == i);
-      if (!used && better(v, i, bv, bi)) { bv = v; bi = i; }
-    }
+#pragma unroll
+    for (int j = 0; j < CAP; ++j)
+      if (better(cv[j], ci[j], bv, bi)) { bv = cv[j]; bi = ci[j]; }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       const float ov = __shfl_xor(bv, o);
@@ -113,7 +123,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
       int i = si[0];
       for (int w = 1; w < 4; ++w)
         if (better(sv[w], si[w], v, i)) { v = sv[w]; i = si[w]; }
-      taken[r] = i;
+      s_win = i;
       const size_t o = (size_t)row * topk + r;
       const bool valid = i >= 0 && i < V;  // no valid candidate left (NaN row): -1
       ids[o] = valid ? (d2t ? d2t[i] : i) : -1;
@@ -121,6 +131,10 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
       probs[o] = valid ? expf(v - s_mu) / s_S : __int_as_float(0x7fc00000);
     }
     __syncthreads();
+    const int win = s_win;
+#pragma unroll
+    for (int j = 0; j < CAP; ++j)
+      if (ci[j] == win) { cv[j] = -INFINITY; ci[j] = 0x7fffffff; }
   }
 }
 
@@ -201,6 +215,18 @@ hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_build_tree, dim3(B), dim3(256), 0, s, N, k, root_tokens, topk_ids,
                      prefix_lens, tokens, parents, depth, positions, mask, retrieve);
+  return hipGetLastError();
+}
+
+__global__ void k_zero_words(uint32_t *p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+hipError_t zero_words(uint32_t *p, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int grid = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  hipLaunchKernelGGL(k_zero_words, dim3(grid), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
 

@@ -30,7 +30,7 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cat, X, Xp, an, bn, q, knew, vnew, part, ao, s, pmax, psum, cval, cidx, total;
+  size_t cat, X, Xp, an, bn, q, knew, vnew, part, cnt, ao, s, pmax, psum, cval, cidx, total;
   int nchmax, nwg;
 };
 
@@ -53,6 +53,7 @@ Layout layout_of(const fe_config &c) {
   L.knew = take(B * N * Hkv * D * 4);
   L.vnew = take(B * N * Hkv * D * 4);
   L.part = take(B * Hq * (size_t)L.nchmax * (D + 2) * 4);
+  L.cnt = take(B * Hq * 4);
   L.ao = take(B * Hq * D * es);
   L.s = take(B * I * es);
   L.pmax = take(B * N * (size_t)L.nwg * 4);
@@ -85,6 +86,8 @@ fe_status check_config(const fe_config *c) {
   if (c->hidden % kstep || c->intermediate % kstep || qd % kstep)
     return fail(FE_E_UNSUPPORTED, "hidden, intermediate and n_q_heads*head_dim must be multiples of %d", kstep);
   if (c->draft_vocab % 16) return fail(FE_E_UNSUPPORTED, "draft_vocab must be a multiple of 16");
+  if ((long)lmhead_tiles(c->draft_vocab) * c->max_topk > kMergeMaxCand)
+    return fail(FE_E_UNSUPPORTED, "draft_vocab * max_topk too large for the top-k merge");
   if ((long)c->n_feat_levels * c->hidden > (1L << 30)) return fail(FE_E_UNSUPPORTED, "feature width too large");
   return FE_OK;
 }
@@ -99,6 +102,7 @@ struct fe_drafter {
   Layout L;
   hipStream_t cap_stream = nullptr;
   bool graph_mode = false;
+  bool counters_zeroed = false;  // attention completion counters set to zero once
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
   hipGraph_t graph = nullptr;
@@ -250,6 +254,10 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
   const int nch_ld = L.nchmax;
   h->prof_count = 0;
+  if (!h->counters_zeroed) {  // first pass on this handle: counters start at zero
+    FE_TRY(zero_words((uint32_t *)(ws + L.cnt), (size_t)c.max_batch * c.n_q_heads, s));
+    h->counters_zeroed = true;
+  }
 
   // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
   FE_TIMED(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
@@ -267,10 +275,9 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
                (double)c.rope_theta, q, knew, vnew};
     FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, an, d, B * nctx, qa, s));
     // attention over the layer's prefix cache plus the cascade keys
-    FE_TIMED(FE_STAGE_ATTN, attn_prefix(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, part, B, Hq, Hkv, D,
-                       nch, nch_ld, s));
-    FE_TRY(attn_combine(dt, part, nch, nch_ld, kv->cu_prefix, q, knew, vnew, nctx, ao, B, Hq,
-                        Hkv, D, s));
+    FE_TIMED(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
+                                      vnew, nctx, part, nch, nch_ld,
+                                      (int *)(ws + L.cnt), ao, B, Hq, Hkv, D, s));
     // x' = x_{i-1} + W_o o
     FE_TIMED(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d, X + (size_t)(i - 1) * d, xrow, s));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
