@@ -61,9 +61,9 @@ __device__ __forceinline__ u32x4 ldg_stream(const u32x4 *p) { return __builtin_n
 constexpr int kStageRowBytes = 512 + 16;  // padded LDS row: 16 rows hit distinct banks
 
 template <typename T, int MT, int NT, class Epi>
-__device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, int M, int K,
-                                             const Epi &epi, int c0, int wk, int WKn,
-                                             char *stage, f32x4 (&acc)[MT][NT]) {
+__device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, const ARows &ar_,
+                                             int M, int K, const Epi &epi, int c0, int wk,
+                                             int WKn, char *stage, f32x4 (&acc)[MT][NT]) {
   constexpr int E = Elt<T>::kPer16B;
   constexpr int KC = 32 * E;       // elements per chunk: 512 bytes of a row
   constexpr int KS = 4 * E;        // elements per MFMA step
@@ -84,7 +84,7 @@ __device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, i
   for (int i = 0; i < MT; ++i) {
     const int m = i * 16 + r;
     am[i] = m < M;
-    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
+    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? ar_.row(m) : 0) * lda) + g;
   }
   const u32x4 zero = {0u, 0u, 0u, 0u};
   u32x4 wr[NLD], ar[STEPS][MT];
@@ -133,9 +133,9 @@ __device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, i
 // Direct path (larger M): lane (r, g) loads 16 bytes of weight row r per
 // K step straight into the B operand; U steps double-buffered in registers.
 template <typename T, int MT, int NT, int U, class Epi>
-__device__ __forceinline__ void accum_direct(const T *__restrict__ A, int lda, int M, int K,
-                                             const Epi &epi, int c0, int wk, int WKn,
-                                             f32x4 (&acc)[MT][NT]) {
+__device__ __forceinline__ void accum_direct(const T *__restrict__ A, int lda, const ARows &ar_,
+                                             int M, int K, const Epi &epi, int c0, int wk,
+                                             int WKn, f32x4 (&acc)[MT][NT]) {
   constexpr int E = Elt<T>::kPer16B;
   constexpr int KS = 4 * E;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -152,7 +152,7 @@ __device__ __forceinline__ void accum_direct(const T *__restrict__ A, int lda, i
   for (int i = 0; i < MT; ++i) {
     const int m = i * 16 + r;
     am[i] = m < M;
-    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? m : 0) * lda) + g;
+    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? ar_.row(m) : 0) * lda) + g;
   }
   const u32x4 zero = {0u, 0u, 0u, 0u};
   u32x4 wc[U][NT], ac[U][MT];
@@ -202,16 +202,19 @@ template <int MT> struct Unroll {
   static constexpr int value = MT <= 2 ? 8 : (MT <= 4 ? 4 : (MT <= 8 ? 2 : 1));
 };
 
-template <typename T, int MT, int NT, int WK, int WN, class Epi>
-__global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, int lda, int M,
-                                                       int K, Epi epi) {
+template <typename T, int MT, int NT, int WK, int WN, bool NORM, class Epi>
+__global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, int lda, ARows arows,
+                                                       int M, int K, NormA na, Epi epi) {
   constexpr bool kStaged = MT <= 2;
+  static_assert(!NORM || MT == 1, "fused RMSNorm is for M <= 16");
+  constexpr int NTHR = 64 * WK * WN;
   constexpr int SPAN = WN * NT * 16;
   constexpr int LDT = SPAN + 1;
   constexpr int kStageBytes = kStaged ? WK * WN * NT * 16 * kStageRowBytes : 0;
   constexpr int kRedBytes = WK * MT * 16 * LDT * 4;
   constexpr int kSmem = kStageBytes > kRedBytes ? kStageBytes : kRedBytes;
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
+  __shared__ float s_inv[16];
   float(*red)[MT * 16][LDT] = reinterpret_cast<float(*)[MT * 16][LDT]>(smem);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -219,6 +222,20 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
   const int r = lane & 15, g = lane >> 4;
   const int c0_wg = blockIdx.x * SPAN;
   const int c0 = c0_wg + wn * NT * 16;
+
+  // Fused RMSNorm: A holds gamma * x rows; each row's 1/rms comes from the
+  // producer's per-tile sums of squares.  Thread t sums tiles p, p+PARTS, ...
+  // of row t / PARTS; the loads are issued here and consumed after the main
+  // loop, so their latency hides behind the weight stream.
+  constexpr int PARTS = NTHR / 16;
+  constexpr int kNormLoads = 16;  // tiles per thread covered by the unrolled loads
+  float nv[NORM ? kNormLoads : 1];
+  const int nrow = threadIdx.x / PARTS, npart = threadIdx.x % PARTS;
+  if constexpr (NORM) {
+    const float *sr = na.ssq + (size_t)na.row(min(nrow, M - 1)) * na.ntile;
+#pragma unroll
+    for (int u = 0; u < kNormLoads; ++u) nv[u] = sr[min(npart + PARTS * u, na.ntile - 1)];
+  }
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -228,10 +245,20 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
 
   if (c0 < epi.nvcols) {
     if constexpr (kStaged)
-      accum_staged<T, MT, NT>(A, lda, M, K, epi, c0, wk, WK,
+      accum_staged<T, MT, NT>(A, lda, arows, M, K, epi, c0, wk, WK,
                               smem + wave * NT * 16 * kStageRowBytes, acc);
     else
-      accum_direct<T, MT, NT, Unroll<MT>::value>(A, lda, M, K, epi, c0, wk, WK, acc);
+      accum_direct<T, MT, NT, Unroll<MT>::value>(A, lda, arows, M, K, epi, c0, wk, WK, acc);
+  }
+  if constexpr (NORM) {
+    float ssum = 0.f;
+#pragma unroll
+    for (int u = 0; u < kNormLoads; ++u) ssum += (npart + PARTS * u < na.ntile) ? nv[u] : 0.f;
+    const float *sr = na.ssq + (size_t)na.row(min(nrow, M - 1)) * na.ntile;
+    for (int t = npart + PARTS * kNormLoads; t < na.ntile; t += PARTS) ssum += sr[t];
+#pragma unroll
+    for (int off = PARTS / 2; off >= 1; off >>= 1) ssum += __shfl_xor(ssum, off);
+    if (npart == 0 && nrow < M) s_inv[nrow] = 1.0f / sqrtf(ssum / (float)na.d + na.eps);
   }
   __syncthreads();  // staging tiles are dead; the buffer becomes the reduction tile
 
@@ -243,12 +270,13 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
 #pragma unroll
       for (int v = 0; v < 4; ++v) red[wk][i * 16 + 4 * g + v][wn * NT * 16 + f * 16 + r] = acc[i][f][v];
   __syncthreads();
-  if (WK > 1) {
-    for (int idx = threadIdx.x; idx < MT * 16 * SPAN; idx += 64 * WK * WN) {
+  if (WK > 1 || NORM) {
+    for (int idx = threadIdx.x; idx < MT * 16 * SPAN; idx += NTHR) {
       const int m = idx / SPAN, c = idx % SPAN;
       float sum = red[0][m][c];
 #pragma unroll
       for (int w = 1; w < WK; ++w) sum += red[w][m][c];
+      if constexpr (NORM) sum *= (m < M ? s_inv[m] : 0.f);
       red[0][m][c] = sum;
     }
     __syncthreads();
@@ -270,7 +298,7 @@ template <typename T> struct EpiStore {
   T *gather_out;
   int ld_gather, d, B;
   __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
-  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
       if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = Elt<T>::from_f(tile[m * ldt + c]);
@@ -299,14 +327,32 @@ template <typename T> struct EpiResid {
   long ldo;
   const float *resid;
   long ldr;
+  float *ssq;  // optional per-(row, 16-column tile) sums of squares of the output
+  int ssq_rs, ssq_off;
+  GainCopies gc;
   __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
-  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
       if (c0 + c >= nvcols) continue;
       float v = tile[m * ldt + c];
       if (resid) v = resid[(size_t)m * ldr + c0 + c] + v;
       out[(size_t)m * ldo + c0 + c] = v;
+      tile[m * ldt + c] = v;
+      for (int q = 0; q < gc.n; ++q)
+        ((T *)gc.dst[q])[(size_t)m * gc.ld[q] + c0 + c] =
+            Elt<T>::from_f(Elt<T>::to_f(((const T *)gc.gamma[q])[c0 + c]) * v);
+    }
+    if (ssq) {
+      __syncthreads();
+      const int ntile = nvcols / 16;
+      for (int idx = threadIdx.x; idx < M * (span / 16); idx += blockDim.x) {
+        const int m = idx / (span / 16), t = idx % (span / 16);
+        if (c0 + 16 * t >= nvcols) continue;
+        float sq = 0.f;
+        for (int c = 16 * t; c < 16 * t + 16; ++c) sq += tile[m * ldt + c] * tile[m * ldt + c];
+        ssq[((size_t)m * ssq_rs + ssq_off) * ntile + c0 / 16 + t] = sq;
+      }
     }
   }
 };
@@ -338,7 +384,7 @@ template <typename T> struct EpiQkv {
     }
     return base + (size_t)row * a.d;
   }
-  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
     const int qd = a.Hq * a.D, kvd = a.Hkv * a.D, D = a.D;
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
@@ -382,7 +428,7 @@ template <typename T> struct EpiSwiglu {
     const int p = c >> 5, f = (c >> 4) & 1, n = c & 15;
     return (f ? wu : wg) + (size_t)(p * 16 + n) * ldw;
   }
-  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
     const int half = span >> 1;
     for (int idx = threadIdx.x; idx < M * half; idx += blockDim.x) {
       const int m = idx / half, q = idx % half;
@@ -403,7 +449,7 @@ template <typename T> struct EpiLm {
   LmArgs a;
   int ldw, nvcols;
   __device__ const T *wrow(int c) const { return (const T *)a.w + (size_t)c * ldw; }
-  __device__ void finish(const float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int nvalid = min(span, nvcols - c0);
     const int nwg = gridDim.x, tileid = blockIdx.x;
@@ -474,13 +520,21 @@ template <int WKmax, int MT> struct SplitK {
 };
 
 template <typename T, int NT, int WKmax, int WN, class Epi>
-static hipError_t run_gemm(const T *A, int lda, int M, int K, const Epi &epi, hipStream_t s) {
+static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K, const Epi &epi,
+                           const NormA *na, hipStream_t s) {
   constexpr int SPAN = WN * NT * 16;
   const int grid = (epi.nvcols + SPAN - 1) / SPAN;
   const int mt = (M + 15) / 16;
+  const NormA n0 = na ? *na : NormA{nullptr, 0, 1, 0, 1, 1, 0.f};
+  if (na) {
+    if (mt != 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gemm<T, 1, NT, SplitK<WKmax, 1>::value, WN, true, Epi>), dim3(grid),
+                       dim3(64 * SplitK<WKmax, 1>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
+    return hipGetLastError();
+  }
 #define FE_GEMM_CASE(MTV)                                                              \
-  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, Epi>), \
-                     dim3(grid), dim3(64 * SplitK<WKmax, MTV>::value * WN), 0, s, A, lda, M, K, epi)
+  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, false, Epi>), \
+                     dim3(grid), dim3(64 * SplitK<WKmax, MTV>::value * WN), 0, s, A, lda, arows, M, K, n0, epi)
   if (mt <= 1) FE_GEMM_CASE(1);
   else if (mt <= 2) FE_GEMM_CASE(2);
   else if (mt <= 4) FE_GEMM_CASE(4);
@@ -496,56 +550,61 @@ hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *
   if (dt) {
     EpiStore<bf16_t> e{(const bf16_t *)W, K, ncols, (bf16_t *)out, ldo, (const bf16_t *)embed,
                        tokens, vocab, (bf16_t *)gather_out, ld_gather, d, B};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, K, e, s);
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s);
   }
   EpiStore<float> e{(const float *)W, K, ncols, (float *)out, ldo, (const float *)embed,
                     tokens, vocab, (float *)gather_out, ld_gather, d, B};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, K, e, s);
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s);
 }
 
 hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
-                      float *out, long ldo, const float *resid, long ldr, hipStream_t s) {
+                      float *out, long ldo, const float *resid, long ldr, float *ssq, int ssq_rs,
+                      int ssq_off, const GainCopies *gains, hipStream_t s) {
+  GainCopies gc{};
+  if (gains) gc = *gains;
   if (dt) {
-    EpiResid<bf16_t> e{(const bf16_t *)W, K, ncols, out, ldo, resid, ldr};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, K, e, s);
+    EpiResid<bf16_t> e{(const bf16_t *)W, K, ncols, out, ldo, resid, ldr, ssq, ssq_rs, ssq_off, gc};
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s);
   }
-  EpiResid<float> e{(const float *)W, K, ncols, out, ldo, resid, ldr};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, K, e, s);
+  EpiResid<float> e{(const float *)W, K, ncols, out, ldo, resid, ldr, ssq, ssq_rs, ssq_off, gc};
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s);
 }
 
-hipError_t gemm_qkv(int dt, const void *A, int lda, int M, const QkvArgs &a, hipStream_t s) {
+hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
+                    const NormA *na, hipStream_t s) {
   const int nv = (a.Hq + 2 * a.Hkv) * a.D;
   if (dt) {
     EpiQkv<bf16_t> e{a, nv};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, M, a.d, e, s);
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, arows, M, a.d, e, na, s);
   }
   EpiQkv<float> e{a, nv};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, M, a.d, e, s);
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, arows, M, a.d, e, na, s);
 }
 
-hipError_t gemm_swiglu(int dt, const void *A, int lda, int M, int K, const void *w_gate,
-                       const void *w_up, int I, void *s_out, int lds, hipStream_t s) {
+hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,
+                       const void *w_gate, const void *w_up, int I, void *s_out, int lds,
+                       const NormA *na, hipStream_t s) {
   if (dt) {
     EpiSwiglu<bf16_t> e{(const bf16_t *)w_gate, (const bf16_t *)w_up, K, I, 2 * I,
                         (bf16_t *)s_out, lds};
-    return run_gemm<bf16_t, 2, 4, 1>((const bf16_t *)A, lda, M, K, e, s);
+    return run_gemm<bf16_t, 2, 4, 1>((const bf16_t *)A, lda, arows, M, K, e, na, s);
   }
   EpiSwiglu<float> e{(const float *)w_gate, (const float *)w_up, K, I, 2 * I, (float *)s_out, lds};
-  return run_gemm<float, 2, 4, 1>((const float *)A, lda, M, K, e, s);
+  return run_gemm<float, 2, 4, 1>((const float *)A, lda, arows, M, K, e, na, s);
 }
 
 constexpr int kLmWN = 4;
 int lmhead_tiles(int V) { return (V + kLmWN * 16 - 1) / (kLmWN * 16); }
 
-hipError_t gemm_lmhead(int dt, const void *A, int lda, int M, int K, const LmArgs &a,
-                       int *nwg_out, hipStream_t s) {
+hipError_t gemm_lmhead(int dt, const void *A, int lda, const ARows &arows, int M, int K,
+                       const LmArgs &a, const NormA *na, int *nwg_out, hipStream_t s) {
   *nwg_out = lmhead_tiles(a.V);
   if (dt) {
     EpiLm<bf16_t> e{a, K, a.V};
-    return run_gemm<bf16_t, 1, 2, kLmWN>((const bf16_t *)A, lda, M, K, e, s);
+    return run_gemm<bf16_t, 1, 2, kLmWN>((const bf16_t *)A, lda, arows, M, K, e, na, s);
   }
   EpiLm<float> e{a, K, a.V};
-  return run_gemm<float, 1, 2, kLmWN>((const float *)A, lda, M, K, e, s);
+  return run_gemm<float, 1, 2, kLmWN>((const float *)A, lda, arows, M, K, e, na, s);
 }
 
 }  // namespace fe

@@ -37,6 +37,7 @@ template <> struct Elt<float> {
   __device__ static __forceinline__ float from_f(float f) { return f; }
 };
 
+constexpr int kMaxLayers = 16;
 // Prefix keys per attention workgroup (4 waves of 32 keys).
 constexpr int kAttnChunk = 128;
 // Tile candidates the top-k merge holds in registers: 256 threads x 32.
@@ -44,7 +45,36 @@ constexpr int kMergeMaxCand = 256 * 32;
 // Largest M (rows) one GEMM launch handles; larger M is split on the host.
 constexpr int kGemmMaxRows = 256;
 constexpr int kMaxTopk = 16;
-constexpr int kMaxLayers = 16;
+
+// Row m of a GEMM's A operand is row (m / per) * outer + j0 + m % per of its buffer.
+struct ARows {
+  int per, j0, outer;
+  __host__ __device__ int row(int m) const { return (m / per) * outer + j0 + m % per; }
+};
+constexpr ARows kDenseRows{1, 0, 1};
+
+// RMSNorm fused into a GEMM (M <= 16): A holds the rows gamma * x in storage
+// precision, and output row m is scaled by 1/sqrt(sum(x^2)/d + eps), with
+// sum(x^2) the sum of the ntile per-16-column partials in row
+// (m / per) * outer + j0 + m % per of ssq, written by the GEMM that produced x.
+struct NormA {
+  const float *ssq;
+  int ntile;
+  int per, j0, outer;
+  int d;
+  float eps;
+  __host__ __device__ int row(int m) const { return (m / per) * outer + j0 + m % per; }
+};
+
+// Storage-type copies gamma_g * y of an fp32 output row y, written by the
+// producing GEMM for later fused-RMSNorm GEMMs: row m of copy g goes to
+// dst[g] + m * ld[g] (elements).
+struct GainCopies {
+  int n;
+  const void *gamma[kMaxLayers + 1];
+  void *dst[kMaxLayers + 1];
+  long ld[kMaxLayers + 1];
+};
 
 // ---------------------------------------------------------------------------
 // Launchers.  `dt` is 0 for fp32 storage, 1 for bf16.  All return the status
@@ -59,9 +89,13 @@ hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *
                       void *out, int ldo, const void *embed, const int32_t *tokens, int vocab,
                       void *gather_out, int ld_gather, int d, int B, hipStream_t s);
 
-// out[m, c] = (resid ? resid[m, c] : 0) + sum_k A[m,k] W[c,k]   (fp32 out/resid)
+// out[m, c] = (resid ? resid[m, c] : 0) + sum_k A[m,k] W[c,k]   (fp32 out/resid).
+// When ssq is not null, also writes the sum of squares of every output row over
+// each 16-column tile t to ssq[(m * ssq_rs + ssq_off) * (ncols/16) + t]; when
+// gains is not null, also writes its gain copies of every output row.
 hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
-                      float *out, long ldo, const float *resid, long ldr, hipStream_t s);
+                      float *out, long ldo, const float *resid, long ldr, float *ssq, int ssq_rs,
+                      int ssq_off, const GainCopies *gains, hipStream_t s);
 
 struct QkvArgs {
   const void *wq, *wk, *wv;
@@ -73,11 +107,14 @@ struct QkvArgs {
   float *k_out, *v_out;      // [B, nctx, Hkv, D]
 };
 // Q/K/V projections of the RMS-normed context rows with rotary embedding of Q and K.
-hipError_t gemm_qkv(int dt, const void *A, int lda, int M, const QkvArgs &a, hipStream_t s);
+// With `na` (M <= 16) A holds gamma * x rows and the RMSNorm scale is fused.
+hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
+                    const NormA *na, hipStream_t s);
 
 // s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
-hipError_t gemm_swiglu(int dt, const void *A, int lda, int M, int K, const void *w_gate,
-                       const void *w_up, int I, void *s_out, int lds, hipStream_t s);
+hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,
+                       const void *w_gate, const void *w_up, int I, void *s_out, int lds,
+                       const NormA *na, hipStream_t s);
 
 struct LmArgs {
   const void *w;             // [V, d]
@@ -90,8 +127,8 @@ struct LmArgs {
 };
 // LM head tiles with per-tile max, sum of exponentials and top-k candidates.
 // Returns the number of column tiles (nwg) through *nwg_out.
-hipError_t gemm_lmhead(int dt, const void *A, int lda, int M, int K, const LmArgs &a,
-                       int *nwg_out, hipStream_t s);
+hipError_t gemm_lmhead(int dt, const void *A, int lda, const ARows &arows, int M, int K,
+                       const LmArgs &a, const NormA *na, int *nwg_out, hipStream_t s);
 int lmhead_tiles(int V);
 
 // RMSNorm of rows r < rows: source row = X + (r / per)*outer + (j0 + r % per)*inner.

@@ -30,7 +30,8 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cat, X, Xp, an, bn, q, knew, vnew, part, cnt, ao, s, pmax, psum, cval, cidx, total;
+  size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, cnt, ao, s, pmax, psum,
+      cval, cidx, total;
   int nchmax, nwg;
 };
 
@@ -47,6 +48,13 @@ Layout layout_of(const fe_config &c) {
   L.cat = take(B * 2 * d * es);
   L.X = take(B * (N + 1) * d * 4);
   L.Xp = take(B * d * 4);
+  L.ssqX = take(B * (N + 1) * (d / 16) * 4);  // sums of squares of x_j per 16-column tile
+  L.ssqP = take(B * (d / 16) * 4);            // ... of x' (post-attention residual)
+  // gamma * x operands of the fused-RMSNorm GEMMs: per layer l the QKV rows
+  // (b, j) of x_j, the MLP rows of x', the final-norm rows (b, i-1) of x_i
+  L.AQ = take(N * B * N * d * es);
+  L.AM = take(B * d * es);
+  L.AF = take(B * N * d * es);
   L.an = take(B * N * d * es);
   L.bn = take(B * d * es);
   L.q = take(B * Hq * D * 4);
@@ -253,45 +261,96 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const int esz = dt ? 2 : 4;
   const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
   const int nch_ld = L.nchmax;
+  const int ntile = d / 16;
+  float *ssqX = (float *)(ws + L.ssqX), *ssqP = (float *)(ws + L.ssqP);
   h->prof_count = 0;
-  if (!h->counters_zeroed) {  // first pass on this handle: counters start at zero
-    FE_TRY(zero_words((uint32_t *)(ws + L.cnt), (size_t)c.max_batch * c.n_q_heads, s));
-    h->counters_zeroed = true;
-  }
 
   // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
   FE_TIMED(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
                     next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s));
   // x_0 = FC(concat(g_t, e_{t+1}))  (Eq. 1)
-  FE_TIMED(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr, 0, s));
+  // Fused RMSNorm (up to 16 rows per GEMM): every producer of a residual row
+  // also writes gamma * row for the later GEMMs that normalise it.
+  const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
+  char *AQ = ws + L.AQ, *AM = ws + L.AM, *AF = ws + L.AF;
+  const size_t aq_layer = (size_t)c.max_batch * N * d * esz;  // bytes per layer block of AQ
+  auto nctx_of = [&](int l) { return cascade ? l : 1; };
+  auto fuse_q = [&](int l) { return B * nctx_of(l) <= 16; };
+  const bool fuse_m = B <= 16, fuse_f = B * N <= 16;
+  // copies of x_j (j = 0 from the input FC, j = i from layer i's down projection)
+  auto x_copies = [&](int j) {
+    GainCopies gc{};
+    for (int l = j + 1; l <= N; ++l) {
+      if (!(cascade || l == j + 1) || !fuse_q(l)) continue;
+      gc.gamma[gc.n] = h->layers[l - 1].attn_norm;
+      gc.dst[gc.n] = AQ + (size_t)(l - 1) * aq_layer + (size_t)j * d * esz;
+      gc.ld[gc.n] = (long)N * d;
+      ++gc.n;
+    }
+    if (j >= 1 && fuse_f) {
+      gc.gamma[gc.n] = h->w.final_norm;
+      gc.dst[gc.n] = AF + (size_t)(j - 1) * d * esz;
+      gc.ld[gc.n] = (long)N * d;
+      ++gc.n;
+    }
+    return gc;
+  };
+  const GainCopies gc_x0 = x_copies(0);
+  FE_TIMED(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr,
+                                      0, ssqX, N + 1, 0, &gc_x0, s));
 
   for (int i = 1; i <= N; ++i) {
     const fe_layer_weights &lw = h->layers[i - 1];
-    const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
-    const int nctx = cascade ? i : 1, j0 = cascade ? 0 : i - 1;
-    // pre-attention RMSNorm of the context rows
-    FE_TRY(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
+    const int nctx = nctx_of(i), j0 = cascade ? 0 : i - 1;
+    // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
+    // separate pass otherwise
     QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
                (double)c.rope_theta, q, knew, vnew};
-    FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, an, d, B * nctx, qa, s));
+    if (fuse_q(i)) {
+      const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
+      FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
+                                      B * nctx, qa, &na1, s));
+    } else {
+      FE_TRY(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
+      FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s));
+    }
     // attention over the layer's prefix cache plus the cascade keys
     FE_TIMED(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
                                       vnew, nctx, part, nch, nch_ld,
                                       (int *)(ws + L.cnt), ao, B, Hq, Hkv, D, s));
     // x' = x_{i-1} + W_o o
-    FE_TIMED(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d, X + (size_t)(i - 1) * d, xrow, s));
+    GainCopies gc_p{};
+    if (fuse_m) {
+      gc_p.n = 1;
+      gc_p.gamma[0] = lw.mlp_norm;
+      gc_p.dst[0] = AM;
+      gc_p.ld[0] = d;
+    }
+    FE_TIMED(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
+                                        X + (size_t)(i - 1) * d, xrow, ssqP, 1, 0, &gc_p, s));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
-    FE_TRY(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
-    FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, B, d, lw.w_gate, lw.w_up, I, sbuf, I, s));
-    FE_TIMED(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow, Xp, d, s));
+    if (fuse_m) {
+      const NormA na2{ssqP, ntile, 1, 0, 1, d, c.rms_eps};
+      FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, AM, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
+                                            sbuf, I, &na2, s));
+    } else {
+      FE_TRY(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
+      FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
+                                            sbuf, I, nullptr, s));
+    }
+    const GainCopies gc_xi = x_copies(i);
+    FE_TIMED(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow,
+                                       Xp, d, ssqX, N + 1, i, &gc_xi, s));
   }
 
   // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
-  FE_TRY(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
+  const NormA naf{ssqX, ntile, N, 1, N + 1, d, c.rms_eps};
+  if (!fuse_f) FE_TRY(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
   LmArgs la{h->w.lm_head, c.draft_vocab, topk, out->logits, (float *)(ws + L.pmax),
             (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx)};
   int nwg = 0;
-  FE_TIMED(FE_STAGE_LMHEAD, gemm_lmhead(dt, an, d, B * N, d, la, &nwg, s));
+  FE_TIMED(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
+                                        d, la, fuse_f ? &naf : nullptr, &nwg, s));
   FE_TRY(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx, B * N, nwg, topk,
                     c.draft_vocab, h->w.d2t, out->topk_ids, out->topk_draft, out->topk_probs, s));
   if (out->hidden)
@@ -325,6 +384,10 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   }
   if (out->logits && ((uintptr_t)out->logits & 3u)) return fail(FE_E_ALIGN, "logits misaligned");
   hipStream_t s = (hipStream_t)stream;
+  if (!h->counters_zeroed) {  // first pass on this handle: attention counters start at zero
+    FE_TRY(zero_words((uint32_t *)(h->ws + h->L.cnt), (size_t)c.max_batch * c.n_q_heads, s));
+    h->counters_zeroed = true;
+  }
 
   if (!h->graph_mode || h->prof_stage != FE_STAGE_NONE)
     return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
