@@ -173,7 +173,6 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
 
 /* Stages of the pass whose kernel launches can be timed with HIP events. */
 typedef enum {
-  FE_STAGE_NONE = -1,
   FE_STAGE_FUSE = 0,     /* g_t = FC(l, m, h) and the embedding gather (one launch) */
   FE_STAGE_INPUT = 1,    /* x_0 = FC(g_t, e_{t+1}) (one launch) */
   FE_STAGE_QKV = 2,      /* per layer: Q/K/V projections + rotary embedding */
@@ -184,17 +183,16 @@ typedef enum {
   FE_STAGE_LMHEAD = 7    /* LM head on all N states + tile softmax statistics and top-k */
 } fe_stage;
 
-/* Times every launch of `stage` (FE_STAGE_NONE turns timing off): from the
- * next fe_draft_forward on, a pair of HIP events owned by the handle is
- * recorded on the launch stream around each launch of that stage.  While a
- * stage is timed, fe_draft_forward launches its kernels one by one (no graph
- * replay) so that every launch can be bracketed. */
-fe_status fe_profile_stage(fe_drafter *h, int32_t stage);
-
-/* Waits for the events of the most recent pass and writes the duration in
- * milliseconds of each timed launch, in launch order, to ms[0..cap-1];
- * *count receives the number of timed launches of that pass. */
-fe_status fe_profile_read(fe_drafter *h, float *ms, int32_t cap, int32_t *count);
+/* Kernel timing for roofline measurements: replays every launch of `stage`
+ * from the most recent fe_draft_forward on this handle, `repeats` times back to
+ * back on `stream`, between two HIP events recorded on that stream, waits for
+ * them, and writes the mean duration of one launch (ms) to *ms_per_launch and
+ * the number of launches of the stage in one pass to *launches.  The buffers
+ * of that fe_draft_forward call must still be valid.  The replays rewrite
+ * workspace scratch (and `logits`, with the same values), so the workspace is
+ * unspecified until the next fe_draft_forward. */
+fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
+                        float *ms_per_launch, int32_t *launches);
 
 void fe_drafter_destroy(fe_drafter *h);
 

@@ -69,7 +69,6 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   __shared__ float s_m[4][GH], s_l[4][GH];
   __shared__ float s_o[4][GH][D];
   __shared__ float s_sc[GH][kMaxLayers];
-  __shared__ float s_M[GH], s_L[GH];
   __shared__ int s_last;
 
   const int G = Hq / Hkv, ngrp = G / GH;
@@ -86,11 +85,13 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   const size_t rowstride = (size_t)Hkv * D;
   const T *kbase = Kc + ((size_t)start * Hkv + c) * D + dp * DL;
   const T *vbase = Vc + ((size_t)start * Hkv + c) * D + dp * DL;
+  // Rows are loaded unconditionally at clamped keys (missing keys get weight 0
+  // below); an empty prefix reads nothing.
   KvRow<T, D> kr[kSteps], vr[kSteps];
+  if (P > 0) {
 #pragma unroll
-  for (int st = 0; st < kSteps; ++st) {
-    const int key = key0 + st * 8 + slot;
-    if (key < P) {
+    for (int st = 0; st < kSteps; ++st) {
+      const int key = min(key0 + st * 8 + slot, P - 1);
       kr[st].load(kbase + (size_t)key * rowstride);
       vr[st].load(vbase + (size_t)key * rowstride);
     }
@@ -100,6 +101,19 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   for (int gh = 0; gh < GH; ++gh)
 #pragma unroll
     for (int e = 0; e < DL; ++e) qv[gh][e] = q[((size_t)b * Hq + h0 + gh) * D + dp * DL + e];
+  // cascade keys of head group member `wave` (waves < GH): loaded now, scored
+  // below, so that the final merge needs no further inputs but the partials
+  constexpr int DPL = D / 64;
+  float qd[DPL], kd[kMaxLayers][DPL];
+  if (wave < GH) {
+#pragma unroll
+    for (int t = 0; t < DPL; ++t) qd[t] = q[((size_t)b * Hq + h0 + wave) * D + lane * DPL + t];
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j)
+#pragma unroll
+      for (int t = 0; t < DPL; ++t)
+        kd[j][t] = knew[(((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + lane * DPL + t];
+  }
 
   float s[kSteps][GH];
 #pragma unroll
@@ -139,17 +153,15 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
 #pragma unroll
     for (int e = 0; e < DL; ++e) o[gh][e] = 0.f;
   }
+  if (P > 0) {
 #pragma unroll
-  for (int st = 0; st < kSteps; ++st) {
-    const int key = key0 + st * 8 + slot;
-    if (key < P) {
+    for (int st = 0; st < kSteps; ++st)
 #pragma unroll
       for (int e = 0; e < DL; ++e) {
         const float ve = vr[st].at(e);
 #pragma unroll
-        for (int gh = 0; gh < GH; ++gh) o[gh][e] += s[st][gh] * ve;
+        for (int gh = 0; gh < GH; ++gh) o[gh][e] += s[st][gh] * ve;  // weight 0 past P
       }
-    }
   }
 #pragma unroll
   for (int gh = 0; gh < GH; ++gh)
@@ -170,6 +182,17 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
         s_m[wave][gh] = mx[gh];
         s_l[wave][gh] = l[gh];
       }
+    }
+  }
+  if (wave < GH) {  // scores of the cascade keys for head h0 + wave
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) {
+      float v = 0.f;
+#pragma unroll
+      for (int t = 0; t < DPL; ++t) v += qd[t] * kd[j][t];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+      if (lane == 0) s_sc[wave][j] = j < nctx ? v * scale : -INFINITY;
     }
   }
   __syncthreads();
@@ -203,58 +226,52 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   __threadfence();
 
   // ---- last chunk workgroup: merge every chunk and the cascade keys ---------
-  constexpr int DPL = D / 64;
-  if (wave < GH) {
-    const int gh = wave, h = h0 + gh;
-    float qd[DPL];
-#pragma unroll
-    for (int t = 0; t < DPL; ++t) qd[t] = q[((size_t)b * Hq + h) * D + lane * DPL + t];
-    float sj[kMaxLayers];
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) {
-      sj[j] = -INFINITY;
-      if (j < nctx) {
-        float v = 0.f;
-#pragma unroll
-        for (int t = 0; t < DPL; ++t)
-          v += qd[t] * knew[(((size_t)b * nctx + j) * Hkv + c) * D + lane * DPL + t];
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-        sj[j] = v * scale;
-      }
-    }
-    const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
-    float M = -INFINITY;
-    for (int k = lane; k < nv; k += 64) M = fmaxf(M, pp[(size_t)k * (D + 2) + D]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) M = fmaxf(M, sj[j]);
-    float L = 0.f;
-    for (int k = lane; k < nv; k += 64)
-      L += pp[(size_t)k * (D + 2) + D + 1] * scaled_exp(pp[(size_t)k * (D + 2) + D], M);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) L += scaled_exp(sj[j], M);
-    if (lane == 0) {
-      s_M[gh] = M;
-      s_L[gh] = L;
-#pragma unroll
-      for (int j = 0; j < kMaxLayers; ++j) s_sc[gh][j] = sj[j];
-    }
-  }
-  __syncthreads();
+  // Thread (gh, e) reads what it needs in one round trip (8 chunks per group,
+  // clamped in-bounds indices, unused values masked) and merges with a running
+  // max in a fixed order.
   for (int idx = tid; idx < GH * D; idx += 256) {
     const int gh = idx / D, e = idx % D, h = h0 + gh;
-    const float M = s_M[gh];
     const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
-    float acc = 0.f;
-    for (int k = 0; k < nv; ++k)
-      acc += pp[(size_t)k * (D + 2) + e] * scaled_exp(pp[(size_t)k * (D + 2) + D], M);
-    for (int j = 0; j < nctx; ++j)
-      acc += scaled_exp(s_sc[gh][j], M) * vnew[(((size_t)b * nctx + j) * Hkv + c) * D + e];
-    out[(size_t)b * Hq * D + (size_t)h * D + e] = Elt<T>::from_f(acc / s_L[gh]);
+    float vv[kMaxLayers];
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j)
+      vv[j] = vnew[(((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + e];
+    float M = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) M = fmaxf(M, s_sc[gh][j]);
+    float L = 0.f, acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j) {
+      const float w = scaled_exp(s_sc[gh][j], M);
+      L += w;
+      acc += w * vv[j];
+    }
+    for (int k0 = 0; k0 < nv; k0 += 8) {
+      float ov[8], mv[8], lv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float *pk = pp + (size_t)min(k0 + u, nv - 1) * (D + 2);
+        ov[u] = pk[e];
+        mv[u] = pk[D];
+        lv[u] = pk[D + 1];
+      }
+      float Mn = M;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < nv) Mn = fmaxf(Mn, mv[u]);
+      const float rs = scaled_exp(M, Mn);
+      L *= rs;
+      acc *= rs;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < nv) {
+          const float w = scaled_exp(mv[u], Mn);
+          L += lv[u] * w;
+          acc += ov[u] * w;
+        }
+      M = Mn;
+    }
+    out[(size_t)b * Hq * D + (size_t)h * D + e] = Elt<T>::from_f(acc / L);
   }
   if (tid == 0) counters[((size_t)b * Hkv + c) * ngrp + hg] = 0;
 }

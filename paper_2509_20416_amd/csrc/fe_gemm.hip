@@ -399,12 +399,10 @@ template <typename T> struct EpiQkv {
         const int h = lc / D, cc = lc % D, dd = rope_dim(cc, D);
         const float pv = tile[m * ldt + (c ^ 8)];
         const int P = a.cu_prefix[b + 1] - a.cu_prefix[b];
-        const long pos = a.cascade ? (long)P + j : (long)P;
+        const int pos = min(a.cascade ? P + j : P, a.rope_npos - 1);
         const int pm = 8 * (cc >> 4) + (cc & 7);
-        const double ang = (double)pos * pow(a.theta, -2.0 * (double)pm / (double)D);
-        double sn, cs;
-        sincos(ang, &sn, &cs);
-        const float c_ = (float)cs, s_ = (float)sn;
+        const float c_ = a.rope[((size_t)pos * (D / 2) + pm) * 2];
+        const float s_ = a.rope[((size_t)pos * (D / 2) + pm) * 2 + 1];
         const float o = (cc & 8) ? (val * c_ + pv * s_) : (val * c_ - pv * s_);
         if (isq)
           a.q_out[((size_t)b * a.Hq + h) * D + dd] = o;
@@ -484,25 +482,21 @@ template <typename T> struct EpiLm {
         a.part_max[pb] = mx;
         a.part_sum[pb] = se;
       }
+      uint64_t key[PER];
+#pragma unroll
+      for (int p = 0; p < PER; ++p) key[p] = id[p] != 0x7fffffff ? topk_key(v[p], id[p]) : kNoKey;
       for (int r = 0; r < a.topk; ++r) {
-        // lane-local best, then wave argmax with the lower-id tie-break
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
+        // lane-local best, then wave max of the ordering keys (lower id wins ties)
+        uint64_t best = kNoKey;
 #pragma unroll
-        for (int p = 0; p < PER; ++p)
-          if (v[p] > bv || (v[p] == bv && id[p] < bi)) { bv = v[p]; bi = id[p]; }
+        for (int p = 0; p < PER; ++p) best = key[p] > best ? key[p] : best;
+        best = wave_max_u64(best);
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-          const float ov = __shfl_xor(bv, o);
-          const int oi = __shfl_xor(bi, o);
-          if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-        }
-#pragma unroll
-        for (int p = 0; p < PER; ++p)
-          if (id[p] == bi) { v[p] = -INFINITY; id[p] = 0x7fffffff; }
+        for (int p = 0; p < PER; ++p) key[p] = key[p] == best ? kNoKey : key[p];
         if (lane == 0) {
-          a.cand_val[pb * kMaxTopk + r] = bv;
-          a.cand_idx[pb * kMaxTopk + r] = bi;
+          const bool got = best != kNoKey;
+          a.cand_val[pb * kMaxTopk + r] = got ? topk_key_value(best) : -INFINITY;
+          a.cand_idx[pb * kMaxTopk + r] = got ? topk_key_id(best) : 0x7fffffff;
         }
       }
     }
@@ -593,18 +587,19 @@ hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M
   return run_gemm<float, 2, 4, 1>((const float *)A, lda, arows, M, K, e, na, s);
 }
 
-constexpr int kLmWN = 4;
-int lmhead_tiles(int V) { return (V + kLmWN * 16 - 1) / (kLmWN * 16); }
+// LM head: 64-column tiles; 2 x 2 waves, each 32 weight rows x half of K.
+constexpr int kLmWN = 2, kLmNT = 2;
+int lmhead_tiles(int V) { return (V + kLmWN * kLmNT * 16 - 1) / (kLmWN * kLmNT * 16); }
 
 hipError_t gemm_lmhead(int dt, const void *A, int lda, const ARows &arows, int M, int K,
                        const LmArgs &a, const NormA *na, int *nwg_out, hipStream_t s) {
   *nwg_out = lmhead_tiles(a.V);
   if (dt) {
     EpiLm<bf16_t> e{a, K, a.V};
-    return run_gemm<bf16_t, 1, 2, kLmWN>((const bf16_t *)A, lda, arows, M, K, e, na, s);
+    return run_gemm<bf16_t, kLmNT, 2, kLmWN>((const bf16_t *)A, lda, arows, M, K, e, na, s);
   }
   EpiLm<float> e{a, K, a.V};
-  return run_gemm<float, 1, 2, kLmWN>((const float *)A, lda, arows, M, K, e, na, s);
+  return run_gemm<float, kLmNT, 2, kLmWN>((const float *)A, lda, arows, M, K, e, na, s);
 }
 
 }  // namespace fe

@@ -25,6 +25,32 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Top-k ordering key: larger logit first, equal logits by lower id.  The float
+// is mapped to an order-preserving 32-bit integer (NaN lowest), the id stored
+// inverted below it, so one unsigned 64-bit compare decides.
+__device__ __forceinline__ uint64_t topk_key(float v, int id) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t k = (v != v) ? 0u : ((u & 0x80000000u) ? ~u : (u | 0x80000000u));
+  return ((uint64_t)k << 32) | (uint64_t)(0xffffffffu - (uint32_t)id);
+}
+__device__ __forceinline__ float topk_key_value(uint64_t key) {
+  const uint32_t k = (uint32_t)(key >> 32);
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+__device__ __forceinline__ int topk_key_id(uint64_t key) {
+  return (int)(0xffffffffu - (uint32_t)key);
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint64_t w = ((uint64_t)(uint32_t)__shfl_xor((int)(v >> 32), o) << 32) |
+                       (uint32_t)__shfl_xor((int)(uint32_t)v, o);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+constexpr uint64_t kNoKey = 0ull;  // below every real key (the id 0xffffffff never occurs)
+
 template <typename T> struct Elt;
 template <> struct Elt<uint16_t> {
   static constexpr int kPer16B = 8;
@@ -102,7 +128,8 @@ struct QkvArgs {
   int d, D, Hq, Hkv;
   int nctx, j0, cascade;     // rows are (b, t) with t < nctx, cascade state j = j0 + t
   const int32_t *cu_prefix;  // [B+1]
-  double theta;
+  const float *rope;         // [rope_npos, D/2, 2]: cos, sin of pos * theta^(-2m/D)
+  int rope_npos;
   float *q_out;              // [B, Hq, D]       (row t == nctx-1 only)
   float *k_out, *v_out;      // [B, nctx, Hkv, D]
 };
@@ -145,6 +172,10 @@ hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_pre
                      const float *q, const float *knew, const float *vnew, int nctx,
                      float *part, int nch, int nch_ld, int *counters, void *out, int B, int Hq,
                      int Hkv, int D, hipStream_t s);
+
+// Rotary table: tab[(p * D/2 + m) * 2 + {0,1}] = cos, sin of p * theta^(-2m/D),
+// formed in double precision and rounded to fp32, for p < npos.
+hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s);
 
 // Sets n 32-bit words to zero (a kernel, so it is safe inside graph capture).
 hipError_t zero_words(uint32_t *p, size_t n, hipStream_t s);

@@ -48,10 +48,11 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // S = sum_t s_t exp(m_t - mu); the global top-k is the best k of all tile
 // candidates (larger logit first, lower draft id on ties); p = exp(z - mu)/S.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
-  return v > bv || (v == bv && i < bi);
-}
 
+// One workgroup (4 waves) per row.  Each wave selects the top-k of the
+// candidates its lanes hold (k rounds of butterfly max over ordering keys, no
+// block barrier), then wave 0 selects the top-k of the 4k wave winners and
+// writes them.
 __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
                                                     const float *__restrict__ psum,
                                                     const float *__restrict__ cval,
@@ -61,80 +62,83 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
                                                     float *probs) {
   constexpr int CAP = kMergeMaxCand / 256;
   __shared__ float sv[4];
-  __shared__ int si[4];
-  __shared__ float s_mu, s_S;
-  __shared__ int s_win;
+  __shared__ uint64_t s_key[4][kMaxTopk];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *pm = pmax + (size_t)row * nwg;
   const float *ps = psum + (size_t)row * nwg;
-  // every candidate of the row into registers (thread t holds t, t+256, ...)
+  // every candidate of the row into registers (thread t holds t, t+256, ...):
+  // unconditional loads at clamped indices (one memory round trip), masked after
   const int ncand = nwg * topk;
   float cv[CAP];
   int ci[CAP];
 #pragma unroll
   for (int j = 0; j < CAP; ++j) {
-    const int c = tid + 256 * j;
-    cv[j] = -INFINITY;
-    ci[j] = 0x7fffffff;
-    if (c < ncand) {
-      const size_t o = ((size_t)row * nwg + c / topk) * kMaxTopk + c % topk;
-      cv[j] = cval[o];
-      ci[j] = cidx[o];
-    }
+    const int c = min(tid + 256 * j, ncand - 1);
+    const size_t o = ((size_t)row * nwg + c / topk) * kMaxTopk + c % topk;
+    cv[j] = cval[o];
+    ci[j] = cidx[o];
   }
-  // mu
+  // softmax statistics: mu = max_t m_t, S = sum_t s_t exp(m_t - mu), fixed
+  // order; the tile statistics are loaded with the candidates (kStatLoads per
+  // thread cover nwg <= 1024; a loop covers the rest)
+  constexpr int kStatLoads = 4;
+  float pmv[kStatLoads], psv[kStatLoads];
+#pragma unroll
+  for (int u = 0; u < kStatLoads; ++u) {
+    const int t = min(tid + 256 * u, nwg - 1);
+    pmv[u] = pm[t];
+    psv[u] = ps[t];
+  }
+  uint64_t key[CAP];
+#pragma unroll
+  for (int j = 0; j < CAP; ++j) key[j] = tid + 256 * j < ncand ? topk_key(cv[j], ci[j]) : kNoKey;
   float m = -INFINITY;
-  for (int t = tid; t < nwg; t += 256) m = fmaxf(m, pm[t]);
+#pragma unroll
+  for (int u = 0; u < kStatLoads; ++u)
+    if (tid + 256 * u < nwg) m = fmaxf(m, pmv[u]);
+  for (int t = tid + 256 * kStatLoads; t < nwg; t += 256) m = fmaxf(m, pm[t]);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
   if (lane == 0) sv[wave] = m;
   __syncthreads();
   const float mu = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
   __syncthreads();
-  // S, fixed order: per-thread strided partial sums, then a fixed tree
   float S = 0.f;
-  for (int t = tid; t < nwg; t += 256) S += ps[t] * expf(pm[t] - mu);
+#pragma unroll
+  for (int u = 0; u < kStatLoads; ++u)
+    if (tid + 256 * u < nwg) S += psv[u] * expf(pmv[u] - mu);
+  for (int t = tid + 256 * kStatLoads; t < nwg; t += 256) S += ps[t] * expf(pm[t] - mu);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) S += __shfl_xor(S, o);
   if (lane == 0) sv[wave] = S;
-  __syncthreads();
-  if (tid == 0) {
-    s_mu = mu;
-    s_S = (sv[0] + sv[1]) + (sv[2] + sv[3]);
+  // per-wave top-k
+  for (int r = 0; r < topk; ++r) {
+    uint64_t best = kNoKey;
+#pragma unroll
+    for (int j = 0; j < CAP; ++j) best = key[j] > best ? key[j] : best;
+    best = wave_max_u64(best);
+#pragma unroll
+    for (int j = 0; j < CAP; ++j) key[j] = key[j] == best ? kNoKey : key[j];
+    if (lane == 0) s_key[wave][r] = best;
   }
   __syncthreads();
-  // k rounds of block argmax over the register-held candidates
-  for (int r = 0; r < topk; ++r) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int j = 0; j < CAP; ++j)
-      if (better(cv[j], ci[j], bv, bi)) { bv = cv[j]; bi = ci[j]; }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const float ov = __shfl_xor(bv, o);
-      const int oi = __shfl_xor(bi, o);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  if (wave == 0) {
+    const float Ssum = (sv[0] + sv[1]) + (sv[2] + sv[3]);
+    uint64_t k = lane < 4 * topk ? s_key[lane / topk][lane % topk] : kNoKey;
+    uint64_t mine = kNoKey;
+    for (int r = 0; r < topk; ++r) {
+      const uint64_t best = wave_max_u64(k);
+      k = k == best ? kNoKey : k;
+      if (lane == r) mine = best;
     }
-    if (lane == 0) { sv[wave] = bv; si[wave] = bi; }
-    __syncthreads();
-    if (tid == 0) {
-      float v = sv[0];
-      int i = si[0];
-      for (int w = 1; w < 4; ++w)
-        if (better(sv[w], si[w], v, i)) { v = sv[w]; i = si[w]; }
-      s_win = i;
-      const size_t o = (size_t)row * topk + r;
-      const bool valid = i >= 0 && i < V;  // no valid candidate left (NaN row): -1
+    if (lane < topk) {
+      const size_t o = (size_t)row * topk + lane;
+      const int i = topk_key_id(mine);
+      const bool valid = mine != kNoKey && i >= 0 && i < V;  // none left (NaN row): -1
       ids[o] = valid ? (d2t ? d2t[i] : i) : -1;
       if (draft_ids) draft_ids[o] = valid ? i : -1;
-      probs[o] = valid ? expf(v - s_mu) / s_S : __int_as_float(0x7fc00000);
+      probs[o] = valid ? expf(topk_key_value(mine) - mu) / Ssum : __int_as_float(0x7fc00000);
     }
-    __syncthreads();
-    const int win = s_win;
-#pragma unroll
-    for (int j = 0; j < CAP; ++j)
-      if (ci[j] == win) { cv[j] = -INFINITY; ci[j] = 0x7fffffff; }
   }
 }
 
@@ -215,6 +219,25 @@ hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_build_tree, dim3(B), dim3(256), 0, s, N, k, root_tokens, topk_ids,
                      prefix_lens, tokens, parents, depth, positions, mask, retrieve);
+  return hipGetLastError();
+}
+
+__global__ void k_rope_table(float *tab, int npos, int D, double theta) {
+  const int half = D / 2;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < npos * half; i += gridDim.x * blockDim.x) {
+    const int p = i / half, m = i % half;
+    const double ang = (double)p * pow(theta, -2.0 * (double)m / (double)D);
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    tab[2 * (size_t)i] = (float)cs;
+    tab[2 * (size_t)i + 1] = (float)sn;
+  }
+}
+
+hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s) {
+  const long n = (long)npos * (D / 2);
+  const int grid = (int)((n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048);
+  hipLaunchKernelGGL(k_rope_table, dim3(grid), dim3(256), 0, s, tab, npos, D, theta);
   return hipGetLastError();
 }
 

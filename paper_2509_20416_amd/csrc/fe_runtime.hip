@@ -30,9 +30,9 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, cnt, ao, s, pmax, psum,
-      cval, cidx, total;
-  int nchmax, nwg;
+  size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, cnt, rope, ao, s, pmax,
+      psum, cval, cidx, total;
+  int nchmax, nwg, npos;
 };
 
 int es_of(const fe_config &c) { return c.dtype == FE_BF16 ? 2 : 4; }
@@ -62,6 +62,8 @@ Layout layout_of(const fe_config &c) {
   L.vnew = take(B * N * Hkv * D * 4);
   L.part = take(B * Hq * (size_t)L.nchmax * (D + 2) * 4);
   L.cnt = take(B * Hq * 4);
+  L.npos = c.max_prefix + c.n_layers;  // positions P_b + j, j < N
+  L.rope = take((size_t)L.npos * (D / 2) * 2 * 4);
   L.ao = take(B * Hq * D * es);
   L.s = take(B * I * es);
   L.pmax = take(B * N * (size_t)L.nwg * 4);
@@ -110,15 +112,20 @@ struct fe_drafter {
   Layout L;
   hipStream_t cap_stream = nullptr;
   bool graph_mode = false;
-  bool counters_zeroed = false;  // attention completion counters set to zero once
+  bool counters_zeroed = false;  // attention counters zeroed and rotary table built once
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
-  // launch timing of one stage
-  int prof_stage = FE_STAGE_NONE;
-  int prof_count = 0;  // launches timed in the last enqueued pass
-  hipEvent_t ev_start[kMaxLayers] = {}, ev_stop[kMaxLayers] = {};
+  // arguments of the most recent fe_draft_forward, for fe_time_stage
+  bool have_last = false;
+  int last_batch = 0, last_topk = 0;
+  const void *last_features = nullptr;
+  const int32_t *last_tokens = nullptr;
+  std::vector<const void *> last_k, last_v;
+  fe_kv_view last_kv{};
+  fe_draft_out last_out{};
+  hipEvent_t ev_a = nullptr, ev_b = nullptr;
 };
 
 extern "C" {
@@ -174,37 +181,10 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on) {
   return FE_OK;
 }
 
-fe_status fe_profile_stage(fe_drafter *h, int32_t stage) {
-  if (!h) return fail(FE_E_INVALID, "handle is NULL");
-  if (stage < FE_STAGE_NONE || stage > FE_STAGE_LMHEAD) return fail(FE_E_INVALID, "unknown stage %d", stage);
-  if (stage != FE_STAGE_NONE && !h->ev_start[0]) {
-    for (int i = 0; i < kMaxLayers; ++i) {
-      if (hipEventCreate(&h->ev_start[i]) != hipSuccess || hipEventCreate(&h->ev_stop[i]) != hipSuccess)
-        return fail(FE_E_HIP, "hipEventCreate failed");
-    }
-  }
-  h->prof_stage = stage;
-  h->prof_count = 0;
-  return FE_OK;
-}
-
-fe_status fe_profile_read(fe_drafter *h, float *ms, int32_t cap, int32_t *count) {
-  if (!h || !count || (cap > 0 && !ms)) return fail(FE_E_INVALID, "bad arguments");
-  *count = h->prof_stage == FE_STAGE_NONE ? 0 : h->prof_count;
-  for (int i = 0; i < *count && i < cap; ++i) {
-    hipError_t e = hipEventSynchronize(h->ev_stop[i]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms[i], h->ev_start[i], h->ev_stop[i]);
-    if (e != hipSuccess) return fail(FE_E_HIP, "event timing: %s", hipGetErrorString(e));
-  }
-  return FE_OK;
-}
-
 void fe_drafter_destroy(fe_drafter *h) {
   if (!h) return;
-  for (int i = 0; i < kMaxLayers; ++i) {
-    if (h->ev_start[i]) (void)hipEventDestroy(h->ev_start[i]);
-    if (h->ev_stop[i]) (void)hipEventDestroy(h->ev_stop[i]);
-  }
+  if (h->ev_a) (void)hipEventDestroy(h->ev_a);
+  if (h->ev_b) (void)hipEventDestroy(h->ev_b);
   if (h->exec) (void)hipGraphExecDestroy(h->exec);
   if (h->graph) (void)hipGraphDestroy(h->graph);
   if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
@@ -221,31 +201,21 @@ namespace {
     if (e_ != hipSuccess) return fail(FE_E_HIP, "%s: %s", #x, hipGetErrorString(e_)); \
   } while (0)
 
-// Brackets one launch with the handle's timing events when its stage is timed.
-struct StageTimer {
-  fe_drafter *h;
-  hipStream_t s;
-  int stage, idx = -1;
-  StageTimer(fe_drafter *h_, int stage_, hipStream_t s_) : h(h_), s(s_), stage(stage_) {
-    if (h->prof_stage == stage && h->prof_count < kMaxLayers) {
-      idx = h->prof_count++;
-      (void)hipEventRecord(h->ev_start[idx], s);
-    }
-  }
-  ~StageTimer() {
-    if (idx >= 0) (void)hipEventRecord(h->ev_stop[idx], s);
-  }
-};
-#define FE_TIMED(stage, x) \
-  do {                     \
-    StageTimer t_(h, stage, s); \
-    FE_TRY(x);             \
+// With only_stage >= 0, a pass launches just the kernels of that stage (used
+// to time them); every other launch is skipped.
+#define FE_STAGE_RUN(stage, x)                       \
+  do {                                               \
+    if (only_stage < 0 || only_stage == (stage)) FE_TRY(x); \
+  } while (0)
+#define FE_OTHER(x)                  \
+  do {                               \
+    if (only_stage < 0) FE_TRY(x);   \
   } while (0)
 
 // The whole pass: FCs of Eq. 1, N cascade layers (Eq. 2), LM head + top-k.
 fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int32_t *next_tokens,
                           const fe_kv_view *kv, int topk, const fe_draft_out *out,
-                          hipStream_t s) {
+                          hipStream_t s, int only_stage = -1) {
   const fe_config &c = h->cfg;
   const Layout &L = h->L;
   const int dt = c.dtype == FE_BF16 ? 1 : 0;
@@ -263,10 +233,9 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const int nch_ld = L.nchmax;
   const int ntile = d / 16;
   float *ssqX = (float *)(ws + L.ssqX), *ssqP = (float *)(ws + L.ssqP);
-  h->prof_count = 0;
 
   // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
-  FE_TIMED(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
+  FE_STAGE_RUN(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
                     next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s));
   // x_0 = FC(concat(g_t, e_{t+1}))  (Eq. 1)
   // Fused RMSNorm (up to 16 rows per GEMM): every producer of a residual row
@@ -296,7 +265,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     return gc;
   };
   const GainCopies gc_x0 = x_copies(0);
-  FE_TIMED(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr,
+  FE_STAGE_RUN(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr,
                                       0, ssqX, N + 1, 0, &gc_x0, s));
 
   for (int i = 1; i <= N; ++i) {
@@ -305,17 +274,17 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
     // separate pass otherwise
     QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
-               (double)c.rope_theta, q, knew, vnew};
+               (const float *)(ws + L.rope), L.npos, q, knew, vnew};
     if (fuse_q(i)) {
       const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
-      FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
+      FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
                                       B * nctx, qa, &na1, s));
     } else {
-      FE_TRY(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
-      FE_TIMED(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s));
+      FE_OTHER(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
+      FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s));
     }
     // attention over the layer's prefix cache plus the cascade keys
-    FE_TIMED(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
+    FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
                                       vnew, nctx, part, nch, nch_ld,
                                       (int *)(ws + L.cnt), ao, B, Hq, Hkv, D, s));
     // x' = x_{i-1} + W_o o
@@ -326,36 +295,36 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
       gc_p.dst[0] = AM;
       gc_p.ld[0] = d;
     }
-    FE_TIMED(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
+    FE_STAGE_RUN(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
                                         X + (size_t)(i - 1) * d, xrow, ssqP, 1, 0, &gc_p, s));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
     if (fuse_m) {
       const NormA na2{ssqP, ntile, 1, 0, 1, d, c.rms_eps};
-      FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, AM, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
+      FE_STAGE_RUN(FE_STAGE_GATEUP, gemm_swiglu(dt, AM, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
                                             sbuf, I, &na2, s));
     } else {
-      FE_TRY(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
-      FE_TIMED(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
+      FE_OTHER(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
+      FE_STAGE_RUN(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
                                             sbuf, I, nullptr, s));
     }
     const GainCopies gc_xi = x_copies(i);
-    FE_TIMED(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow,
+    FE_STAGE_RUN(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow,
                                        Xp, d, ssqX, N + 1, i, &gc_xi, s));
   }
 
   // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
   const NormA naf{ssqX, ntile, N, 1, N + 1, d, c.rms_eps};
-  if (!fuse_f) FE_TRY(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
+  if (!fuse_f) FE_OTHER(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
   LmArgs la{h->w.lm_head, c.draft_vocab, topk, out->logits, (float *)(ws + L.pmax),
             (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx)};
   int nwg = 0;
-  FE_TIMED(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
+  FE_STAGE_RUN(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
                                         d, la, fuse_f ? &naf : nullptr, &nwg, s));
-  FE_TRY(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx, B * N, nwg, topk,
+  FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx, B * N, nwg, topk,
                     c.draft_vocab, h->w.d2t, out->topk_ids, out->topk_draft, out->topk_probs, s));
   if (out->hidden)
-    FE_TRY(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
-                          hipMemcpyDeviceToDevice, s));
+    FE_OTHER(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
+                            hipMemcpyDeviceToDevice, s));
   return FE_OK;
 }
 
@@ -386,11 +355,24 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   hipStream_t s = (hipStream_t)stream;
   if (!h->counters_zeroed) {  // first pass on this handle: attention counters start at zero
     FE_TRY(zero_words((uint32_t *)(h->ws + h->L.cnt), (size_t)c.max_batch * c.n_q_heads, s));
+    FE_TRY(rope_table((float *)(h->ws + h->L.rope), h->L.npos, c.head_dim, (double)c.rope_theta, s));
     h->counters_zeroed = true;
   }
 
-  if (!h->graph_mode || h->prof_stage != FE_STAGE_NONE)
-    return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
+  // remember the call for fe_time_stage
+  h->have_last = true;
+  h->last_batch = batch;
+  h->last_topk = topk;
+  h->last_features = features;
+  h->last_tokens = next_tokens;
+  h->last_k.assign(kv->k, kv->k + c.n_layers);
+  h->last_v.assign(kv->v, kv->v + c.n_layers);
+  h->last_kv = *kv;
+  h->last_kv.k = h->last_k.data();
+  h->last_kv.v = h->last_v.data();
+  h->last_out = *out;
+
+  if (!h->graph_mode) return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
 
   std::vector<uintptr_t> key = {(uintptr_t)batch, (uintptr_t)features, (uintptr_t)next_tokens,
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
@@ -417,6 +399,32 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
     h->key = key;
   }
   FE_TRY(hipGraphLaunch(h->exec, s));
+  return FE_OK;
+}
+
+extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
+                                   float *ms_per_launch, int32_t *launches) {
+  if (!h || !ms_per_launch || !launches) return fail(FE_E_INVALID, "bad arguments");
+  if (stage < FE_STAGE_FUSE || stage > FE_STAGE_LMHEAD) return fail(FE_E_INVALID, "unknown stage %d", stage);
+  if (repeats < 1) return fail(FE_E_INVALID, "repeats must be >= 1");
+  if (!h->have_last) return fail(FE_E_INVALID, "no fe_draft_forward call to replay yet");
+  const int N = h->cfg.n_layers;
+  const int per_pass = (stage == FE_STAGE_FUSE || stage == FE_STAGE_INPUT || stage == FE_STAGE_LMHEAD) ? 1 : N;
+  hipStream_t s = (hipStream_t)stream;
+  if (!h->ev_a) FE_TRY(hipEventCreate(&h->ev_a));
+  if (!h->ev_b) FE_TRY(hipEventCreate(&h->ev_b));
+  FE_TRY(hipEventRecord(h->ev_a, s));
+  for (int r = 0; r < repeats; ++r) {
+    const fe_status st = enqueue_forward(h, h->last_batch, h->last_features, h->last_tokens,
+                                         &h->last_kv, h->last_topk, &h->last_out, s, stage);
+    if (st != FE_OK) return st;
+  }
+  FE_TRY(hipEventRecord(h->ev_b, s));
+  FE_TRY(hipEventSynchronize(h->ev_b));
+  float ms = 0.f;
+  FE_TRY(hipEventElapsedTime(&ms, h->ev_a, h->ev_b));
+  *ms_per_launch = ms / (float)(repeats * per_pass);
+  *launches = per_pass;
   return FE_OK;
 }
 

@@ -20,9 +20,8 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
-           "fe_set_graph_mode", "fe_profile_stage", "fe_profile_read", "fe_drafter_destroy",
-           "fe_last_error")
-FE_STAGE = dict(none=-1, fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
+           "fe_set_graph_mode", "fe_time_stage", "fe_drafter_destroy", "fe_last_error")
+FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
 
 class fe_config(C.Structure):
@@ -91,11 +90,9 @@ def lib() -> C.CDLL:
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
-        L.fe_profile_stage.restype = C.c_int
-        L.fe_profile_stage.argtypes = [C.c_void_p, C.c_int32]
-        L.fe_profile_read.restype = C.c_int
-        L.fe_profile_read.argtypes = [C.c_void_p, C.POINTER(C.c_float), C.c_int32,
-                                      C.POINTER(C.c_int32)]
+        L.fe_time_stage.restype = C.c_int
+        L.fe_time_stage.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                    C.POINTER(C.c_float), C.POINTER(C.c_int32)]
         L.fe_drafter_destroy.restype = None
         L.fe_drafter_destroy.argtypes = [C.c_void_p]
         L.fe_last_error.restype = C.c_char_p
@@ -143,15 +140,13 @@ def fe_set_graph_mode(h: int, on: bool) -> None:
     check(lib().fe_set_graph_mode(C.c_void_p(h), 1 if on else 0))
 
 
-def fe_profile_stage(h: int, stage: int) -> None:
-    check(lib().fe_profile_stage(C.c_void_p(h), int(stage)))
-
-
-def fe_profile_read(h: int, cap: int = 16):
-    ms = (C.c_float * cap)()
+def fe_time_stage(h: int, stage: int, repeats: int, stream: int):
+    """Mean duration (ms) of one launch of `stage` and launches per pass."""
+    ms = C.c_float()
     n = C.c_int32()
-    check(lib().fe_profile_read(C.c_void_p(h), ms, cap, C.byref(n)))
-    return [float(ms[i]) for i in range(min(cap, n.value))]
+    check(lib().fe_time_stage(C.c_void_p(h), int(stage), int(repeats), C.c_void_p(stream),
+                              C.byref(ms), C.byref(n)))
+    return float(ms.value), int(n.value)
 
 
 def fe_drafter_destroy(h: int) -> None:
