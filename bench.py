@@ -44,16 +44,34 @@ def pass_bytes(cfg, plens):
     return cfg.weight_bytes() + kv + emb + feats
 
 
+def gemm_source_sha1():
+    import hashlib
+    h = hashlib.sha1()
+    for f in ("fe_gemm.hip", "fe_internal.h"):
+        with open(os.path.join(ROOT, "paper_2509_20416_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def read_traffic():
     """HBM bytes per gate/up launch from the committed rocprofv3 counter summary
-    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel factor), if present."""
+    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel factor); None when the
+    summary is missing or was taken from other kernel sources than these."""
+    vals = {}
     try:
         for line in open(TRAFFIC_FILE):
-            if line.startswith("traffic_bytes_per_launch:"):
-                return float(line.split(":", 1)[1])
+            if ":" in line and not line.startswith(("#", " ", "|")):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
     except OSError:
-        pass
-    return None
+        return None
+    if vals.get("source_sha1") != gemm_source_sha1():
+        log("traffic summary was taken from other GEMM sources; reporting traffic null")
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(cfg, w, inp, budget_s):
@@ -88,6 +106,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--prof-repeats", type=int, default=8)
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: a few eager passes, one round of the gate/up "
+                         "launches, then a plain 512 MiB device copy as the counter scale "
+                         "reference; prints what ran, no benchmark line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the drafter pass runs on a single MI355X "
@@ -105,7 +127,8 @@ def main():
     inp = make_inputs(cfg, args.seed)
     log(f"{cfg.name}: inputs generated in {time.time() - t0:.1f}s")
     plens = np.asarray(inp.prefix_lens)
-    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=not args.eager)
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()),
+                 graph=not (args.eager or args.traffic_probe))
     di = dr.upload_inputs(inp)
     out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
     tree = dr.alloc_tree(cfg.batch, cfg.topk)
@@ -114,6 +137,23 @@ def main():
         dr.forward(di, out=out)
         dr.build_tree(di, out["topk_ids"], out=tree)
 
+    if args.traffic_probe:
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        _, per_pass = fe.fe_time_stage(dr.handle, fe.FE_STAGE["gateup"], 1, dr.stream())
+        copy_bytes = 512 << 20
+        src = torch.ones(copy_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": cfg.name, "gateup_launches": per_pass,
+                          "gateup_algorithmic_bytes": gateup_bytes(cfg, cfg.batch),
+                          "copy_bytes_read": copy_bytes, "copy_bytes_written": copy_bytes}),
+              flush=True)
+        dr.close()
+        return
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()

@@ -171,6 +171,15 @@ fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk, const int32_
  * arguments and replayed while they stay the same. */
 fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
 
+/* Attention work split: each attention workgroup covers this many 128-key
+ * chunks of one sequence's prefix (0 = automatic, the default, which sizes the
+ * grid to keep every compute unit streaming).  A sequence longer than one
+ * workgroup's span leaves partial softmax states that a second launch merges;
+ * every split gives the same result up to rounding.  Meant for tuning and
+ * testing.  Errors: FE_E_INVALID for a NULL handle or a value outside
+ * [0, 65536]. */
+fe_status fe_set_attention_split(fe_drafter *h, int32_t chunks_per_workgroup);
+
 /* Stages of the pass whose kernel launches can be timed with HIP events. */
 typedef enum {
   FE_STAGE_FUSE = 0,     /* g_t = FC(l, m, h) and the embedding gather (one launch) */

@@ -8,52 +8,91 @@
 //
 //  * One workgroup (4 waves) per (sequence, KV head, head group, chunk of
 //    kAttnChunk prefix keys); the GH query heads sharing a KV head are done
-//    together so every K/V byte is read once.  Each wave takes 32 keys: 8 lanes
-//    per key row (D/8 dims each, 16-byte loads, the row contiguous), 8 keys
-//    per load step, K and V loads issued together.
-//  * Dot products reduce over the 8 lanes of a key with xor-shuffles; the
-//    softmax max/sum and the value sums reduce across key slots with
-//    xor-shuffles, then across the 4 waves in LDS.  Each chunk leaves
-//    (sum, max, o[D]) per head in the workspace.
-//  * Split-K completion: every chunk workgroup bumps a counter after a
-//    release fence; the last one (acquire fence) merges all chunk partials and
-//    the nctx cascade keys, held in fp32, in a fixed order, writes the output
-//    row and resets the counter for the next launch.  A sequence with an empty
-//    prefix still runs chunk 0, which carries no keys.
+//    together so every K/V byte is read once.  Each wave takes 32 keys.  A key
+//    row is split in 16-byte pieces over RL = D*sizeof(T)/16 lanes, so one
+//    load instruction covers 64/RL whole rows; K and V are loaded together.
+//  * A score is reduced over its RL lanes with DPP row operations and leaves
+//    every lane of the row with the same value, which is exactly what the
+//    value pass needs: each lane accumulates p*V for its own dims and key
+//    rows, so the value sums need no cross-lane traffic.  Row-group maxima use
+//    gfx950's permlane swaps.  The per-(wave, row group) sums meet in LDS.
+//  * Chunk 0 also takes the nctx cascade keys (fp32, one extra load per lane).
+//  * Each chunk leaves o[D] (scaled to the chunk max) and (max, sum) per head
+//    in the workspace; every chunk workgroup bumps a counter after a release
+//    fence and the last one (acquire fence) merges the chunks in a fixed
+//    order, writes the output row and resets the counter for the next launch.
+//    A sequence with an empty prefix still runs chunk 0 for its cascade keys.
 #include "fe_internal.h"
 
 namespace fe {
 
-template <typename T, int D> struct KvRow {
-  static constexpr int DL = D / 8;                      // dims per lane
-  static constexpr int NV = DL * sizeof(T) / 16;        // 16-byte loads per lane
-  uint32_t w[NV * 4];  // plain words: element access by index never touches a vector
-  __device__ __forceinline__ void load(const T *p) {
-    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const u32x4 v = q[i];
-      w[4 * i + 0] = v.x;
-      w[4 * i + 1] = v.y;
-      w[4 * i + 2] = v.z;
-      w[4 * i + 3] = v.w;
-    }
-  }
-  __device__ __forceinline__ float at(int e) const {
-    if constexpr (sizeof(T) == 2) {
-      const uint32_t u = w[e / 2];
-      return (e & 1) ? __uint_as_float(u & 0xffff0000u) : __uint_as_float(u << 16);
-    } else {
-      return __uint_as_float(w[e]);
-    }
-  }
-};
-
 constexpr int kWaveKeys = kAttnChunk / 4;   // keys per wave
-constexpr int kSteps = kWaveKeys / 8;       // load steps per wave
 
 __device__ __forceinline__ float scaled_exp(float m, float M) {
   return m == -INFINITY ? 0.f : expf(m - M);
+}
+
+// ---- cross-lane reductions in registers ----------------------------------------
+// DPP controls: quad_perm [1,0,3,2] (lane^1), [2,3,0,1] (lane^2), row_half_mirror
+// (the other quad of an 8-lane half once quads are uniform), row_ror:8 (lane^8).
+template <int CTRL> __device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+// permlane16_swap / permlane32_swap of a register with itself return, in every
+// lane, the pair {x[lane], x[lane ^ 16]} (resp. lane ^ 32) in some order.
+__device__ __forceinline__ float xor16_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor16_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// Sum over aligned groups of RL lanes (8, 16, 32), result in every lane of the
+// group; each step adds two equal-valued halves in either order, so all lanes
+// of a group hold bit-identical sums.
+template <int RL> __device__ __forceinline__ float group_sum(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x141>(x);
+  if constexpr (RL >= 16) x += dpp_f<0x128>(x);
+  if constexpr (RL >= 32) x = xor16_sum(x);
+  if constexpr (RL >= 64) x = xor32_sum(x);
+  return x;
+}
+template <int RL> __device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, dpp_f<0xB1>(x));
+  x = fmaxf(x, dpp_f<0x4E>(x));
+  x = fmaxf(x, dpp_f<0x141>(x));
+  if constexpr (RL >= 16) x = fmaxf(x, dpp_f<0x128>(x));
+  if constexpr (RL >= 32) x = xor16_max(x);
+  if constexpr (RL >= 64) x = xor32_max(x);
+  return x;
+}
+// Max over the row groups of a wave, given values uniform within RL-lane groups.
+template <int RL> __device__ __forceinline__ float across_groups_max(float x) {
+  if constexpr (RL <= 8) x = fmaxf(x, dpp_f<0x128>(x));
+  if constexpr (RL <= 16) x = xor16_max(x);
+  if constexpr (RL <= 32) x = xor32_max(x);
+  return x;
+}
+
+// element e of a 16-byte piece holding 16/sizeof(T) values
+template <typename T> __device__ __forceinline__ float piece_at(const u32x4 &w, int e) {
+  const uint32_t u = (e >> (sizeof(T) == 2 ? 1 : 0)) == 0   ? w.x
+                     : (e >> (sizeof(T) == 2 ? 1 : 0)) == 1 ? w.y
+                     : (e >> (sizeof(T) == 2 ? 1 : 0)) == 2 ? w.z
+                                                            : w.w;
+  if constexpr (sizeof(T) == 2) return (e & 1) ? __uint_as_float(u & 0xffff0000u) : __uint_as_float(u << 16);
+  else return __uint_as_float(u);
 }
 
 template <typename T, int D, int GH>
@@ -63,231 +102,566 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
                                               const float *__restrict__ knew,
                                               const float *__restrict__ vnew, int nctx,
                                               float *__restrict__ part, int nch, int nch_ld,
-                                              int *__restrict__ counters, T *__restrict__ out,
-                                              int Hq, int Hkv) {
-  constexpr int DL = D / 8;
-  __shared__ float s_m[4][GH], s_l[4][GH];
-  __shared__ float s_o[4][GH][D];
-  __shared__ float s_sc[GH][kMaxLayers];
-  __shared__ int s_last;
+                                              int cpw,
+                                              T *__restrict__ out, int Hq, int Hkv) {
+  constexpr int RL = D * (int)sizeof(T) / 16;  // lanes per key row
+  constexpr int KPL = 64 / RL;                  // key rows per load instruction
+  constexpr int DPL = 16 / (int)sizeof(T);      // dims per lane
+  constexpr int NLD = kWaveKeys / KPL;          // K (and V) loads per lane per sub-chunk
+  constexpr int CW = DPL / 4;                   // fp32 16-byte pieces per lane of a cascade row
+  constexpr int NCX = (kMaxLayers + 4 * KPL - 1) / (4 * KPL);  // cascade rows per lane (chunk 0)
+  __shared__ float s_o[4][KPL][GH][D];
+  __shared__ float s_l[4][KPL][GH];
+  __shared__ float s_m[4][GH];
 
   const int G = Hq / Hkv, ngrp = G / GH;
   const int ch = blockIdx.x, c = blockIdx.y / ngrp, hg = blockIdx.y % ngrp, b = blockIdx.z;
   const int start = cu[b], P = cu[b + 1] - start;
-  const int nv = max(1, min((P + kAttnChunk - 1) / kAttnChunk, nch));
+  const int span = kAttnChunk * cpw;  // prefix keys per workgroup
+  const int nv = max(1, min((P + span - 1) / span, nch));
   if (ch >= nv) return;  // chunk beyond this sequence's prefix
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, slot = lane >> 3, dp = lane & 7;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, kg = lane / RL, dl = lane % RL;
   const int h0 = c * G + hg * GH;
   const float scale = rsqrtf((float)D);
-  const int key0 = ch * kAttnChunk + wave * kWaveKeys;
+  const int base = ch * span;
+  // sub-chunks of kAttnChunk keys this workgroup visits (0 for an empty prefix)
+  const int nsc = P > 0 ? min(cpw, (P - base + kAttnChunk - 1) / kAttnChunk) : 0;
+  const int lkey = wave * kWaveKeys + kg;  // this lane's first key within a sub-chunk; step KPL
+  const bool casc = ch == 0;
+  float *part_o = part;
+  float *part_ml = part + (size_t)gridDim.z * Hq * nch_ld * D;
 
-  // ---- this wave's 32 keys -------------------------------------------------
-  const size_t rowstride = (size_t)Hkv * D;
-  const T *kbase = Kc + ((size_t)start * Hkv + c) * D + dp * DL;
-  const T *vbase = Vc + ((size_t)start * Hkv + c) * D + dp * DL;
-  // Rows are loaded unconditionally at clamped keys (missing keys get weight 0
-  // below); an empty prefix reads nothing.
-  KvRow<T, D> kr[kSteps], vr[kSteps];
-  if (P > 0) {
+  const size_t rs = (size_t)Hkv * D;
+  const T *kb = Kc + ((size_t)start * Hkv + c) * D + dl * DPL;
+  const T *vb = Vc + ((size_t)start * Hkv + c) * D + dl * DPL;
+  // rows of sub-chunk `sc` at clamped in-bounds keys (masked when scored)
+  auto load_rows = [&](int sc, u32x4 (&kr)[NLD], u32x4 (&vr)[NLD]) {
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      const int key = min(key0 + st * 8 + slot, P - 1);
-      kr[st].load(kbase + (size_t)key * rowstride);
-      vr[st].load(vbase + (size_t)key * rowstride);
+    for (int t = 0; t < NLD; ++t) {
+      const size_t key = (size_t)min(base + sc * kAttnChunk + lkey + t * KPL, P - 1);
+      kr[t] = *reinterpret_cast<const u32x4 *>(kb + key * rs);
+      vr[t] = *reinterpret_cast<const u32x4 *>(vb + key * rs);
     }
-  }
-  float qv[GH][DL];
-#pragma unroll
-  for (int gh = 0; gh < GH; ++gh)
-#pragma unroll
-    for (int e = 0; e < DL; ++e) qv[gh][e] = q[((size_t)b * Hq + h0 + gh) * D + dp * DL + e];
-  // cascade keys of head group member `wave` (waves < GH): loaded now, scored
-  // below, so that the final merge needs no further inputs but the partials
-  constexpr int DPL = D / 64;
-  float qd[DPL], kd[kMaxLayers][DPL];
-  if (wave < GH) {
-#pragma unroll
-    for (int t = 0; t < DPL; ++t) qd[t] = q[((size_t)b * Hq + h0 + wave) * D + lane * DPL + t];
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j)
-#pragma unroll
-      for (int t = 0; t < DPL; ++t)
-        kd[j][t] = knew[(((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + lane * DPL + t];
-  }
-
-  float s[kSteps][GH];
-#pragma unroll
-  for (int st = 0; st < kSteps; ++st)
-#pragma unroll
-    for (int gh = 0; gh < GH; ++gh) {
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < DL; ++e) acc += qv[gh][e] * kr[st].at(e);
-      acc += __shfl_xor(acc, 1);
-      acc += __shfl_xor(acc, 2);
-      acc += __shfl_xor(acc, 4);
-      const int key = key0 + st * 8 + slot;
-      s[st][gh] = key < P ? acc * scale : -INFINITY;
-    }
-  float mx[GH], l[GH], o[GH][DL];
+  };
+  u32x4 kr[NLD], vr[NLD];
+  if (nsc > 0) load_rows(0, kr, vr);
+  float qv[GH][DPL];
 #pragma unroll
   for (int gh = 0; gh < GH; ++gh) {
-    float m = -INFINITY;
+    const f32x4 *qp = reinterpret_cast<const f32x4 *>(q + ((size_t)b * Hq + h0 + gh) * D + dl * DPL);
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st) m = fmaxf(m, s[st][gh]);
-    m = fmaxf(m, __shfl_xor(m, 8));
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    mx[gh] = m;
-    float sum = 0.f;
-#pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      const float p = scaled_exp(s[st][gh], m);
-      s[st][gh] = p;
-      sum += p;
+    for (int w = 0; w < DPL / 4; ++w) {
+      const f32x4 v = qp[w];
+      qv[gh][4 * w + 0] = v.x;
+      qv[gh][4 * w + 1] = v.y;
+      qv[gh][4 * w + 2] = v.z;
+      qv[gh][4 * w + 3] = v.w;
     }
-    sum += __shfl_xor(sum, 8);
-    sum += __shfl_xor(sum, 16);
-    sum += __shfl_xor(sum, 32);
-    l[gh] = sum;
-#pragma unroll
-    for (int e = 0; e < DL; ++e) o[gh][e] = 0.f;
   }
-  if (P > 0) {
+
+  // running softmax state of this lane's row group, per head: m (uniform over
+  // the wave), l and o (the group's own keys)
+  float m[GH], l[GH], o[GH][DPL];
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st)
+  for (int gh = 0; gh < GH; ++gh) {
+    m[gh] = -INFINITY;
+    l[gh] = 0.f;
 #pragma unroll
-      for (int e = 0; e < DL; ++e) {
-        const float ve = vr[st].at(e);
-#pragma unroll
-        for (int gh = 0; gh < GH; ++gh) o[gh][e] += s[st][gh] * ve;  // weight 0 past P
-      }
+    for (int e = 0; e < DPL; ++e) o[gh][e] = 0.f;
   }
-#pragma unroll
-  for (int gh = 0; gh < GH; ++gh)
-#pragma unroll
-    for (int e = 0; e < DL; ++e) {
-      float v = o[gh][e];
-      v += __shfl_xor(v, 8);
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      o[gh][e] = v;
-    }
-  if (slot == 0) {
+  // online update with NS scored keys: s[t][gh] (masked -inf), value dims val(t, e)
+  auto absorb = [&](auto &s, auto val) {
+    constexpr int NS = sizeof(s) / sizeof(s[0]);
 #pragma unroll
     for (int gh = 0; gh < GH; ++gh) {
+      float mx = m[gh];
 #pragma unroll
-      for (int e = 0; e < DL; ++e) s_o[wave][gh][dp * DL + e] = o[gh][e];
-      if (dp == 0) {
-        s_m[wave][gh] = mx[gh];
-        s_l[wave][gh] = l[gh];
+      for (int t = 0; t < NS; ++t) mx = fmaxf(mx, s[t][gh]);
+      mx = across_groups_max<RL>(mx);
+      const float alpha = scaled_exp(m[gh], mx);
+      m[gh] = mx;
+      float sum = l[gh] * alpha;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) o[gh][e] *= alpha;
+#pragma unroll
+      for (int t = 0; t < NS; ++t) {
+        s[t][gh] = scaled_exp(s[t][gh], mx);
+        sum += s[t][gh];
+      }
+      l[gh] = sum;
+    }
+#pragma unroll
+    for (int t = 0; t < NS; ++t)
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) {
+        const float ve = val(t, e);
+#pragma unroll
+        for (int gh = 0; gh < GH; ++gh) o[gh][e] += s[t][gh] * ve;  // weight 0 when masked
+      }
+  };
+
+  // ---- chunk 0: the cascade keys (fp32) --------------------------------------
+  if (casc) {
+    f32x4 kx[NCX][CW], vx[NCX][CW];
+#pragma unroll
+    for (int t = 0; t < NCX; ++t) {
+      const int j = min((t * 4 + wave) * KPL + kg, nctx - 1);
+      const size_t off = (((size_t)b * nctx + j) * Hkv + c) * D + dl * DPL;
+#pragma unroll
+      for (int w = 0; w < CW; ++w) {
+        kx[t][w] = reinterpret_cast<const f32x4 *>(knew + off)[w];
+        vx[t][w] = reinterpret_cast<const f32x4 *>(vnew + off)[w];
       }
     }
+    float sx[NCX][GH];
+#pragma unroll
+    for (int t = 0; t < NCX; ++t)
+#pragma unroll
+      for (int gh = 0; gh < GH; ++gh) {
+        float acc = 0.f;
+#pragma unroll
+        for (int w = 0; w < CW; ++w)
+          acc += qv[gh][4 * w] * kx[t][w].x + qv[gh][4 * w + 1] * kx[t][w].y +
+                 qv[gh][4 * w + 2] * kx[t][w].z + qv[gh][4 * w + 3] * kx[t][w].w;
+        acc = group_sum<RL>(acc);
+        sx[t][gh] = (t * 4 + wave) * KPL + kg < nctx ? acc * scale : -INFINITY;
+      }
+    absorb(sx, [&](int t, int e) {
+      const f32x4 &v = vx[t][e >> 2];
+      return (e & 3) == 0 ? v.x : (e & 3) == 1 ? v.y : (e & 3) == 2 ? v.z : v.w;
+    });
   }
-  if (wave < GH) {  // scores of the cascade keys for head h0 + wave
+
+  // ---- prefix keys, sub-chunk by sub-chunk (next rows in flight) -------------
+  // The prefetch is unconditional (the last one re-reads clamped in-bounds
+  // rows): under a branch the compiler would wait for it before the compute.
+  for (int sc = 0; sc < nsc; ++sc) {
+    u32x4 kn[NLD], vn[NLD];
+    load_rows(sc + 1, kn, vn);
+    const int key0 = base + sc * kAttnChunk + lkey;
+    float s[NLD][GH];
 #pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) {
-      float v = 0.f;
+    for (int t = 0; t < NLD; ++t)
 #pragma unroll
-      for (int t = 0; t < DPL; ++t) v += qd[t] * kd[j][t];
+      for (int gh = 0; gh < GH; ++gh) {
+        float acc = 0.f;
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-      if (lane == 0) s_sc[wave][j] = j < nctx ? v * scale : -INFINITY;
+        for (int e = 0; e < DPL; ++e) acc += qv[gh][e] * piece_at<T>(kr[t], e);
+        acc = group_sum<RL>(acc);
+        s[t][gh] = key0 + t * KPL < P ? acc * scale : -INFINITY;
+      }
+    absorb(s, [&](int t, int e) { return piece_at<T>(vr[t], e); });
+#pragma unroll
+    for (int t = 0; t < NLD; ++t) {
+      kr[t] = kn[t];
+      vr[t] = vn[t];
     }
+  }
+
+#pragma unroll
+  for (int gh = 0; gh < GH; ++gh) {
+#pragma unroll
+    for (int w = 0; w < DPL / 4; ++w)
+      *reinterpret_cast<f32x4 *>(&s_o[wave][kg][gh][dl * DPL + 4 * w]) =
+          f32x4{o[gh][4 * w], o[gh][4 * w + 1], o[gh][4 * w + 2], o[gh][4 * w + 3]};
+    if (dl == 0) s_l[wave][kg][gh] = l[gh];
+    if (lane == 0) s_m[wave][gh] = m[gh];
   }
   __syncthreads();
 
-  // ---- merge the 4 waves into this chunk's partial: [o[D], max, sum] --------
-  for (int idx = tid; idx < GH * (D + 2); idx += 256) {
-    const int gh = idx / (D + 2), e = idx % (D + 2);
+  // ---- this workgroup's result: the output row when it holds the whole
+  //      sequence, else its partial (o scaled to its max, (max, sum))
+  const bool whole = nv == 1;
+  for (int idx = tid; idx < GH * D; idx += 256) {
+    const int gh = idx / D, e = idx % D;
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][gh]);
-    float acc = 0.f;
-    if (e == D) {
-      acc = M;
-    } else {
+    float acc = 0.f, L = 0.f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w)
-        acc += scaled_exp(s_m[w][gh], M) * (e < D ? s_o[w][gh][e] : s_l[w][gh]);
+    for (int w = 0; w < 4; ++w) {
+      float g = 0.f, gl = 0.f;
+#pragma unroll
+      for (int k = 0; k < KPL; ++k) {
+        g += s_o[w][k][gh][e];
+        gl += s_l[w][k][gh];
+      }
+      const float sw = scaled_exp(s_m[w][gh], M);
+      acc += sw * g;
+      L += sw * gl;
     }
-    part[(((size_t)b * Hq + h0 + gh) * nch_ld + ch) * (D + 2) + e] = acc;
+    if (whole) {
+      out[(size_t)b * Hq * D + (size_t)(h0 + gh) * D + e] = Elt<T>::from_f(acc / L);
+    } else {
+      part_o[(((size_t)b * Hq + h0 + gh) * nch_ld + ch) * D + e] = acc;
+      if (e == 0) {
+        float *ml = part_ml + (((size_t)b * Hq + h0 + gh) * nch_ld + ch) * 2;
+        ml[0] = M;
+        ml[1] = L;
+      }
+    }
   }
+}
 
-  // ---- split-K completion ---------------------------------------------------
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int old = atomicAdd(&counters[((size_t)b * Hkv + c) * ngrp + hg], 1);
-    s_last = (old == nv - 1);
+
+// ---- bf16 caches: both contractions on the matrix cores -------------------------
+//
+// Per wave and sub-chunk: 32 keys as two 16-key tiles.  QK^T runs with the keys
+// as MFMA rows (A = 16-byte pieces of K rows, straight from HBM) and the GH
+// query heads as columns (B = q, zero-padded to 16 heads).  q is split into a
+// bf16 high part and a bf16 remainder, two MFMAs each, which keeps the scores
+// at fp32-level accuracy against the bf16 keys.  q is pre-scaled by
+// log2(e)/sqrt(D), so scores are in log2 units and every exponential is one
+// v_exp_f32.  The result leaves each lane with 8 scores of one head, which is
+// exactly the B operand of the value product O^T = V^T P^T (keys as the
+// contraction index, in the order the score tiles produced them), so the
+// probabilities never move between lanes; V goes through LDS (padded rows,
+// conflict-free transposed 16-bit reads) to form the A operand.  The
+// probabilities enter the product as bf16 and the running sum adds the same
+// rounded values, so the output is an exact weighted mean of V.
+// The nctx cascade keys (fp32) are done on the vector ALU by chunk 0 and enter
+// the workgroup merge as a fifth partial.
+__device__ __forceinline__ float sexp2(float m, float M) {
+  return m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+}
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+template <int D, int GH>
+__global__ __launch_bounds__(256) void k_attn_mma(const bf16_t *__restrict__ Kc,
+                                                  const bf16_t *__restrict__ Vc,
+                                                  const int32_t *__restrict__ cu,
+                                                  const float *__restrict__ q,
+                                                  const float *__restrict__ knew,
+                                                  const float *__restrict__ vnew, int nctx,
+                                                  float *__restrict__ part, int nch, int nch_ld,
+                                                  int cpw, bf16_t *__restrict__ out, int Hq,
+                                                  int Hkv) {
+  constexpr int NKC = D / 32;         // 32-dim steps of QK^T
+  constexpr int NDT = D / 16;         // 16-dim tiles of the value product
+  constexpr int VPR = D / 8;          // 16-byte pieces per V row
+  constexpr int NVL = 32 * VPR / 64;  // V pieces per lane per sub-chunk
+  constexpr int RSB = 2 * D + 16;     // LDS bytes per staged V row
+  constexpr int EPL = D / 64;         // dims per lane in the cascade-key step
+  __shared__ __align__(16) unsigned char s_v[4][32 * RSB];
+  __shared__ float s_o[5][GH][D];
+  __shared__ float s_l[5][GH], s_m[5][GH];
+
+  const int G = Hq / Hkv, ngrp = G / GH;
+  const int ch = blockIdx.x, c = blockIdx.y / ngrp, hg = blockIdx.y % ngrp, b = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int h0 = c * G + hg * GH;
+  const float qscale = 1.4426950408889634f * rsqrtf((float)D);
+  const bool casc = ch == 0;
+  constexpr int GHW = (GH + 3) / 4;  // cascade-step heads per wave
+
+  // Loads that do not depend on the prefix bounds go first, so their latency
+  // overlaps the read of cu: q (B-operand layout), and in chunk 0 the cascade
+  // rows and this wave's cascade-step q.
+  f32x4 qraw[NKC][2];
+  {
+    const float *qp = q + ((size_t)b * Hq + h0 + min(r, GH - 1)) * D;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      qraw[kc][0] = *reinterpret_cast<const f32x4 *>(qp + 32 * kc + 8 * g);
+      qraw[kc][1] = *reinterpret_cast<const f32x4 *>(qp + 32 * kc + 8 * g + 4);
+    }
   }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  // ---- last chunk workgroup: merge every chunk and the cascade keys ---------
-  // Thread (gh, e) reads what it needs in one round trip (8 chunks per group,
-  // clamped in-bounds indices, unused values masked) and merges with a running
-  // max in a fixed order.
-  for (int idx = tid; idx < GH * D; idx += 256) {
-    const int gh = idx / D, e = idx % D, h = h0 + gh;
-    const float *pp = part + ((size_t)b * Hq + h) * nch_ld * (D + 2);
-    float vv[kMaxLayers];
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j)
-      vv[j] = vnew[(((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + e];
-    float M = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) M = fmaxf(M, s_sc[gh][j]);
-    float L = 0.f, acc = 0.f;
+  float kj[kMaxLayers][EPL], vj[kMaxLayers][EPL], qc[GHW][EPL];
+  if (casc) {
 #pragma unroll
     for (int j = 0; j < kMaxLayers; ++j) {
-      const float w = scaled_exp(s_sc[gh][j], M);
-      L += w;
-      acc += w * vv[j];
-    }
-    for (int k0 = 0; k0 < nv; k0 += 8) {
-      float ov[8], mv[8], lv[8];
+      const size_t off = (((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + lane * EPL;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float *pk = pp + (size_t)min(k0 + u, nv - 1) * (D + 2);
-        ov[u] = pk[e];
-        mv[u] = pk[D];
-        lv[u] = pk[D + 1];
+      for (int e = 0; e < EPL; ++e) {
+        kj[j][e] = knew[off + e];
+        vj[j][e] = vnew[off + e];
       }
-      float Mn = M;
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (k0 + u < nv) Mn = fmaxf(Mn, mv[u]);
-      const float rs = scaled_exp(M, Mn);
-      L *= rs;
-      acc *= rs;
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (k0 + u < nv) {
-          const float w = scaled_exp(mv[u], Mn);
-          L += lv[u] * w;
-          acc += ov[u] * w;
-        }
-      M = Mn;
     }
-    out[(size_t)b * Hq * D + (size_t)h * D + e] = Elt<T>::from_f(acc / L);
+#pragma unroll
+    for (int i = 0; i < GHW; ++i) {
+      const int gh = min(wave + 4 * i, GH - 1);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) qc[i][e] = q[((size_t)b * Hq + h0 + gh) * D + lane * EPL + e];
+    }
   }
-  if (tid == 0) counters[((size_t)b * Hkv + c) * ngrp + hg] = 0;
+
+  const int start = cu[b], P = cu[b + 1] - start;
+  const int span = kAttnChunk * cpw;
+  const int nv = max(1, min((P + span - 1) / span, nch));
+  if (ch >= nv) return;  // chunk beyond this sequence's prefix
+  const int base = ch * span;
+  const int nsc = P > 0 ? min(cpw, (P - base + kAttnChunk - 1) / kAttnChunk) : 0;
+  float *part_o = part;
+  float *part_ml = part + (size_t)gridDim.z * Hq * nch_ld * D;
+
+  const size_t rs = (size_t)Hkv * D;
+  const bf16_t *kb = Kc + ((size_t)start * Hkv + c) * D;
+  const bf16_t *vb = Vc + ((size_t)start * Hkv + c) * D;
+  // sub-chunk sc: K pieces (key 16t + r of the wave's 32, dims 32kc + 8g) and V
+  // pieces (row p / VPR, piece p % VPR for p = lane + 64i), clamped in bounds
+  auto load_rows = [&](int sc, u32x4 (&ka)[2][NKC], u32x4 (&vv)[NVL]) {
+    const int k0 = base + sc * kAttnChunk + wave * kWaveKeys;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const size_t key = (size_t)min(k0 + 16 * t + r, P - 1);
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc)
+        ka[t][kc] = *reinterpret_cast<const u32x4 *>(kb + key * rs + 32 * kc + 8 * g);
+    }
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int pc = lane + 64 * i;
+      const size_t key = (size_t)min(k0 + pc / VPR, P - 1);
+      vv[i] = *reinterpret_cast<const u32x4 *>(vb + key * rs + 8 * (pc % VPR));
+    }
+  };
+  u32x4 ka[2][NKC], vv[NVL];
+  if (nsc > 0) load_rows(0, ka, vv);
+
+  // ---- chunk 0: the cascade keys, fp32 on the vector ALU -> partial slot 4 ----
+  if (casc) {
+#pragma unroll
+    for (int i = 0; i < GHW; ++i) {
+      const int gh = wave + 4 * i;
+      if (gh >= GH) break;
+      float sj[kMaxLayers];
+#pragma unroll
+      for (int j = 0; j < kMaxLayers; ++j) {
+        float d = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) d += qc[i][e] * qscale * kj[j][e];
+        d = group_sum<64>(d);
+        sj[j] = j < nctx ? d : -INFINITY;
+      }
+      float m = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < kMaxLayers; ++j) m = fmaxf(m, sj[j]);
+      float L = 0.f, o[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[e] = 0.f;
+#pragma unroll
+      for (int j = 0; j < kMaxLayers; ++j) {
+        const float pj = sexp2(sj[j], m);
+        L += pj;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[e] += pj * vj[j][e];
+      }
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_o[4][gh][lane * EPL + e] = o[e];
+      if (lane == 0) {
+        s_m[4][gh] = m;
+        s_l[4][gh] = L;
+      }
+    }
+  }
+
+  // q as B operands: column r = head h0 + r (zero for r >= GH), high and low parts
+  u32x4 qh[NKC], ql[NKC];
+#pragma unroll
+  for (int kc = 0; kc < NKC; ++kc) {
+    const float x[8] = {qraw[kc][0].x, qraw[kc][0].y, qraw[kc][0].z, qraw[kc][0].w,
+                        qraw[kc][1].x, qraw[kc][1].y, qraw[kc][1].z, qraw[kc][1].w};
+    uint32_t hw[4], lw[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const float a0 = r < GH ? x[e] * qscale : 0.f, a1 = r < GH ? x[e + 1] * qscale : 0.f;
+      const uint16_t h0b = f2bf(a0), h1b = f2bf(a1);
+      hw[e / 2] = (uint32_t)h0b | ((uint32_t)h1b << 16);
+      lw[e / 2] = pack_bf16(a0 - bf2f(h0b), a1 - bf2f(h1b));
+    }
+    qh[kc] = u32x4{hw[0], hw[1], hw[2], hw[3]};
+    ql[kc] = u32x4{lw[0], lw[1], lw[2], lw[3]};
+  }
+
+  // ---- prefix keys: online softmax over sub-chunks, next rows in flight ----------
+  float m = -INFINITY, l = 0.f;  // head r: running max (uniform over g), this lane's sum
+  f32x4 oacc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) oacc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  unsigned char *sv = s_v[wave];
+  for (int sc = 0; sc < nsc; ++sc) {
+    u32x4 kn[2][NKC], vn[NVL];
+    load_rows(sc + 1, kn, vn);  // unconditional: clamped rows past the end
+    // V rows of this sub-chunk -> LDS (LDS ops of one wave complete in order, so
+    // the previous sub-chunk's reads are done before these writes land)
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int pc = lane + 64 * i;
+      *reinterpret_cast<u32x4 *>(sv + (pc / VPR) * RSB + 16 * (pc % VPR)) = vv[i];
+    }
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[0][kc]),
+                                                   __builtin_bit_cast(bf16x8, qh[kc]), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[1][kc]),
+                                                   __builtin_bit_cast(bf16x8, qh[kc]), s1, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[0][kc]),
+                                                   __builtin_bit_cast(bf16x8, ql[kc]), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[1][kc]),
+                                                   __builtin_bit_cast(bf16x8, ql[kc]), s1, 0, 0, 0);
+    }
+    // lane holds S[key 4g+v (+16 for s1)][head r]; mask keys past P
+    const int kq = base + sc * kAttnChunk + wave * kWaveKeys + 4 * g;
+    float sv8[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      sv8[v] = kq + v < P ? s0[v] : -INFINITY;
+      sv8[4 + v] = kq + 16 + v < P ? s1[v] : -INFINITY;
+    }
+    float mx = m;
+#pragma unroll
+    for (int v = 0; v < 8; ++v) mx = fmaxf(mx, sv8[v]);
+    mx = xor32_max(xor16_max(mx));
+    const float alpha = sexp2(m, mx);
+    m = mx;
+    uint32_t pw[4];
+    float ps = 0.f;
+#pragma unroll
+    for (int v = 0; v < 8; v += 2) {
+      const uint16_t p0 = f2bf(sexp2(sv8[v], mx)), p1 = f2bf(sexp2(sv8[v + 1], mx));
+      ps += bf2f(p0) + bf2f(p1);
+      pw[v / 2] = (uint32_t)p0 | ((uint32_t)p1 << 16);
+    }
+    l = l * alpha + ps;
+    const u32x4 pb = {pw[0], pw[1], pw[2], pw[3]};
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      // A = V^T: dim 16dt + r, keys (4g + j) and (16 + 4g + j), j < 4
+      const unsigned char *col = sv + 2 * (16 * dt + r);
+      uint32_t aw[4];
+#pragma unroll
+      for (int j = 0; j < 4; j += 2) {
+        const uint16_t v0 = *reinterpret_cast<const uint16_t *>(col + (4 * g + j) * RSB);
+        const uint16_t v1 = *reinterpret_cast<const uint16_t *>(col + (4 * g + j + 1) * RSB);
+        const uint16_t v2 = *reinterpret_cast<const uint16_t *>(col + (16 + 4 * g + j) * RSB);
+        const uint16_t v3 = *reinterpret_cast<const uint16_t *>(col + (17 + 4 * g + j) * RSB);
+        aw[j / 2] = (uint32_t)v0 | ((uint32_t)v1 << 16);
+        aw[2 + j / 2] = (uint32_t)v2 | ((uint32_t)v3 << 16);
+      }
+      const u32x4 av = {aw[0], aw[1], aw[2], aw[3]};
+      oacc[dt] *= alpha;
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                         __builtin_bit_cast(bf16x8, pb), oacc[dt],
+                                                         0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc) ka[t][kc] = kn[t][kc];
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) vv[i] = vn[i];
+  }
+  // wave partial: O^T[16dt + 4g + v][head r], max m, sum over the 4 lanes of head r
+  l = xor32_sum(xor16_sum(l));
+  if (r < GH) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) s_o[wave][r][16 * dt + 4 * g + v] = oacc[dt][v];
+    if (g == 0) {
+      s_m[wave][r] = m;
+      s_l[wave][r] = l;
+    }
+  }
+  __syncthreads();
+
+  // ---- this workgroup's result: the output row, or its partial ----------------
+  const bool whole = nv == 1;
+  const int nslot = casc ? 5 : 4;
+  for (int idx = tid; idx < GH * D; idx += 256) {
+    const int gh = idx / D, e = idx % D;
+    float M = -INFINITY;
+    for (int w = 0; w < nslot; ++w) M = fmaxf(M, s_m[w][gh]);
+    float acc = 0.f, L = 0.f;
+    for (int w = 0; w < nslot; ++w) {
+      const float sw = sexp2(s_m[w][gh], M);
+      acc += sw == 0.f ? 0.f : sw * s_o[w][gh][e];
+      L += sw * s_l[w][gh];
+    }
+    if (whole) {
+      out[(size_t)b * Hq * D + (size_t)(h0 + gh) * D + e] = f2bf(acc / L);
+    } else {
+      part_o[(((size_t)b * Hq + h0 + gh) * nch_ld + ch) * D + e] = acc;
+      if (e == 0) {
+        float *ml = part_ml + (((size_t)b * Hq + h0 + gh) * nch_ld + ch) * 2;
+        ml[0] = M;
+        ml[1] = L;
+      }
+    }
+  }
+}
+
+
+// ---- chunk merge (second launch) -------------------------------------------------
+// A sequence whose prefix spans several workgroups leaves one partial per
+// workgroup: o (scaled to that workgroup's max), max and sum per head.  This
+// launch combines them in chunk order, 16 per round trip.  Sequences that fit
+// one workgroup wrote their rows directly and are skipped.  Keeping the merge in
+// its own launch means no workgroup ever waits on another: the kernel boundary
+// publishes the partials once, where per-workgroup device-scope fences would
+// write back the L2 once per workgroup.  LOG2: maxima in log2 units.
+template <typename T, bool LOG2>
+__global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ part, int nch_ld,
+                                                    const int32_t *__restrict__ cu, int span,
+                                                    int nwg, T *__restrict__ out, int Hq, int D) {
+  const int b = blockIdx.y;
+  const int P = cu[b + 1] - cu[b];
+  const int nv = max(1, min((P + span - 1) / span, nwg));
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (nv == 1 || idx >= Hq * D / 2) return;
+  const int h = (2 * idx) / D, e = (2 * idx) % D;
+  const float *po = part + ((size_t)b * Hq + h) * nch_ld * D + e;
+  const float *pml = part + (size_t)gridDim.y * Hq * nch_ld * D + ((size_t)b * Hq + h) * nch_ld * 2;
+  auto ex = [](float m, float M) {
+    return m == -INFINITY ? 0.f : (LOG2 ? __builtin_amdgcn_exp2f(m - M) : expf(m - M));
+  };
+  float M = -INFINITY, L = 0.f, ax = 0.f, ay = 0.f;
+  for (int c0 = 0; c0 < nv; c0 += 16) {
+    float2 ov[16], ml[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int k = min(c0 + u, nv - 1);
+      ov[u] = *reinterpret_cast<const float2 *>(po + (size_t)k * D);
+      ml[u] = *reinterpret_cast<const float2 *>(pml + 2 * k);
+    }
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (c0 + u < nv) Mn = fmaxf(Mn, ml[u].x);
+    const float rr = ex(M, Mn);
+    L *= rr;
+    ax *= rr;
+    ay *= rr;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (c0 + u < nv) {
+        const float w = ex(ml[u].x, Mn);
+        L += w * ml[u].y;
+        ax += w * ov[u].x;
+        ay += w * ov[u].y;
+      }
+    M = Mn;
+  }
+  T *op = out + (size_t)b * Hq * D + (size_t)h * D + e;
+  op[0] = Elt<T>::from_f(ax / L);
+  op[1] = Elt<T>::from_f(ay / L);
 }
 
 template <typename T, int D>
 static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const float *q,
                          const float *knew, const float *vnew, int nctx, float *part, int nch,
-                         int nch_ld, int *counters, void *out, int B, int Hq, int Hkv,
+                         int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
                          hipStream_t s) {
   const int G = Hq / Hkv;
   const int GH = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
-  const int nchl = nch < 1 ? 1 : nch;
-  const dim3 grid(nchl, Hkv * (G / GH), B);
+  const int nwg = nch < 1 ? 1 : (nch + cpw - 1) / cpw;
+  const dim3 grid(nwg, Hkv * (G / GH), B);
 #define FE_ATTN(GHV)                                                                            \
   hipLaunchKernelGGL((k_attn<T, D, GHV>), grid, dim3(256), 0, s, (const T *)K, (const T *)V, cu, \
-                     q, knew, vnew, nctx, part, nchl, nch_ld, counters, (T *)out, Hq, Hkv)
+                     q, knew, vnew, nctx, part, nwg, nch_ld, cpw, (T *)out, Hq, Hkv)
   if (GH == 4) FE_ATTN(4);
   else if (GH == 2) FE_ATTN(2);
   else FE_ATTN(1);
@@ -295,20 +669,68 @@ static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const 
   return hipGetLastError();
 }
 
+template <int D>
+static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, const float *q,
+                             const float *knew, const float *vnew, int nctx, float *part, int nch,
+                             int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
+                             hipStream_t s) {
+  const int G = Hq / Hkv;
+  const int GH = G % 16 == 0 ? 16 : G % 8 == 0 ? 8 : G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1;
+  const int nwg = nch < 1 ? 1 : (nch + cpw - 1) / cpw;
+  const dim3 grid(nwg, Hkv * (G / GH), B);
+#define FE_ATTN(GHV)                                                                             \
+  hipLaunchKernelGGL((k_attn_mma<D, GHV>), grid, dim3(256), 0, s, (const bf16_t *)K,             \
+                     (const bf16_t *)V, cu, q, knew, vnew, nctx, part, nwg, nch_ld, cpw, \
+                     (bf16_t *)out, Hq, Hkv)
+  switch (GH) {
+    case 16: FE_ATTN(16); break;
+    case 8: FE_ATTN(8); break;
+    case 4: FE_ATTN(4); break;
+    case 2: FE_ATTN(2); break;
+    default: FE_ATTN(1); break;
+  }
+#undef FE_ATTN
+  return hipGetLastError();
+}
+
+// Enough workgroups to keep every CU streaming (about one each) and no more:
+// a sequence split over more workgroups only adds partials to merge.
+int attention_cpw(int B, int Hkv, int ngroups, int nch) {
+  constexpr long kTargetWorkgroups = 256;
+  const long cols = (long)B * Hkv * ngroups;
+  long cpw = (cols * nch + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  if (cpw > nch) cpw = nch;
+  return cpw < 1 ? 1 : (int)cpw;
+}
+
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
                      const float *knew, const float *vnew, int nctx, float *part, int nch,
-                     int nch_ld, int *counters, void *out, int B, int Hq, int Hkv, int D,
+                     int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int D,
                      hipStream_t s) {
   if (B <= 0) return hipSuccess;
+  if (cpw < 1) cpw = 1;
+  hipError_t e;
   if (dt)
-    return D == 128 ? attn_t<bf16_t, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
-                                          counters, out, B, Hq, Hkv, s)
-                    : attn_t<bf16_t, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
-                                         counters, out, B, Hq, Hkv, s);
-  return D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld,
-                                       counters, out, B, Hq, Hkv, s)
-                  : attn_t<float, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, counters,
-                                      out, B, Hq, Hkv, s);
+    e = D == 128 ? attn_mma_t<128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
+                                   Hq, Hkv, s)
+                 : attn_mma_t<64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
+                                  Hq, Hkv, s);
+  else
+    e = D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
+                                      B, Hq, Hkv, s)
+                 : attn_t<float, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
+                                     B, Hq, Hkv, s);
+  if (e != hipSuccess) return e;
+  const int nwg = nch < 1 ? 1 : (nch + cpw - 1) / cpw;
+  if (nwg == 1) return hipSuccess;  // every sequence fits one workgroup
+  const dim3 grid((Hq * D / 2 + 255) / 256, B);
+  if (dt)
+    hipLaunchKernelGGL((k_attn_merge<bf16_t, true>), grid, dim3(256), 0, s, part, nch_ld, cu,
+                       kAttnChunk * cpw, nwg, (bf16_t *)out, Hq, D);
+  else
+    hipLaunchKernelGGL((k_attn_merge<float, false>), grid, dim3(256), 0, s, part, nch_ld, cu,
+                       kAttnChunk * cpw, nwg, (float *)out, Hq, D);
+  return hipGetLastError();
 }
 
 }  // namespace fe

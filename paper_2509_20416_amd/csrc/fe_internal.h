@@ -166,19 +166,20 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // Attention of the query rows q [B, Hq, D] over the prefix cache (chunks
 // 0..nch-1 of kAttnChunk keys; keys beyond are not read) and the nctx cascade
 // keys/values knew/vnew [B, nctx, Hkv, D] -> out [B, Hq*D] (storage type).
-// part [B, Hq, nch_ld, D+2] holds chunk partials; counters [B*Hq] must be zero
-// before the first launch and are left zero after each launch.
+// Each workgroup covers cpw chunks of one sequence; part (B*Hq*nch_ld*(D+2)
+// floats, nch_ld >= ceil(nch / cpw)) holds the partials of sequences that span
+// several workgroups, merged by a second launch.
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
                      const float *q, const float *knew, const float *vnew, int nctx,
-                     float *part, int nch, int nch_ld, int *counters, void *out, int B, int Hq,
+                     float *part, int nch, int nch_ld, int cpw, void *out, int B, int Hq,
                      int Hkv, int D, hipStream_t s);
+// 128-key sub-chunks per attention workgroup for a launch of B sequences over
+// nch = ceil(max_prefix / 128) sub-chunks
+int attention_cpw(int B, int Hkv, int ngroups, int nch);
 
 // Rotary table: tab[(p * D/2 + m) * 2 + {0,1}] = cos, sin of p * theta^(-2m/D),
 // formed in double precision and rounded to fp32, for p < npos.
 hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s);
-
-// Sets n 32-bit words to zero (a kernel, so it is safe inside graph capture).
-hipError_t zero_words(uint32_t *p, size_t n, hipStream_t s);
 
 // Global top-k of every row from the tile candidates; softmax statistics merge.
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,

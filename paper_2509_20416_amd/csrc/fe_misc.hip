@@ -241,16 +241,4 @@ hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s) 
   return hipGetLastError();
 }
 
-__global__ void k_zero_words(uint32_t *p, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    p[i] = 0u;
-}
-
-hipError_t zero_words(uint32_t *p, size_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  const int grid = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
-  hipLaunchKernelGGL(k_zero_words, dim3(grid), dim3(256), 0, s, p, n);
-  return hipGetLastError();
-}
-
 }  // namespace fe

@@ -30,7 +30,7 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, cnt, rope, ao, s, pmax,
+  size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
       psum, cval, cidx, total;
   int nchmax, nwg, npos;
 };
@@ -61,7 +61,6 @@ Layout layout_of(const fe_config &c) {
   L.knew = take(B * N * Hkv * D * 4);
   L.vnew = take(B * N * Hkv * D * 4);
   L.part = take(B * Hq * (size_t)L.nchmax * (D + 2) * 4);
-  L.cnt = take(B * Hq * 4);
   L.npos = c.max_prefix + c.n_layers;  // positions P_b + j, j < N
   L.rope = take((size_t)L.npos * (D / 2) * 2 * 4);
   L.ao = take(B * Hq * D * es);
@@ -112,7 +111,8 @@ struct fe_drafter {
   Layout L;
   hipStream_t cap_stream = nullptr;
   bool graph_mode = false;
-  bool counters_zeroed = false;  // attention counters zeroed and rotary table built once
+  int attn_split = 0;  // 128-key chunks per attention workgroup (0 = automatic)
+  bool table_ready = false;  // rotary table built (first pass on the handle)
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
   hipGraph_t graph = nullptr;
@@ -181,6 +181,14 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on) {
   return FE_OK;
 }
 
+fe_status fe_set_attention_split(fe_drafter *h, int32_t chunks_per_workgroup) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  if (chunks_per_workgroup < 0 || chunks_per_workgroup > (1 << 16))
+    return fail(FE_E_INVALID, "chunks_per_workgroup %d outside [0, 65536]", chunks_per_workgroup);
+  h->attn_split = chunks_per_workgroup;
+  return FE_OK;
+}
+
 void fe_drafter_destroy(fe_drafter *h) {
   if (!h) return;
   if (h->ev_a) (void)hipEventDestroy(h->ev_a);
@@ -231,6 +239,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const int esz = dt ? 2 : 4;
   const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
   const int nch_ld = L.nchmax;
+  const int cpw = h->attn_split > 0 ? h->attn_split : attention_cpw(B, Hkv, 1, nch);
   const int ntile = d / 16;
   float *ssqX = (float *)(ws + L.ssqX), *ssqP = (float *)(ws + L.ssqP);
 
@@ -285,8 +294,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     }
     // attention over the layer's prefix cache plus the cascade keys
     FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
-                                      vnew, nctx, part, nch, nch_ld,
-                                      (int *)(ws + L.cnt), ao, B, Hq, Hkv, D, s));
+                                      vnew, nctx, part, nch, nch_ld, cpw, ao, B, Hq, Hkv, D,
+                                      s));
     // x' = x_{i-1} + W_o o
     GainCopies gc_p{};
     if (fuse_m) {
@@ -353,10 +362,9 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   }
   if (out->logits && ((uintptr_t)out->logits & 3u)) return fail(FE_E_ALIGN, "logits misaligned");
   hipStream_t s = (hipStream_t)stream;
-  if (!h->counters_zeroed) {  // first pass on this handle: attention counters start at zero
-    FE_TRY(zero_words((uint32_t *)(h->ws + h->L.cnt), (size_t)c.max_batch * c.n_q_heads, s));
+  if (!h->table_ready) {  // first pass on this handle: the rotary table
     FE_TRY(rope_table((float *)(h->ws + h->L.rope), h->L.npos, c.head_dim, (double)c.rope_theta, s));
-    h->counters_zeroed = true;
+    h->table_ready = true;
   }
 
   // remember the call for fe_time_stage
@@ -378,7 +386,8 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
                                 (uintptr_t)topk, (uintptr_t)out->topk_ids,
                                 (uintptr_t)out->topk_probs, (uintptr_t)out->topk_draft,
-                                (uintptr_t)out->logits, (uintptr_t)out->hidden};
+                                (uintptr_t)out->logits, (uintptr_t)out->hidden,
+                                (uintptr_t)h->attn_split};
   for (int l = 0; l < c.n_layers; ++l) {
     key.push_back((uintptr_t)kv->k[l]);
     key.push_back((uintptr_t)kv->v[l]);

@@ -86,6 +86,10 @@ class Drafter:
     def set_graph_mode(self, on: bool) -> None:
         fe.fe_set_graph_mode(self.handle, on)
 
+    def set_attention_split(self, chunks_per_workgroup: int) -> None:
+        """128-key prefix chunks per attention workgroup; 0 = automatic."""
+        fe.fe_set_attention_split(self.handle, chunks_per_workgroup)
+
     def upload_inputs(self, inp, max_prefix: Optional[int] = None) -> DeviceInputs:
         torch = _torch()
         dev, dt = self.device, self.cfg.dtype

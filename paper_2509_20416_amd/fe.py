@@ -20,7 +20,8 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
-           "fe_set_graph_mode", "fe_time_stage", "fe_drafter_destroy", "fe_last_error")
+           "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_drafter_destroy",
+           "fe_last_error")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
 
@@ -90,6 +91,8 @@ def lib() -> C.CDLL:
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
+        L.fe_set_attention_split.restype = C.c_int
+        L.fe_set_attention_split.argtypes = [C.c_void_p, C.c_int32]
         L.fe_time_stage.restype = C.c_int
         L.fe_time_stage.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
                                     C.POINTER(C.c_float), C.POINTER(C.c_int32)]
@@ -138,6 +141,10 @@ def fe_build_tree(h: int, batch: int, topk: int, root_tokens: int, topk_ids: int
 
 def fe_set_graph_mode(h: int, on: bool) -> None:
     check(lib().fe_set_graph_mode(C.c_void_p(h), 1 if on else 0))
+
+
+def fe_set_attention_split(h: int, chunks_per_workgroup: int) -> None:
+    check(lib().fe_set_attention_split(C.c_void_p(h), int(chunks_per_workgroup)))
 
 
 def fe_time_stage(h: int, stage: int, repeats: int, stream: int):

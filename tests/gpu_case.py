@@ -18,7 +18,8 @@ def log(*a):
 
 
 def run_case(cfg, seed=0, prefix_lens=None, topk=None, sample=None, graph=False,
-             with_debug=True, weights=None, inputs=None, feo=None, check_tree_struct=True):
+             with_debug=True, weights=None, inputs=None, feo=None, check_tree_struct=True,
+             attn_split=None):
     import torch
     from paper_2509_20416_amd import Drafter
     if feo is None:
@@ -33,6 +34,8 @@ def run_case(cfg, seed=0, prefix_lens=None, topk=None, sample=None, graph=False,
         f"inputs ready in {time.time() - t0:.1f}s")
     dr = Drafter(cfg, w, max_batch=B, max_prefix=int(plens.max()), max_topk=max(k, cfg.topk),
                  graph=graph)
+    if attn_split is not None:
+        dr.set_attention_split(attn_split)
     di = dr.upload_inputs(inp)
     out = dr.forward(di, k)                                   # the benchmarked configuration
     tree = dr.build_tree(di, out["topk_ids"], k)

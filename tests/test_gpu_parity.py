@@ -74,6 +74,17 @@ def test_small_parity(cfg, ctx):
         assert rep["decided"] >= rep["ranks"] // 2, rep
 
 
+# Attention work split: 1 chunk per workgroup (every 128-key chunk its own
+# partial, merged by the second launch), 2 and 3 (the sub-chunk loop with a
+# ragged last workgroup), 8 (one workgroup per sequence, no merge launch).
+@pytest.mark.parametrize("split", [1, 2, 3, 8])
+@pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128],
+                         ids=lambda c: c.name)
+def test_attention_split_parity(cfg, split):
+    plens = np.array([0, 700, 65], np.int32) if cfg.batch == 3 else np.array([300, 129], np.int32)
+    _run(cfg, seed=4, prefix_lens=plens, attn_split=split)
+
+
 def test_topk_edge_values():
     """k = 1 (chain tree) and k = max (16)."""
     for k in (1, 16):
