@@ -133,9 +133,8 @@ def main():
     out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
     tree = dr.alloc_tree(cfg.batch, cfg.topk)
 
-    def step():
-        dr.forward(di, out=out)
-        dr.build_tree(di, out["topk_ids"], out=tree)
+    def step():  # one pass: forward + tree, one graph replay
+        dr.forward(di, out=out, tree=tree)
 
     if args.traffic_probe:
         for _ in range(3):

@@ -109,6 +109,8 @@ typedef struct {
   int32_t max_prefix;        /* HOST bound: every P_b <= max_prefix <= cfg.max_prefix */
 } fe_kv_view;
 
+typedef struct fe_tree_out fe_tree_out;
+
 typedef struct {
   int32_t *topk_ids;  /* [B, N, k]: target-vocabulary ids, rank order (largest logit
                          first; equal logits -> lower draft id first) */
@@ -116,9 +118,12 @@ typedef struct {
   int32_t *topk_draft;/* optional [B, N, k] draft-vocabulary ids; NULL = not written */
   float *logits;      /* optional [B, N, V] fp32; NULL = never materialised */
   float *hidden;      /* optional [B, N+1, d] fp32 cascade states x_0..x_N; NULL = not written */
+  const fe_tree_out *tree; /* optional: also build the Backbone Expansion tree of this pass
+                         (root = next_tokens, P_b from kv->cu_prefix), as fe_build_tree would,
+                         in the same launch sequence; NULL = no tree */
 } fe_draft_out;
 
-typedef struct {
+struct fe_tree_out {
   int32_t *tokens;    /* [B, T], T = 1 + N*k: root token, then level by level in rank order */
   int32_t *parents;   /* [B, T]: parent node index, -1 for the root */
   int32_t *depth;     /* [B, T]: 0 for the root, level l for level-l nodes */
@@ -126,7 +131,7 @@ typedef struct {
   uint8_t *mask;      /* [B, T, T]: mask[a][c] = 1 iff c is on the root->a path (inclusive) */
   int32_t *retrieve;  /* [B, N*(k-1)+1, N+1]: root->leaf node paths of the leaves in node
                          order, -1 padded */
-} fe_tree_out;
+};
 
 typedef struct fe_drafter fe_drafter;
 
@@ -134,12 +139,12 @@ typedef struct fe_drafter fe_drafter;
 size_t fe_workspace_bytes(const fe_config *cfg);
 
 /* Creates a drafter over borrowed weights and workspace (Section 2.1).
- * Supported shapes: head_dim 64 or 128; d, I, H_q*D multiples of 32 (bf16) or
- * 16 (fp32); V a multiple of 16 with ceil(V/64)*max_topk <= 8192;
+ * Supported shapes: head_dim 64 or 128; d <= 8192; d, I, H_q*D multiples of 32
+ * (bf16) or 16 (fp32); V a multiple of 16 with ceil(V/64)*max_topk <= 8192;
  * 1 <= n_layers <= 16; 1 <= max_topk <= 16; H_q % H_kv == 0;
  * max_batch*n_layers <= 256.  `workspace` (256-byte aligned) must hold
- * fe_workspace_bytes(cfg) bytes; the first fe_draft_forward initialises the
- * small part of it that persists between calls.  Creation makes no HIP call;
+ * fe_workspace_bytes(cfg) bytes; the first fe_draft_forward builds the rotary
+ * table in it, which persists between calls.  Creation makes no HIP call;
  * `stream` is unused.  On success *out receives the handle. */
 fe_status fe_drafter_create(const fe_config *cfg, const fe_weights *w, void *workspace,
                             size_t workspace_bytes, void *stream, fe_drafter **out);

@@ -32,59 +32,6 @@ __device__ __forceinline__ float scaled_exp(float m, float M) {
   return m == -INFINITY ? 0.f : expf(m - M);
 }
 
-// ---- cross-lane reductions in registers ----------------------------------------
-// DPP controls: quad_perm [1,0,3,2] (lane^1), [2,3,0,1] (lane^2), row_half_mirror
-// (the other quad of an 8-lane half once quads are uniform), row_ror:8 (lane^8).
-template <int CTRL> __device__ __forceinline__ float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
-}
-// permlane16_swap / permlane32_swap of a register with itself return, in every
-// lane, the pair {x[lane], x[lane ^ 16]} (resp. lane ^ 32) in some order.
-__device__ __forceinline__ float xor16_sum(float x) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float xor32_sum(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float xor16_max(float x) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xor32_max(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-// Sum over aligned groups of RL lanes (8, 16, 32), result in every lane of the
-// group; each step adds two equal-valued halves in either order, so all lanes
-// of a group hold bit-identical sums.
-template <int RL> __device__ __forceinline__ float group_sum(float x) {
-  x += dpp_f<0xB1>(x);
-  x += dpp_f<0x4E>(x);
-  x += dpp_f<0x141>(x);
-  if constexpr (RL >= 16) x += dpp_f<0x128>(x);
-  if constexpr (RL >= 32) x = xor16_sum(x);
-  if constexpr (RL >= 64) x = xor32_sum(x);
-  return x;
-}
-template <int RL> __device__ __forceinline__ float group_max(float x) {
-  x = fmaxf(x, dpp_f<0xB1>(x));
-  x = fmaxf(x, dpp_f<0x4E>(x));
-  x = fmaxf(x, dpp_f<0x141>(x));
-  if constexpr (RL >= 16) x = fmaxf(x, dpp_f<0x128>(x));
-  if constexpr (RL >= 32) x = xor16_max(x);
-  if constexpr (RL >= 64) x = xor32_max(x);
-  return x;
-}
-// Max over the row groups of a wave, given values uniform within RL-lane groups.
-template <int RL> __device__ __forceinline__ float across_groups_max(float x) {
-  if constexpr (RL <= 8) x = fmaxf(x, dpp_f<0x128>(x));
-  if constexpr (RL <= 16) x = xor16_max(x);
-  if constexpr (RL <= 32) x = xor32_max(x);
-  return x;
-}
-
 // element e of a 16-byte piece holding 16/sizeof(T) values
 template <typename T> __device__ __forceinline__ float piece_at(const u32x4 &w, int e) {
   const uint32_t u = (e >> (sizeof(T) == 2 ? 1 : 0)) == 0   ? w.x
@@ -337,13 +284,14 @@ __global__ __launch_bounds__(256) void k_attn_mma(const bf16_t *__restrict__ Kc,
                                                   const float *__restrict__ vnew, int nctx,
                                                   float *__restrict__ part, int nch, int nch_ld,
                                                   int cpw, bf16_t *__restrict__ out, int Hq,
-                                                  int Hkv) {
+                                                  int Hkv, const float *__restrict__ rope,
+                                                  int cascade) {
   constexpr int NKC = D / 32;         // 32-dim steps of QK^T
   constexpr int NDT = D / 16;         // 16-dim tiles of the value product
   constexpr int VPR = D / 8;          // 16-byte pieces per V row
   constexpr int NVL = 32 * VPR / 64;  // V pieces per lane per sub-chunk
   constexpr int RSB = 2 * D + 16;     // LDS bytes per staged V row
-  constexpr int EPL = D / 64;         // dims per lane in the cascade-key step
+  constexpr int HD = D / 2;           // rotary pairs (m, m + D/2)
   __shared__ __align__(16) unsigned char s_v[4][32 * RSB];
   __shared__ float s_o[5][GH][D];
   __shared__ float s_l[5][GH], s_m[5][GH];
@@ -368,26 +316,47 @@ __global__ __launch_bounds__(256) void k_attn_mma(const bf16_t *__restrict__ Kc,
       qraw[kc][1] = *reinterpret_cast<const f32x4 *>(qp + 32 * kc + 8 * g + 4);
     }
   }
-  float kj[kMaxLayers][EPL], vj[kMaxLayers][EPL], qc[GHW][EPL];
+  // cascade step: lane l < D/2 holds the rotary pair (m, m + D/2), m = l
+  const int m2 = min(lane, HD - 1);
+  const bool cact = lane < HD;
+  float kj[kMaxLayers][2], vj[kMaxLayers][2], qc[GHW][2];
   if (casc) {
 #pragma unroll
     for (int j = 0; j < kMaxLayers; ++j) {
-      const size_t off = (((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + lane * EPL;
+      const size_t off = (((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + m2;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        kj[j][e] = knew[off + e];
-        vj[j][e] = vnew[off + e];
+      for (int e = 0; e < 2; ++e) {
+        kj[j][e] = knew[off + e * HD];
+        vj[j][e] = vnew[off + e * HD];
       }
     }
 #pragma unroll
     for (int i = 0; i < GHW; ++i) {
       const int gh = min(wave + 4 * i, GH - 1);
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) qc[i][e] = q[((size_t)b * Hq + h0 + gh) * D + lane * EPL + e];
+      for (int e = 0; e < 2; ++e) qc[i][e] = q[((size_t)b * Hq + h0 + gh) * D + m2 + e * HD];
     }
   }
 
   const int start = cu[b], P = cu[b + 1] - start;
+  // rotary coefficients (Section 2.1's decoder layers use RoPE; the cached
+  // prefix keys are stored rotated): the query sits at the last cascade
+  // position, cascade key j at P + j (one position, P, per layer otherwise).
+  // Loaded with the first K/V rows: no round trip of their own.
+  const int pos_q = cascade ? P + nctx - 1 : P;
+  f32x4 rq[NKC / 2][4];
+#pragma unroll
+  for (int kc = 0; kc < NKC / 2; ++kc)
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      rq[kc][w] = *reinterpret_cast<const f32x4 *>(rope + ((size_t)pos_q * HD + 32 * kc + 8 * g) * 2 + 4 * w);
+  float2 rcj[kMaxLayers], rcq;
+  if (casc) {
+#pragma unroll
+    for (int j = 0; j < kMaxLayers; ++j)
+      rcj[j] = *reinterpret_cast<const float2 *>(rope + ((size_t)(cascade ? P + min(j, nctx - 1) : P) * HD + m2) * 2);
+    rcq = *reinterpret_cast<const float2 *>(rope + ((size_t)pos_q * HD + m2) * 2);
+  }
   const int span = kAttnChunk * cpw;
   const int nv = max(1, min((P + span - 1) / span, nch));
   if (ch >= nv) return;  // chunk beyond this sequence's prefix
@@ -426,30 +395,32 @@ __global__ __launch_bounds__(256) void k_attn_mma(const bf16_t *__restrict__ Kc,
     for (int i = 0; i < GHW; ++i) {
       const int gh = wave + 4 * i;
       if (gh >= GH) break;
+      // rotate-half on the pair (m, m + D/2)
+      const float q0 = qc[i][0] * rcq.x - qc[i][1] * rcq.y, q1 = qc[i][1] * rcq.x + qc[i][0] * rcq.y;
       float sj[kMaxLayers];
 #pragma unroll
       for (int j = 0; j < kMaxLayers; ++j) {
-        float d = 0.f;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) d += qc[i][e] * qscale * kj[j][e];
+        const float k0 = kj[j][0] * rcj[j].x - kj[j][1] * rcj[j].y;
+        const float k1 = kj[j][1] * rcj[j].x + kj[j][0] * rcj[j].y;
+        float d = cact ? (q0 * k0 + q1 * k1) * qscale : 0.f;
         d = group_sum<64>(d);
         sj[j] = j < nctx ? d : -INFINITY;
       }
       float m = -INFINITY;
 #pragma unroll
       for (int j = 0; j < kMaxLayers; ++j) m = fmaxf(m, sj[j]);
-      float L = 0.f, o[EPL];
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) o[e] = 0.f;
+      float L = 0.f, o[2] = {0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < kMaxLayers; ++j) {
         const float pj = sexp2(sj[j], m);
         L += pj;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) o[e] += pj * vj[j][e];
+        for (int e = 0; e < 2; ++e) o[e] += pj * vj[j][e];
       }
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) s_o[4][gh][lane * EPL + e] = o[e];
+      if (cact) {
+        s_o[4][gh][m2] = o[0];
+        s_o[4][gh][m2 + HD] = o[1];
+      }
       if (lane == 0) {
         s_m[4][gh] = m;
         s_l[4][gh] = L;
@@ -458,11 +429,27 @@ __global__ __launch_bounds__(256) void k_attn_mma(const bf16_t *__restrict__ Kc,
   }
 
   // q as B operands: column r = head h0 + r (zero for r >= GH), high and low parts
+  // rotate-half: dims 32kc + 8g + e and their partners D/2 later (kc + NKC/2)
+  float qf[NKC][8];
+#pragma unroll
+  for (int kc = 0; kc < NKC; ++kc) {
+    qf[kc][0] = qraw[kc][0].x; qf[kc][1] = qraw[kc][0].y; qf[kc][2] = qraw[kc][0].z; qf[kc][3] = qraw[kc][0].w;
+    qf[kc][4] = qraw[kc][1].x; qf[kc][5] = qraw[kc][1].y; qf[kc][6] = qraw[kc][1].z; qf[kc][7] = qraw[kc][1].w;
+  }
+#pragma unroll
+  for (int kc = 0; kc < NKC / 2; ++kc)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const f32x4 cw = rq[kc][e >> 1];
+      const float cs = (e & 1) ? cw.z : cw.x, sn = (e & 1) ? cw.w : cw.y;
+      const float x1 = qf[kc][e], x2 = qf[kc + NKC / 2][e];
+      qf[kc][e] = x1 * cs - x2 * sn;
+      qf[kc + NKC / 2][e] = x2 * cs + x1 * sn;
+    }
   u32x4 qh[NKC], ql[NKC];
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    const float x[8] = {qraw[kc][0].x, qraw[kc][0].y, qraw[kc][0].z, qraw[kc][0].w,
-                        qraw[kc][1].x, qraw[kc][1].y, qraw[kc][1].z, qraw[kc][1].w};
+    const float *x = qf[kc];
     uint32_t hw[4], lw[4];
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
@@ -673,7 +660,7 @@ template <int D>
 static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, const float *q,
                              const float *knew, const float *vnew, int nctx, float *part, int nch,
                              int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
-                             hipStream_t s) {
+                             const float *rope, int cascade, hipStream_t s) {
   const int G = Hq / Hkv;
   const int GH = G % 16 == 0 ? 16 : G % 8 == 0 ? 8 : G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1;
   const int nwg = nch < 1 ? 1 : (nch + cpw - 1) / cpw;
@@ -681,7 +668,7 @@ static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, co
 #define FE_ATTN(GHV)                                                                             \
   hipLaunchKernelGGL((k_attn_mma<D, GHV>), grid, dim3(256), 0, s, (const bf16_t *)K,             \
                      (const bf16_t *)V, cu, q, knew, vnew, nctx, part, nwg, nch_ld, cpw, \
-                     (bf16_t *)out, Hq, Hkv)
+                     (bf16_t *)out, Hq, Hkv, rope, cascade)
   switch (GH) {
     case 16: FE_ATTN(16); break;
     case 8: FE_ATTN(8); break;
@@ -706,15 +693,15 @@ int attention_cpw(int B, int Hkv, int ngroups, int nch) {
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
                      const float *knew, const float *vnew, int nctx, float *part, int nch,
                      int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int D,
-                     hipStream_t s) {
+                     const float *rope, int cascade, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   if (cpw < 1) cpw = 1;
   hipError_t e;
   if (dt)
     e = D == 128 ? attn_mma_t<128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                   Hq, Hkv, s)
+                                   Hq, Hkv, rope, cascade, s)
                  : attn_mma_t<64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                  Hq, Hkv, s);
+                                  Hq, Hkv, rope, cascade, s);
   else
     e = D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
                                       B, Hq, Hkv, s)

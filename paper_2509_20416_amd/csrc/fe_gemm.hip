@@ -48,9 +48,9 @@ template <> __device__ __forceinline__ void mma16<float>(f32x4 &acc, u32x4 a, u3
 __device__ __forceinline__ u32x4 ldg_stream(const u32x4 *p) { return __builtin_nontemporal_load(p); }
 
 // ---------------------------------------------------------------------------
-// Accumulation paths.  Both leave, in lane (r, g) of a wave, the 16x16 tiles
-// acc[i][f] = rows 16i.. of A times weight rows of virtual columns c0+16f..,
-// summed over this wave's share of K.
+// Accumulation (up to 32 rows).  Leaves, in lane (r, g) of a wave, the 16x16
+// tiles acc[i][f] = rows 16i.. of A times weight rows of virtual columns
+// c0+16f.., summed over this wave's share of K.
 // ---------------------------------------------------------------------------
 
 // Staged path (M <= 32): weights are read as 512-byte contiguous pieces of
@@ -130,87 +130,20 @@ __device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, c
   }
 }
 
-// Direct path (larger M): lane (r, g) loads 16 bytes of weight row r per
-// K step straight into the B operand; U steps double-buffered in registers.
-template <typename T, int MT, int NT, int U, class Epi>
-__device__ __forceinline__ void accum_direct(const T *__restrict__ A, int lda, const ARows &ar_,
-                                             int M, int K, const Epi &epi, int c0, int wk,
-                                             int WKn, f32x4 (&acc)[MT][NT]) {
-  constexpr int E = Elt<T>::kPer16B;
-  constexpr int KS = 4 * E;
-  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-  const int nsteps = K / KS;
-  const int s0 = (int)(((long)nsteps * wk) / WKn);
-  const int s1 = (int)(((long)nsteps * (wk + 1)) / WKn);
-  const u32x4 *wp[NT];
-#pragma unroll
-  for (int f = 0; f < NT; ++f)
-    wp[f] = reinterpret_cast<const u32x4 *>(epi.wrow(c0 + f * 16 + r)) + g;
-  const u32x4 *ap[MT];
-  bool am[MT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    const int m = i * 16 + r;
-    am[i] = m < M;
-    ap[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(am[i] ? ar_.row(m) : 0) * lda) + g;
-  }
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  u32x4 wc[U][NT], ac[U][MT];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int s = s0 + u;
-    const bool ok = s < s1;
-#pragma unroll
-    for (int f = 0; f < NT; ++f) wc[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
-#pragma unroll
-    for (int i = 0; i < MT; ++i) ac[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
-  }
-  for (int sb = s0; sb < s1; sb += U) {
-    u32x4 wn_[U][NT], an_[U][MT];
-    const int sn = sb + U;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int s = sn + u;
-      const bool ok = s < s1;
-#pragma unroll
-      for (int f = 0; f < NT; ++f) wn_[u][f] = ok ? ldg_stream(wp[f] + 4 * s) : zero;
-#pragma unroll
-      for (int i = 0; i < MT; ++i) an_[u][i] = (ok && am[i]) ? ap[i][4 * s] : zero;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int f = 0; f < NT; ++f) mma16<T>(acc[i][f], ac[u][i], wc[u][f]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-      for (int f = 0; f < NT; ++f) wc[u][f] = wn_[u][f];
-#pragma unroll
-      for (int i = 0; i < MT; ++i) ac[u][i] = an_[u][i];
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
 // The GEMM body: WN x WK waves; wave (wn, wk) owns NT 16-column tiles and the
 // wk-th share of K.  Partial tiles are summed over wk in LDS in a fixed order
 // (deterministic, no atomics), then the epilogue consumes the [M, span] tile.
 // ---------------------------------------------------------------------------
-template <int MT> struct Unroll {
-  static constexpr int value = MT <= 2 ? 8 : (MT <= 4 ? 4 : (MT <= 8 ? 2 : 1));
-};
-
 template <typename T, int MT, int NT, int WK, int WN, bool NORM, class Epi>
 __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, int lda, ARows arows,
                                                        int M, int K, NormA na, Epi epi) {
-  constexpr bool kStaged = MT <= 2;
+  static_assert(MT <= 2, "more than 32 rows take k_gemm_mid");
   static_assert(!NORM || MT == 1, "fused RMSNorm is for M <= 16");
   constexpr int NTHR = 64 * WK * WN;
   constexpr int SPAN = WN * NT * 16;
   constexpr int LDT = SPAN + 1;
-  constexpr int kStageBytes = kStaged ? WK * WN * NT * 16 * kStageRowBytes : 0;
+  constexpr int kStageBytes = WK * WN * NT * 16 * kStageRowBytes;
   constexpr int kRedBytes = WK * MT * 16 * LDT * 4;
   constexpr int kSmem = kStageBytes > kRedBytes ? kStageBytes : kRedBytes;
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
@@ -243,21 +176,18 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
 #pragma unroll
     for (int f = 0; f < NT; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (c0 < epi.nvcols) {
-    if constexpr (kStaged)
-      accum_staged<T, MT, NT>(A, lda, arows, M, K, epi, c0, wk, WK,
-                              smem + wave * NT * 16 * kStageRowBytes, acc);
-    else
-      accum_direct<T, MT, NT, Unroll<MT>::value>(A, lda, arows, M, K, epi, c0, wk, WK, acc);
-  }
+  const typename Epi::Pre pre{};  // the epilogue loads its own values here
+  if (c0 < epi.nvcols)
+    accum_staged<T, MT, NT>(A, lda, arows, M, K, epi, c0, wk, WK,
+                            smem + wave * NT * 16 * kStageRowBytes, acc);
   if constexpr (NORM) {
     float ssum = 0.f;
 #pragma unroll
     for (int u = 0; u < kNormLoads; ++u) ssum += (npart + PARTS * u < na.ntile) ? nv[u] : 0.f;
     const float *sr = na.ssq + (size_t)na.row(min(nrow, M - 1)) * na.ntile;
     for (int t = npart + PARTS * kNormLoads; t < na.ntile; t += PARTS) ssum += sr[t];
-#pragma unroll
-    for (int off = PARTS / 2; off >= 1; off >>= 1) ssum += __shfl_xor(ssum, off);
+    static_assert(PARTS >= 8 && PARTS <= 64, "row partials reduce over 8..64 lanes");
+    ssum = group_sum<PARTS>(ssum);
     if (npart == 0 && nrow < M) s_inv[nrow] = 1.0f / sqrtf(ssum / (float)na.d + na.eps);
   }
   __syncthreads();  // staging tiles are dead; the buffer becomes the reduction tile
@@ -281,13 +211,286 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
     }
     __syncthreads();
   }
-  epi.finish(&red[0][0][0], LDT, M, c0_wg, SPAN);
+  epi.finish(&red[0][0][0], LDT, M, c0_wg, SPAN, pre);
 }
 
 // ---------------------------------------------------------------------------
+// Row-streaming path for 1..8 input rows (batch-1 layers, bf16 weights): no
+// matrix cores, no weight staging.  A workgroup of W waves owns SPAN = 4W
+// virtual columns; wave w takes weight rows 4w..4w+3 with 16 lanes per row,
+// so every load instruction reads 256 contiguous bytes of each of 4 rows and
+// a lane only ever accumulates its own row.  The input rows are in LDS as
+// bf16 (zero-padded to a multiple of 128) and meet the weights in
+// v_dot2c_f32_bf16 as they arrive; two register banks of kGvDepth pieces per
+// lane alternate, one in flight while the other is consumed.  Each row's sum
+// is reduced over its 16 lanes with DPP; the [M, SPAN] tile goes to the same
+// epilogues as the matrix-core paths.
+// ---------------------------------------------------------------------------
+constexpr int kGvDepth = 8;
+constexpr int kGvMaxLds = 64 * 1024;  // bytes of input rows in LDS
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// Each 32-bit word goes through a scalar before the bit cast: a bit cast of a
+// vector element (w.y) itself is compiled as a read of element 0.
+__device__ __forceinline__ float dot8(u32x4 w, u32x4 x, float acc) {
+  const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
+  const uint32_t x0 = x[0], x1 = x[1], x2 = x[2], x3 = x[3];
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w0), __builtin_bit_cast(bf16x2_t, x0), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w1), __builtin_bit_cast(bf16x2_t, x1), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w2), __builtin_bit_cast(bf16x2_t, x2), acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w3), __builtin_bit_cast(bf16x2_t, x3), acc, false);
+}
+
+template <int MR, int W, bool NORM, class Epi>
+__global__ __launch_bounds__(64 * W) void k_gemv(const bf16_t *__restrict__ A, int lda, ARows arows,
+                                                 int M, int K, NormA na, Epi epi) {
+  constexpr int SPAN = 4 * W;
+  constexpr int NTHR = 64 * W;
+  extern __shared__ __attribute__((aligned(16))) char xs_raw[];
+  __shared__ float tile[MR][SPAN + 1];
+  __shared__ float s_inv[MR];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rq = lane >> 4, l16 = lane & 15;
+  const int c0 = blockIdx.x * SPAN;
+  const int kpad = (K + 127) & ~127;
+  const int npc = kpad / 128;  // 16-byte pieces per lane per row
+  bf16_t *xs = reinterpret_cast<bf16_t *>(xs_raw);
+
+  // weight row of this lane (clamped; columns past the end are dropped at the end)
+  const int col = c0 + wave * 4 + rq;
+  const bf16_t *wr = epi.wrow(min(col, epi.nvcols - 1));
+  // piece p of the row: elements p*128 + 8*l16 .. +7; past K the address is
+  // clamped in bounds and the (finite) weights meet zero-padded inputs
+  auto ldw = [&](int p) {
+    return ldg_stream(reinterpret_cast<const u32x4 *>(wr + min(p * 128 + l16 * 8, K - 8)));
+  };
+  // every independent load is issued before anything is consumed, so the
+  // whole prologue costs one memory round trip: the first weight pieces, the
+  // input rows (registers, then LDS), the norm partials, the epilogue's values
+  u32x4 ba[kGvDepth], bb[kGvDepth];
+#pragma unroll
+  for (int i = 0; i < kGvDepth; ++i) ba[i] = ldw(min(i, npc - 1));
+
+  constexpr int XPT = kGvMaxLds / 16 / NTHR;  // input pieces per thread, at most
+  const int xper = kpad / 8, xtot = MR * xper;
+  u32x4 xr[XPT];
+#pragma unroll
+  for (int u = 0; u < XPT; ++u)
+    if (NTHR * u < xtot) {  // uniform: batch u holds at least one piece
+      const int idx = min(tid + NTHR * u, xtot - 1);
+      const int m = idx / xper, e = min((idx % xper) * 8, K - 8);
+      xr[u] = *reinterpret_cast<const u32x4 *>(A + (size_t)arows.row(min(m, M - 1)) * lda + e);
+    }
+
+  constexpr int PARTS = NTHR / 16;
+  constexpr int kNormLoads = 16;
+  float nv[NORM ? kNormLoads : 1];
+  const int nrow = tid / PARTS, npart = tid % PARTS;
+  if constexpr (NORM) {
+    const float *sr = na.ssq + (size_t)na.row(min(nrow, M - 1)) * na.ntile;
+#pragma unroll
+    for (int u = 0; u < kNormLoads; ++u) nv[u] = sr[min(npart + PARTS * u, na.ntile - 1)];
+  }
+  const typename Epi::Pre pre = epi.prefetch(M, c0, SPAN);
+
+  // input rows -> LDS, zero past K and past M
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int u = 0; u < XPT; ++u) {
+    const int idx = tid + NTHR * u;
+    if (NTHR * u < xtot && idx < xtot) {
+      const int m = idx / xper, e = (idx % xper) * 8;
+      *reinterpret_cast<u32x4 *>(xs + (size_t)m * kpad + e) = (m < M && e < K) ? xr[u] : zero;
+    }
+  }
+  if constexpr (NORM) {
+    float ssum = 0.f;
+#pragma unroll
+    for (int u = 0; u < kNormLoads; ++u) ssum += (npart + PARTS * u < na.ntile) ? nv[u] : 0.f;
+    const float *sr = na.ssq + (size_t)na.row(min(nrow, M - 1)) * na.ntile;
+    for (int t = npart + PARTS * kNormLoads; t < na.ntile; t += PARTS) ssum += sr[t];
+    static_assert(PARTS >= 8 && PARTS <= 64, "row partials reduce over 8..64 lanes");
+    ssum = group_sum<PARTS>(ssum);
+    if (npart == 0 && nrow < MR) s_inv[nrow] = nrow < M ? 1.0f / sqrtf(ssum / (float)na.d + na.eps) : 0.f;
+  }
+  __syncthreads();
+
+  float acc[MR];
+#pragma unroll
+  for (int m = 0; m < MR; ++m) acc[m] = 0.f;
+  const bf16_t *xl = xs + l16 * 8;
+  auto consume = [&](const u32x4 (&bw)[kGvDepth], int p0) {
+#pragma unroll
+    for (int i = 0; i < kGvDepth; ++i) {
+      const int p = p0 + i;
+      if (p < npc) {
+#pragma unroll
+        for (int m = 0; m < MR; ++m)
+          acc[m] = dot8(bw[i], *reinterpret_cast<const u32x4 *>(xl + (size_t)m * kpad + p * 128), acc[m]);
+      }
+    }
+  };
+  for (int p0 = 0; p0 < npc; p0 += 2 * kGvDepth) {
+#pragma unroll
+    for (int i = 0; i < kGvDepth; ++i) bb[i] = ldw(min(p0 + kGvDepth + i, npc - 1));
+    consume(ba, p0);
+#pragma unroll
+    for (int i = 0; i < kGvDepth; ++i) ba[i] = ldw(min(p0 + 2 * kGvDepth + i, npc - 1));
+    consume(bb, p0 + kGvDepth);
+  }
+#pragma unroll
+  for (int m = 0; m < MR; ++m) {
+    float v = group_sum<16>(acc[m]);
+    if constexpr (NORM) v *= s_inv[m];
+    if (l16 == 0) tile[m][wave * 4 + rq] = v;
+  }
+  __syncthreads();
+  epi.finish(&tile[0][0], SPAN + 1, M, c0, SPAN, pre);
+}
+
+// ---------------------------------------------------------------------------
+// Batched rows (17..256): one workgroup owns BN = 16*NTW output columns and
+// every row; wave w computes rows 64w..64w+63.  K advances in chunks of 128
+// bytes per row.  Each chunk of A (all rows) and of the BN weight rows is
+// staged in LDS (rows padded to 144 bytes) and feeds the MFMAs from there,
+// while the next A chunk and the next kWPre weight chunks are already in
+// registers.  Weights are read from HBM once; A (at most 256 rows) is served
+// by L2 to every workgroup.
+// ---------------------------------------------------------------------------
+constexpr int kMidRows = 256;
+constexpr int kMidRowBytes = 144;
+constexpr int kWPre = 3;  // weight chunks in flight per thread
+
+template <typename T, int NTW, class Epi>
+__global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
+                                                  int M, int K, Epi epi) {
+  constexpr int E = Elt<T>::kPer16B;  // elements per 16-byte piece
+  constexpr int KC = 8 * E;           // elements of K per chunk
+  constexpr int BN = NTW * 16;
+  constexpr int ALD = kMidRows * 8 / 256;     // A pieces per thread per chunk
+  constexpr int WLD = (BN * 8 + 255) / 256;   // weight pieces per thread per chunk
+  constexpr int kStage = (kMidRows + BN) * kMidRowBytes;
+  constexpr int LDT = BN + 1;
+  constexpr int kTile = kMidRows * LDT * 4;
+  __shared__ __attribute__((aligned(16))) char smem[kStage > kTile ? kStage : kTile];
+  char *sA = smem, *sW = smem + kMidRows * kMidRowBytes;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int c0 = blockIdx.x * BN;
+  const int nch = (K + KC - 1) / KC;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+
+  // piece p = tid + 256 i of a chunk: row p / 8, 16-byte piece p % 8 (element
+  // offset po); loads are unconditional at clamped in-bounds addresses and
+  // pieces past K, past the rows or past the columns are replaced by zero
+  const T *arow[ALD];
+  bool aok[ALD];
+#pragma unroll
+  for (int i = 0; i < ALD; ++i) {
+    const int row = (tid + 256 * i) >> 3;
+    aok[i] = row < M;
+    arow[i] = A + (size_t)arows.row(min(row, M - 1)) * lda;
+  }
+  const T *wrw[WLD];
+  bool wok[WLD];
+#pragma unroll
+  for (int i = 0; i < WLD; ++i) {
+    const int n = (tid + 256 * i) >> 3;
+    wok[i] = n < BN && c0 + n < epi.nvcols;
+    wrw[i] = epi.wrow(min(c0 + min(n, BN - 1), epi.nvcols - 1));
+  }
+  const int po = (tid & 7) * E;  // 256 is a multiple of 8: same piece for every i
+  auto ldA = [&](int ch, u32x4 (&ra)[ALD]) {
+    const int kk = ch * KC + po;
+    const int ka = min(kk, K - E);
+#pragma unroll
+    for (int i = 0; i < ALD; ++i) {
+      const u32x4 v = *reinterpret_cast<const u32x4 *>(arow[i] + ka);
+      ra[i] = (aok[i] && kk < K) ? v : zero;
+    }
+  };
+  auto ldW = [&](int ch, u32x4 (&rw)[WLD]) {
+    const int kk = ch * KC + po;
+    const int ka = min(kk, K - E);
+#pragma unroll
+    for (int i = 0; i < WLD; ++i) {
+      const u32x4 v = ldg_stream(reinterpret_cast<const u32x4 *>(wrw[i] + ka));
+      rw[i] = (wok[i] && kk < K) ? v : zero;
+    }
+  };
+
+  f32x4 acc[4][NTW];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int f = 0; f < NTW; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int mrow0 = wave * 64;
+  const int mtiles = min(4, (M - mrow0 + 15) / 16);  // this wave's live 16-row tiles (may be <= 0)
+
+  u32x4 ra[ALD], rw[kWPre][WLD];
+  ldA(0, ra);
+#pragma unroll
+  for (int d = 0; d < kWPre; ++d) ldW(d, rw[d]);
+  for (int ch = 0; ch < nch; ++ch) {
+    __syncthreads();  // every wave is done reading the previous chunk
+#pragma unroll
+    for (int i = 0; i < ALD; ++i)
+      *reinterpret_cast<u32x4 *>(sA + ((tid + 256 * i) >> 3) * kMidRowBytes + (tid & 7) * 16) = ra[i];
+#pragma unroll
+    for (int i = 0; i < WLD; ++i)
+      if (tid + 256 * i < BN * 8)
+        *reinterpret_cast<u32x4 *>(sW + ((tid + 256 * i) >> 3) * kMidRowBytes + (tid & 7) * 16) = rw[0][i];
+    __syncthreads();
+    // next loads: A one chunk ahead, weights kWPre chunks ahead (past the end:
+    // clamped re-reads, masked to zero and never used)
+    ldA(ch + 1, ra);
+#pragma unroll
+    for (int d = 0; d + 1 < kWPre; ++d)
+#pragma unroll
+      for (int i = 0; i < WLD; ++i) rw[d][i] = rw[d + 1][i];
+    ldW(ch + kWPre, rw[kWPre - 1]);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4 bf[NTW];
+#pragma unroll
+      for (int f = 0; f < NTW; ++f)
+        bf[f] = *reinterpret_cast<const u32x4 *>(sW + (f * 16 + r) * kMidRowBytes + ks * 64 + g * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < mtiles) {
+          const u32x4 af = *reinterpret_cast<const u32x4 *>(
+              sA + (mrow0 + i * 16 + r) * kMidRowBytes + ks * 64 + g * 16);
+#pragma unroll
+          for (int f = 0; f < NTW; ++f) mma16<T>(acc[i][f], af, bf[f]);
+        }
+    }
+  }
+  __syncthreads();  // staging is dead; the buffer becomes the output tile
+  float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (i < mtiles)
+#pragma unroll
+      for (int f = 0; f < NTW; ++f)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][f * 16 + r] = acc[i][f][v];
+  __syncthreads();
+  epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
+}
+// ---------------------------------------------------------------------------
 // Epilogues.
 // ---------------------------------------------------------------------------
+// kMidNtw: 16-column tiles per workgroup on the batched-rows path (0 = chosen
+// from the column count); kMidNtwMin: the smallest the epilogue accepts.
+// prefetch() runs before the main loop and may load, into registers, what
+// finish() needs for this thread's first output element (Pre::ok), so those
+// loads ride along with the first weight chunk.
+struct NoPre {
+  bool ok = false;
+};
 template <typename T> struct EpiStore {
+  static constexpr bool kRowStream = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   const T *w;
   int ldw, nvcols;
   T *out;
@@ -298,7 +501,7 @@ template <typename T> struct EpiStore {
   T *gather_out;
   int ld_gather, d, B;
   __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
       if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = Elt<T>::from_f(tile[m * ldt + c]);
@@ -321,6 +524,8 @@ template <typename T> struct EpiStore {
 };
 
 template <typename T> struct EpiResid {
+  static constexpr bool kRowStream = true;
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   const T *w;
   int ldw, nvcols;
   float *out;
@@ -330,18 +535,47 @@ template <typename T> struct EpiResid {
   float *ssq;  // optional per-(row, 16-column tile) sums of squares of the output
   int ssq_rs, ssq_off;
   GainCopies gc;
+  struct Pre {  // raw values: converted where used, so no load is waited for early
+    bool ok = false;
+    float r = 0.f;
+    T g[kMaxLayers + 1];
+  };
   __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
+  // residual and gains of element idx = threadIdx.x, when every element has
+  // its own thread (clamped in-bounds loads)
+  __device__ Pre prefetch(int M, int c0, int span) const {
+    Pre p;
+    const int idx = threadIdx.x;
+    if (M * span > (int)blockDim.x || idx >= M * span) return p;
+    const int m = idx / span, cc = min(c0 + idx % span, nvcols - 1);
+    p.ok = true;
+    if (resid) p.r = resid[(size_t)m * ldr + cc];
+    if (gc.n > 0) {
+#pragma unroll
+      for (int q = 0; q < kMaxLayers + 1; ++q)
+        p.g[q] = ((const T *)gc.gamma[min(q, gc.n - 1)])[cc];
+    }
+    return p;
+  }
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &pre) const {
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
       if (c0 + c >= nvcols) continue;
+      const bool own = pre.ok && idx == (int)threadIdx.x;
       float v = tile[m * ldt + c];
-      if (resid) v = resid[(size_t)m * ldr + c0 + c] + v;
+      if (resid) v = (own ? pre.r : resid[(size_t)m * ldr + c0 + c]) + v;
       out[(size_t)m * ldo + c0 + c] = v;
       tile[m * ldt + c] = v;
-      for (int q = 0; q < gc.n; ++q)
-        ((T *)gc.dst[q])[(size_t)m * gc.ld[q] + c0 + c] =
-            Elt<T>::from_f(Elt<T>::to_f(((const T *)gc.gamma[q])[c0 + c]) * v);
+      if (own) {
+#pragma unroll
+        for (int q = 0; q < kMaxLayers + 1; ++q)
+          if (q < gc.n)
+            ((T *)gc.dst[q])[(size_t)m * gc.ld[q] + c0 + c] = Elt<T>::from_f(Elt<T>::to_f(pre.g[q]) * v);
+      } else {
+        for (int q = 0; q < gc.n; ++q)
+          ((T *)gc.dst[q])[(size_t)m * gc.ld[q] + c0 + c] =
+              Elt<T>::from_f(Elt<T>::to_f(((const T *)gc.gamma[q])[c0 + c]) * v);
+      }
     }
     if (ssq) {
       __syncthreads();
@@ -365,6 +599,10 @@ __device__ __forceinline__ int rope_dim(int cc, int D) {
 }
 
 template <typename T> struct EpiQkv {
+  static constexpr bool kRowStream = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   QkvArgs a;
   int nvcols;
   __device__ const T *wrow(int c) const {
@@ -384,7 +622,7 @@ template <typename T> struct EpiQkv {
     }
     return base + (size_t)row * a.d;
   }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     const int qd = a.Hq * a.D, kvd = a.Hkv * a.D, D = a.D;
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
@@ -397,6 +635,13 @@ template <typename T> struct EpiQkv {
         if (isq && t != a.nctx - 1) continue;
         const int lc = isq ? vc : vc - qd;
         const int h = lc / D, cc = lc % D, dd = rope_dim(cc, D);
+        if (!a.rotate) {  // attention rotates
+          if (isq)
+            a.q_out[((size_t)b * a.Hq + h) * D + dd] = val;
+          else
+            a.k_out[(((size_t)b * a.nctx + t) * a.Hkv + h) * D + dd] = val;
+          continue;
+        }
         const float pv = tile[m * ldt + (c ^ 8)];
         const int P = a.cu_prefix[b + 1] - a.cu_prefix[b];
         const int pos = min(a.cascade ? P + j : P, a.rope_npos - 1);
@@ -417,6 +662,10 @@ template <typename T> struct EpiQkv {
 };
 
 template <typename T> struct EpiSwiglu {
+  static constexpr bool kRowStream = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 2;  // gate/up tile pairs
   const T *wg, *wu;
   int ldw, I, nvcols;  // nvcols = 2*I
   T *out;
@@ -426,7 +675,7 @@ template <typename T> struct EpiSwiglu {
     const int p = c >> 5, f = (c >> 4) & 1, n = c & 15;
     return (f ? wu : wg) + (size_t)(p * 16 + n) * ldw;
   }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     const int half = span >> 1;
     for (int idx = threadIdx.x; idx < M * half; idx += blockDim.x) {
       const int m = idx / half, q = idx % half;
@@ -444,10 +693,69 @@ template <typename T> struct EpiSwiglu {
 // Shared LM head: per (row, column tile) max, sum of exp(z - max) and the top-k
 // (largest logit first, equal logits by lower draft id); logits optionally kept.
 template <typename T> struct EpiLm {
+  static constexpr bool kRowStream = false;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 4, kMidNtwMin = 4;  // 64-column tiles, as lmhead_tiles counts
   LmArgs a;
   int ldw, nvcols;
   __device__ const T *wrow(int c) const { return (const T *)a.w + (size_t)c * ldw; }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span) const {
+
+  // Many rows (batched drafting): thread = row.  The tile's columns are
+  // scanned in increasing id order into a sorted list of KL (value, id)
+  // pairs; an equal value never displaces an earlier entry, so ties go to the
+  // lower id without comparing ids.  NaN compares false and is never taken.
+  template <int KL>
+  __device__ void finish_rows(const float *tile, int ldt, int M, int c0, int span) const {
+    const int m = threadIdx.x;
+    if (m >= M) return;
+    const int nvalid = min(span, nvcols - c0);
+    const int nwg = gridDim.x, tileid = blockIdx.x;
+    const float *row = tile + m * ldt;
+    float mx = -INFINITY;
+    for (int c = 0; c < nvalid; ++c) mx = fmaxf(mx, row[c]);
+    float se = 0.f;
+    float vs[KL];
+    int is[KL];
+#pragma unroll
+    for (int j = 0; j < KL; ++j) {
+      vs[j] = -INFINITY;
+      is[j] = 0x7fffffff;
+    }
+    for (int c = 0; c < nvalid; ++c) {
+      const float x = row[c];
+      se += expf(x - mx);
+      if (a.logits) a.logits[(size_t)m * nvcols + c0 + c] = x;
+#pragma unroll
+      for (int j = KL - 1; j >= 1; --j) {
+        const bool prev = vs[j - 1] < x, here = vs[j] < x;
+        vs[j] = prev ? vs[j - 1] : (here ? x : vs[j]);
+        is[j] = prev ? is[j - 1] : (here ? c0 + c : is[j]);
+      }
+      if (vs[0] < x) {
+        vs[0] = x;
+        is[0] = c0 + c;
+      }
+    }
+    const size_t pb = (size_t)m * nwg + tileid;
+    a.part_max[pb] = mx;
+    a.part_sum[pb] = se;
+#pragma unroll
+    for (int j = 0; j < KL; ++j)
+      if (j < a.topk) {
+        a.cand_val[pb * kMaxTopk + j] = is[j] != 0x7fffffff ? vs[j] : -INFINITY;
+        a.cand_idx[pb * kMaxTopk + j] = is[j];
+      }
+  }
+
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
+    if (M > 16) {
+      if (a.topk <= 2) finish_rows<2>(tile, ldt, M, c0, span);
+      else if (a.topk <= 4) finish_rows<4>(tile, ldt, M, c0, span);
+      else if (a.topk <= 8) finish_rows<8>(tile, ldt, M, c0, span);
+      else finish_rows<16>(tile, ldt, M, c0, span);
+      return;
+    }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int nvalid = min(span, nvcols - c0);
     const int nwg = gridDim.x, tileid = blockIdx.x;
@@ -465,13 +773,11 @@ template <typename T> struct EpiLm {
         id[p] = ok ? c0 + c : 0x7fffffff;
         mx = fmaxf(mx, v[p]);
       }
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      mx = group_max<64>(mx);
       float se = 0.f;
 #pragma unroll
       for (int p = 0; p < PER; ++p) se += (id[p] != 0x7fffffff) ? expf(v[p] - mx) : 0.f;
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) se += __shfl_xor(se, o);
+      se = group_sum<64>(se);
       if (a.logits) {
 #pragma unroll
         for (int p = 0; p < PER; ++p)
@@ -506,12 +812,33 @@ template <typename T> struct EpiLm {
 // ---------------------------------------------------------------------------
 // Dispatch.
 // ---------------------------------------------------------------------------
-// Unroll depth of the load pipeline and split-K width shrink as the number of
-// 16-row tiles grows, to bound registers and the LDS reduction buffer.
+// Split-K width of the up-to-32-row kernel.
 template <int WKmax, int MT> struct SplitK {
-  static constexpr int cap = MT <= 2 ? 8 : (MT <= 4 ? 2 : 1);
+  static constexpr int cap = 8;
   static constexpr int value = WKmax < cap ? WKmax : cap;
 };
+
+template <class Epi>
+static hipError_t run_gemv(const bf16_t *A, int lda, const ARows &arows, int M, int K,
+                           const Epi &epi, const NormA *na, int mr, size_t lds, hipStream_t s) {
+  constexpr int W = 4 * (Epi::kMidNtwMin > 1 ? Epi::kMidNtwMin : 1);  // SPAN = 16 * kMidNtwMin
+  constexpr int SPAN = 4 * W;
+  const int grid = (epi.nvcols + SPAN - 1) / SPAN;
+  const NormA n0 = na ? *na : NormA{nullptr, 0, 1, 0, 1, 1, 0.f};
+#define FE_GEMV(MRV, NORMV)                                                                      \
+  hipLaunchKernelGGL((k_gemv<MRV, W, NORMV, Epi>), dim3(grid), dim3(64 * W), lds, s, A, lda, arows, \
+                     M, K, n0, epi)
+#define FE_GEMV_M(NORMV)              \
+  switch (mr) {                       \
+    case 1: FE_GEMV(1, NORMV); break; \
+    case 2: FE_GEMV(2, NORMV); break; \
+    default: FE_GEMV(4, NORMV); break; \
+  }
+  if (na) FE_GEMV_M(true) else FE_GEMV_M(false)
+#undef FE_GEMV_M
+#undef FE_GEMV
+  return hipGetLastError();
+}
 
 template <typename T, int NT, int WKmax, int WN, class Epi>
 static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K, const Epi &epi,
@@ -520,21 +847,42 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
   const int grid = (epi.nvcols + SPAN - 1) / SPAN;
   const int mt = (M + 15) / 16;
   const NormA n0 = na ? *na : NormA{nullptr, 0, 1, 0, 1, 1, 0.f};
+  if constexpr (sizeof(T) == 2) {
+    // up to 4 rows whose padded input rows fit the LDS budget: row streaming
+    // (the LM head's per-row top-k is cheaper on the matrix-core tiles)
+    if constexpr (Epi::kRowStream) {
+      const int mr = M <= 1 ? 1 : M <= 2 ? 2 : 4;
+      const size_t lds = (size_t)mr * ((K + 127) & ~127) * 2;
+      if (M <= 4 && lds <= (size_t)kGvMaxLds && K >= 8) return run_gemv(A, lda, arows, M, K, epi, na, mr, lds, s);
+    }
+  }
   if (na) {
     if (mt != 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_gemm<T, 1, NT, SplitK<WKmax, 1>::value, WN, true, Epi>), dim3(grid),
                        dim3(64 * SplitK<WKmax, 1>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
     return hipGetLastError();
   }
-#define FE_GEMM_CASE(MTV)                                                              \
-  hipLaunchKernelGGL((k_gemm<T, MTV, NT, SplitK<WKmax, MTV>::value, WN, false, Epi>), \
-                     dim3(grid), dim3(64 * SplitK<WKmax, MTV>::value * WN), 0, s, A, lda, arows, M, K, n0, epi)
-  if (mt <= 1) FE_GEMM_CASE(1);
-  else if (mt <= 2) FE_GEMM_CASE(2);
-  else if (mt <= 4) FE_GEMM_CASE(4);
-  else if (mt <= 8) FE_GEMM_CASE(8);
-  else FE_GEMM_CASE(16);
-#undef FE_GEMM_CASE
+  if (mt <= 2) {
+    if (mt <= 1)
+      hipLaunchKernelGGL((k_gemm<T, 1, NT, SplitK<WKmax, 1>::value, WN, false, Epi>), dim3(grid),
+                         dim3(64 * SplitK<WKmax, 1>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
+    else
+      hipLaunchKernelGGL((k_gemm<T, 2, NT, SplitK<WKmax, 2>::value, WN, false, Epi>), dim3(grid),
+                         dim3(64 * SplitK<WKmax, 2>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
+    return hipGetLastError();
+  }
+  // batched rows: all M rows per workgroup, columns split over the grid
+  if (M > kMidRows) return hipErrorInvalidValue;
+  int ntw = Epi::kMidNtw;
+  if (ntw == 0) ntw = epi.nvcols >= 64 * 256 ? 4 : (epi.nvcols >= 32 * 256 ? 2 : 1);
+  if (ntw < Epi::kMidNtwMin) ntw = Epi::kMidNtwMin;
+#define FE_GEMM_MID(NTWV)                                                                    \
+  hipLaunchKernelGGL((k_gemm_mid<T, NTWV, Epi>), dim3((epi.nvcols + 16 * NTWV - 1) / (16 * NTWV)), \
+                     dim3(256), 0, s, A, lda, arows, M, K, epi)
+  if (ntw >= 4) FE_GEMM_MID(4);
+  else if (ntw == 2) FE_GEMM_MID(2);
+  else if constexpr (Epi::kMidNtwMin <= 1) FE_GEMM_MID(1);
+#undef FE_GEMM_MID
   return hipGetLastError();
 }
 
@@ -569,7 +917,7 @@ hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, c
   const int nv = (a.Hq + 2 * a.Hkv) * a.D;
   if (dt) {
     EpiQkv<bf16_t> e{a, nv};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, arows, M, a.d, e, na, s);
+    return run_gemm<bf16_t, 1, 4, 1>((const bf16_t *)A, lda, arows, M, a.d, e, na, s);
   }
   EpiQkv<float> e{a, nv};
   return run_gemm<float, 1, 8, 1>((const float *)A, lda, arows, M, a.d, e, na, s);

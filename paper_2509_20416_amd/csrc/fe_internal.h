@@ -40,14 +40,84 @@ __device__ __forceinline__ float topk_key_value(uint64_t key) {
 __device__ __forceinline__ int topk_key_id(uint64_t key) {
   return (int)(0xffffffffu - (uint32_t)key);
 }
+// ---- cross-lane reductions in registers (no LDS traffic) -------------------------
+// DPP controls: quad_perm [1,0,3,2] (lane^1), [2,3,0,1] (lane^2), row_half_mirror
+// (the other quad of an 8-lane half once quads are uniform), row_ror:8 (lane^8).
+template <int CTRL> __device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+// permlane16_swap / permlane32_swap of a register with itself return, in every
+// lane, the pair {x[lane], x[lane ^ 16]} (resp. lane ^ 32) in some order.
+__device__ __forceinline__ float xor16_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor16_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// Sum over aligned groups of RL lanes (8, 16, 32), result in every lane of the
+// group; each step adds two equal-valued halves in either order, so all lanes
+// of a group hold bit-identical sums.
+template <int RL> __device__ __forceinline__ float group_sum(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x141>(x);
+  if constexpr (RL >= 16) x += dpp_f<0x128>(x);
+  if constexpr (RL >= 32) x = xor16_sum(x);
+  if constexpr (RL >= 64) x = xor32_sum(x);
+  return x;
+}
+template <int RL> __device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, dpp_f<0xB1>(x));
+  x = fmaxf(x, dpp_f<0x4E>(x));
+  x = fmaxf(x, dpp_f<0x141>(x));
+  if constexpr (RL >= 16) x = fmaxf(x, dpp_f<0x128>(x));
+  if constexpr (RL >= 32) x = xor16_max(x);
+  if constexpr (RL >= 64) x = xor32_max(x);
+  return x;
+}
+// Max over the row groups of a wave, given values uniform within RL-lane groups.
+template <int RL> __device__ __forceinline__ float across_groups_max(float x) {
+  if constexpr (RL <= 8) x = fmaxf(x, dpp_f<0x128>(x));
+  if constexpr (RL <= 16) x = xor16_max(x);
+  if constexpr (RL <= 32) x = xor32_max(x);
+  return x;
+}
+
+// 64-bit versions: both halves take the same lane permutation.
+template <int CTRL> __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, 0xf, 0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, 0xf, 0xf, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint64_t xor16_max_u64(uint64_t x) {
+  const auto l = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
+  const auto h = __builtin_amdgcn_permlane16_swap((uint32_t)(x >> 32), (uint32_t)(x >> 32), false, false);
+  return umax64(((uint64_t)h[0] << 32) | l[0], ((uint64_t)h[1] << 32) | l[1]);
+}
+__device__ __forceinline__ uint64_t xor32_max_u64(uint64_t x) {
+  const auto l = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);
+  const auto h = __builtin_amdgcn_permlane32_swap((uint32_t)(x >> 32), (uint32_t)(x >> 32), false, false);
+  return umax64(((uint64_t)h[0] << 32) | l[0], ((uint64_t)h[1] << 32) | l[1]);
+}
+// Maximum over the whole wave, in every lane.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const uint64_t w = ((uint64_t)(uint32_t)__shfl_xor((int)(v >> 32), o) << 32) |
-                       (uint32_t)__shfl_xor((int)(uint32_t)v, o);
-    v = w > v ? w : v;
-  }
-  return v;
+  v = umax64(v, dpp_u64<0xB1>(v));
+  v = umax64(v, dpp_u64<0x4E>(v));
+  v = umax64(v, dpp_u64<0x141>(v));
+  v = umax64(v, dpp_u64<0x128>(v));
+  v = xor16_max_u64(v);
+  return xor32_max_u64(v);
 }
 constexpr uint64_t kNoKey = 0ull;  // below every real key (the id 0xffffffff never occurs)
 
@@ -132,8 +202,9 @@ struct QkvArgs {
   int rope_npos;
   float *q_out;              // [B, Hq, D]       (row t == nctx-1 only)
   float *k_out, *v_out;      // [B, nctx, Hkv, D]
+  int rotate;                // apply the rotary embedding here (else attention does)
 };
-// Q/K/V projections of the RMS-normed context rows with rotary embedding of Q and K.
+// Q/K/V projections of the RMS-normed context rows; with a.rotate, rotary embedding of Q and K.
 // With `na` (M <= 16) A holds gamma * x rows and the RMSNorm scale is fused.
 hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
                     const NormA *na, hipStream_t s);
@@ -166,13 +237,15 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // Attention of the query rows q [B, Hq, D] over the prefix cache (chunks
 // 0..nch-1 of kAttnChunk keys; keys beyond are not read) and the nctx cascade
 // keys/values knew/vnew [B, nctx, Hkv, D] -> out [B, Hq*D] (storage type).
-// Each workgroup covers cpw chunks of one sequence; part (B*Hq*nch_ld*(D+2)
+// bf16: q and the cascade keys arrive unrotated and are rotated here with the
+// table `rope` (cascade != 0: cascade row j at position P + j, else P); fp32:
+// they arrive rotated.  Each workgroup covers cpw chunks of one sequence; part (B*Hq*nch_ld*(D+2)
 // floats, nch_ld >= ceil(nch / cpw)) holds the partials of sequences that span
 // several workgroups, merged by a second launch.
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
                      const float *q, const float *knew, const float *vnew, int nctx,
                      float *part, int nch, int nch_ld, int cpw, void *out, int B, int Hq,
-                     int Hkv, int D, hipStream_t s);
+                     int Hkv, int D, const float *rope, int cascade, hipStream_t s);
 // 128-key sub-chunks per attention workgroup for a launch of B sequences over
 // nch = ceil(max_prefix / 128) sub-chunks
 int attention_cpw(int B, int Hkv, int ngroups, int nch);
@@ -187,10 +260,11 @@ hipError_t topk_merge(const float *part_max, const float *part_sum, const float 
                       const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
                       hipStream_t s);
 
-// Backbone Expansion tree of every sequence.
+// Backbone Expansion tree of every sequence; P_b from prefix_lens, or from
+// cu_prefix when prefix_lens is NULL.
 hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int32_t *topk_ids,
-                      const int32_t *prefix_lens, int32_t *tokens, int32_t *parents,
-                      int32_t *depth, int32_t *positions, uint8_t *mask, int32_t *retrieve,
-                      hipStream_t s);
+                      const int32_t *prefix_lens, const int32_t *cu_prefix, int32_t *tokens,
+                      int32_t *parents, int32_t *depth, int32_t *positions, uint8_t *mask,
+                      int32_t *retrieve, hipStream_t s);
 
 }  // namespace fe

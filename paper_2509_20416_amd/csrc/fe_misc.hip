@@ -9,36 +9,67 @@ namespace fe {
 // y = gamma * x / sqrt(mean(x^2) + eps), fp32 statistics, storage-type output.
 // One workgroup per row; fixed-order reductions.
 // ---------------------------------------------------------------------------
-template <typename T>
+// One workgroup per row; the row (NV float4 per thread, d <= 1024*NV) and its
+// gains are loaded once, up front, and stay in registers.
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float *__restrict__ X, int per, int j0,
                                                  long outer, long inner,
                                                  const T *__restrict__ gamma, T *__restrict__ out,
                                                  int d, float eps) {
   __shared__ float red[4];
-  const int r = blockIdx.x;
+  const int r = blockIdx.x, tid = threadIdx.x;
   const float *x = X + (long)(r / per) * outer + (long)(j0 + r % per) * inner;
-  float ss = 0.f;
-  for (int e = threadIdx.x; e < d; e += 256) ss += x[e] * x[e];
+  f32x4 xv[NV];
+  float gv[NV][4];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  for (int u = 0; u < NV; ++u) {
+    const int e = 4 * (tid + 256 * u);
+    const int ec = min(e, d - 4);
+    xv[u] = *reinterpret_cast<const f32x4 *>(x + ec);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) gv[u][q] = Elt<T>::to_f(gamma[ec + q]);
+    if (e >= d) xv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u) ss += xv[u].x * xv[u].x + xv[u].y * xv[u].y + xv[u].z * xv[u].z + xv[u].w * xv[u].w;
+  ss = group_sum<64>(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
   T *y = out + (long)r * d;
-  for (int e = threadIdx.x; e < d; e += 256)
-    y[e] = Elt<T>::from_f(Elt<T>::to_f(gamma[e]) * (x[e] * inv));
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int e = 4 * (tid + 256 * u);
+    if (e < d) {
+      y[e] = Elt<T>::from_f(gv[u][0] * (xv[u].x * inv));
+      y[e + 1] = Elt<T>::from_f(gv[u][1] * (xv[u].y * inv));
+      y[e + 2] = Elt<T>::from_f(gv[u][2] * (xv[u].z * inv));
+      y[e + 3] = Elt<T>::from_f(gv[u][3] * (xv[u].w * inv));
+    }
+  }
+}
+
+template <typename T>
+static void launch_rmsnorm(const float *X, int rows, int per, int j0, long outer, long inner,
+                           const void *gamma, void *out, int d, float eps, hipStream_t s) {
+#define FE_RMS(NVV)                                                                         \
+  hipLaunchKernelGGL((k_rmsnorm<T, NVV>), dim3(rows), dim3(256), 0, s, X, per, j0, outer, inner, \
+                     (const T *)gamma, (T *)out, d, eps)
+  if (d <= 1024) FE_RMS(1);
+  else if (d <= 2048) FE_RMS(2);
+  else if (d <= 4096) FE_RMS(4);
+  else FE_RMS(8);
+#undef FE_RMS
 }
 
 hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long outer, long inner,
                         const void *gamma, void *out, int d, float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (dt)
-    hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(rows), dim3(256), 0, s, X, per, j0, outer, inner,
-                       (const bf16_t *)gamma, (bf16_t *)out, d, eps);
-  else
-    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, X, per, j0, outer, inner,
-                       (const float *)gamma, (float *)out, d, eps);
+  if (d > 8192 || d % 4) return hipErrorInvalidValue;
+  if (dt) launch_rmsnorm<bf16_t>(X, rows, per, j0, outer, inner, gamma, out, d, eps, s);
+  else launch_rmsnorm<float>(X, rows, per, j0, outer, inner, gamma, out, d, eps, s);
   return hipGetLastError();
 }
 
@@ -97,8 +128,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
   for (int u = 0; u < kStatLoads; ++u)
     if (tid + 256 * u < nwg) m = fmaxf(m, pmv[u]);
   for (int t = tid + 256 * kStatLoads; t < nwg; t += 256) m = fmaxf(m, pm[t]);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  m = group_max<64>(m);
   if (lane == 0) sv[wave] = m;
   __syncthreads();
   const float mu = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
@@ -108,8 +138,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
   for (int u = 0; u < kStatLoads; ++u)
     if (tid + 256 * u < nwg) S += psv[u] * expf(pmv[u] - mu);
   for (int t = tid + 256 * kStatLoads; t < nwg; t += 256) S += ps[t] * expf(pm[t] - mu);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) S += __shfl_xor(S, o);
+  S = group_sum<64>(S);
   if (lane == 0) sv[wave] = S;
   // per-wave top-k
   for (int r = 0; r < topk; ++r) {
@@ -165,11 +194,12 @@ __global__ __launch_bounds__(256) void k_build_tree(int N, int k,
                                                     const int32_t *__restrict__ root_tokens,
                                                     const int32_t *__restrict__ topk_ids,
                                                     const int32_t *__restrict__ prefix_lens,
+                                                    const int32_t *__restrict__ cu_prefix,
                                                     int32_t *tokens, int32_t *parents,
                                                     int32_t *depth, int32_t *positions,
                                                     uint8_t *mask, int32_t *retrieve) {
   const int b = blockIdx.x, T = 1 + N * k, NL = N * (k - 1) + 1;
-  const int P = prefix_lens[b];
+  const int P = prefix_lens ? prefix_lens[b] : cu_prefix[b + 1] - cu_prefix[b];
   for (int n = threadIdx.x; n < T; n += blockDim.x) {
     int lvl = 0, tok = root_tokens[b], par = -1;
     if (n > 0) {
@@ -213,12 +243,12 @@ __global__ __launch_bounds__(256) void k_build_tree(int N, int k,
 }
 
 hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int32_t *topk_ids,
-                      const int32_t *prefix_lens, int32_t *tokens, int32_t *parents,
-                      int32_t *depth, int32_t *positions, uint8_t *mask, int32_t *retrieve,
-                      hipStream_t s) {
+                      const int32_t *prefix_lens, const int32_t *cu_prefix, int32_t *tokens,
+                      int32_t *parents, int32_t *depth, int32_t *positions, uint8_t *mask,
+                      int32_t *retrieve, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_build_tree, dim3(B), dim3(256), 0, s, N, k, root_tokens, topk_ids,
-                     prefix_lens, tokens, parents, depth, positions, mask, retrieve);
+                     prefix_lens, cu_prefix, tokens, parents, depth, positions, mask, retrieve);
   return hipGetLastError();
 }
 

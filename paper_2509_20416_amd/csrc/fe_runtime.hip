@@ -94,6 +94,7 @@ fe_status check_config(const fe_config *c) {
   const long qd = (long)c->n_q_heads * c->head_dim;
   if (c->hidden % kstep || c->intermediate % kstep || qd % kstep)
     return fail(FE_E_UNSUPPORTED, "hidden, intermediate and n_q_heads*head_dim must be multiples of %d", kstep);
+  if (c->hidden > 8192) return fail(FE_E_UNSUPPORTED, "hidden > 8192");
   if (c->draft_vocab % 16) return fail(FE_E_UNSUPPORTED, "draft_vocab must be a multiple of 16");
   if ((long)lmhead_tiles(c->draft_vocab) * c->max_topk > kMergeMaxCand)
     return fail(FE_E_UNSUPPORTED, "draft_vocab * max_topk too large for the top-k merge");
@@ -125,6 +126,7 @@ struct fe_drafter {
   std::vector<const void *> last_k, last_v;
   fe_kv_view last_kv{};
   fe_draft_out last_out{};
+  fe_tree_out last_tree{};
   hipEvent_t ev_a = nullptr, ev_b = nullptr;
 };
 
@@ -283,7 +285,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
     // separate pass otherwise
     QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
-               (const float *)(ws + L.rope), L.npos, q, knew, vnew};
+               (const float *)(ws + L.rope), L.npos, q, knew, vnew, dt ? 0 : 1};
     if (fuse_q(i)) {
       const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
       FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
@@ -295,7 +297,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     // attention over the layer's prefix cache plus the cascade keys
     FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
                                       vnew, nctx, part, nch, nch_ld, cpw, ao, B, Hq, Hkv, D,
-                                      s));
+                                      (const float *)(ws + L.rope), cascade ? 1 : 0, s));
     // x' = x_{i-1} + W_o o
     GainCopies gc_p{};
     if (fuse_m) {
@@ -334,6 +336,11 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   if (out->hidden)
     FE_OTHER(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
                             hipMemcpyDeviceToDevice, s));
+  if (out->tree) {  // Backbone Expansion tree of this pass: root = next token
+    const fe_tree_out *t = out->tree;
+    FE_OTHER(build_tree(B, N, topk, next_tokens, out->topk_ids, nullptr, kv->cu_prefix, t->tokens,
+                        t->parents, t->depth, t->positions, t->mask, t->retrieve, s));
+  }
   return FE_OK;
 }
 
@@ -361,6 +368,11 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
       return fail(FE_E_ALIGN, "kv cache of layer %d is not 16-byte aligned", l);
   }
   if (out->logits && ((uintptr_t)out->logits & 3u)) return fail(FE_E_ALIGN, "logits misaligned");
+  if (out->tree) {
+    const fe_tree_out *t = out->tree;
+    if (!t->tokens || !t->parents || !t->depth || !t->positions || !t->mask || !t->retrieve)
+      return fail(FE_E_INVALID, "every tree output is required when out->tree is set");
+  }
   hipStream_t s = (hipStream_t)stream;
   if (!h->table_ready) {  // first pass on this handle: the rotary table
     FE_TRY(rope_table((float *)(h->ws + h->L.rope), h->L.npos, c.head_dim, (double)c.rope_theta, s));
@@ -379,6 +391,10 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   h->last_kv.k = h->last_k.data();
   h->last_kv.v = h->last_v.data();
   h->last_out = *out;
+  if (out->tree) {
+    h->last_tree = *out->tree;
+    h->last_out.tree = &h->last_tree;
+  }
 
   if (!h->graph_mode) return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
 
@@ -386,6 +402,12 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
                                 (uintptr_t)topk, (uintptr_t)out->topk_ids,
                                 (uintptr_t)out->topk_probs, (uintptr_t)out->topk_draft,
+                                (uintptr_t)(out->tree ? out->tree->tokens : nullptr),
+                                (uintptr_t)(out->tree ? out->tree->parents : nullptr),
+                                (uintptr_t)(out->tree ? out->tree->depth : nullptr),
+                                (uintptr_t)(out->tree ? out->tree->positions : nullptr),
+                                (uintptr_t)(out->tree ? out->tree->mask : nullptr),
+                                (uintptr_t)(out->tree ? out->tree->retrieve : nullptr),
                                 (uintptr_t)out->logits, (uintptr_t)out->hidden,
                                 (uintptr_t)h->attn_split};
   for (int l = 0; l < c.n_layers; ++l) {
@@ -450,7 +472,7 @@ extern "C" fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk,
   if (!out || !out->tokens || !out->parents || !out->depth || !out->positions || !out->mask ||
       !out->retrieve)
     return fail(FE_E_INVALID, "every tree output is required");
-  FE_TRY(build_tree(batch, c.n_layers, topk, root_tokens, topk_ids, prefix_lens, out->tokens,
+  FE_TRY(build_tree(batch, c.n_layers, topk, root_tokens, topk_ids, prefix_lens, nullptr, out->tokens,
                     out->parents, out->depth, out->positions, out->mask, out->retrieve,
                     (hipStream_t)stream));
   return FE_OK;

@@ -126,13 +126,21 @@ class Drafter:
         return o
 
     def forward(self, di: DeviceInputs, topk: Optional[int] = None, logits=False, hidden=False,
-                out: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+                out: Optional[Dict[str, object]] = None,
+                tree: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+        """One drafting pass; with `tree` (from alloc_tree) the Backbone Expansion
+        tree of the pass is built in the same launch sequence."""
         k = int(topk or self.cfg.topk)
         if out is None:
             out = self.alloc_outputs(di.batch, k, logits, hidden)
         p = lambda n: out[n].data_ptr() if n in out else None
         self._out = fe.fe_draft_out(p("topk_ids"), p("topk_probs"), p("topk_draft"),
                                     p("logits"), p("hidden"))
+        if tree is not None:
+            self._fwd_tree = fe.fe_tree_out(*[tree[n].data_ptr() for n in
+                                              ("tokens", "parents", "depth", "positions", "mask",
+                                               "retrieve")])
+            self._out.tree = fe.C.pointer(self._fwd_tree)
         fe.fe_draft_forward(self.handle, di.batch, di.features.data_ptr(),
                             di.next_tokens.data_ptr(), self.kv_view(di), k, self._out,
                             self.stream())

@@ -50,14 +50,15 @@ class fe_kv_view(C.Structure):
                 ("cu_prefix", C.c_void_p), ("max_prefix", C.c_int32)]
 
 
-class fe_draft_out(C.Structure):
-    _fields_ = [("topk_ids", C.c_void_p), ("topk_probs", C.c_void_p), ("topk_draft", C.c_void_p),
-                ("logits", C.c_void_p), ("hidden", C.c_void_p)]
-
-
 class fe_tree_out(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("tokens", "parents", "depth", "positions", "mask",
                                           "retrieve")]
+
+
+class fe_draft_out(C.Structure):
+    _fields_ = [("topk_ids", C.c_void_p), ("topk_probs", C.c_void_p), ("topk_draft", C.c_void_p),
+                ("logits", C.c_void_p), ("hidden", C.c_void_p),
+                ("tree", C.POINTER(fe_tree_out))]
 
 
 _lib = None

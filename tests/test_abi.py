@@ -50,7 +50,7 @@ def test_workspace_bytes(fe):
     (dict(head_dim=96), "FE_E_UNSUPPORTED"), (dict(n_q_heads=30), "FE_E_INVALID"),
     (dict(dtype=7), "FE_E_INVALID"), (dict(cascade_ctx=3), "FE_E_INVALID"),
     (dict(max_topk=17), "FE_E_UNSUPPORTED"), (dict(n_layers=17), "FE_E_UNSUPPORTED"),
-    (dict(hidden=4100), "FE_E_UNSUPPORTED"), (dict(max_batch=64, n_layers=5), "FE_E_UNSUPPORTED"),
+    (dict(hidden=4100), "FE_E_UNSUPPORTED"), (dict(hidden=8224), "FE_E_UNSUPPORTED"), (dict(max_batch=64, n_layers=5), "FE_E_UNSUPPORTED"),
     (dict(hidden=0), "FE_E_INVALID"), (dict(rope_theta=0.0), "FE_E_INVALID"),
 ])
 def test_create_rejects_bad_config(fe, kw, status):

@@ -85,6 +85,17 @@ def test_attention_split_parity(cfg, split):
     _run(cfg, seed=4, prefix_lens=plens, attn_split=split)
 
 
+# More than 32 rows take the batched-rows GEMM (all rows per workgroup, LDS-
+# staged A and weights) and the per-row LM-head top-k: batch 12 x N 3 = 36
+# LM-head rows and up to 36 QKV rows; the MHA config with batch 9 x N 4.
+@pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16.with_(batch=12, name="small_gqa_bf16_b12"),
+                                 C.SMALL_GQA_F32.with_(batch=12, name="small_gqa_f32_b12"),
+                                 C.SMALL_MHA_BF16_D128.with_(batch=9, name="small_mha_bf16_d128_b9")],
+                         ids=lambda c: c.name)
+def test_batched_rows_parity(cfg):
+    _run(cfg, seed=5)
+
+
 def test_topk_edge_values():
     """k = 1 (chain tree) and k = max (16)."""
     for k in (1, 16):
@@ -135,6 +146,27 @@ def test_deterministic_and_graph_replay_bitwise():
         _ = torch.ones(1000, device="cuda").sum().item()
         for n in a:
             np.testing.assert_array_equal(out[n].cpu().numpy(), a[n], err_msg=f"replay {rep} {n}")
+    dr.close()
+
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_tree_in_forward_matches_separate_build(graph):
+    """The tree built inside fe_draft_forward (P_b from cu_prefix) equals
+    fe_build_tree on the same top-k ids, bit for bit, on every replay."""
+    import torch
+    from paper_2509_20416_amd import Drafter
+    cfg = C.SMALL_GQA_BF16
+    w, inp = make_weights(cfg, 3), make_inputs(cfg, 3, np.array([0, 700, 65], np.int32))
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(inp.prefix_lens.max()), graph=graph)
+    di = dr.upload_inputs(inp)
+    for rep in range(3):
+        out = dr.alloc_outputs(cfg.batch, cfg.topk)
+        t1 = dr.alloc_tree(cfg.batch, cfg.topk)
+        dr.forward(di, out=out, tree=t1)
+        t2 = dr.build_tree(di, out["topk_ids"])
+        torch.cuda.synchronize()
+        for n in t1:
+            assert torch.equal(t1[n], t2[n]), (rep, n)
     dr.close()
 
 
