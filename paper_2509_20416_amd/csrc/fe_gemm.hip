@@ -348,73 +348,89 @@ __global__ __launch_bounds__(64 * W) void k_gemv(const bf16_t *__restrict__ A, i
 }
 
 // ---------------------------------------------------------------------------
-// Batched rows (17..256): one workgroup owns BN = 16*NTW output columns and
-// every row; wave w computes rows 64w..64w+63.  K advances in chunks of 128
-// bytes per row.  Each chunk of A (all rows) and of the BN weight rows is
-// staged in LDS (rows padded to 144 bytes) and feeds the MFMAs from there,
-// while the next A chunk and the next kWPre weight chunks are already in
-// registers.  Weights are read from HBM once; A (at most 256 rows) is served
-// by L2 to every workgroup.
+// Batched rows (17..256): one workgroup owns BN = 16*NTW*WN output columns and
+// every row; its four waves form WM = 4/WN row groups of 64 rows and WN column
+// groups of 16*NTW columns.  K advances in chunks of 128 bytes per row.  The
+// chunks of A (all rows) and of the BN weight rows go straight from memory to
+// an S-stage LDS ring with direct-to-LDS loads (global_load_lds_dwordx4), so
+// S-1 chunks are in flight without holding registers.  One load instruction
+// fills 1 KB of LDS contiguously (lane l -> byte 16l); 16-byte piece p of row
+// R sits at slot p ^ ((R >> 1) & 7) of its row, which keeps the MFMA fragment
+// reads free of bank conflicts without padding.  Weights are read from HBM
+// once; A (at most 256/WN rows) is served by L2 to every workgroup.
+// Synchronisation is a plain s_barrier after an explicit vmcnt wait: the
+// workgroup fence of __syncthreads would drain every load in flight.
 // ---------------------------------------------------------------------------
-constexpr int kMidRows = 256;
-constexpr int kMidRowBytes = 144;
-constexpr int kWPre = 3;  // weight chunks in flight per thread
+// 16 bytes per lane from global memory straight into LDS: lane l writes bytes
+// 16l..16l+15 after `lds` (wave-uniform).  A plain device function: called
+// directly from a kernel template the builtin leaves the kernel without its
+// host-side launch stub.
+__device__ __forceinline__ void lds_dma16(const void *src, void *lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
+}
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ int ring_slot(int row, int piece) { return row * 8 + (piece ^ ((row >> 1) & 7)); }
 
-template <typename T, int NTW, class Epi>
+template <typename T, int NTW, int WN, int S, class Epi>
 __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
                                                   int M, int K, Epi epi) {
   constexpr int E = Elt<T>::kPer16B;  // elements per 16-byte piece
   constexpr int KC = 8 * E;           // elements of K per chunk
-  constexpr int BN = NTW * 16;
-  constexpr int ALD = kMidRows * 8 / 256;     // A pieces per thread per chunk
-  constexpr int WLD = (BN * 8 + 255) / 256;   // weight pieces per thread per chunk
-  constexpr int kStage = (kMidRows + BN) * kMidRowBytes;
+  constexpr int WM = 4 / WN;
+  constexpr int MROWS = 64 * WM;      // rows this configuration holds
+  constexpr int BN = NTW * WN * 16;
+  static_assert(BN % 32 == 0, "weight slots must split evenly over the four waves");
+  constexpr int AI = MROWS / 32;      // A load instructions per wave per stage
+  constexpr int WI = BN / 32;         // weight load instructions per wave per stage
+  constexpr int CNT = AI + WI;
+  static_assert((S - 2) * CNT <= 63, "vmcnt range");
+  constexpr int ABYTES = MROWS * 128, STAGE = ABYTES + BN * 128;
   constexpr int LDT = BN + 1;
-  constexpr int kTile = kMidRows * LDT * 4;
-  __shared__ __attribute__((aligned(16))) char smem[kStage > kTile ? kStage : kTile];
-  char *sA = smem, *sW = smem + kMidRows * kMidRowBytes;
+  constexpr int TILE = MROWS * LDT * 4;
+  constexpr int SMEM = S * STAGE > TILE ? S * STAGE : TILE;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int wm = wave / WN, wn = wave % WN;
   const int c0 = blockIdx.x * BN;
   const int nch = (K + KC - 1) / KC;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
 
-  // piece p = tid + 256 i of a chunk: row p / 8, 16-byte piece p % 8 (element
-  // offset po); loads are unconditional at clamped in-bounds addresses and
-  // pieces past K, past the rows or past the columns are replaced by zero
-  const T *arow[ALD];
-  bool aok[ALD];
+  // the lane's slot in each of its load instructions, and the source row and
+  // piece offset that belong there (rows past M repeat row M-1: their products
+  // land in output rows that are never stored)
+  const T *asrc[AI];
+  int aoff[AI];
 #pragma unroll
-  for (int i = 0; i < ALD; ++i) {
-    const int row = (tid + 256 * i) >> 3;
-    aok[i] = row < M;
-    arow[i] = A + (size_t)arows.row(min(row, M - 1)) * lda;
+  for (int j = 0; j < AI; ++j) {
+    const int q = (j * 4 + wave) * 64 + lane, row = q >> 3;
+    asrc[j] = A + (size_t)arows.row(min(row, M - 1)) * lda;
+    aoff[j] = ((q & 7) ^ ((row >> 1) & 7)) * E;
   }
-  const T *wrw[WLD];
-  bool wok[WLD];
+  const T *wsrc[WI];
+  int woff[WI];
 #pragma unroll
-  for (int i = 0; i < WLD; ++i) {
-    const int n = (tid + 256 * i) >> 3;
-    wok[i] = n < BN && c0 + n < epi.nvcols;
-    wrw[i] = epi.wrow(min(c0 + min(n, BN - 1), epi.nvcols - 1));
+  for (int j = 0; j < WI; ++j) {
+    const int q = (j * 4 + wave) * 64 + lane, n = q >> 3;
+    wsrc[j] = epi.wrow(min(c0 + n, epi.nvcols - 1));
+    woff[j] = ((q & 7) ^ ((n >> 1) & 7)) * E;
   }
-  const int po = (tid & 7) * E;  // 256 is a multiple of 8: same piece for every i
-  auto ldA = [&](int ch, u32x4 (&ra)[ALD]) {
-    const int kk = ch * KC + po;
-    const int ka = min(kk, K - E);
+  // chunk ch (clamped: past the end the last chunk is fetched again, so every
+  // wave issues the same count), addresses clamped inside the rows
+  auto issue = [&](int ch) {
+    char *st = smem + (ch % S) * STAGE;
+    const int k = min(ch, nch - 1) * KC;
 #pragma unroll
-    for (int i = 0; i < ALD; ++i) {
-      const u32x4 v = *reinterpret_cast<const u32x4 *>(arow[i] + ka);
-      ra[i] = (aok[i] && kk < K) ? v : zero;
-    }
-  };
-  auto ldW = [&](int ch, u32x4 (&rw)[WLD]) {
-    const int kk = ch * KC + po;
-    const int ka = min(kk, K - E);
+    for (int j = 0; j < AI; ++j)
+      lds_dma16(asrc[j] + min(k + aoff[j], K - E), st + (j * 4 + wave) * 1024);
 #pragma unroll
-    for (int i = 0; i < WLD; ++i) {
-      const u32x4 v = ldg_stream(reinterpret_cast<const u32x4 *>(wrw[i] + ka));
-      rw[i] = (wok[i] && kk < K) ? v : zero;
-    }
+    for (int j = 0; j < WI; ++j)
+      lds_dma16(wsrc[j] + min(k + woff[j], K - E), st + ABYTES + (j * 4 + wave) * 1024);
   };
 
   f32x4 acc[4][NTW];
@@ -422,48 +438,41 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int f = 0; f < NTW; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int mrow0 = wave * 64;
+  const int mrow0 = wm * 64, ncol0 = wn * NTW * 16;
   const int mtiles = min(4, (M - mrow0 + 15) / 16);  // this wave's live 16-row tiles (may be <= 0)
 
-  u32x4 ra[ALD], rw[kWPre][WLD];
-  ldA(0, ra);
 #pragma unroll
-  for (int d = 0; d < kWPre; ++d) ldW(d, rw[d]);
+  for (int st = 0; st < S - 1; ++st) issue(st);
   for (int ch = 0; ch < nch; ++ch) {
-    __syncthreads();  // every wave is done reading the previous chunk
-#pragma unroll
-    for (int i = 0; i < ALD; ++i)
-      *reinterpret_cast<u32x4 *>(sA + ((tid + 256 * i) >> 3) * kMidRowBytes + (tid & 7) * 16) = ra[i];
-#pragma unroll
-    for (int i = 0; i < WLD; ++i)
-      if (tid + 256 * i < BN * 8)
-        *reinterpret_cast<u32x4 *>(sW + ((tid + 256 * i) >> 3) * kMidRowBytes + (tid & 7) * 16) = rw[0][i];
-    __syncthreads();
-    // next loads: A one chunk ahead, weights kWPre chunks ahead (past the end:
-    // clamped re-reads, masked to zero and never used)
-    ldA(ch + 1, ra);
-#pragma unroll
-    for (int d = 0; d + 1 < kWPre; ++d)
-#pragma unroll
-      for (int i = 0; i < WLD; ++i) rw[d][i] = rw[d + 1][i];
-    ldW(ch + kWPre, rw[kWPre - 1]);
+    wait_vmcnt<(S - 2) * CNT>();  // this wave's part of chunk ch has landed
+    wg_barrier();                 // so has everyone's; ring slot of chunk ch-1 is free
+    issue(ch + S - 1);
+    const char *st = smem + (ch % S) * STAGE;
+    if (ch == nch - 1 && K % KC) {  // ragged last chunk: zero the pieces past K
+      const int k = ch * KC;
+      for (int q = tid; q < (MROWS + BN) * 8; q += 256) {
+        const int row = q >> 3, piece = (q & 7) ^ ((row >> 1) & 7);
+        if (k + piece * E >= K) *reinterpret_cast<u32x4 *>(const_cast<char *>(st) + q * 16) = u32x4{0u, 0u, 0u, 0u};
+      }
+      wg_barrier();
+    }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       u32x4 bf[NTW];
 #pragma unroll
       for (int f = 0; f < NTW; ++f)
-        bf[f] = *reinterpret_cast<const u32x4 *>(sW + (f * 16 + r) * kMidRowBytes + ks * 64 + g * 16);
+        bf[f] = *reinterpret_cast<const u32x4 *>(st + ABYTES + ring_slot(ncol0 + f * 16 + r, ks * 4 + g) * 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         if (i < mtiles) {
-          const u32x4 af = *reinterpret_cast<const u32x4 *>(
-              sA + (mrow0 + i * 16 + r) * kMidRowBytes + ks * 64 + g * 16);
+          const u32x4 af = *reinterpret_cast<const u32x4 *>(st + ring_slot(mrow0 + i * 16 + r, ks * 4 + g) * 16);
 #pragma unroll
           for (int f = 0; f < NTW; ++f) mma16<T>(acc[i][f], af, bf[f]);
         }
     }
   }
-  __syncthreads();  // staging is dead; the buffer becomes the output tile
+  wait_vmcnt<0>();  // the chunks fetched past the end land before the ring is reused or freed
+  wg_barrier();
   float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -471,10 +480,11 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
 #pragma unroll
       for (int f = 0; f < NTW; ++f)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][f * 16 + r] = acc[i][f][v];
+        for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][ncol0 + f * 16 + r] = acc[i][f][v];
   __syncthreads();
   epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
 }
+
 // ---------------------------------------------------------------------------
 // Epilogues.
 // ---------------------------------------------------------------------------
@@ -862,7 +872,11 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
                        dim3(64 * SplitK<WKmax, 1>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
     return hipGetLastError();
   }
-  if (mt <= 2) {
+  // 17..32 rows over wide outputs (the batch-32 gate/up): the LDS-ring kernel
+  // with column-split waves beats the per-wave staging; narrow outputs would
+  // leave it too few workgroups
+  const bool ring_wide = mt == 2 && epi.nvcols >= 64 * 256;
+  if (mt <= 2 && !ring_wide) {
     if (mt <= 1)
       hipLaunchKernelGGL((k_gemm<T, 1, NT, SplitK<WKmax, 1>::value, WN, false, Epi>), dim3(grid),
                          dim3(64 * SplitK<WKmax, 1>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
@@ -871,17 +885,33 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
                          dim3(64 * SplitK<WKmax, 2>::value * WN), 0, s, A, lda, arows, M, K, n0, epi);
     return hipGetLastError();
   }
-  // batched rows: all M rows per workgroup, columns split over the grid
-  if (M > kMidRows) return hipErrorInvalidValue;
-  int ntw = Epi::kMidNtw;
-  if (ntw == 0) ntw = epi.nvcols >= 64 * 256 ? 4 : (epi.nvcols >= 32 * 256 ? 2 : 1);
-  if (ntw < Epi::kMidNtwMin) ntw = Epi::kMidNtwMin;
-#define FE_GEMM_MID(NTWV)                                                                    \
-  hipLaunchKernelGGL((k_gemm_mid<T, NTWV, Epi>), dim3((epi.nvcols + 16 * NTWV - 1) / (16 * NTWV)), \
-                     dim3(256), 0, s, A, lda, arows, M, K, epi)
-  if (ntw >= 4) FE_GEMM_MID(4);
-  else if (ntw == 2) FE_GEMM_MID(2);
-  else if constexpr (Epi::kMidNtwMin <= 1) FE_GEMM_MID(1);
+  // batched rows: all M rows per workgroup, columns split over the grid; the
+  // waves split columns as well when the rows do not fill four row groups
+  if (M > 256) return hipErrorInvalidValue;
+  const int wn = M <= 64 ? 4 : (M <= 128 ? 2 : 1);
+  int tt = Epi::kMidNtw;  // 16-column tiles per workgroup
+  if (tt == 0) {
+    tt = 2;
+    while (tt < 4 && (epi.nvcols + 32 * tt - 1) / (32 * tt) >= 192) tt *= 2;
+  }
+  if (tt < Epi::kMidNtwMin) tt = Epi::kMidNtwMin;
+  if (tt < wn) tt = wn;  // a tile per column group at least
+  if (tt < 2) tt = 2;    // weight slots split evenly over the waves
+  const int ntw = tt / wn;
+#define FE_GEMM_MID(NTWV, WNV, SV)                                                                   \
+  hipLaunchKernelGGL((k_gemm_mid<T, NTWV, WNV, SV, Epi>),                                           \
+                     dim3((epi.nvcols + 16 * NTWV * WNV - 1) / (16 * NTWV * WNV)), dim3(256), 0, s, A, \
+                     lda, arows, M, K, epi)
+  if (wn == 4) {
+    if (ntw >= 2) FE_GEMM_MID(2, 4, 4);
+    else FE_GEMM_MID(1, 4, 4);
+  } else if (wn == 2) {
+    if (ntw >= 2) FE_GEMM_MID(2, 2, 4);
+    else FE_GEMM_MID(1, 2, 4);
+  } else {
+    if (ntw >= 4) FE_GEMM_MID(4, 1, 2);  // the LM head's grid is wide: two workgroups per CU
+    else FE_GEMM_MID(2, 1, 3);
+  }
 #undef FE_GEMM_MID
   return hipGetLastError();
 }

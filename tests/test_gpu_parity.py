@@ -85,12 +85,16 @@ def test_attention_split_parity(cfg, split):
     _run(cfg, seed=4, prefix_lens=plens, attn_split=split)
 
 
-# More than 32 rows take the batched-rows GEMM (all rows per workgroup, LDS-
-# staged A and weights) and the per-row LM-head top-k: batch 12 x N 3 = 36
-# LM-head rows and up to 36 QKV rows; the MHA config with batch 9 x N 4.
+# More than 32 rows take the batched-rows GEMM (all rows per workgroup, A and
+# weights through an LDS ring) and the per-row LM-head top-k: batch 12 x N 3 =
+# 36 LM-head rows and up to 36 QKV rows; the MHA config with batch 9 x N 4.
 @pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16.with_(batch=12, name="small_gqa_bf16_b12"),
                                  C.SMALL_GQA_F32.with_(batch=12, name="small_gqa_f32_b12"),
-                                 C.SMALL_MHA_BF16_D128.with_(batch=9, name="small_mha_bf16_d128_b9")],
+                                 C.SMALL_MHA_BF16_D128.with_(batch=9, name="small_mha_bf16_d128_b9"),
+                                 # 36 rows through every GEMM; the down projection's K = 1376
+                                 # ends in a ragged 128-byte chunk
+                                 C.SMALL_GQA_BF16.with_(batch=36, prefix=(0, 300),
+                                                        name="small_gqa_bf16_b36")],
                          ids=lambda c: c.name)
 def test_batched_rows_parity(cfg):
     _run(cfg, seed=5)
