@@ -176,10 +176,10 @@ fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk, const int32_
  * arguments and replayed while they stay the same. */
 fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
 
-/* Attention work split: each attention workgroup covers this many 128-key
+/* Attention work split: each attention work unit covers this many 64-key
  * chunks of one sequence's prefix (0 = automatic, the default, which sizes the
- * grid to keep every compute unit streaming).  A sequence longer than one
- * workgroup's span leaves partial softmax states that a second launch merges;
+ * units to keep every compute unit streaming).  A sequence longer than one
+ * unit's span leaves partial softmax states that a second launch merges;
  * every split gives the same result up to rounding.  Meant for tuning and
  * testing.  Errors: FE_E_INVALID for a NULL handle or a value outside
  * [0, 65536]. */

@@ -361,16 +361,6 @@ __global__ __launch_bounds__(64 * W) void k_gemv(const bf16_t *__restrict__ A, i
 // Synchronisation is a plain s_barrier after an explicit vmcnt wait: the
 // workgroup fence of __syncthreads would drain every load in flight.
 // ---------------------------------------------------------------------------
-// 16 bytes per lane from global memory straight into LDS: lane l writes bytes
-// 16l..16l+15 after `lds` (wave-uniform).  A plain device function: called
-// directly from a kernel template the builtin leaves the kernel without its
-// host-side launch stub.
-__device__ __forceinline__ void lds_dma16(const void *src, void *lds) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
-}
-template <int N> __device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
 __device__ __forceinline__ void wg_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();

@@ -11,18 +11,23 @@ namespace fe {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // Storage types: bf16 is carried as its 16-bit pattern.
 typedef uint16_t bf16_t;
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// float -> bf16, round to nearest even (NaN stays NaN).
+// float -> bf16, round to nearest even (NaN stays NaN): gfx950's
+// v_cvt_pk_bf16_f32, two values per instruction.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
 __device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // Top-k ordering key: larger logit first, equal logits by lower id.  The float
@@ -40,6 +45,17 @@ __device__ __forceinline__ float topk_key_value(uint64_t key) {
 __device__ __forceinline__ int topk_key_id(uint64_t key) {
   return (int)(0xffffffffu - (uint32_t)key);
 }
+// 16 bytes per lane from global memory straight into LDS: lane l writes bytes
+// 16l..16l+15 after `lds` (wave-uniform).  A plain device function: called
+// directly from a kernel template the builtin leaves the kernel without its
+// host-side launch stub.
+__device__ __forceinline__ void lds_dma16(const void *src, void *lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
+}
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // ---- cross-lane reductions in registers (no LDS traffic) -------------------------
 // DPP controls: quad_perm [1,0,3,2] (lane^1), [2,3,0,1] (lane^2), row_half_mirror
 // (the other quad of an 8-lane half once quads are uniform), row_ror:8 (lane^8).
@@ -135,7 +151,7 @@ template <> struct Elt<float> {
 
 constexpr int kMaxLayers = 16;
 // Prefix keys per attention workgroup (4 waves of 32 keys).
-constexpr int kAttnChunk = 128;
+constexpr int kAttnChunk = 64;
 // Tile candidates the top-k merge holds in registers: 256 threads x 32.
 constexpr int kMergeMaxCand = 256 * 32;
 // Largest M (rows) one GEMM launch handles; larger M is split on the host.
@@ -239,15 +255,18 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // keys/values knew/vnew [B, nctx, Hkv, D] -> out [B, Hq*D] (storage type).
 // bf16: q and the cascade keys arrive unrotated and are rotated here with the
 // table `rope` (cascade != 0: cascade row j at position P + j, else P); fp32:
-// they arrive rotated.  Each workgroup covers cpw chunks of one sequence; part (B*Hq*nch_ld*(D+2)
-// floats, nch_ld >= ceil(nch / cpw)) holds the partials of sequences that span
-// several workgroups, merged by a second launch.
+// they arrive rotated.  A work unit covers cpw chunks (kAttnChunk keys) of
+// one sequence; bf16 launches with more units than resident waves instead
+// give every resident wave an equal share of all chunks.  part
+// (B*Hq*(nch_ld*(D+2) + 1) floats, nch_ld >= nch = chunks of the longest
+// prefix) holds the partials of sequences that span several units (and, for
+// the equal shares, the partial count per head), merged by a second launch.
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
                      const float *q, const float *knew, const float *vnew, int nctx,
                      float *part, int nch, int nch_ld, int cpw, void *out, int B, int Hq,
                      int Hkv, int D, const float *rope, int cascade, hipStream_t s);
-// 128-key sub-chunks per attention workgroup for a launch of B sequences over
-// nch = ceil(max_prefix / 128) sub-chunks
+// kAttnChunk-key chunks per attention work unit for a launch of B sequences
+// over nch = ceil(max_prefix / kAttnChunk) chunks
 int attention_cpw(int B, int Hkv, int ngroups, int nch);
 
 // Rotary table: tab[(p * D/2 + m) * 2 + {0,1}] = cos, sin of p * theta^(-2m/D),

@@ -60,7 +60,7 @@ Layout layout_of(const fe_config &c) {
   L.q = take(B * Hq * D * 4);
   L.knew = take(B * N * Hkv * D * 4);
   L.vnew = take(B * N * Hkv * D * 4);
-  L.part = take(B * Hq * (size_t)L.nchmax * (D + 2) * 4);
+  L.part = take(B * Hq * ((size_t)L.nchmax * (D + 2) + 1) * 4);  // + partial counts
   L.npos = c.max_prefix + c.n_layers;  // positions P_b + j, j < N
   L.rope = take((size_t)L.npos * (D / 2) * 2 * 4);
   L.ao = take(B * Hq * D * es);

@@ -100,6 +100,19 @@ def test_batched_rows_parity(cfg):
     _run(cfg, seed=5)
 
 
+# More attention work units than resident waves: persistent waves, each taking
+# every W-th unit of the dense numbering over ragged sequences (the debug
+# forward, and every replay of the captured pass, run it again).  Default split
+# and a split of 2 chunks; GQA head dim 64 and MHA head dim 128.
+@pytest.mark.parametrize("graph", [False, True])
+@pytest.mark.parametrize("cfg,split", [
+    (C.SMALL_GQA_BF16.with_(batch=36, prefix=(0, 3000), name="small_gqa_bf16_b36_p3000"), None),
+    (C.SMALL_MHA_BF16_D128.with_(batch=24, prefix=(0, 2000), name="small_mha_bf16_d128_b24"), 2)],
+    ids=lambda v: v.name if hasattr(v, "name") else str(v))
+def test_attention_queue_parity(cfg, split, graph):
+    _run(cfg, seed=6, attn_split=split, graph=graph)
+
+
 def test_topk_edge_values():
     """k = 1 (chain tree) and k = max (16)."""
     for k in (1, 16):
