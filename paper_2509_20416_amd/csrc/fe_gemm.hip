@@ -370,7 +370,8 @@ __device__ __forceinline__ int ring_slot(int row, int piece) { return row * 8 + 
 
 template <typename T, int NTW, int WN, int S, class Epi>
 __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
-                                                  int M, int K, Epi epi) {
+                                                  int M, int K, Epi epi, float *__restrict__ splitp,
+                                                  int ldp) {
   constexpr int E = Elt<T>::kPer16B;  // elements per 16-byte piece
   constexpr int KC = 8 * E;           // elements of K per chunk
   constexpr int WM = 4 / WN;
@@ -389,7 +390,10 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
   const int wm = wave / WN, wn = wave % WN;
   const int c0 = blockIdx.x * BN;
-  const int nch = (K + KC - 1) / KC;
+  // split K over gridDim.y: this workgroup's chunks [cb, cb + nch)
+  const int nchk = (K + KC - 1) / KC;
+  const int cb = (int)((long)nchk * blockIdx.y / gridDim.y);
+  const int nch = (int)((long)nchk * (blockIdx.y + 1) / gridDim.y) - cb;
 
   // the lane's slot in each of its load instructions, and the source row and
   // piece offset that belong there (rows past M repeat row M-1: their products
@@ -414,7 +418,7 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   // wave issues the same count), addresses clamped inside the rows
   auto issue = [&](int ch) {
     char *st = smem + (ch % S) * STAGE;
-    const int k = min(ch, nch - 1) * KC;
+    const int k = (cb + min(ch, nch - 1)) * KC;
 #pragma unroll
     for (int j = 0; j < AI; ++j)
       lds_dma16(asrc[j] + min(k + aoff[j], K - E), st + (j * 4 + wave) * 1024);
@@ -438,8 +442,8 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
     wg_barrier();                 // so has everyone's; ring slot of chunk ch-1 is free
     issue(ch + S - 1);
     const char *st = smem + (ch % S) * STAGE;
-    if (ch == nch - 1 && K % KC) {  // ragged last chunk: zero the pieces past K
-      const int k = ch * KC;
+    if (cb + ch == nchk - 1 && K % KC) {  // ragged last chunk: zero the pieces past K
+      const int k = (cb + ch) * KC;
       for (int q = tid; q < (MROWS + BN) * 8; q += 256) {
         const int row = q >> 3, piece = (q & 7) ^ ((row >> 1) & 7);
         if (k + piece * E >= K) *reinterpret_cast<u32x4 *>(const_cast<char *>(st) + q * 16) = u32x4{0u, 0u, 0u, 0u};
@@ -462,6 +466,20 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
     }
   }
   wait_vmcnt<0>();  // the chunks fetched past the end land before the ring is reused or freed
+  if (splitp) {  // split K: this slice's fp32 sums, reduced (and finished) by a second launch
+    float *dst = splitp + (size_t)blockIdx.y * M * ldp + c0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (i < mtiles)
+#pragma unroll
+        for (int f = 0; f < NTW; ++f)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int m = mrow0 + i * 16 + 4 * g + v;
+            if (m < M) dst[(size_t)m * ldp + ncol0 + f * 16 + r] = acc[i][f][v];
+          }
+    return;
+  }
   wg_barrier();
   float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
 #pragma unroll
@@ -473,6 +491,34 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
         for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][ncol0 + f * 16 + r] = acc[i][f][v];
   __syncthreads();
   epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
+}
+
+// Split-K reduction: sums the ks partial slices of a 16-column span in a fixed
+// order and hands the span to the epilogue, like k_gemm_mid would.  A thread
+// takes 4 adjacent columns of a row and issues all of its slice loads before
+// adding.
+template <class Epi>
+__global__ __launch_bounds__(256) void k_splitk_finish(const float *__restrict__ splitp, int ldp,
+                                                       int ks, int M, Epi epi) {
+  constexpr int BNR = 16, LDT = BNR + 1;
+  __shared__ float tile[256 * LDT];
+  const int c0 = blockIdx.x * BNR;
+  const size_t slice = (size_t)M * ldp;
+  for (int q = threadIdx.x; q < M * (BNR / 4); q += 256) {
+    const int m = q / (BNR / 4), c = (q % (BNR / 4)) * 4;
+    const float *src = splitp + (size_t)m * ldp + c0 + c;
+    f32x4 part[8];
+#pragma unroll
+    for (int y = 0; y < 8; ++y)
+      part[y] = y < ks ? *reinterpret_cast<const f32x4 *>(src + y * slice) : f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 v = part[0];
+#pragma unroll
+    for (int y = 1; y < 8; ++y) v += part[y];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[m * LDT + c + e] = v[e];
+  }
+  __syncthreads();
+  epi.finish(tile, LDT, M, c0, BNR, typename Epi::Pre{});
 }
 
 // ---------------------------------------------------------------------------
@@ -487,7 +533,7 @@ struct NoPre {
   bool ok = false;
 };
 template <typename T> struct EpiStore {
-  static constexpr bool kRowStream = true;
+  static constexpr bool kRowStream = true, kSplitK = true;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
@@ -524,7 +570,7 @@ template <typename T> struct EpiStore {
 };
 
 template <typename T> struct EpiResid {
-  static constexpr bool kRowStream = true;
+  static constexpr bool kRowStream = true, kSplitK = true;
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   const T *w;
   int ldw, nvcols;
@@ -599,7 +645,7 @@ __device__ __forceinline__ int rope_dim(int cc, int D) {
 }
 
 template <typename T> struct EpiQkv {
-  static constexpr bool kRowStream = true;
+  static constexpr bool kRowStream = true, kSplitK = true;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
@@ -662,7 +708,7 @@ template <typename T> struct EpiQkv {
 };
 
 template <typename T> struct EpiSwiglu {
-  static constexpr bool kRowStream = true;
+  static constexpr bool kRowStream = true, kSplitK = false;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 2;  // gate/up tile pairs
@@ -693,7 +739,7 @@ template <typename T> struct EpiSwiglu {
 // Shared LM head: per (row, column tile) max, sum of exp(z - max) and the top-k
 // (largest logit first, equal logits by lower draft id); logits optionally kept.
 template <typename T> struct EpiLm {
-  static constexpr bool kRowStream = false;
+  static constexpr bool kRowStream = false, kSplitK = false;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 4, kMidNtwMin = 4;  // 64-column tiles, as lmhead_tiles counts
@@ -842,7 +888,7 @@ static hipError_t run_gemv(const bf16_t *A, int lda, const ARows &arows, int M, 
 
 template <typename T, int NT, int WKmax, int WN, class Epi>
 static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K, const Epi &epi,
-                           const NormA *na, hipStream_t s) {
+                           const NormA *na, hipStream_t s, const SplitScratch *ss = nullptr) {
   constexpr int SPAN = WN * NT * 16;
   const int grid = (epi.nvcols + SPAN - 1) / SPAN;
   const int mt = (M + 15) / 16;
@@ -863,9 +909,12 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
     return hipGetLastError();
   }
   // 17..32 rows over wide outputs (the batch-32 gate/up): the LDS-ring kernel
-  // with column-split waves beats the per-wave staging; narrow outputs would
-  // leave it too few workgroups
-  const bool ring_wide = mt == 2 && epi.nvcols >= 64 * 256;
+  // with column-split waves beats the per-wave staging; narrow outputs take
+  // it too when their epilogue can follow a split-K reduction, else they
+  // would leave it too few workgroups
+  bool splittable = false;
+  if constexpr (Epi::kSplitK) splittable = ss != nullptr && ss->p != nullptr;
+  const bool ring_wide = mt == 2 && (epi.nvcols >= 64 * 256 || splittable);
   if (mt <= 2 && !ring_wide) {
     if (mt <= 1)
       hipLaunchKernelGGL((k_gemm<T, 1, NT, SplitK<WKmax, 1>::value, WN, false, Epi>), dim3(grid),
@@ -888,10 +937,40 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
   if (tt < wn) tt = wn;  // a tile per column group at least
   if (tt < 2) tt = 2;    // weight slots split evenly over the waves
   const int ntw = tt / wn;
+  // Narrow outputs whose epilogue allows it: 128-column tiles (a quarter of
+  // the re-reading of A that 32-column tiles cost) and K split over enough
+  // workgroups to cover the CUs; the fp32 slices are summed, in a fixed order,
+  // by a second launch that runs the epilogue.
+  int ks = 1;
+  float *sp = nullptr;
+  int ldp = 0;
+  if (splittable) {
+    constexpr int KC = 8 * Elt<T>::kPer16B;
+    const int gx = (epi.nvcols + 127) / 128, nchk = (K + KC - 1) / KC;
+    // about one workgroup per CU (k_splitk_finish sums at most 8 slices); many
+    // rows make each slice heavier and its partial sums larger: fewer slices
+    ks = min(M > 128 ? 4 : 8, max(1, (256 + gx - 1) / gx));
+    ks = min(ks, max(1, nchk / 4));  // a few chunks per slice for the ring
+    ldp = gx * 128;
+    if ((size_t)ks * M * ldp > ss->floats) ks = 1;
+    if (ks > 1) sp = ss->p;
+  }
 #define FE_GEMM_MID(NTWV, WNV, SV)                                                                   \
   hipLaunchKernelGGL((k_gemm_mid<T, NTWV, WNV, SV, Epi>),                                           \
-                     dim3((epi.nvcols + 16 * NTWV * WNV - 1) / (16 * NTWV * WNV)), dim3(256), 0, s, A, \
-                     lda, arows, M, K, epi)
+                     dim3((epi.nvcols + 16 * NTWV * WNV - 1) / (16 * NTWV * WNV), ks), dim3(256), 0,  \
+                     s, A, lda, arows, M, K, epi, sp, ldp)
+  if constexpr (Epi::kSplitK) {
+    if (sp) {
+      if (wn == 4) FE_GEMM_MID(2, 4, 4);
+      else if (wn == 2) FE_GEMM_MID(4, 2, 4);
+      else FE_GEMM_MID(8, 1, 3);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((k_splitk_finish<Epi>), dim3((epi.nvcols + 15) / 16), dim3(256), 0, s,
+                         (const float *)sp, ldp, ks, M, epi);
+      return hipGetLastError();
+    }
+  }
   if (wn == 4) {
     if (ntw >= 2) FE_GEMM_MID(2, 4, 4);
     else FE_GEMM_MID(1, 4, 4);
@@ -908,39 +987,40 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
 
 hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
                       void *out, int ldo, const void *embed, const int32_t *tokens, int vocab,
-                      void *gather_out, int ld_gather, int d, int B, hipStream_t s) {
+                      void *gather_out, int ld_gather, int d, int B, hipStream_t s,
+                      const SplitScratch *ss) {
   if (dt) {
     EpiStore<bf16_t> e{(const bf16_t *)W, K, ncols, (bf16_t *)out, ldo, (const bf16_t *)embed,
                        tokens, vocab, (bf16_t *)gather_out, ld_gather, d, B};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s);
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s, ss);
   }
   EpiStore<float> e{(const float *)W, K, ncols, (float *)out, ldo, (const float *)embed,
                     tokens, vocab, (float *)gather_out, ld_gather, d, B};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s);
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s, ss);
 }
 
 hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
                       float *out, long ldo, const float *resid, long ldr, float *ssq, int ssq_rs,
-                      int ssq_off, const GainCopies *gains, hipStream_t s) {
+                      int ssq_off, const GainCopies *gains, hipStream_t s, const SplitScratch *ss) {
   GainCopies gc{};
   if (gains) gc = *gains;
   if (dt) {
     EpiResid<bf16_t> e{(const bf16_t *)W, K, ncols, out, ldo, resid, ldr, ssq, ssq_rs, ssq_off, gc};
-    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s);
+    return run_gemm<bf16_t, 1, 8, 1>((const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, s, ss);
   }
   EpiResid<float> e{(const float *)W, K, ncols, out, ldo, resid, ldr, ssq, ssq_rs, ssq_off, gc};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s);
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, K, e, nullptr, s, ss);
 }
 
 hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
-                    const NormA *na, hipStream_t s) {
+                    const NormA *na, hipStream_t s, const SplitScratch *ss) {
   const int nv = (a.Hq + 2 * a.Hkv) * a.D;
   if (dt) {
     EpiQkv<bf16_t> e{a, nv};
-    return run_gemm<bf16_t, 1, 4, 1>((const bf16_t *)A, lda, arows, M, a.d, e, na, s);
+    return run_gemm<bf16_t, 1, 4, 1>((const bf16_t *)A, lda, arows, M, a.d, e, na, s, ss);
   }
   EpiQkv<float> e{a, nv};
-  return run_gemm<float, 1, 8, 1>((const float *)A, lda, arows, M, a.d, e, na, s);
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, arows, M, a.d, e, na, s, ss);
 }
 
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,

@@ -193,13 +193,21 @@ struct GainCopies {
 // of hipGetLastError() after the launch.
 // ---------------------------------------------------------------------------
 
+// fp32 scratch for split-K partial sums (batched rows over narrow outputs);
+// without it those GEMMs run unsplit.
+struct SplitScratch {
+  float *p = nullptr;
+  size_t floats = 0;
+};
+
 // out[m, c] = round_T(sum_k A[m,k] W[c,k]) for c < ncols; when `embed` is not
 // null, also copies embed[tokens[b]] (d elements) to gather_out + b*ld_gather.
 // Token ids outside [0, vocab) get a NaN row, so a bad id poisons that sequence's
 // outputs instead of reading outside the table.
 hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
                       void *out, int ldo, const void *embed, const int32_t *tokens, int vocab,
-                      void *gather_out, int ld_gather, int d, int B, hipStream_t s);
+                      void *gather_out, int ld_gather, int d, int B, hipStream_t s,
+                      const SplitScratch *ss = nullptr);
 
 // out[m, c] = (resid ? resid[m, c] : 0) + sum_k A[m,k] W[c,k]   (fp32 out/resid).
 // When ssq is not null, also writes the sum of squares of every output row over
@@ -207,7 +215,8 @@ hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *
 // gains is not null, also writes its gain copies of every output row.
 hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
                       float *out, long ldo, const float *resid, long ldr, float *ssq, int ssq_rs,
-                      int ssq_off, const GainCopies *gains, hipStream_t s);
+                      int ssq_off, const GainCopies *gains, hipStream_t s,
+                      const SplitScratch *ss = nullptr);
 
 struct QkvArgs {
   const void *wq, *wk, *wv;
@@ -223,7 +232,7 @@ struct QkvArgs {
 // Q/K/V projections of the RMS-normed context rows; with a.rotate, rotary embedding of Q and K.
 // With `na` (M <= 16) A holds gamma * x rows and the RMSNorm scale is fused.
 hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
-                    const NormA *na, hipStream_t s);
+                    const NormA *na, hipStream_t s, const SplitScratch *ss = nullptr);
 
 // s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,

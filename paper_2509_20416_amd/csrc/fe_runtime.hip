@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -31,7 +32,8 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
-      psum, cval, cidx, total;
+      psum, cval, cidx, splitk, total;
+  size_t splitk_floats;
   int nchmax, nwg, npos;
 };
 
@@ -69,6 +71,14 @@ Layout layout_of(const fe_config &c) {
   L.psum = take(B * N * (size_t)L.nwg * 4);
   L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
+  // split-K slices of the batched GEMMs with narrow outputs: up to 8 slices of
+  // the QKV rows (B * N at most, 256 per launch) over 128-column tiles
+  {
+    const size_t rows = std::min<size_t>(256, B * N);
+    const size_t cols = (std::max<size_t>((Hq + 2 * Hkv) * D, d) + 127) / 128 * 128;
+    L.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
+    L.splitk = take(L.splitk_floats * 4);
+  }
   L.total = o;
   return L;
 }
@@ -246,8 +256,9 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   float *ssqX = (float *)(ws + L.ssqX), *ssqP = (float *)(ws + L.ssqP);
 
   // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
+  const SplitScratch ss{(float *)(ws + L.splitk), L.splitk_floats};
   FE_STAGE_RUN(FE_STAGE_FUSE, gemm_store(dt, features, F * d, B, F * d, h->w.w_fuse, d, cat, 2 * d, h->w.embed,
-                    next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s));
+                    next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s, &ss));
   // x_0 = FC(concat(g_t, e_{t+1}))  (Eq. 1)
   // Fused RMSNorm (up to 16 rows per GEMM): every producer of a residual row
   // also writes gamma * row for the later GEMMs that normalise it.
@@ -277,7 +288,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   };
   const GainCopies gc_x0 = x_copies(0);
   FE_STAGE_RUN(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr,
-                                      0, ssqX, N + 1, 0, &gc_x0, s));
+                                      0, ssqX, N + 1, 0, &gc_x0, s, &ss));
 
   for (int i = 1; i <= N; ++i) {
     const fe_layer_weights &lw = h->layers[i - 1];
@@ -289,10 +300,10 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     if (fuse_q(i)) {
       const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
       FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
-                                      B * nctx, qa, &na1, s));
+                                      B * nctx, qa, &na1, s, &ss));
     } else {
       FE_OTHER(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
-      FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s));
+      FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s, &ss));
     }
     // attention over the layer's prefix cache plus the cascade keys
     FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
@@ -307,7 +318,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
       gc_p.ld[0] = d;
     }
     FE_STAGE_RUN(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
-                                        X + (size_t)(i - 1) * d, xrow, ssqP, 1, 0, &gc_p, s));
+                                        X + (size_t)(i - 1) * d, xrow, ssqP, 1, 0, &gc_p, s, &ss));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
     if (fuse_m) {
       const NormA na2{ssqP, ntile, 1, 0, 1, d, c.rms_eps};
@@ -320,7 +331,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     }
     const GainCopies gc_xi = x_copies(i);
     FE_STAGE_RUN(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow,
-                                       Xp, d, ssqX, N + 1, i, &gc_xi, s));
+                                       Xp, d, ssqX, N + 1, i, &gc_xi, s, &ss));
   }
 
   // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
