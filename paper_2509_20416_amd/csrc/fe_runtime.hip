@@ -122,7 +122,7 @@ struct fe_drafter {
   Layout L;
   hipStream_t cap_stream = nullptr;
   bool graph_mode = false;
-  int attn_split = 0;  // 128-key chunks per attention workgroup (0 = automatic)
+  int attn_split = 0;  // 64-key chunks per attention work unit (0 = automatic)
   bool table_ready = false;  // rotary table built (first pass on the handle)
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
