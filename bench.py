@@ -20,6 +20,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "µs per N-token cascaded draft pass and drafts/s, 8B-shaped bf16, batch 1 / 32"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+MFMA_PEAK_TFS = {"bf16": 2500.0, "f32": 157.3}  # dense matrix-core peaks (fp32: the vector figure)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gateup_llama8b_bf16_b1.txt")
 
 
@@ -42,6 +43,22 @@ def pass_bytes(cfg, plens):
     emb = len(plens) * cfg.hidden * es
     feats = len(plens) * cfg.n_feat_levels * cfg.hidden * es
     return cfg.weight_bytes() + kv + emb + feats
+
+
+def pass_flops(cfg, plens):
+    """Algorithmic FLOPs of one pass (2 per multiply-add): q, O and the MLP at
+    B rows, layer i's K/V over its context rows (B*i under the cascade context,
+    B otherwise), the LM head over all B*N rows, and per layer the attention's
+    two contractions over P_b + nctx keys."""
+    B, d, N = len(plens), cfg.hidden, cfg.n_layers
+    qd, kvd, I, V = cfg.n_q_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim, cfg.intermediate, cfg.draft_vocab
+    f = 2 * B * cfg.n_feat_levels * d * d + 2 * B * 2 * d * d
+    for i in range(1, N + 1):
+        nctx = i if cfg.cascade_ctx == "cascade" else 1
+        f += 2 * B * d * qd + 2 * B * nctx * d * 2 * kvd + 2 * B * qd * d
+        f += 2 * B * d * 2 * I + 2 * B * I * d
+        f += sum(4 * qd * (int(p) + nctx) for p in plens)
+    return f + 2 * B * N * d * V
 
 
 def gemm_source_sha1():
@@ -76,23 +93,32 @@ def read_traffic():
 
 def cpu_baseline(cfg, w, inp, budget_s):
     """The oracle, as it stands, on the machine's host cores: whole passes (+ tree)
-    of the same workload until about budget_s seconds have been spent."""
+    of the same workload until about budget_s seconds have been spent, a third
+    of the budget on one thread and the rest on all the threads it may use."""
     from oracle import feo
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
-    feo.set_threads(threads)
-    n, t0 = 0, time.time()
-    while True:
-        ref = feo.draft_forward(cfg, w, inp, want_logits=False)
-        feo.build_tree(cfg.n_layers, cfg.topk, inp.next_tokens, ref["topk_ids"], inp.prefix_lens)
-        n += 1
-        el = time.time() - t0
-        if el >= budget_s:
-            break
-    drafts = n * len(inp.prefix_lens)
-    return {"value": drafts / el, "unit": "drafts/s", "cores": threads, "kind": "oracle",
+    affinity = len(os.sched_getaffinity(0))
+    threads = max(1, min(16, affinity))
+
+    def run(nthreads, budget):
+        feo.set_threads(nthreads)
+        n, t0 = 0, time.time()
+        while True:
+            ref = feo.draft_forward(cfg, w, inp, want_logits=False)
+            feo.build_tree(cfg.n_layers, cfg.topk, inp.next_tokens, ref["topk_ids"], inp.prefix_lens)
+            n += 1
+            el = time.time() - t0
+            if el >= budget:
+                return n, el
+
+    n1, el1 = run(1, budget_s / 3)
+    n, el = run(threads, budget_s * 2 / 3)
+    B = len(inp.prefix_lens)
+    return {"value": n * B / el, "unit": "drafts/s", "cores": threads, "kind": "oracle",
+            "ms_per_pass": el / n * 1e3, "ms_per_pass_1_thread": el1 / n1 * 1e3,
+            "nproc": os.cpu_count(), "affinity": affinity,
             "sample": f"{n} full pass(es) + tree of the {cfg.name} workload "
-                      f"(batch {len(inp.prefix_lens)}) in {el:.1f} s, fp64, "
-                      f"{threads} OpenMP threads"}
+                      f"(batch {B}) in {el:.1f} s on {threads} OpenMP threads, and "
+                      f"{n1} in {el1:.1f} s on 1 thread; fp64"}
 
 
 def main():
@@ -179,6 +205,7 @@ def main():
     achieved = gbytes / (gu_avg * 1e-3) / 1e9
     traffic = read_traffic()
     pbytes = pass_bytes(cfg, plens)
+    pflops = pass_flops(cfg, plens)
     res = {
         "metric": METRIC,
         "value": B * 1000.0 / ms,
@@ -203,6 +230,14 @@ def main():
         "pass_roofline": {"bytes_per_pass": pbytes,
                           "achieved_GBs": pbytes / (ms * 1e-3) / 1e9,
                           "frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        # matrix-core use over the whole pass, against the most that an
+        # HBM-bound pass of this arithmetic intensity could reach
+        "pass_mfma": {"flops_per_pass": pflops,
+                      "achieved_TFLOPs": pflops / (ms * 1e-3) / 1e12,
+                      "peak_TFLOPs": MFMA_PEAK_TFS[cfg.dtype],
+                      "frac": pflops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFS[cfg.dtype],
+                      "ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3
+                                          / MFMA_PEAK_TFS[cfg.dtype])},
     }
     dr.close()
     if not args.no_cpu_baseline:

@@ -341,3 +341,36 @@ int feo_build_tree(int32_t batch, int32_t n_layers, int32_t topk, const int32_t 
   free(path);
   return 0;
 }
+
+/* Greedy acceptance (Section 2.4, parallel verification at temperature 0):
+ * every root->leaf path is walked from the root while each next node carries
+ * the token the target predicts after its predecessor; the longest accepted
+ * prefix wins, the first such path on a tie. */
+int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32_t *tokens,
+                      const int32_t *retrieve, const int32_t *target_next, int32_t *accept_len,
+                      int32_t *accept_path, int32_t *accepted) {
+  if (batch < 0 || n_layers < 1 || topk < 1) return -1;
+  const int32_t N = n_layers, T = 1 + N * topk, NL = N * (topk - 1) + 1;
+  for (int32_t b = 0; b < batch; ++b) {
+    const int32_t *tok = tokens + (size_t)b * T, *nxt = target_next + (size_t)b * T;
+    const int32_t *ret = retrieve + (size_t)b * NL * (N + 1);
+    int32_t best = -1, best_len = -1;
+    for (int32_t p = 0; p < NL; ++p) {
+      const int32_t *path = ret + (size_t)p * (N + 1);
+      int32_t m = 0;
+      while (m < N && path[m + 1] >= 0 && tok[path[m + 1]] == nxt[path[m]]) ++m;
+      if (m > best_len) {
+        best_len = m;
+        best = p;
+      }
+    }
+    const int32_t *path = ret + (size_t)best * (N + 1);
+    int32_t *acc = accepted + (size_t)b * (N + 1);
+    for (int32_t t = 0; t <= N; ++t) acc[t] = -1;
+    for (int32_t t = 1; t <= best_len; ++t) acc[t - 1] = tok[path[t]];
+    acc[best_len] = nxt[path[best_len]];
+    accept_len[b] = best_len;
+    accept_path[b] = best;
+  }
+  return 0;
+}

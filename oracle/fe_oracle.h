@@ -87,6 +87,23 @@ int feo_build_tree(int32_t batch, int32_t n_layers, int32_t topk, const int32_t 
                    int32_t *parents, int32_t *depth, int32_t *positions, uint8_t *mask,
                    int32_t *retrieve);
 
+/*
+ * Greedy acceptance of one drafting cycle (Section 2.4, parallel verification,
+ * read at temperature 0): target_next[b][n] is the target model's greedy next
+ * token after the tree path that ends at node n.  Along a root->leaf path
+ * r_0 = root, r_1, ..., node r_m is accepted when every r_t, t <= m, carries
+ * the token the target predicts after r_{t-1}.  Per sequence the path with
+ * the most accepted nodes wins (the first such path in retrieve order on a
+ * tie).  Inputs: tokens [B, T], retrieve [B, NL, N+1] as built above,
+ * target_next [B, T].  Outputs: accept_len [B] (accepted draft tokens, 0..N),
+ * accept_path [B] (row of retrieve), accepted [B, N+1]: the accepted draft
+ * tokens in path order, then the target's token after the last accepted node,
+ * then -1.  Returns 0, or -1 on invalid arguments.
+ */
+int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32_t *tokens,
+                      const int32_t *retrieve, const int32_t *target_next, int32_t *accept_len,
+                      int32_t *accept_path, int32_t *accepted);
+
 #ifdef __cplusplus
 }
 #endif

@@ -43,6 +43,7 @@ def lib():
         L = C.CDLL(_build.LIB)
         L.feo_draft_forward.restype = C.c_int
         L.feo_build_tree.restype = C.c_int
+        L.feo_accept_greedy.restype = C.c_int
         L.feo_get_threads.restype = C.c_int
         _lib = L
     return _lib
@@ -166,4 +167,22 @@ def build_tree(n_layers: int, topk: int, root_tokens: np.ndarray, topk_ids: np.n
                               _p(out["mask"]), _pi(out["retrieve"]))
     if rc != 0:
         raise ValueError("oracle build_tree rejected its arguments")
+    return out
+
+
+def accept_greedy(n_layers: int, topk: int, tokens: np.ndarray, retrieve: np.ndarray,
+                  target_next: np.ndarray) -> Dict[str, np.ndarray]:
+    """Greedy acceptance of one cycle (Section 2.4, temperature 0): see
+    feo_accept_greedy in fe_oracle.h."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    retrieve = np.ascontiguousarray(retrieve, dtype=np.int32)
+    target_next = np.ascontiguousarray(target_next, dtype=np.int32)
+    B, N = tokens.shape[0], int(n_layers)
+    out = dict(accept_len=np.zeros(B, np.int32), accept_path=np.zeros(B, np.int32),
+               accepted=np.zeros((B, N + 1), np.int32))
+    rc = lib().feo_accept_greedy(C.c_int32(B), C.c_int32(N), C.c_int32(int(topk)), _pi(tokens),
+                                 _pi(retrieve), _pi(target_next), _pi(out["accept_len"]),
+                                 _pi(out["accept_path"]), _pi(out["accepted"]))
+    if rc != 0:
+        raise ValueError("oracle accept_greedy rejected its arguments")
     return out
