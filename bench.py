@@ -121,6 +121,43 @@ def cpu_baseline(cfg, w, inp, budget_s):
                       f"{n1} in {el1:.1f} s on 1 thread; fp64"}
 
 
+def time_second(name, seed, steps, warmup):
+    """The other half of the metric (by default the batch-32 workload): passes
+    (forward + tree, graph replays) timed the same way as the primary one."""
+    import numpy as np
+    import torch
+    from fe_synth import NAMED, make_inputs, make_weights
+    from paper_2509_20416_amd import Drafter
+    cfg = NAMED[name]
+    w = make_weights(cfg, seed)
+    inp = make_inputs(cfg, seed)
+    plens = np.asarray(inp.prefix_lens)
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=True)
+    di = dr.upload_inputs(inp)
+    out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
+    tree = dr.alloc_tree(cfg.batch, cfg.topk)
+    for _ in range(warmup):
+        dr.forward(di, out=out, tree=tree)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        dr.forward(di, out=out, tree=tree)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    dr.close()
+    pbytes, pflops = pass_bytes(cfg, plens), pass_flops(cfg, plens)
+    peak = MFMA_PEAK_TFS[cfg.dtype]
+    log(f"{name}: {ms * 1000:.1f} us/pass")
+    return {"workload": name, "batch": cfg.batch, "steps": steps, "warmup": warmup,
+            "us_per_pass": ms * 1000.0, "drafts_per_s": cfg.batch * 1000.0 / ms,
+            "hbm_frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "mfma_frac": pflops / (ms * 1e-3) / 1e12 / peak,
+            "mfma_ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3 / peak)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +169,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--prof-repeats", type=int, default=8)
+    ap.add_argument("--second", default="llama8b_bf16_b32",
+                    help="second workload timed in the same run and reported in its own "
+                         "object ('' = none; the batch-32 half of the metric by default)")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: a few eager passes, one round of the gate/up "
                          "launches, then a plain 512 MiB device copy as the counter scale "
@@ -200,6 +240,29 @@ def main():
     n_timed = per_pass * args.prof_repeats
     log(f"{ms * 1000:.1f} us/pass; gate/up: {n_timed} launches, mean {gu_avg * 1000:.1f} us")
 
+    # NEXT-2, greedy acceptance of the cycle's tree (after verification, not
+    # part of the drafting pass): target predictions that follow the backbone
+    # for half the levels; mean launch time over back-to-back calls
+    T = 1 + cfg.n_layers * cfg.topk
+    tok = tree["tokens"].cpu().numpy()
+    nx = np.full((cfg.batch, T), -7, np.int32)
+    for b in range(cfg.batch):
+        cur = 0
+        for lvl in range(cfg.n_layers // 2):
+            child = 1 + lvl * cfg.topk          # rank-0 node of the level: the backbone
+            nx[b, cur] = tok[b, child]
+            cur = child
+    nx_d = torch.from_numpy(nx).cuda()
+    acc = dr.accept_greedy(tree, nx_d, cfg.topk)
+    torch.cuda.synchronize()
+    accept_len0 = int(acc["accept_len"][0].item())
+    ev0.record(stream)
+    for _ in range(100):
+        dr.accept_greedy(tree, nx_d, cfg.topk, out=acc)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    accept_us = ev0.elapsed_time(ev1) * 1000.0 / 100
+
     B = cfg.batch
     gbytes = gateup_bytes(cfg, B)
     achieved = gbytes / (gu_avg * 1e-3) / 1e9
@@ -232,6 +295,10 @@ def main():
                           "frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
         # matrix-core use over the whole pass, against the most that an
         # HBM-bound pass of this arithmetic intensity could reach
+        # host-issued launches back to back: the rate is bound by the Python
+        # call, the kernel itself is a few microseconds
+        "next_accept_greedy": {"us_per_call": accept_us, "batch": B,
+                               "accept_len_seq0": accept_len0, "issue": "eager, from Python"},
         "pass_mfma": {"flops_per_pass": pflops,
                       "achieved_TFLOPs": pflops / (ms * 1e-3) / 1e12,
                       "peak_TFLOPs": MFMA_PEAK_TFS[cfg.dtype],
@@ -240,6 +307,9 @@ def main():
                                           / MFMA_PEAK_TFS[cfg.dtype])},
     }
     dr.close()
+    if args.second and args.second != cfg.name:
+        res["second_workload"] = time_second(args.second, args.seed, max(10, args.steps // 4),
+                                             max(3, args.warmup // 4))
     if not args.no_cpu_baseline:
         log("timing the oracle on the host cores ...")
         res["cpu_baseline"] = cpu_baseline(cfg, w, inp, args.cpu_budget)

@@ -171,6 +171,29 @@ fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk, const int32_
                         const int32_t *topk_ids, const int32_t *prefix_lens,
                         const fe_tree_out *out, void *stream);
 
+/* Greedy acceptance of a drafting cycle (Section 2.4, parallel verification,
+ * read at temperature 0) for every sequence in one launch.  target_next[b][n]
+ * is the target model's greedy next token after the tree path that ends at
+ * node n (what tree-attention verification produces).  Along a root->leaf path
+ * r_0 = root, r_1, ..., node r_m is accepted when every r_t (t <= m) carries
+ * the token predicted after r_{t-1}; the path with the most accepted nodes
+ * wins, the first in retrieve order on a tie.
+ *  tokens      [B, T] int32, retrieve [B, N*(k-1)+1, N+1] int32: a tree from
+ *              fe_build_tree (or fe_draft_out.tree) with the same topk
+ *  target_next [B, T] int32
+ *  accept_len  [B] out: accepted draft tokens, 0..N
+ *  accept_path [B] out: the winning row of retrieve
+ *  accepted    [B, N+1] out: the accepted draft tokens in path order, then the
+ *              target's token after the last accepted node, then -1
+ * All device pointers, 4-byte aligned, owned by the caller.  Errors:
+ * FE_E_INVALID (NULL handle or array, batch outside [0, max_batch], topk
+ * outside [1, max_topk]), FE_E_ALIGN; nothing is launched on an error.  Node
+ * indices outside the tree end a path's walk. */
+fe_status fe_accept_greedy(fe_drafter *h, int32_t batch, int32_t topk, const int32_t *tokens,
+                           const int32_t *retrieve, const int32_t *target_next,
+                           int32_t *accept_len, int32_t *accept_path, int32_t *accepted,
+                           void *stream);
+
 /* Replays fe_draft_forward through a captured HIP graph when on != 0 (the
  * default is off).  A graph is captured on the first call with a given set of
  * arguments and replayed while they stay the same. */

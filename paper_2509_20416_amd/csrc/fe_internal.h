@@ -282,6 +282,14 @@ int attention_cpw(int B, int Hkv, int ngroups, int nch);
 // formed in double precision and rounded to fp32, for p < npos.
 hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s);
 
+// Greedy acceptance over the trees of B sequences (N levels, k per level):
+// tokens/target_next [B, 1+N*k], retrieve [B, N*(k-1)+1, N+1] -> accept_len [B],
+// accept_path [B], accepted [B, N+1] (accepted draft tokens, the target's next
+// token, -1 padding).
+hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32_t *retrieve,
+                         const int32_t *target_next, int32_t *accept_len, int32_t *accept_path,
+                         int32_t *accepted, hipStream_t s);
+
 // Global top-k of every row from the tile candidates; softmax statistics merge.
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
                       const int32_t *cand_idx, int rows, int nwg, int topk, int V,

@@ -252,6 +252,63 @@ hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int
   return hipGetLastError();
 }
 
+// ---- greedy acceptance of a drafting cycle --------------------------------------
+// Section 2.4 (parallel verification) at temperature 0: along a root->leaf path
+// of the tree, node r_t is accepted while every node up to it carries the token
+// the target predicts after its predecessor.  One wave per sequence, one lane
+// per path (64 at a time): the accepted length, then a wave max over the key
+// (length << 16 | 0xffff - path), so ties go to the first path.  Node indices
+// outside the tree end a walk (they cannot occur in a tree built here).
+__global__ __launch_bounds__(64) void k_accept_greedy(int N, int k, const int32_t *__restrict__ tokens,
+                                                      const int32_t *__restrict__ retrieve,
+                                                      const int32_t *__restrict__ target_next,
+                                                      int32_t *__restrict__ accept_len,
+                                                      int32_t *__restrict__ accept_path,
+                                                      int32_t *__restrict__ accepted) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int T = 1 + N * k, NL = N * (k - 1) + 1;
+  const int32_t *tok = tokens + (size_t)b * T, *nxt = target_next + (size_t)b * T;
+  const int32_t *ret = retrieve + (size_t)b * NL * (N + 1);
+  uint32_t best = 0;
+  for (int p = lane; p < NL; p += 64) {
+    const int32_t *path = ret + (size_t)p * (N + 1);
+    int m = 0, prev = path[0];
+    while (m < N && prev >= 0 && prev < T) {
+      const int nn = path[m + 1];
+      if (nn < 0 || nn >= T || tok[nn] != nxt[prev]) break;
+      prev = nn;
+      ++m;
+    }
+    best = max(best, ((uint32_t)m << 16) | (uint32_t)(0xffff - p));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) best = max(best, (uint32_t)__shfl_xor((int)best, o, 64));
+  const int m = (int)(best >> 16), p = 0xffff - (int)(best & 0xffffu);
+  const int32_t *path = ret + (size_t)p * (N + 1);
+  for (int t = lane; t <= N; t += 64) {
+    int32_t v = -1;
+    if (t < m) {
+      v = tok[path[t + 1]];
+    } else if (t == m) {
+      const int last = path[m];
+      v = last >= 0 && last < T ? nxt[last] : -1;
+    }
+    accepted[(size_t)b * (N + 1) + t] = v;
+  }
+  if (lane == 0) {
+    accept_len[b] = m;
+    accept_path[b] = p;
+  }
+}
+hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32_t *retrieve,
+                         const int32_t *target_next, int32_t *accept_len, int32_t *accept_path,
+                         int32_t *accepted, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_accept_greedy, dim3(B), dim3(64), 0, s, N, k, tokens, retrieve, target_next,
+                     accept_len, accept_path, accepted);
+  return hipGetLastError();
+}
+
 __global__ void k_rope_table(float *tab, int npos, int D, double theta) {
   const int half = D / 2;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < npos * half; i += gridDim.x * blockDim.x) {

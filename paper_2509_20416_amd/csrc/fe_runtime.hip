@@ -470,6 +470,25 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
   return FE_OK;
 }
 
+extern "C" fe_status fe_accept_greedy(fe_drafter *h, int32_t batch, int32_t topk,
+                                      const int32_t *tokens, const int32_t *retrieve,
+                                      const int32_t *target_next, int32_t *accept_len,
+                                      int32_t *accept_path, int32_t *accepted, void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const fe_config &c = h->cfg;
+  if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
+  if (topk < 1 || topk > c.max_topk) return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
+  if (batch == 0) return FE_OK;
+  if (!tokens || !retrieve || !target_next || !accept_len || !accept_path || !accepted)
+    return fail(FE_E_INVALID, "every acceptance input and output is required");
+  const void *ptrs[] = {tokens, retrieve, target_next, accept_len, accept_path, accepted};
+  for (const void *q : ptrs)
+    if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "acceptance arrays must be 4-byte aligned");
+  FE_TRY(accept_greedy(batch, c.n_layers, topk, tokens, retrieve, target_next, accept_len,
+                       accept_path, accepted, (hipStream_t)stream));
+  return FE_OK;
+}
+
 extern "C" fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk,
                                    const int32_t *root_tokens, const int32_t *topk_ids,
                                    const int32_t *prefix_lens, const fe_tree_out *out,

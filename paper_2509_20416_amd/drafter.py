@@ -169,6 +169,26 @@ class Drafter:
                          self.stream())
         return out
 
+    def accept_greedy(self, tree: Dict[str, object], target_next, topk: Optional[int] = None,
+                      batch: Optional[int] = None,
+                      out: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+        """Greedy acceptance of one cycle (fe_accept_greedy): tree as returned by
+        build_tree, target_next [B, T] int32 on the device."""
+        import torch
+        k = int(topk or self.cfg.topk)
+        B = int(batch if batch is not None else tree["tokens"].shape[0])
+        N = self.cfg.n_layers
+        dev = tree["tokens"].device
+        if out is None:
+            out = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+                   "accept_path": torch.empty(B, dtype=torch.int32, device=dev),
+                   "accepted": torch.empty(B, N + 1, dtype=torch.int32, device=dev)}
+        fe.fe_accept_greedy(self.handle, B, k, tree["tokens"].data_ptr(),
+                            tree["retrieve"].data_ptr(), target_next.data_ptr(),
+                            out["accept_len"].data_ptr(), out["accept_path"].data_ptr(),
+                            out["accepted"].data_ptr(), self.stream())
+        return out
+
     def close(self) -> None:
         if getattr(self, "handle", None):
             fe.fe_drafter_destroy(self.handle)

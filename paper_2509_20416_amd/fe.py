@@ -20,8 +20,8 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
-           "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_drafter_destroy",
-           "fe_last_error")
+           "fe_accept_greedy", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
+           "fe_drafter_destroy", "fe_last_error")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
 
@@ -90,6 +90,8 @@ def lib() -> C.CDLL:
         L.fe_build_tree.restype = C.c_int
         L.fe_build_tree.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
+        L.fe_accept_greedy.restype = C.c_int
+        L.fe_accept_greedy.argtypes = [C.c_void_p, C.c_int32, C.c_int32] + [C.c_void_p] * 7
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
         L.fe_set_attention_split.restype = C.c_int
@@ -138,6 +140,14 @@ def fe_build_tree(h: int, batch: int, topk: int, root_tokens: int, topk_ids: int
     check(lib().fe_build_tree(C.c_void_p(h), batch, topk, C.c_void_p(root_tokens),
                               C.c_void_p(topk_ids), C.c_void_p(prefix_lens), C.byref(out),
                               C.c_void_p(stream)))
+
+
+def fe_accept_greedy(h: int, batch: int, topk: int, tokens: int, retrieve: int, target_next: int,
+                     accept_len: int, accept_path: int, accepted: int, stream: int) -> None:
+    check(lib().fe_accept_greedy(C.c_void_p(h), batch, topk, C.c_void_p(tokens),
+                                 C.c_void_p(retrieve), C.c_void_p(target_next),
+                                 C.c_void_p(accept_len), C.c_void_p(accept_path),
+                                 C.c_void_p(accepted), C.c_void_p(stream)))
 
 
 def fe_set_graph_mode(h: int, on: bool) -> None:

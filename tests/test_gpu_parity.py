@@ -58,6 +58,57 @@ def test_tree_kernel_bit_exact(N, k, B):
     dr.close()
 
 
+# --- greedy acceptance (NEXT-2): bit-exact on every output -----------------------------------
+# Trees from the GPU tree kernel; target predictions planted along a random
+# walk from the root for a random number of steps, random elsewhere (so every
+# accepted length 0..N occurs), plus a batch with nothing accepted.
+@pytest.mark.parametrize("N,k,B", [(1, 1, 1), (3, 3, 4), (5, 8, 1), (7, 8, 32), (5, 10, 3),
+                                   (16, 16, 2), (4, 1, 5)])
+def test_accept_greedy_bit_exact(N, k, B):
+    import torch
+    from oracle import feo
+    from paper_2509_20416_amd import Drafter
+    cfg = C.TINY_F32_B1.with_(n_layers=N, topk=k, batch=B, draft_vocab=max(1024, 16 * k))
+    rng = np.random.default_rng(N * 1000 + k * 10 + B + 7)
+    ids = np.stack([np.stack([rng.choice(1000, k, replace=False) for _ in range(N)])
+                    for _ in range(B)]).astype(np.int32)
+    roots = rng.integers(0, 1000, B).astype(np.int32)
+    w = make_weights(cfg.with_(n_layers=1), 0)
+    w.layers = w.layers * N
+    dr = Drafter(cfg, w, max_batch=B, max_prefix=0, max_topk=k)
+    inp = make_inputs(cfg.with_(n_layers=N, prefix=0), 0)
+    inp.next_tokens = roots
+    inp.prefix_lens = np.zeros(B, np.int32)
+    inp.kcache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim), np.float32)] * N
+    inp.vcache = inp.kcache
+    di = dr.upload_inputs(inp, max_prefix=0)
+    di.next_tokens = torch.from_numpy(roots).cuda()
+    tree = dr.build_tree(di, torch.from_numpy(ids).cuda(), k)
+    torch.cuda.synchronize()
+    tok, par = tree["tokens"].cpu().numpy(), tree["parents"].cpu().numpy()
+    T = 1 + N * k
+    for nothing in (False, True):
+        nx = rng.integers(1000, 2000, (B, T)).astype(np.int32)   # no node carries these
+        if not nothing:
+            for b in range(B):
+                cur = 0
+                for _ in range(rng.integers(0, N + 1)):
+                    kids = [n for n in range(T) if par[b, n] == cur]
+                    if not kids:
+                        break
+                    c = kids[rng.integers(0, len(kids))]
+                    nx[b, cur] = tok[b, c]
+                    cur = c
+        got = dr.accept_greedy(tree, torch.from_numpy(nx).cuda(), k)
+        torch.cuda.synchronize()
+        ref = feo.accept_greedy(N, k, tok, tree["retrieve"].cpu().numpy(), nx)
+        for n in ref:
+            np.testing.assert_array_equal(got[n].cpu().numpy(), ref[n], err_msg=n)
+        if nothing:
+            assert (ref["accept_len"] == 0).all()
+    dr.close()
+
+
 # --- small shapes: several tiles, ragged chunks, ragged batch, P = 0 -----------------------
 SMALL = [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128, C.TINY_F32_B1]
 
