@@ -5,5 +5,6 @@ imported from here.
 """
 from .configs import DrafterConfig, NAMED, prefix_range  # noqa: F401
 from . import configs  # noqa: F401
-from .gen import (Inputs, LayerWeights, Weights, float_tensor, make_inputs,  # noqa: F401
+from .gen import (Inputs, LayerWeights, UpdateRows, Weights, float_tensor, make_inputs,  # noqa: F401
+                  make_update_rows,
                   make_prefix_lens, make_weights, to_f64)

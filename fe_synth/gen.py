@@ -182,3 +182,34 @@ def to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
     return a.astype(np.float64)
+
+
+@dataclasses.dataclass
+class UpdateRows:
+    """Verified positions whose drafter-cache rows are to be written: row m has
+    the target's features at position positions[m], the token after it, and
+    the cache row dst_rows[m] it goes to (caches of cache_rows rows)."""
+    features: np.ndarray   # [M, 3d]
+    tokens: np.ndarray     # int32 [M]
+    positions: np.ndarray  # int32 [M]
+    dst_rows: np.ndarray   # int32 [M]
+    cache_rows: int
+
+
+def make_update_rows(cfg: DrafterConfig, accepted: np.ndarray, prefix_lens: np.ndarray,
+                     capacity: int, seed: int = 0) -> UpdateRows:
+    """Sequence b appends accepted[b] positions P_b .. P_b + accepted[b] - 1 to
+    its cache, which owns rows b*capacity .. (b+1)*capacity - 1 (row = position)."""
+    accepted = np.asarray(accepted, dtype=np.int32)
+    prefix_lens = np.asarray(prefix_lens, dtype=np.int32)
+    assert np.all(prefix_lens + accepted <= capacity)
+    b_of = np.repeat(np.arange(len(accepted), dtype=np.int64), accepted)
+    j = np.concatenate([np.arange(a, dtype=np.int64) for a in accepted]) if len(accepted) else \
+        np.zeros(0, np.int64)
+    pos = (prefix_lens[b_of] + j).astype(np.int32)
+    dst = (b_of * capacity + pos).astype(np.int32)
+    M = len(pos)
+    feats = float_tensor("update.features", (M, cfg.n_feat_levels * cfg.hidden), seed, cfg.dtype)
+    toks = int_rng("update.tokens", seed).integers(0, cfg.target_vocab, size=M).astype(np.int32)
+    return UpdateRows(features=feats, tokens=toks, positions=pos, dst_rows=dst,
+                      cache_rows=int(len(accepted) * capacity))

@@ -221,6 +221,19 @@ static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, do
   free(bn); free(gt); free(up); free(dn);
 }
 
+/* x_0 of one row (Section 2.1, Eq. 1): g_t = FC(concat(l_t, m_t, h_t)) from
+ * row `row` of the features, then x_0 = FC(concat(g_t, e_{t+1})) with e_{t+1}
+ * the embedding of token `tok`.  f [F*d] and ge [2d] are scratch. */
+static void fused_input(const feo_config *c, const feo_weights *w, const void *features,
+                        size_t row, int32_t tok, double *f, double *ge, double *x0) {
+  const int32_t d = c->hidden, F = c->n_feat_levels;
+  for (int64_t e = 0; e < (int64_t)F * d; ++e)
+    f[e] = widen(features, c->dtype, row * F * d + (size_t)e);
+  matvec(w->w_fuse, c->dtype, d, (int64_t)F * d, f, ge);
+  for (int32_t e = 0; e < d; ++e) ge[d + e] = widen(w->embed, c->dtype, (size_t)tok * d + e);
+  matvec(w->w_in, c->dtype, d, 2 * d, ge, x0);
+}
+
 int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
                       const void *features, const int32_t *next_tok,
                       const void *const *kcache, const void *const *vcache,
@@ -243,15 +256,7 @@ int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
       free(xs); free(f); free(ge); free(hn); free(z); free(ord);
       return -1;
     }
-    /* g_t = FC(concat(l_t, m_t, h_t)) */
-    for (int64_t e = 0; e < (int64_t)F * d; ++e)
-      f[e] = widen(features, c->dtype, (size_t)b * F * d + (size_t)e);
-    matvec(w->w_fuse, c->dtype, d, (int64_t)F * d, f, ge);
-    /* e_{t+1}: row of the target's embedding table */
-    for (int32_t e = 0; e < d; ++e)
-      ge[d + e] = widen(w->embed, c->dtype, (size_t)next_tok[b] * d + e);
-    /* x_0 = FC(concat(g_t, e_{t+1})), the input of L_1 (Eq. 1) */
-    matvec(w->w_in, c->dtype, d, 2 * d, ge, xs);
+    fused_input(c, w, features, b, next_tok[b], f, ge, xs);
     /* h_i = L_i(h_{i-1}) (Eq. 1-2) */
     for (int32_t i = 1; i <= N; ++i)
       cascade_layer(c, &w->layers[i - 1], i, xs, kcache[i - 1], vcache[i - 1], prefix_off, P);
@@ -372,5 +377,39 @@ int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32
     accept_len[b] = best_len;
     accept_path[b] = best;
   }
+  return 0;
+}
+
+/* Drafter cache rows of verified positions (Section 2.4: after verification
+ * the accepted tokens' target features become the drafter's new context; the
+ * cache step is read under the cascade context of Section 2.1).  Every layer
+ * i keeps, for position p, its own key and value of the fused input x_0(p):
+ * the same projections it applies to the cascade entry x_0 of a pass whose
+ * prefix ends at p. */
+int feo_kv_update(const feo_config *c, const feo_weights *w, int32_t n_rows, const void *features,
+                  const int32_t *tokens, const int32_t *positions, double *const *k_out,
+                  double *const *v_out) {
+  if (!c || !w || n_rows < 0 || c->n_layers < 1 || c->cascade_ctx != FEO_CTX_CASCADE) return -1;
+  if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0) return -1;
+  const int32_t d = c->hidden, F = c->n_feat_levels, D = c->head_dim, Hkv = c->n_kv_heads;
+  const int32_t kvd = Hkv * D;
+  for (int32_t m = 0; m < n_rows; ++m)
+    if (tokens[m] < 0 || tokens[m] >= c->target_vocab || positions[m] < 0) return -1;
+  double *f = (double *)malloc(sizeof(double) * (size_t)F * d);
+  double *ge = (double *)malloc(sizeof(double) * (size_t)2 * d);
+  double *x0 = (double *)malloc(sizeof(double) * (size_t)d);
+  double *a = (double *)malloc(sizeof(double) * (size_t)d);
+  for (int32_t m = 0; m < n_rows; ++m) {
+    fused_input(c, w, features, (size_t)m, tokens[m], f, ge, x0);
+    for (int32_t i = 1; i <= c->n_layers; ++i) {
+      const feo_layer *L = &w->layers[i - 1];
+      double *k = k_out[i - 1] + (size_t)m * kvd, *v = v_out[i - 1] + (size_t)m * kvd;
+      feo_rmsnorm(x0, L->attn_norm, c->dtype, d, c->rms_eps, a);
+      matvec(L->wk, c->dtype, kvd, d, a, k);
+      matvec(L->wv, c->dtype, kvd, d, a, v);
+      for (int32_t h = 0; h < Hkv; ++h) feo_rope(k + (size_t)h * D, D, positions[m], c->rope_theta);
+    }
+  }
+  free(f); free(ge); free(x0); free(a);
   return 0;
 }

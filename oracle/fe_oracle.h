@@ -104,6 +104,21 @@ int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32
                       const int32_t *retrieve, const int32_t *target_next, int32_t *accept_len,
                       int32_t *accept_path, int32_t *accepted);
 
+/*
+ * Drafter KV-cache rows for verified positions (Section 2.4 update step, read
+ * under FEO_CTX_CASCADE; FEO_CTX_SELF is rejected).  Row m carries the
+ * target's features at position positions[m], features [n_rows,
+ * n_feat_levels*d] (dtype), and the token that follows it, tokens[m].  With
+ * x_0(m) = FC(concat(FC(f_m), e_{tokens[m]})) as in Eq. 1, every layer i
+ * gets a = RMSNorm(x_0(m); attn_norm_i), k = RoPE(W_k^i a, positions[m]) and
+ * v = W_v^i a.  k_out / v_out: [n_layers] pointers, each [n_rows, H_kv, D]
+ * double.  Returns 0, or -1 on invalid arguments (a token outside
+ * [0, target_vocab), a negative position).
+ */
+int feo_kv_update(const feo_config *cfg, const feo_weights *w, int32_t n_rows,
+                  const void *features, const int32_t *tokens, const int32_t *positions,
+                  double *const *k_out, double *const *v_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -44,6 +44,7 @@ def lib():
         L.feo_draft_forward.restype = C.c_int
         L.feo_build_tree.restype = C.c_int
         L.feo_accept_greedy.restype = C.c_int
+        L.feo_kv_update.restype = C.c_int
         L.feo_get_threads.restype = C.c_int
         _lib = L
     return _lib
@@ -105,6 +106,18 @@ def attend(q: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
     return out
 
 
+def _weights(w, N):
+    """FeoWeights pointing into the numpy arrays of w (plus what must stay alive)."""
+    layers = (FeoLayer * N)()
+    for i, lw in enumerate(w.layers):
+        for f in FeoLayer._fields_:
+            setattr(layers[i], f[0], _p(getattr(lw, f[0])))
+    d2t = np.ascontiguousarray(w.d2t, dtype=np.int32)
+    W = FeoWeights(_p(w.w_fuse), _p(w.w_in), _p(w.embed), _p(w.final_norm), _p(w.lm_head),
+                   _pi(d2t), C.cast(layers, C.POINTER(FeoLayer)))
+    return W, (layers, d2t)
+
+
 def draft_forward(cfg, w, inp, topk: Optional[int] = None, want_logits: bool = True,
                   batch_index: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
     """Run the oracle pass.  `batch_index` restricts it to some sequences of the
@@ -124,13 +137,7 @@ def draft_forward(cfg, w, inp, topk: Optional[int] = None, want_logits: bool = T
         kc = [np.ascontiguousarray(np.concatenate([a[cu[i]:cu[i + 1]] for i in idx])) for a in inp.kcache]
         vc = [np.ascontiguousarray(np.concatenate([a[cu[i]:cu[i + 1]] for i in idx])) for a in inp.vcache]
     B, N, d, V = len(idx), cfg.n_layers, cfg.hidden, cfg.draft_vocab
-    layers = (FeoLayer * N)()
-    for i, lw in enumerate(w.layers):
-        for f in FeoLayer._fields_:
-            setattr(layers[i], f[0], _p(getattr(lw, f[0])))
-    d2t = np.ascontiguousarray(w.d2t, dtype=np.int32)
-    W = FeoWeights(_p(w.w_fuse), _p(w.w_in), _p(w.embed), _p(w.final_norm), _p(w.lm_head),
-                   _pi(d2t), C.cast(layers, C.POINTER(FeoLayer)))
+    W, _keep = _weights(w, N)
     kp = (C.c_void_p * N)(*[a.ctypes.data for a in kc])
     vp = (C.c_void_p * N)(*[a.ctypes.data for a in vc])
     hidden = np.zeros((B, N + 1, d), dtype=np.float64)
@@ -186,3 +193,26 @@ def accept_greedy(n_layers: int, topk: int, tokens: np.ndarray, retrieve: np.nda
     if rc != 0:
         raise ValueError("oracle accept_greedy rejected its arguments")
     return out
+
+
+def kv_update(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.ndarray):
+    """Per-layer cache rows of verified positions (see feo_kv_update in
+    fe_oracle.h).  features [M, n_feat_levels*d] in storage precision, tokens
+    and positions [M].  Returns (k, v): lists over layers of [M, H_kv, D]
+    float64, keys rotated."""
+    features = np.ascontiguousarray(features)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    positions = np.ascontiguousarray(positions, dtype=np.int32)
+    M, N = len(tokens), cfg.n_layers
+    assert features.shape[0] == M and len(positions) == M
+    W, _keep = _weights(w, N)
+    ks = [np.zeros((M, cfg.n_kv_heads, cfg.head_dim)) for _ in range(N)]
+    vs = [np.zeros((M, cfg.n_kv_heads, cfg.head_dim)) for _ in range(N)]
+    kp = (C.POINTER(C.c_double) * N)(*[_pd(a) for a in ks])
+    vp = (C.POINTER(C.c_double) * N)(*[_pd(a) for a in vs])
+    cfgc = make_config(cfg)
+    rc = lib().feo_kv_update(C.byref(cfgc), C.byref(W), C.c_int32(M), _p(features), _pi(tokens),
+                             _pi(positions), kp, vp)
+    if rc != 0:
+        raise ValueError("oracle kv_update rejected its arguments")
+    return ks, vs
