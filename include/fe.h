@@ -194,6 +194,48 @@ fe_status fe_accept_greedy(fe_drafter *h, int32_t batch, int32_t topk, const int
                            int32_t *accept_len, int32_t *accept_path, int32_t *accepted,
                            void *stream);
 
+/* Destination of fe_kv_update: the N per-layer caches, each an array of
+ * `rows` rows of [H_kv, D] elements in the config's dtype (row r at element
+ * offset r * H_kv * D). */
+typedef struct {
+  void *const *k;  /* HOST array [n_layers] of device pointers, 16-byte aligned */
+  void *const *v;  /* HOST array [n_layers] of device pointers, 16-byte aligned */
+  int64_t rows;    /* rows of every cache array */
+} fe_kv_cache;
+
+/* Device workspace (bytes) fe_kv_update needs to process `chunk_rows` rows per
+ * chunk (0 if cfg is invalid or chunk_rows < 1).  Larger chunks let every
+ * weight matrix serve more rows per read. */
+size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chunk_rows);
+
+/* Drafter cache update after verification (Section 2.4's update step; the
+ * rows are read under FE_CTX_CASCADE, the only context it accepts).  Row m is
+ * a verified position: the target's features there, features[m] (n_feat_levels
+ * * d, as for fe_draft_forward), and the token after it, tokens[m].  With
+ * x_0(m) = FC(concat(FC(features[m]), e_{tokens[m]})) (Eq. 1), every layer i
+ * writes, at cache row dst_rows[m],
+ *   k = RoPE(W_k^i RMSNorm(x_0(m); attn_norm_i), positions[m])   (rotated)
+ *   v = W_v^i RMSNorm(x_0(m); attn_norm_i)
+ * in the storage dtype: the projections the pass applies to its own cascade
+ * entry x_0, so a later pass over the grown prefix reads the row as a cached
+ * key/value.  Nothing else in the caches is written.
+ *  features  [n_rows, n_feat_levels*d] dtype, 16-byte aligned
+ *  tokens, positions, dst_rows  [n_rows] int32, 4-byte aligned
+ *  workspace caller-owned device memory, 256-byte aligned, at least
+ *            fe_kv_update_workspace_bytes(cfg, 1); the rows are processed in
+ *            chunks of the most rows that fit (work on the stream, no
+ *            allocation).  The workspace of the handle is not touched.
+ * Device-side values the host cannot check: a dst_rows entry outside
+ * [0, cache->rows) is not written; a position outside [0, cfg.max_prefix) or a
+ * token outside [0, target_vocab) writes NaN rows.  Rows that share a
+ * destination race.  Errors: FE_E_INVALID (NULL handle, cache or array,
+ * n_rows < 0, cfg.max_prefix == 0), FE_E_UNSUPPORTED (FE_CTX_SELF),
+ * FE_E_ALIGN, FE_E_WORKSPACE (workspace NULL or below one row); nothing is
+ * launched on an error.  n_rows == 0 is a no-op. */
+fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
+                       const int32_t *tokens, const int32_t *positions, const int32_t *dst_rows,
+                       const fe_kv_cache *cache, void *workspace, size_t ws_bytes, void *stream);
+
 /* Replays fe_draft_forward through a captured HIP graph when on != 0 (the
  * default is off).  A graph is captured on the first call with a given set of
  * arguments and replayed while they stay the same. */

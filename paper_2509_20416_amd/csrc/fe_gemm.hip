@@ -707,6 +707,51 @@ template <typename T> struct EpiQkv {
   }
 };
 
+// Cache rows of verified positions: virtual columns [0, kvd) are the key
+// rows of W_k (rotary pairs packed per 16-column tile as for EpiQkv), then
+// the value rows; row m is rotated at positions[m] and stored in the storage
+// type at cache row dst_rows[m].
+template <typename T> struct EpiKvCache {
+  static constexpr bool kRowStream = true, kSplitK = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
+  KvCacheArgs a;
+  int nvcols;  // 2 * Hkv * D
+  __device__ const T *wrow(int c) const {
+    const int kvd = a.Hkv * a.D;
+    if (c < kvd) return (const T *)a.wk + (size_t)((c / a.D) * a.D + rope_dim(c % a.D, a.D)) * a.d;
+    return (const T *)a.wv + (size_t)(c - kvd) * a.d;
+  }
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
+    const int kvd = a.Hkv * a.D, D = a.D;
+    const float qnan = __int_as_float(0x7fc00000);
+    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
+      const int m = idx / span, c = idx % span, vc = c0 + c;
+      if (vc >= nvcols) continue;
+      const long dst = a.dst_rows[m];
+      if (dst < 0 || dst >= a.cache_rows) continue;  // nowhere to write
+      const int pos = a.positions[m];
+      const bool bad = pos < 0 || pos >= a.pos_limit;
+      const float val = tile[m * ldt + c];
+      if (vc < kvd) {
+        const int h = vc / D, cc = vc % D, dd = rope_dim(cc, D);
+        float o = qnan;
+        if (!bad) {
+          const float pv = tile[m * ldt + (c ^ 8)];
+          const int pm = 8 * (cc >> 4) + (cc & 7);
+          const float c_ = a.rope[((size_t)pos * (D / 2) + pm) * 2];
+          const float s_ = a.rope[((size_t)pos * (D / 2) + pm) * 2 + 1];
+          o = (cc & 8) ? (val * c_ + pv * s_) : (val * c_ - pv * s_);
+        }
+        ((T *)a.k_cache)[(size_t)dst * kvd + (size_t)h * D + dd] = Elt<T>::from_f(o);
+      } else {
+        ((T *)a.v_cache)[(size_t)dst * kvd + (vc - kvd)] = Elt<T>::from_f(bad ? qnan : val);
+      }
+    }
+  }
+};
+
 template <typename T> struct EpiSwiglu {
   static constexpr bool kRowStream = true, kSplitK = false;
   using Pre = NoPre;
@@ -1021,6 +1066,18 @@ hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, c
   }
   EpiQkv<float> e{a, nv};
   return run_gemm<float, 1, 8, 1>((const float *)A, lda, arows, M, a.d, e, na, s, ss);
+}
+
+hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs &a,
+                        hipStream_t s, const SplitScratch *ss) {
+  if (M <= 0) return hipSuccess;
+  const int nv = 2 * a.Hkv * a.D;
+  if (dt) {
+    EpiKvCache<bf16_t> e{a, nv};
+    return run_gemm<bf16_t, 1, 4, 1>((const bf16_t *)A, lda, kDenseRows, M, a.d, e, nullptr, s, ss);
+  }
+  EpiKvCache<float> e{a, nv};
+  return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, a.d, e, nullptr, s, ss);
 }
 
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,

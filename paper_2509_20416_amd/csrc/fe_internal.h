@@ -234,6 +234,21 @@ struct QkvArgs {
 hipError_t gemm_qkv(int dt, const void *A, int lda, const ARows &arows, int M, const QkvArgs &a,
                     const NormA *na, hipStream_t s, const SplitScratch *ss = nullptr);
 
+struct KvCacheArgs {
+  const void *wk, *wv;
+  int d, D, Hkv;
+  const int32_t *positions;  // [M] rotary position of each row
+  const int32_t *dst_rows;   // [M] cache row of each row
+  long cache_rows;           // rows outside [0, cache_rows) are not written
+  int pos_limit;             // positions outside [0, pos_limit) give NaN rows
+  const float *rope;         // rotary table covering [0, pos_limit)
+  void *k_cache, *v_cache;   // [cache_rows, Hkv, D] storage type
+};
+// K/V projections of M RMS-normed rows (A [M, d]), keys rotated; written to
+// the cache rows dst_rows[m] in the storage type.
+hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs &a,
+                        hipStream_t s, const SplitScratch *ss = nullptr);
+
 // s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,
                        const void *w_gate, const void *w_up, int I, void *s_out, int lds,

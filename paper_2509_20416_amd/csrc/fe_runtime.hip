@@ -83,6 +83,29 @@ Layout layout_of(const fe_config &c) {
   return L;
 }
 
+// Workspace of fe_kv_update for chunks of C rows: the fused inputs, x_0 in
+// fp32, its per-layer RMSNorm, and split-K slices for the 256-row launches.
+struct UpdLayout {
+  size_t cat, X, an, splitk, total;
+  size_t splitk_floats;
+};
+
+UpdLayout upd_layout_of(const fe_config &c, size_t C) {
+  UpdLayout U{};
+  const size_t d = c.hidden, es = es_of(c), kvd = (size_t)c.n_kv_heads * c.head_dim;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
+  U.cat = take(C * 2 * d * es);
+  U.X = take(C * d * 4);
+  U.an = take(C * d * es);
+  const size_t rows = std::min<size_t>(kGemmMaxRows, C);
+  const size_t cols = (std::max<size_t>(2 * kvd, d) + 127) / 128 * 128;
+  U.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
+  U.splitk = take(U.splitk_floats * 4);
+  U.total = o;
+  return U;
+}
+
 fe_status check_config(const fe_config *c) {
   if (!c) return fail(FE_E_INVALID, "config is NULL");
   if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
@@ -486,6 +509,100 @@ extern "C" fe_status fe_accept_greedy(fe_drafter *h, int32_t batch, int32_t topk
     if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "acceptance arrays must be 4-byte aligned");
   FE_TRY(accept_greedy(batch, c.n_layers, topk, tokens, retrieve, target_next, accept_len,
                        accept_path, accepted, (hipStream_t)stream));
+  return FE_OK;
+}
+
+extern "C" size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chunk_rows) {
+  if (check_config(cfg) != FE_OK) return 0;
+  if (chunk_rows < 1) {
+    fail(FE_E_INVALID, "chunk_rows must be positive");
+    return 0;
+  }
+  return upd_layout_of(*cfg, (size_t)chunk_rows).total;
+}
+
+// Drafter cache rows of verified positions (Section 2.4 update step, cascade
+// context): x_0 of every row as in the pass (Eq. 1), then per layer its
+// RMSNorm and the rotated K / V projections, scattered into the caches.
+extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
+                                  const int32_t *tokens, const int32_t *positions,
+                                  const int32_t *dst_rows, const fe_kv_cache *cache,
+                                  void *workspace, size_t ws_bytes, void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const fe_config &c = h->cfg;
+  if (c.cascade_ctx != FE_CTX_CASCADE)
+    return fail(FE_E_UNSUPPORTED, "the cache update is defined for the cascade context only");
+  if (n_rows < 0) return fail(FE_E_INVALID, "n_rows %d is negative", n_rows);
+  if (!cache || !cache->k || !cache->v) return fail(FE_E_INVALID, "cache and its pointer arrays are required");
+  if (cache->rows < 0) return fail(FE_E_INVALID, "cache->rows is negative");
+  if (n_rows == 0) return FE_OK;
+  if (c.max_prefix < 1) return fail(FE_E_INVALID, "config max_prefix is 0: no cache position is valid");
+  if (!features || !tokens || !positions || !dst_rows)
+    return fail(FE_E_INVALID, "features, tokens, positions and dst_rows are required");
+  if (!aligned16(features)) return fail(FE_E_ALIGN, "features must be 16-byte aligned");
+  const void *ip[] = {tokens, positions, dst_rows};
+  for (const void *q : ip)
+    if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "tokens, positions and dst_rows must be 4-byte aligned");
+  for (int l = 0; l < c.n_layers; ++l) {
+    if (!cache->k[l] || !cache->v[l]) return fail(FE_E_INVALID, "cache pointer of layer %d is NULL", l);
+    if (!aligned16(cache->k[l]) || !aligned16(cache->v[l]))
+      return fail(FE_E_ALIGN, "cache of layer %d is not 16-byte aligned", l);
+  }
+  if (!workspace) return fail(FE_E_WORKSPACE, "workspace is NULL");
+  if (((uintptr_t)workspace & 255u)) return fail(FE_E_ALIGN, "workspace must be 256-byte aligned");
+  // rows per chunk: the most that fit the workspace, up to n_rows
+  size_t lo = 1, hi = (size_t)n_rows;
+  if (upd_layout_of(c, 1).total > ws_bytes)
+    return fail(FE_E_WORKSPACE, "workspace of %zu bytes is below the %zu bytes of one row", ws_bytes,
+                upd_layout_of(c, 1).total);
+  while (lo < hi) {
+    const size_t mid = (lo + hi + 1) / 2;
+    if (upd_layout_of(c, mid).total <= ws_bytes) lo = mid;
+    else hi = mid - 1;
+  }
+  const int C = (int)lo;
+  const UpdLayout U = upd_layout_of(c, (size_t)C);
+  hipStream_t s = (hipStream_t)stream;
+  if (!h->table_ready) {
+    FE_TRY(rope_table((float *)(h->ws + h->L.rope), h->L.npos, c.head_dim, (double)c.rope_theta, s));
+    h->table_ready = true;
+  }
+  const int dt = c.dtype == FE_BF16 ? 1 : 0, es = es_of(c);
+  const int d = c.hidden, F = c.n_feat_levels, kvd = c.n_kv_heads * c.head_dim;
+  char *ws = (char *)workspace;
+  char *cat = ws + U.cat, *an = ws + U.an;
+  float *X = (float *)(ws + U.X);
+  const SplitScratch ss{(float *)(ws + U.splitk), U.splitk_floats};
+  for (int r0 = 0; r0 < n_rows; r0 += C) {
+    const int Mc = std::min(C, n_rows - r0);
+    // stage by stage over the chunk, so that each weight matrix is read by
+    // consecutive launches
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      FE_TRY(gemm_store(dt, (const char *)features + (size_t)(r0 + s0) * F * d * es, F * d, Ms, F * d,
+                        h->w.w_fuse, d, cat + (size_t)s0 * 2 * d * es, 2 * d, h->w.embed,
+                        tokens + r0 + s0, c.target_vocab, cat + ((size_t)s0 * 2 * d + d) * es, 2 * d,
+                        d, Ms, s, &ss));
+    }
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      FE_TRY(gemm_resid(dt, cat + (size_t)s0 * 2 * d * es, 2 * d, Ms, 2 * d, h->w.w_in, d,
+                        X + (size_t)s0 * d, d, nullptr, 0, nullptr, 1, 0, nullptr, s, &ss));
+    }
+    for (int l = 0; l < c.n_layers; ++l) {
+      const fe_layer_weights &lw = h->layers[l];
+      FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an, d, c.rms_eps, s));
+      for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+        const int Ms = std::min(kGemmMaxRows, Mc - s0);
+        const KvCacheArgs ka{lw.wk, lw.wv, d, c.head_dim, c.n_kv_heads,
+                             positions + r0 + s0, dst_rows + r0 + s0, (long)cache->rows,
+                             c.max_prefix, (const float *)(h->ws + h->L.rope),
+                             cache->k[l], cache->v[l]};
+        FE_TRY(gemm_kvcache(dt, an + (size_t)s0 * d * es, d, Ms, ka, s, &ss));
+      }
+    }
+  }
+  (void)kvd;
   return FE_OK;
 }
 

@@ -87,7 +87,7 @@ class Drafter:
         fe.fe_set_graph_mode(self.handle, on)
 
     def set_attention_split(self, chunks_per_workgroup: int) -> None:
-        """128-key prefix chunks per attention workgroup; 0 = automatic."""
+        """64-key prefix chunks per attention work unit; 0 = automatic."""
         fe.fe_set_attention_split(self.handle, chunks_per_workgroup)
 
     def upload_inputs(self, inp, max_prefix: Optional[int] = None) -> DeviceInputs:
@@ -188,6 +188,29 @@ class Drafter:
                             out["accept_len"].data_ptr(), out["accept_path"].data_ptr(),
                             out["accepted"].data_ptr(), self.stream())
         return out
+
+    def kv_update(self, features, tokens, positions, dst_rows, kcache, vcache,
+                  chunk_rows: int = 1024, n_rows: Optional[int] = None) -> None:
+        """Write the drafter cache rows of verified positions (fe_kv_update):
+        features [M, 3d], tokens / positions / dst_rows [M] int32 and the
+        per-layer caches kcache / vcache ([rows, H_kv, D]), all on the device.
+        The workspace for `chunk_rows`-row chunks is allocated once and kept."""
+        torch = _torch()
+        N = self.cfg.n_layers
+        M = int(n_rows if n_rows is not None else tokens.shape[0])
+        need = fe.fe_kv_update_workspace_bytes(self.ccfg, int(chunk_rows))
+        if need == 0:
+            raise fe.FeError(fe.FE_E_INVALID, fe.fe_last_error())
+        if getattr(self, "_upd_ws", None) is None or self._upd_ws.numel() < need:
+            self._upd_ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        self._ukp = (C.c_void_p * N)(*[k.data_ptr() for k in kcache])
+        self._uvp = (C.c_void_p * N)(*[v.data_ptr() for v in vcache])
+        rows = int(kcache[0].shape[0])
+        cache = fe.fe_kv_cache(C.cast(self._ukp, C.POINTER(C.c_void_p)),
+                               C.cast(self._uvp, C.POINTER(C.c_void_p)), rows)
+        fe.fe_kv_update(self.handle, M, features.data_ptr(), tokens.data_ptr(),
+                        positions.data_ptr(), dst_rows.data_ptr(), cache,
+                        self._upd_ws.data_ptr(), need, self.stream())
 
     def close(self) -> None:
         if getattr(self, "handle", None):

@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
-           "fe_accept_greedy", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
+           "fe_accept_greedy", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
            "fe_drafter_destroy", "fe_last_error")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
@@ -48,6 +48,10 @@ class fe_weights(C.Structure):
 class fe_kv_view(C.Structure):
     _fields_ = [("k", C.POINTER(C.c_void_p)), ("v", C.POINTER(C.c_void_p)),
                 ("cu_prefix", C.c_void_p), ("max_prefix", C.c_int32)]
+
+
+class fe_kv_cache(C.Structure):
+    _fields_ = [("k", C.POINTER(C.c_void_p)), ("v", C.POINTER(C.c_void_p)), ("rows", C.c_int64)]
 
 
 class fe_tree_out(C.Structure):
@@ -92,6 +96,11 @@ def lib() -> C.CDLL:
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
         L.fe_accept_greedy.restype = C.c_int
         L.fe_accept_greedy.argtypes = [C.c_void_p, C.c_int32, C.c_int32] + [C.c_void_p] * 7
+        L.fe_kv_update_workspace_bytes.restype = C.c_size_t
+        L.fe_kv_update_workspace_bytes.argtypes = [C.POINTER(fe_config), C.c_int32]
+        L.fe_kv_update.restype = C.c_int
+        L.fe_kv_update.argtypes = [C.c_void_p, C.c_int32] + [C.c_void_p] * 4 + \
+            [C.POINTER(fe_kv_cache), C.c_void_p, C.c_size_t, C.c_void_p]
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
         L.fe_set_attention_split.restype = C.c_int
@@ -148,6 +157,18 @@ def fe_accept_greedy(h: int, batch: int, topk: int, tokens: int, retrieve: int, 
                                  C.c_void_p(retrieve), C.c_void_p(target_next),
                                  C.c_void_p(accept_len), C.c_void_p(accept_path),
                                  C.c_void_p(accepted), C.c_void_p(stream)))
+
+
+def fe_kv_update_workspace_bytes(cfg: fe_config, chunk_rows: int) -> int:
+    return int(lib().fe_kv_update_workspace_bytes(C.byref(cfg), int(chunk_rows)))
+
+
+def fe_kv_update(h: int, n_rows: int, features: int, tokens: int, positions: int, dst_rows: int,
+                 cache: fe_kv_cache, workspace: int, ws_bytes: int, stream: int) -> None:
+    check(lib().fe_kv_update(C.c_void_p(h), int(n_rows), C.c_void_p(features),
+                             C.c_void_p(tokens), C.c_void_p(positions), C.c_void_p(dst_rows),
+                             C.byref(cache), C.c_void_p(workspace), C.c_size_t(ws_bytes),
+                             C.c_void_p(stream)))
 
 
 def fe_set_graph_mode(h: int, on: bool) -> None:

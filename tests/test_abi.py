@@ -137,3 +137,43 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(_fe, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         _fe.lib()
+
+
+def test_kv_update_validates_before_enqueue(fe):
+    """fe_kv_update over fake addresses: every bad call fails on the host."""
+    cfg = _cfg(fe)
+    w, keep = _fake_weights(fe, cfg.n_layers)
+    one = fe.fe_kv_update_workspace_bytes(cfg, 1)
+    big = fe.fe_kv_update_workspace_bytes(cfg, 1024)
+    assert 0 < one < big
+    assert fe.fe_kv_update_workspace_bytes(cfg, 0) == 0
+    assert fe.fe_kv_update_workspace_bytes(_cfg(fe, head_dim=96), 8) == 0
+    h = fe.fe_drafter_create(cfg, w, 1 << 30, fe.fe_workspace_bytes(cfg))
+    try:
+        N = cfg.n_layers
+        kp = (C.c_void_p * N)(*[(1 << 31) + 4096 * i for i in range(N)])
+        cache = fe.fe_kv_cache(C.cast(kp, C.POINTER(C.c_void_p)), C.cast(kp, C.POINTER(C.c_void_p)),
+                               1 << 20)
+        ok = dict(n=3, feat=1 << 34, tok=1 << 35, pos=(1 << 35) + 256, dst=(1 << 35) + 512,
+                  cache=cache, ws=1 << 36, wsb=big)
+        bad = [(dict(n=-1), "FE_E_INVALID"), (dict(feat=0), "FE_E_INVALID"),
+               (dict(feat=(1 << 34) + 8), "FE_E_ALIGN"), (dict(dst=(1 << 35) + 2), "FE_E_ALIGN"),
+               (dict(cache=fe.fe_kv_cache()), "FE_E_INVALID"), (dict(ws=0), "FE_E_WORKSPACE"),
+               (dict(ws=(1 << 36) + 64), "FE_E_ALIGN"), (dict(wsb=one - 1), "FE_E_WORKSPACE")]
+        for case, status in bad:
+            a = dict(ok, **case)
+            with pytest.raises(fe.FeError, match=status):
+                fe.fe_kv_update(h, a["n"], a["feat"], a["tok"], a["pos"], a["dst"], a["cache"],
+                                a["ws"], a["wsb"], 0)
+        fe.fe_kv_update(h, 0, 0, 0, 0, 0, cache, 0, 0, 0)   # no rows: no work, OK
+    finally:
+        fe.fe_drafter_destroy(h)
+    for kw, status in ((dict(cascade_ctx=fe.FE_CTX_SELF), "FE_E_UNSUPPORTED"),
+                       (dict(max_prefix=0), "FE_E_INVALID")):
+        c2 = _cfg(fe, **kw)
+        h = fe.fe_drafter_create(c2, w, 1 << 30, fe.fe_workspace_bytes(c2))
+        try:
+            with pytest.raises(fe.FeError, match=status):
+                fe.fe_kv_update(h, 3, 1 << 34, 1 << 35, 1 << 35, 1 << 35, cache, 1 << 36, big, 0)
+        finally:
+            fe.fe_drafter_destroy(h)
