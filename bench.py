@@ -121,6 +121,60 @@ def cpu_baseline(cfg, w, inp, budget_s):
                       f"{n1} in {el1:.1f} s on 1 thread; fp64"}
 
 
+def kv_update_cost(cfg, M):
+    """Algorithmic FLOPs and bytes of one cache update of M rows: the fusion
+    and input FCs and every layer's K/V projection per row; every weight
+    matrix read once, each row's features and embedding row read, its K/V rows
+    written."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    d, F, N = cfg.hidden, cfg.n_feat_levels, cfg.n_layers
+    kvd = cfg.n_kv_heads * cfg.head_dim
+    per_row_mac = F * d * d + 2 * d * d + N * d * 2 * kvd
+    wbytes = per_row_mac * es
+    rbytes = M * (F * d + d + N * 2 * kvd) * es
+    return 2 * M * per_row_mac, wbytes + rbytes
+
+
+def time_kv_update(dr, cfg, positions, reps=20, warmup=3, chunk_rows=1024):
+    """fe_kv_update of len(positions) rows into fresh caches (rows written in
+    order), eager launches on the current stream, mean per call."""
+    import numpy as np
+    import torch
+    from fe_synth.gen import float_tensor, int_rng
+    from paper_2509_20416_amd.drafter import to_device
+    M = len(positions)
+    dev = dr.device
+    feats = to_device(float_tensor("bench.update.features", (M, cfg.n_feat_levels * cfg.hidden),
+                                   7, cfg.dtype), cfg.dtype, dev)
+    toks = to_device(int_rng("bench.update.tokens", 7).integers(0, cfg.target_vocab, M)
+                     .astype(np.int32), "i32", dev)
+    pos = to_device(np.asarray(positions, np.int32), "i32", dev)
+    dst = to_device(np.arange(M, dtype=np.int32), "i32", dev)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    shape = (M, cfg.n_kv_heads, cfg.head_dim)
+    ks = [torch.empty(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
+    vs = [torch.empty(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
+    for _ in range(warmup):
+        dr.kv_update(feats, toks, pos, dst, ks, vs, chunk_rows=chunk_rows)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(reps):
+        dr.kv_update(feats, toks, pos, dst, ks, vs, chunk_rows=chunk_rows)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    flops, nbytes = kv_update_cost(cfg, M)
+    tfs = flops / (ms * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFS[cfg.dtype]
+    return {"rows": M, "us_per_call": ms * 1000.0, "flops": flops, "bytes": nbytes,
+            "achieved_TFLOPs": tfs, "mfma_frac": tfs / peak,
+            "hbm_frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "bound": "mfma" if flops / nbytes > peak * 1e3 / HBM_PEAK_GBS else "hbm",
+            "issue": "eager, from Python"}
+
+
 def time_second(name, seed, steps, warmup):
     """The other half of the metric (by default the batch-32 workload): passes
     (forward + tree, graph replays) timed the same way as the primary one."""
@@ -147,6 +201,10 @@ def time_second(name, seed, steps, warmup):
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / steps
+    # NEXT-1 for this batch: every sequence appends N+1 verified positions
+    # (the most one cycle accepts) after its prefix
+    upd_pos = np.concatenate([np.arange(p - cfg.n_layers - 1, p) for p in plens])
+    upd = time_kv_update(dr, cfg, upd_pos)
     dr.close()
     pbytes, pflops = pass_bytes(cfg, plens), pass_flops(cfg, plens)
     peak = MFMA_PEAK_TFS[cfg.dtype]
@@ -155,7 +213,8 @@ def time_second(name, seed, steps, warmup):
             "us_per_pass": ms * 1000.0, "drafts_per_s": cfg.batch * 1000.0 / ms,
             "hbm_frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "mfma_frac": pflops / (ms * 1e-3) / 1e12 / peak,
-            "mfma_ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3 / peak)}
+            "mfma_ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3 / peak),
+            "next_kv_update_cycle": upd}
 
 
 def main():
@@ -263,6 +322,16 @@ def main():
     torch.cuda.synchronize()
     accept_us = ev0.elapsed_time(ev1) * 1000.0 / 100
 
+    # NEXT-1, the drafter cache update: one cycle's N+1 verified positions,
+    # and a whole prefix of max_prefix positions (the prompt's cache, the
+    # shape where the update becomes matrix-core bound)
+    P = int(plens.max())
+    upd_cycle = time_kv_update(dr, cfg, np.arange(max(0, P - cfg.n_layers - 1), P))
+    upd_prefill = time_kv_update(dr, cfg, np.arange(P), reps=10)
+    log(f"kv update: {upd_cycle['rows']} rows {upd_cycle['us_per_call']:.1f} us, "
+        f"{upd_prefill['rows']} rows {upd_prefill['us_per_call']:.1f} us "
+        f"({upd_prefill['mfma_frac'] * 100:.1f}% of the MFMA peak)")
+
     B = cfg.batch
     gbytes = gateup_bytes(cfg, B)
     achieved = gbytes / (gu_avg * 1e-3) / 1e9
@@ -293,12 +362,13 @@ def main():
         "pass_roofline": {"bytes_per_pass": pbytes,
                           "achieved_GBs": pbytes / (ms * 1e-3) / 1e9,
                           "frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        # matrix-core use over the whole pass, against the most that an
-        # HBM-bound pass of this arithmetic intensity could reach
         # host-issued launches back to back: the rate is bound by the Python
         # call, the kernel itself is a few microseconds
         "next_accept_greedy": {"us_per_call": accept_us, "batch": B,
                                "accept_len_seq0": accept_len0, "issue": "eager, from Python"},
+        "next_kv_update": {"cycle": upd_cycle, "prefill": upd_prefill},
+        # matrix-core use over the whole pass, against the most that an
+        # HBM-bound pass of this arithmetic intensity could reach
         "pass_mfma": {"flops_per_pass": pflops,
                       "achieved_TFLOPs": pflops / (ms * 1e-3) / 1e12,
                       "peak_TFLOPs": MFMA_PEAK_TFS[cfg.dtype],
