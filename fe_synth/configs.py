@@ -30,7 +30,7 @@ class DrafterConfig:
     prefix: object             # int (every sequence) or (lo, hi) inclusive range
     topk: int
     rms_eps: float = 1e-5
-    cascade_ctx: str = "cascade"   # "cascade" or "self"
+    cascade_ctx: str = "cascade"   # "cascade", "self" or "parallel" (parallel heads)
     n_feat_levels: int = 3
 
     @property

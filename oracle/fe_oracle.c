@@ -147,14 +147,18 @@ static double silu(double u) { return u / (1.0 + exp(-u)); }
 
 /* One decoder layer L_i of the cascade for one sequence (Section 2.1, Eq. 1-2).
  * xs[0..i-1] are the cascade states produced so far (x_0 = fused input);
- * writes x_i into xs[i]. */
+ * writes x_i into xs[i].  Under FEO_CTX_PARALLEL (the ablation of Section 3.2
+ * that replaces the series by parallel heads) every layer reads x_0 instead:
+ * x_i = L_i(x_0), attending to its prefix plus x_0 at position P. */
 static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, double *xs,
                           const void *kc, const void *vc, int64_t prefix_off, int32_t P) {
   const int32_t d = c->hidden, D = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads;
   const int32_t G = Hq / Hkv, I = c->intermediate;
   const int32_t qd = Hq * D, kvd = Hkv * D;
-  const int32_t j0 = (c->cascade_ctx == FEO_CTX_CASCADE) ? 0 : i - 1;
-  const int32_t nctx = i - j0;
+  /* the layer's input: x_{i-1} in series, x_0 for parallel heads */
+  const int32_t src = (c->cascade_ctx == FEO_CTX_PARALLEL) ? 0 : i - 1;
+  const int32_t j0 = (c->cascade_ctx == FEO_CTX_CASCADE) ? 0 : src;
+  const int32_t nctx = (c->cascade_ctx == FEO_CTX_CASCADE) ? i : 1;
 
   /* Pre-attention RMSNorm and projections of every context row. */
   double *a = (double *)malloc(sizeof(double) * (size_t)d);
@@ -168,7 +172,7 @@ static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, do
     matvec(L->wk, c->dtype, kvd, d, a, kn + (size_t)t * kvd);
     matvec(L->wv, c->dtype, kvd, d, a, vn + (size_t)t * kvd);
     for (int32_t h = 0; h < Hkv; ++h) feo_rope(kn + (size_t)t * kvd + (size_t)h * D, D, pos, c->rope_theta);
-    if (j == i - 1) {
+    if (j == src) {
       matvec(L->wq, c->dtype, qd, d, a, q);
       for (int32_t h = 0; h < Hq; ++h) feo_rope(q + (size_t)h * D, D, pos, c->rope_theta);
     }
@@ -203,7 +207,7 @@ static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, do
   /* Output projection and residual. */
   double *xp = (double *)malloc(sizeof(double) * (size_t)d);
   matvec(L->wo, c->dtype, d, qd, o, xp);
-  for (int32_t e = 0; e < d; ++e) xp[e] += xs[(size_t)(i - 1) * d + e];
+  for (int32_t e = 0; e < d; ++e) xp[e] += xs[(size_t)src * d + e];
 
   /* Post-attention RMSNorm, SwiGLU MLP and residual. */
   double *bn = (double *)malloc(sizeof(double) * (size_t)d);
@@ -240,6 +244,7 @@ int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
                       const int32_t *prefix_lens, int32_t topk, double *hidden, double *logits,
                       int32_t *topk_draft, int32_t *topk_ids, double *topk_probs) {
   if (!c || !w || batch < 0 || topk < 1 || topk > c->draft_vocab || c->n_layers < 1) return -1;
+  if (c->cascade_ctx < FEO_CTX_CASCADE || c->cascade_ctx > FEO_CTX_PARALLEL) return -1;
   if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0) return -1;
   const int32_t d = c->hidden, N = c->n_layers, V = c->draft_vocab, F = c->n_feat_levels;
   int64_t prefix_off = 0;
@@ -389,7 +394,7 @@ int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32
 int feo_kv_update(const feo_config *c, const feo_weights *w, int32_t n_rows, const void *features,
                   const int32_t *tokens, const int32_t *positions, double *const *k_out,
                   double *const *v_out) {
-  if (!c || !w || n_rows < 0 || c->n_layers < 1 || c->cascade_ctx != FEO_CTX_CASCADE) return -1;
+  if (!c || !w || n_rows < 0 || c->n_layers < 1 || c->cascade_ctx == FEO_CTX_SELF) return -1;
   if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0) return -1;
   const int32_t d = c->hidden, F = c->n_feat_levels, D = c->head_dim, Hkv = c->n_kv_heads;
   const int32_t kvd = Hkv * D;

@@ -20,7 +20,10 @@ extern "C" {
 #endif
 
 enum { FEO_F32 = 0, FEO_BF16 = 1 };
-enum { FEO_CTX_CASCADE = 0, FEO_CTX_SELF = 1 };
+/* What layer i reads: CASCADE and SELF are the two readings of Eq. 2 (see
+ * feo_draft_forward); PARALLEL is the ablation "w/o cascaded structure"
+ * (Section 3.2, Table 2): every layer takes x_0, x_i = L_i(x_0). */
+enum { FEO_CTX_CASCADE = 0, FEO_CTX_SELF = 1, FEO_CTX_PARALLEL = 2 };
 
 typedef struct {
   int32_t hidden, n_q_heads, n_kv_heads, head_dim, intermediate, n_layers;
@@ -106,7 +109,8 @@ int feo_accept_greedy(int32_t batch, int32_t n_layers, int32_t topk, const int32
 
 /*
  * Drafter KV-cache rows for verified positions (Section 2.4 update step, read
- * under FEO_CTX_CASCADE; FEO_CTX_SELF is rejected).  Row m carries the
+ * under FEO_CTX_CASCADE, where it equals FEO_CTX_PARALLEL's; FEO_CTX_SELF is
+ * rejected).  Row m carries the
  * target's features at position positions[m], features [n_rows,
  * n_feat_levels*d] (dtype), and the token that follows it, tokens[m].  With
  * x_0(m) = FC(concat(FC(f_m), e_{tokens[m]})) as in Eq. 1, every layer i

@@ -77,7 +77,7 @@ def make_config(cfg) -> FeoConfig:
     return FeoConfig(cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.intermediate,
                      cfg.n_layers, cfg.draft_vocab, cfg.target_vocab, cfg.n_feat_levels,
                      1 if cfg.dtype == "bf16" else 0,
-                     0 if cfg.cascade_ctx == "cascade" else 1,
+                     {"cascade": 0, "self": 1, "parallel": 2}[cfg.cascade_ctx],
                      float(cfg.rope_theta), float(cfg.rms_eps))
 
 

@@ -101,6 +101,17 @@ def test_layers_are_independent_and_bf16_widening(feo):
     assert np.abs(ks[0] - ks[1]).max() > 1e-3
 
 
+def test_parallel_heads_share_the_cascade_rows(feo):
+    """Without the cascade every head keys x_0(p) too: the same rows."""
+    cfg = PIN
+    w = make_weights(cfg, 4)
+    up = make_update_rows(cfg, np.array([3]), np.array([2]), capacity=8, seed=4)
+    a = feo.kv_update(cfg, w, up.features, up.tokens, up.positions)
+    b = feo.kv_update(cfg.with_(cascade_ctx="parallel"), w, up.features, up.tokens, up.positions)
+    for x, y in zip(a[0] + a[1], b[0] + b[1]):
+        np.testing.assert_array_equal(x, y)
+
+
 def test_rejects_self_context_and_bad_tokens(feo):
     cfg = PIN
     w = make_weights(cfg, 1)

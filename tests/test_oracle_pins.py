@@ -58,7 +58,7 @@ def _caches_from_hf(cfg, w, plens, seed):
     return Ys, kc, vc
 
 
-@pytest.mark.parametrize("ctx", ["cascade", "self"])
+@pytest.mark.parametrize("ctx", ["cascade", "self", "parallel"])
 def test_cascade_layers_equal_textbook_llama_layer(feo, ctx):
     from tests import hf_ref
     cfg = PIN.with_(cascade_ctx=ctx)
@@ -80,8 +80,9 @@ def test_cascade_layers_equal_textbook_llama_layer(feo, ctx):
             if ctx == "cascade":
                 seq = np.concatenate([Y, xs[b, :i]]) if P else xs[b, :i]
                 pos = np.arange(P + i)
-            else:
-                seq = np.concatenate([Y, xs[b, i - 1:i]]) if P else xs[b, i - 1:i]
+            else:   # self: the layer's own input; parallel: x_0 for every layer
+                src = i - 1 if ctx == "self" else 0
+                seq = np.concatenate([Y, xs[b, src:src + 1]]) if P else xs[b, src:src + 1]
                 pos = np.arange(P + 1)
             ref, _, _ = hf_ref.run_sequence(cfg, layer, seq, pos)
             err = np.abs(ref[-1] - xs[b, i]).max() / np.abs(ref[-1]).max()
@@ -95,8 +96,41 @@ def test_cascade_and_self_agree_on_first_layer(feo):
     inp = make_inputs(cfg, seed=1)
     a = feo.draft_forward(cfg, w, inp)["hidden"]
     b = feo.draft_forward(cfg.with_(cascade_ctx="self"), w, inp)["hidden"]
+    c = feo.draft_forward(cfg.with_(cascade_ctx="parallel"), w, inp)["hidden"]
     np.testing.assert_array_equal(a[:, :2], b[:, :2])
+    np.testing.assert_array_equal(a[:, :2], c[:, :2])
     assert np.abs(a[:, 2] - b[:, 2]).max() > 1e-6   # deeper layers do differ
+    assert np.abs(b[:, 2] - c[:, 2]).max() > 1e-6
+
+
+def test_parallel_heads_are_independent(feo):
+    """Parallel heads (the ablation without the cascade): head i sees x_0, its
+    own weights and its own prefix cache only, so reordering the layers (with
+    their caches) reorders the outputs, and a one-layer drafter holding layer i
+    gives head i."""
+    cfg = PIN.with_(cascade_ctx="parallel")
+    w = _w(cfg)
+    inp = make_inputs(cfg, seed=2)
+    out = feo.draft_forward(cfg, w, inp)
+    xs, z = out["hidden"], out["logits"]
+    perm = [2, 0, 1]
+    w2 = _w(cfg)
+    w2.layers = [w.layers[p] for p in perm]
+    inp2 = make_inputs(cfg, seed=2)   # each layer keeps its own prefix cache
+    inp2.kcache = [inp.kcache[p] for p in perm]
+    inp2.vcache = [inp.vcache[p] for p in perm]
+    xs2 = feo.draft_forward(cfg, w2, inp2)["hidden"]
+    np.testing.assert_array_equal(xs2[:, 0], xs[:, 0])
+    for i, p in enumerate(perm):
+        np.testing.assert_array_equal(xs2[:, 1 + i], xs[:, 1 + p])
+    for li in range(cfg.n_layers):
+        w1 = _w(cfg)
+        w1.layers = [w.layers[li]]
+        inp1 = make_inputs(cfg.with_(n_layers=1), 2)
+        inp1.kcache, inp1.vcache = [inp.kcache[li]], [inp.vcache[li]]
+        one = feo.draft_forward(cfg.with_(n_layers=1), w1, inp1)
+        np.testing.assert_array_equal(one["hidden"][:, 1], xs[:, 1 + li])
+        np.testing.assert_array_equal(one["logits"][:, 0], z[:, li])
 
 
 def _eye_block(d, nblk, which):
