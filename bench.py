@@ -377,6 +377,33 @@ def main():
                                           / MFMA_PEAK_TFS[cfg.dtype])},
     }
     dr.close()
+    # NEXT-4, the ablation without the cascade: every layer reads x_0 (same
+    # weights, same bytes), timed like the primary pass
+    if cfg.cascade_ctx == "cascade":
+        pcfg = cfg.with_(cascade_ctx="parallel")
+        pdr = Drafter(pcfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()),
+                      graph=not args.eager)
+        pdi = pdr.upload_inputs(inp)
+        pout = pdr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
+        ptree = pdr.alloc_tree(cfg.batch, cfg.topk)
+        for _ in range(max(3, args.warmup // 4)):
+            pdr.forward(pdi, out=pout, tree=ptree)
+        torch.cuda.synchronize()
+        psteps = max(10, args.steps // 2)
+        ev0.record(stream)
+        for _ in range(psteps):
+            pdr.forward(pdi, out=pout, tree=ptree)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        pms = ev0.elapsed_time(ev1) / psteps
+        pdr.close()
+        log(f"parallel heads: {pms * 1000:.1f} us/pass")
+        res["next_parallel_heads"] = {
+            "workload": cfg.name, "cascade_ctx": "parallel", "steps": psteps,
+            "us_per_pass": pms * 1000.0, "drafts_per_s": B * 1000.0 / pms,
+            "bytes_per_pass": pass_bytes(pcfg, plens),
+            "hbm_frac": pass_bytes(pcfg, plens) / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "vs_cascade": ms / pms}
     if args.second and args.second != cfg.name:
         res["second_workload"] = time_second(args.second, args.seed, max(10, args.steps // 4),
                                              max(3, args.warmup // 4))

@@ -55,8 +55,11 @@ typedef enum { FE_F32 = 0, FE_BF16 = 1 } fe_dtype;
  * architecture figure is not available; Eq. 2 and Section 2.1 are read as):
  *  FE_CTX_CASCADE: the query is x_{i-1} at position P+i-1; keys/values are
  *    layer i's own projections of x_0..x_{i-1} at positions P..P+i-1;
- *  FE_CTX_SELF: query, key and value come from x_{i-1} alone, at position P. */
-typedef enum { FE_CTX_CASCADE = 0, FE_CTX_SELF = 1 } fe_cascade_ctx;
+ *  FE_CTX_SELF: query, key and value come from x_{i-1} alone, at position P.
+ * FE_CTX_PARALLEL is the ablation without the cascade (Section 3.2, Table 2,
+ * "parallel instead of serial"): every layer reads x_0, x_i = L_i(x_0), with
+ * query, key and value from x_0 at position P and x_0 as the residual. */
+typedef enum { FE_CTX_CASCADE = 0, FE_CTX_SELF = 1, FE_CTX_PARALLEL = 2 } fe_cascade_ctx;
 
 typedef struct {
   int32_t hidden;        /* d */
@@ -209,7 +212,8 @@ typedef struct {
 size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chunk_rows);
 
 /* Drafter cache update after verification (Section 2.4's update step; the
- * rows are read under FE_CTX_CASCADE, the only context it accepts).  Row m is
+ * rows are read under FE_CTX_CASCADE, and FE_CTX_PARALLEL keys the same rows;
+ * FE_CTX_SELF is not accepted).  Row m is
  * a verified position: the target's features there, features[m] (n_feat_levels
  * * d, as for fe_draft_forward), and the token after it, tokens[m].  With
  * x_0(m) = FC(concat(FC(features[m]), e_{tokens[m]})) (Eq. 1), every layer i

@@ -113,7 +113,8 @@ fe_status check_config(const fe_config *c) {
       c->n_feat_levels <= 0 || c->max_batch <= 0 || c->max_topk <= 0 || c->max_prefix < 0)
     return fail(FE_E_INVALID, "config has a non-positive size");
   if (c->dtype != FE_F32 && c->dtype != FE_BF16) return fail(FE_E_INVALID, "unknown dtype %d", c->dtype);
-  if (c->cascade_ctx != FE_CTX_CASCADE && c->cascade_ctx != FE_CTX_SELF)
+  if (c->cascade_ctx != FE_CTX_CASCADE && c->cascade_ctx != FE_CTX_SELF &&
+      c->cascade_ctx != FE_CTX_PARALLEL)
     return fail(FE_E_INVALID, "unknown cascade_ctx %d", c->cascade_ctx);
   if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(FE_E_INVALID, "bad rope_theta or rms_eps");
   if (c->n_q_heads % c->n_kv_heads) return fail(FE_E_INVALID, "n_q_heads must be a multiple of n_kv_heads");
@@ -286,6 +287,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   // Fused RMSNorm (up to 16 rows per GEMM): every producer of a residual row
   // also writes gamma * row for the later GEMMs that normalise it.
   const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
+  const bool parallel = c.cascade_ctx == FE_CTX_PARALLEL;  // every layer reads x_0
   char *AQ = ws + L.AQ, *AM = ws + L.AM, *AF = ws + L.AF;
   const size_t aq_layer = (size_t)c.max_batch * N * d * esz;  // bytes per layer block of AQ
   auto nctx_of = [&](int l) { return cascade ? l : 1; };
@@ -295,7 +297,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   auto x_copies = [&](int j) {
     GainCopies gc{};
     for (int l = j + 1; l <= N; ++l) {
-      if (!(cascade || l == j + 1) || !fuse_q(l)) continue;
+      const bool uses = cascade ? j < l : parallel ? j == 0 : j == l - 1;  // layer l reads x_j
+      if (!uses || !fuse_q(l)) continue;
       gc.gamma[gc.n] = h->layers[l - 1].attn_norm;
       gc.dst[gc.n] = AQ + (size_t)(l - 1) * aq_layer + (size_t)j * d * esz;
       gc.ld[gc.n] = (long)N * d;
@@ -315,7 +318,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
 
   for (int i = 1; i <= N; ++i) {
     const fe_layer_weights &lw = h->layers[i - 1];
-    const int nctx = nctx_of(i), j0 = cascade ? 0 : i - 1;
+    const int src = parallel ? 0 : i - 1;  // the layer's input state
+    const int nctx = nctx_of(i), j0 = cascade ? 0 : src;
     // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
     // separate pass otherwise
     QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
@@ -341,7 +345,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
       gc_p.ld[0] = d;
     }
     FE_STAGE_RUN(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
-                                        X + (size_t)(i - 1) * d, xrow, ssqP, 1, 0, &gc_p, s, &ss));
+                                        X + (size_t)src * d, xrow, ssqP, 1, 0, &gc_p, s, &ss));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
     if (fuse_m) {
       const NormA na2{ssqP, ntile, 1, 0, 1, d, c.rms_eps};
@@ -530,8 +534,8 @@ extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *fea
                                   void *workspace, size_t ws_bytes, void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
-  if (c.cascade_ctx != FE_CTX_CASCADE)
-    return fail(FE_E_UNSUPPORTED, "the cache update is defined for the cascade context only");
+  if (c.cascade_ctx == FE_CTX_SELF)
+    return fail(FE_E_UNSUPPORTED, "the cache update is not defined for FE_CTX_SELF");
   if (n_rows < 0) return fail(FE_E_INVALID, "n_rows %d is negative", n_rows);
   if (!cache || !cache->k || !cache->v) return fail(FE_E_INVALID, "cache and its pointer arrays are required");
   if (cache->rows < 0) return fail(FE_E_INVALID, "cache->rows is negative");

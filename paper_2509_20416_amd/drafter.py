@@ -70,7 +70,8 @@ class Drafter:
             int(max_prefix if max_prefix is not None else lo_hi[1]),
             float(cfg.rope_theta), float(cfg.rms_eps),
             fe.FE_BF16 if dt == "bf16" else fe.FE_F32,
-            fe.FE_CTX_CASCADE if cfg.cascade_ctx == "cascade" else fe.FE_CTX_SELF)
+            {"cascade": fe.FE_CTX_CASCADE, "self": fe.FE_CTX_SELF,
+             "parallel": fe.FE_CTX_PARALLEL}[cfg.cascade_ctx])
         self.ws_bytes = fe.fe_workspace_bytes(self.ccfg)
         if self.ws_bytes == 0:
             raise fe.FeError(fe.FE_E_UNSUPPORTED, fe.fe_last_error())

@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(HERE, "libfe.so")
 
 FE_OK, FE_E_INVALID, FE_E_UNSUPPORTED, FE_E_ALIGN, FE_E_WORKSPACE, FE_E_HIP = range(6)
 FE_F32, FE_BF16 = 0, 1
-FE_CTX_CASCADE, FE_CTX_SELF = 0, 1
+FE_CTX_CASCADE, FE_CTX_SELF, FE_CTX_PARALLEL = 0, 1, 2
 STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_ALIGN",
                 4: "FE_E_WORKSPACE", 5: "FE_E_HIP"}
 

@@ -113,7 +113,7 @@ def test_accept_greedy_bit_exact(N, k, B):
 SMALL = [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128, C.TINY_F32_B1]
 
 
-@pytest.mark.parametrize("ctx", ["cascade", "self"])
+@pytest.mark.parametrize("ctx", ["cascade", "self", "parallel"])
 @pytest.mark.parametrize("cfg", SMALL, ids=lambda c: c.name)
 def test_small_parity(cfg, ctx):
     cfg = cfg.with_(cascade_ctx=ctx)
@@ -145,7 +145,10 @@ def test_attention_split_parity(cfg, split):
                                  # 36 rows through every GEMM; the down projection's K = 1376
                                  # ends in a ragged 128-byte chunk
                                  C.SMALL_GQA_BF16.with_(batch=36, prefix=(0, 300),
-                                                        name="small_gqa_bf16_b36")],
+                                                        name="small_gqa_bf16_b36"),
+                                 # parallel heads over 12 x 3 rows (normalisation unfused)
+                                 C.SMALL_GQA_BF16.with_(batch=12, cascade_ctx="parallel",
+                                                        name="small_gqa_bf16_b12_parallel")],
                          ids=lambda c: c.name)
 def test_batched_rows_parity(cfg):
     _run(cfg, seed=5)
@@ -259,6 +262,12 @@ def test_invalid_token_poisons_only_its_sequence():
 @pytest.mark.timeout(900)
 def test_llama8b_b1_full():
     _run(C.LLAMA8B_BF16_B1, seed=0, graph=True)
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_b1_parallel_heads_full():
+    """The ablation without the cascade, at the 8B shapes the bench times it on."""
+    _run(C.LLAMA8B_BF16_B1.with_(cascade_ctx="parallel"), seed=0, graph=True)
 
 
 @pytest.mark.timeout(900)
