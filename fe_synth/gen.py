@@ -213,3 +213,12 @@ def make_update_rows(cfg: DrafterConfig, accepted: np.ndarray, prefix_lens: np.n
     toks = int_rng("update.tokens", seed).integers(0, cfg.target_vocab, size=M).astype(np.int32)
     return UpdateRows(features=feats, tokens=toks, positions=pos, dst_rows=dst,
                       cache_rows=int(len(accepted) * capacity))
+
+
+def make_uniforms(shape, seed: int = 0, name: str = "uniforms") -> np.ndarray:
+    """float32 uniforms in the open interval (0, 1): (j + 0.5) / 2^23 for a
+    23-bit integer j drawn uniformly, exact in float32 (the noise of
+    stochastic drafting; the extremes are 2^-24 and 1 - 2^-24)."""
+    rng = int_rng(name, seed)
+    j = rng.integers(0, 1 << 23, size=tuple(int(s) for s in shape), dtype=np.int64)
+    return ((j.astype(np.float64) + 0.5) / float(1 << 23)).astype(np.float32)

@@ -243,7 +243,21 @@ int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
                       const void *const *kcache, const void *const *vcache,
                       const int32_t *prefix_lens, int32_t topk, double *hidden, double *logits,
                       int32_t *topk_draft, int32_t *topk_ids, double *topk_probs) {
+  return feo_draft_sample(c, w, batch, features, next_tok, kcache, vcache, prefix_lens, topk, 1.0,
+                          NULL, hidden, logits, topk_draft, topk_ids, topk_probs);
+}
+
+/* -log(-log(u)): a standard Gumbel variate from a uniform u in (0, 1). */
+static double gumbel(float u) { return -log(-log((double)u)); }
+
+int feo_draft_sample(const feo_config *c, const feo_weights *w, int32_t batch,
+                     const void *features, const int32_t *next_tok,
+                     const void *const *kcache, const void *const *vcache,
+                     const int32_t *prefix_lens, int32_t topk, double temperature,
+                     const float *uniforms, double *hidden, double *logits, int32_t *topk_draft,
+                     int32_t *topk_ids, double *topk_probs) {
   if (!c || !w || batch < 0 || topk < 1 || topk > c->draft_vocab || c->n_layers < 1) return -1;
+  if (!(temperature > 0.0)) return -1;
   if (c->cascade_ctx < FEO_CTX_CASCADE || c->cascade_ctx > FEO_CTX_PARALLEL) return -1;
   if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0) return -1;
   const int32_t d = c->hidden, N = c->n_layers, V = c->draft_vocab, F = c->n_feat_levels;
@@ -267,18 +281,26 @@ int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
       cascade_layer(c, &w->layers[i - 1], i, xs, kcache[i - 1], vcache[i - 1], prefix_off, P);
     if (hidden) memcpy(hidden + (size_t)b * (N + 1) * d, xs, sizeof(double) * (size_t)(N + 1) * d);
 
-    /* q_{t+i} = softmax(LMHead(RMSNorm(h_i))) and its k most probable tokens */
+    /* q_{t+i} = softmax(LMHead(RMSNorm(h_i)) / T) and its k candidates
+     * (Section 2.2): the k most probable tokens (uniforms == NULL), or k
+     * tokens sampled without replacement from q_{t+i} (the Gumbel-top-k
+     * construction: the k largest z/T + Gumbel noise), listed most probable
+     * first so that the backbone takes the most probable sampled token. */
     for (int32_t i = 1; i <= N; ++i) {
       feo_rmsnorm(xs + (size_t)i * d, w->final_norm, c->dtype, d, c->rms_eps, hn);
       matvec(w->lm_head, c->dtype, V, d, hn, z);
       const size_t row = (size_t)b * N + (size_t)(i - 1);
       if (logits) memcpy(logits + row * V, z, sizeof(double) * (size_t)V);
+      for (int32_t v = 0; v < V; ++v) z[v] /= temperature;
       double mx = -INFINITY;
       for (int32_t v = 0; v < V; ++v) mx = z[v] > mx ? z[v] : mx;
       double den = 0.0;
       for (int32_t v = 0; v < V; ++v) den += exp(z[v] - mx);
-      for (int32_t v = 0; v < V; ++v) { ord[v].z = z[v]; ord[v].id = v; }
+      const float *u = uniforms ? uniforms + row * (size_t)V : NULL;
+      for (int32_t v = 0; v < V; ++v) { ord[v].z = u ? z[v] + gumbel(u[v]) : z[v]; ord[v].id = v; }
       qsort(ord, (size_t)V, sizeof(scored), by_logit_desc);
+      for (int32_t r = 0; r < topk; ++r) { ord[r].z = z[ord[r].id]; }
+      qsort(ord, (size_t)topk, sizeof(scored), by_logit_desc);
       for (int32_t r = 0; r < topk; ++r) {
         const int32_t id = ord[r].id;
         if (topk_draft) topk_draft[row * topk + r] = id;

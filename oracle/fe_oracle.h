@@ -79,6 +79,25 @@ int feo_draft_forward(const feo_config *cfg, const feo_weights *w, int32_t batch
                       int32_t *topk_draft, int32_t *topk_ids, double *topk_probs);
 
 /*
+ * The drafting pass at temperature T with stochastic candidates (Section 2.2
+ * samples k candidates per level; Section 3 reports temperature 1):
+ * q_{t+i} = softmax(z_i / T).  With uniforms == NULL the candidates are the k
+ * most probable tokens (feo_draft_forward is this call with T = 1).  With
+ * uniforms [B, N, V] (fp32 in (0, 1), one per draft-vocabulary entry) the k
+ * candidates are drawn without replacement from q_{t+i}: the k largest
+ * z_v / T - log(-log(u_v)) (ties to the lower id).  Either way they are
+ * listed most probable first (larger z, then lower id) and topk_probs holds
+ * q_{t+i} of each.  logits are the raw z.  Returns 0, or -1 on invalid
+ * arguments (also T <= 0).
+ */
+int feo_draft_sample(const feo_config *cfg, const feo_weights *w, int32_t batch,
+                     const void *features, const int32_t *next_tok,
+                     const void *const *kcache, const void *const *vcache,
+                     const int32_t *prefix_lens, int32_t topk, double temperature,
+                     const float *uniforms, double *hidden, double *logits, int32_t *topk_draft,
+                     int32_t *topk_ids, double *topk_probs);
+
+/*
  * Backbone Expansion tree for `batch` sequences, T = 1 + N*k nodes each.
  *  root_tokens [B], topk_ids [B, N, k] (rank order), prefix_lens [B]
  * Outputs: tokens/parents/depth/positions [B, T] int32, mask [B, T, T] uint8

@@ -42,6 +42,7 @@ def lib():
             _build.build()
         L = C.CDLL(_build.LIB)
         L.feo_draft_forward.restype = C.c_int
+        L.feo_draft_sample.restype = C.c_int
         L.feo_build_tree.restype = C.c_int
         L.feo_accept_greedy.restype = C.c_int
         L.feo_kv_update.restype = C.c_int
@@ -119,9 +120,12 @@ def _weights(w, N):
 
 
 def draft_forward(cfg, w, inp, topk: Optional[int] = None, want_logits: bool = True,
-                  batch_index: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+                  batch_index: Optional[Sequence[int]] = None, temperature: float = 1.0,
+                  uniforms: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
     """Run the oracle pass.  `batch_index` restricts it to some sequences of the
-    batch (sequences are independent), keeping the given order."""
+    batch (sequences are independent), keeping the given order.  With
+    `uniforms` [B, N, V] (float32 in (0, 1)) the candidates are sampled at
+    `temperature` (see feo_draft_sample in fe_oracle.h)."""
     k = cfg.topk if topk is None else int(topk)
     B_all = len(inp.prefix_lens)
     idx = list(range(B_all)) if batch_index is None else [int(i) for i in batch_index]
@@ -146,10 +150,15 @@ def draft_forward(cfg, w, inp, topk: Optional[int] = None, want_logits: bool = T
     tids = np.zeros((B, N, k), dtype=np.int32)
     tprob = np.zeros((B, N, k), dtype=np.float64)
     cfgc = make_config(cfg)
-    rc = lib().feo_draft_forward(C.byref(cfgc), C.byref(W), C.c_int32(B), _p(feats), _pi(toks),
-                                 kp, vp, _pi(plens), C.c_int32(k), _pd(hidden),
-                                 _pd(logits) if logits is not None else None,
-                                 _pi(tdraft), _pi(tids), _pd(tprob))
+    u = None
+    if uniforms is not None:
+        u = np.ascontiguousarray(np.asarray(uniforms, dtype=np.float32)[idx])
+        assert u.shape == (B, N, V), u.shape
+    rc = lib().feo_draft_sample(C.byref(cfgc), C.byref(W), C.c_int32(B), _p(feats), _pi(toks),
+                                kp, vp, _pi(plens), C.c_int32(k), C.c_double(temperature),
+                                _p(u) if u is not None else None, _pd(hidden),
+                                _pd(logits) if logits is not None else None,
+                                _pi(tdraft), _pi(tids), _pd(tprob))
     if rc != 0:
         raise ValueError("oracle draft_forward rejected its arguments")
     out = dict(hidden=hidden, topk_draft=tdraft, topk_ids=tids, topk_probs=tprob)
