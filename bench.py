@@ -322,6 +322,21 @@ def main():
     torch.cuda.synchronize()
     accept_us = ev0.elapsed_time(ev1) * 1000.0 / 100
 
+    # NEXT-3, stochastic drafting at T = 1: the same pass with k candidates
+    # sampled without replacement (uniforms resident on the device), graph replays
+    from fe_synth import make_uniforms
+    ud = torch.from_numpy(make_uniforms((cfg.batch, cfg.n_layers, cfg.draft_vocab),
+                                        seed=args.seed + 1)).to(dr.device)
+    dr.forward(di, out=out, tree=tree, temperature=1.0, uniforms=ud)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dr.forward(di, out=out, tree=tree, temperature=1.0, uniforms=ud)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    sms = ev0.elapsed_time(ev1) / args.steps
+    log(f"sampled drafting: {sms * 1000:.1f} us/pass")
+
     # NEXT-1, the drafter cache update: one cycle's N+1 verified positions,
     # and a whole prefix of max_prefix positions (the prompt's cache, the
     # shape where the update becomes matrix-core bound)
@@ -367,6 +382,11 @@ def main():
         "next_accept_greedy": {"us_per_call": accept_us, "batch": B,
                                "accept_len_seq0": accept_len0, "issue": "eager, from Python"},
         "next_kv_update": {"cycle": upd_cycle, "prefill": upd_prefill},
+        "next_sampled_drafting": {"temperature": 1.0, "steps": args.steps,
+                                  "us_per_pass": sms * 1000.0,
+                                  "drafts_per_s": cfg.batch * 1000.0 / sms,
+                                  "uniform_bytes": cfg.batch * cfg.n_layers * cfg.draft_vocab * 4,
+                                  "vs_greedy": ms / sms},
         # matrix-core use over the whole pass, against the most that an
         # HBM-bound pass of this arithmetic intensity could reach
         "pass_mfma": {"flops_per_pass": pflops,

@@ -164,6 +164,28 @@ fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *features,
                            const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
                            const fe_draft_out *out, void *stream);
 
+/* fe_draft_forward at temperature T with stochastic candidates: Section 2.2
+ * samples k candidates per level from q_{t+i} (Section 3 evaluates at
+ * temperature 0 and 1).  Here q_{t+i} = softmax(z_i / T).  With uniforms ==
+ * NULL the candidates are the k most probable tokens (fe_draft_forward is
+ * this call with T = 1).  With uniforms, [B, N, V] fp32 values in the open
+ * interval (0, 1), one per draft-vocabulary entry of every LM-head row
+ * (b, i-1), the k candidates are drawn without replacement from q_{t+i}: the
+ * k largest z_v / T - log(-log(u_v)) (Gumbel-top-k; ties to the lower id).
+ * Either way topk_ids / topk_draft list them most probable first (larger
+ * z, then lower id), so the tree's backbone takes the most probable sampled
+ * token, and topk_probs holds q_{t+i} of each.  `logits` (if asked) are the
+ * raw z.  The caller draws the uniforms (e.g. a counter-based generator on
+ * the device); a u of 0 excludes its token, a u of 1 forces it in.
+ * Errors as fe_draft_forward, plus FE_E_INVALID for a temperature that is
+ * not positive and finite (or whose reciprocal overflows) and FE_E_ALIGN for
+ * uniforms not 4-byte aligned.  With graph replay on, the temperature and
+ * the uniforms pointer are part of the captured arguments. */
+fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *features,
+                          const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
+                          float temperature, const float *uniforms, const fe_draft_out *out,
+                          void *stream);
+
 /* Backbone Expansion tree (Section 2.2) of every sequence in one launch:
  * level 1 hangs the k candidates of q_{t+1} under the root; the most probable
  * extends the backbone, the other k-1 are side branches; every later level hangs

@@ -796,6 +796,14 @@ template <typename T> struct EpiLm {
   // scanned in increasing id order into a sorted list of KL (value, id)
   // pairs; an equal value never displaces an earlier entry, so ties go to the
   // lower id without comparing ids.  NaN compares false and is never taken.
+  // selection key of tempered logit xt at column col of row m: xt, or
+  // xt + Gumbel(u) = xt - log(-log(u)) for sampling without replacement
+  __device__ float sel_key(float xt, int m, int col) const {
+    if (!a.uniforms) return xt;
+    const float u = a.uniforms[(size_t)m * nvcols + col];
+    return xt - logf(-logf(u));
+  }
+
   template <int KL>
   __device__ void finish_rows(const float *tile, int ldt, int M, int c0, int span) const {
     const int m = threadIdx.x;
@@ -804,27 +812,30 @@ template <typename T> struct EpiLm {
     const int nwg = gridDim.x, tileid = blockIdx.x;
     const float *row = tile + m * ldt;
     float mx = -INFINITY;
-    for (int c = 0; c < nvalid; ++c) mx = fmaxf(mx, row[c]);
+    for (int c = 0; c < nvalid; ++c) mx = fmaxf(mx, row[c] * a.inv_temp);
     float se = 0.f;
-    float vs[KL];
+    float vs[KL], zs[KL];
     int is[KL];
 #pragma unroll
     for (int j = 0; j < KL; ++j) {
       vs[j] = -INFINITY;
+      zs[j] = -INFINITY;
       is[j] = 0x7fffffff;
     }
     for (int c = 0; c < nvalid; ++c) {
-      const float x = row[c];
-      se += expf(x - mx);
+      const float x = row[c], xt = x * a.inv_temp, key = sel_key(xt, m, c0 + c);
+      se += expf(xt - mx);
       if (a.logits) a.logits[(size_t)m * nvcols + c0 + c] = x;
 #pragma unroll
       for (int j = KL - 1; j >= 1; --j) {
-        const bool prev = vs[j - 1] < x, here = vs[j] < x;
-        vs[j] = prev ? vs[j - 1] : (here ? x : vs[j]);
+        const bool prev = vs[j - 1] < key, here = vs[j] < key;
+        vs[j] = prev ? vs[j - 1] : (here ? key : vs[j]);
+        zs[j] = prev ? zs[j - 1] : (here ? xt : zs[j]);
         is[j] = prev ? is[j - 1] : (here ? c0 + c : is[j]);
       }
-      if (vs[0] < x) {
-        vs[0] = x;
+      if (vs[0] < key) {
+        vs[0] = key;
+        zs[0] = xt;
         is[0] = c0 + c;
       }
     }
@@ -836,6 +847,7 @@ template <typename T> struct EpiLm {
       if (j < a.topk) {
         a.cand_val[pb * kMaxTopk + j] = is[j] != 0x7fffffff ? vs[j] : -INFINITY;
         a.cand_idx[pb * kMaxTopk + j] = is[j];
+        if (a.uniforms) a.cand_z[pb * kMaxTopk + j] = zs[j];
       }
   }
 
@@ -862,6 +874,8 @@ template <typename T> struct EpiLm {
         const bool ok = c < nvalid;
         v[p] = ok ? row[c] : -INFINITY;
         id[p] = ok ? c0 + c : 0x7fffffff;
+        if (a.logits && ok) a.logits[(size_t)m * nvcols + id[p]] = v[p];
+        v[p] *= a.inv_temp;   // statistics and candidates at temperature T
         mx = fmaxf(mx, v[p]);
       }
       mx = group_max<64>(mx);
@@ -869,11 +883,6 @@ template <typename T> struct EpiLm {
 #pragma unroll
       for (int p = 0; p < PER; ++p) se += (id[p] != 0x7fffffff) ? expf(v[p] - mx) : 0.f;
       se = group_sum<64>(se);
-      if (a.logits) {
-#pragma unroll
-        for (int p = 0; p < PER; ++p)
-          if (id[p] != 0x7fffffff) a.logits[(size_t)m * nvcols + id[p]] = v[p];
-      }
       const size_t pb = (size_t)m * nwg + tileid;
       if (lane == 0) {
         a.part_max[pb] = mx;
@@ -881,19 +890,26 @@ template <typename T> struct EpiLm {
       }
       uint64_t key[PER];
 #pragma unroll
-      for (int p = 0; p < PER; ++p) key[p] = id[p] != 0x7fffffff ? topk_key(v[p], id[p]) : kNoKey;
+      for (int p = 0; p < PER; ++p)
+        key[p] = id[p] != 0x7fffffff ? topk_key(sel_key(v[p], m, id[p]), id[p]) : kNoKey;
       for (int r = 0; r < a.topk; ++r) {
         // lane-local best, then wave max of the ordering keys (lower id wins ties)
         uint64_t best = kNoKey;
 #pragma unroll
         for (int p = 0; p < PER; ++p) best = key[p] > best ? key[p] : best;
         best = wave_max_u64(best);
+        float zb = -INFINITY;  // z / T of the winner, from the lane that holds it
 #pragma unroll
-        for (int p = 0; p < PER; ++p) key[p] = key[p] == best ? kNoKey : key[p];
+        for (int p = 0; p < PER; ++p) {
+          zb = key[p] == best ? v[p] : zb;
+          key[p] = key[p] == best ? kNoKey : key[p];
+        }
+        if (a.uniforms) zb = group_max<64>(zb);
         if (lane == 0) {
           const bool got = best != kNoKey;
           a.cand_val[pb * kMaxTopk + r] = got ? topk_key_value(best) : -INFINITY;
           a.cand_idx[pb * kMaxTopk + r] = got ? topk_key_id(best) : 0x7fffffff;
+          if (a.uniforms) a.cand_z[pb * kMaxTopk + r] = got ? zb : -INFINITY;
         }
       }
     }

@@ -258,10 +258,13 @@ struct LmArgs {
   const void *w;             // [V, d]
   int V;
   int topk;
-  float *logits;             // optional [M, V]
-  float *part_max, *part_sum;// [M, nwg]
-  float *cand_val;           // [M, nwg, kMaxTopk]
+  float *logits;             // optional [M, V] (raw logits z)
+  float *part_max, *part_sum;// [M, nwg] statistics of z / T
+  float *cand_val;           // [M, nwg, kMaxTopk] selection keys
   int32_t *cand_idx;         // [M, nwg, kMaxTopk]
+  float inv_temp;            // 1 / T
+  const float *uniforms;     // optional [M, V] in (0, 1): key = z/T + Gumbel(u), else z/T
+  float *cand_z;             // [M, nwg, kMaxTopk] z / T of each candidate (with uniforms)
 };
 // LM head tiles with per-tile max, sum of exponentials and top-k candidates.
 // Returns the number of column tiles (nwg) through *nwg_out.
@@ -305,10 +308,12 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
                          const int32_t *target_next, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s);
 
-// Global top-k of every row from the tile candidates; softmax statistics merge.
+// Global top-k of every row from the tile candidates (by key); softmax
+// statistics merge.  With cand_z (sampled candidates) the k winners are
+// listed by z / T (larger first, lower id on ties), else in key order.
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
-                      const int32_t *cand_idx, int rows, int nwg, int topk, int V,
-                      const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
+                      const int32_t *cand_idx, const float *cand_z, int rows, int nwg, int topk,
+                      int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
                       hipStream_t s);
 
 // Backbone Expansion tree of every sequence; P_b from prefix_lens, or from

@@ -87,13 +87,15 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
                                                     const float *__restrict__ psum,
                                                     const float *__restrict__ cval,
-                                                    const int32_t *__restrict__ cidx, int nwg,
+                                                    const int32_t *__restrict__ cidx,
+                                                    const float *__restrict__ cz, int nwg,
                                                     int topk, int V, const int32_t *__restrict__ d2t,
                                                     int32_t *ids, int32_t *draft_ids,
                                                     float *probs) {
   constexpr int CAP = kMergeMaxCand / 256;
   __shared__ float sv[4];
   __shared__ uint64_t s_key[4][kMaxTopk];
+  __shared__ float s_z[4][kMaxTopk];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *pm = pmax + (size_t)row * nwg;
   const float *ps = psum + (size_t)row * nwg;
@@ -140,44 +142,83 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
   for (int t = tid + 256 * kStatLoads; t < nwg; t += 256) S += ps[t] * expf(pm[t] - mu);
   S = group_sum<64>(S);
   if (lane == 0) sv[wave] = S;
+  // sampled candidates: their z / T, loaded beside the keys
+  float czv[CAP];
+  if (cz) {
+#pragma unroll
+    for (int j = 0; j < CAP; ++j) {
+      const int c = min(tid + 256 * j, ncand - 1);
+      czv[j] = cz[((size_t)row * nwg + c / topk) * kMaxTopk + c % topk];
+    }
+  }
   // per-wave top-k
   for (int r = 0; r < topk; ++r) {
     uint64_t best = kNoKey;
 #pragma unroll
     for (int j = 0; j < CAP; ++j) best = key[j] > best ? key[j] : best;
     best = wave_max_u64(best);
+    float zb = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < CAP; ++j) key[j] = key[j] == best ? kNoKey : key[j];
-    if (lane == 0) s_key[wave][r] = best;
+    for (int j = 0; j < CAP; ++j) {
+      if (cz && key[j] == best && best != kNoKey) zb = czv[j];
+      key[j] = key[j] == best ? kNoKey : key[j];
+    }
+    if (cz) zb = group_max<64>(zb);  // one lane held the winner
+    if (lane == 0) {
+      s_key[wave][r] = best;
+      s_z[wave][r] = zb;
+    }
   }
   __syncthreads();
   if (wave == 0) {
     const float Ssum = (sv[0] + sv[1]) + (sv[2] + sv[3]);
     uint64_t k = lane < 4 * topk ? s_key[lane / topk][lane % topk] : kNoKey;
+    const float kz = lane < 4 * topk ? s_z[lane / topk][lane % topk] : -INFINITY;
     uint64_t mine = kNoKey;
+    float mz = -INFINITY;
     for (int r = 0; r < topk; ++r) {
       const uint64_t best = wave_max_u64(k);
+      // the lane holding the winner (keys are distinct) gives its z / T
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(k == best && best != kNoKey);
+      const float bz = hit ? __shfl(kz, __builtin_ctzll(hit)) : -INFINITY;
       k = k == best ? kNoKey : k;
-      if (lane == r) mine = best;
+      if (lane == r) {
+        mine = best;
+        mz = bz;
+      }
+    }
+    const int i = topk_key_id(mine);
+    const bool valid = lane < topk && mine != kNoKey && i >= 0 && i < V;  // none left (NaN row): -1
+    const float z = cz ? mz : topk_key_value(mine);
+    // listing position: key order, or for sampled candidates the order of z / T
+    // (larger first, lower id on ties, NaN after numbers, invalid entries last
+    // in lane order): the rank of the lane's ordering key among the winners
+    int pos = lane;
+    if (cz) {
+      const uint64_t zk = valid ? topk_key(z, i) : kNoKey;
+      pos = 0;
+      for (int t = 0; t < topk; ++t) {
+        const uint64_t kt = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(zk >> 32), t) << 32) |
+                            (uint32_t)__shfl((int)(uint32_t)zk, t);
+        pos += (kt > zk || (kt == zk && t < lane)) ? 1 : 0;
+      }
     }
     if (lane < topk) {
-      const size_t o = (size_t)row * topk + lane;
-      const int i = topk_key_id(mine);
-      const bool valid = mine != kNoKey && i >= 0 && i < V;  // none left (NaN row): -1
+      const size_t o = (size_t)row * topk + pos;
       ids[o] = valid ? (d2t ? d2t[i] : i) : -1;
       if (draft_ids) draft_ids[o] = valid ? i : -1;
-      probs[o] = valid ? expf(topk_key_value(mine) - mu) / Ssum : __int_as_float(0x7fc00000);
+      probs[o] = valid ? expf(z - mu) / Ssum : __int_as_float(0x7fc00000);
     }
   }
 }
 
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
-                      const int32_t *cand_idx, int rows, int nwg, int topk, int V,
-                      const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
+                      const int32_t *cand_idx, const float *cand_z, int rows, int nwg, int topk,
+                      int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
                       hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, s, part_max, part_sum, cand_val,
-                     cand_idx, nwg, topk, V, d2t, ids, draft_ids, probs);
+                     cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
   return hipGetLastError();
 }
 

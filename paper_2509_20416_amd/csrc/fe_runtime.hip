@@ -32,7 +32,7 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
-      psum, cval, cidx, splitk, total;
+      psum, cval, cidx, cz, splitk, total;
   size_t splitk_floats;
   int nchmax, nwg, npos;
 };
@@ -71,6 +71,7 @@ Layout layout_of(const fe_config &c) {
   L.psum = take(B * N * (size_t)L.nwg * 4);
   L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
+  L.cz = take(B * N * (size_t)L.nwg * kMaxTopk * 4);  // z / T of sampled candidates
   // split-K slices of the batched GEMMs with narrow outputs: up to 8 slices of
   // the QKV rows (B * N at most, 256 per launch) over 128-column tiles
   {
@@ -155,6 +156,8 @@ struct fe_drafter {
   // arguments of the most recent fe_draft_forward, for fe_time_stage
   bool have_last = false;
   int last_batch = 0, last_topk = 0;
+  float last_inv_temp = 1.f;
+  const float *last_uniforms = nullptr;
   const void *last_features = nullptr;
   const int32_t *last_tokens = nullptr;
   std::vector<const void *> last_k, last_v;
@@ -258,8 +261,8 @@ namespace {
 
 // The whole pass: FCs of Eq. 1, N cascade layers (Eq. 2), LM head + top-k.
 fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int32_t *next_tokens,
-                          const fe_kv_view *kv, int topk, const fe_draft_out *out,
-                          hipStream_t s, int only_stage = -1) {
+                          const fe_kv_view *kv, int topk, float inv_temp, const float *uniforms,
+                          const fe_draft_out *out, hipStream_t s, int only_stage = -1) {
   const fe_config &c = h->cfg;
   const Layout &L = h->L;
   const int dt = c.dtype == FE_BF16 ? 1 : 0;
@@ -365,12 +368,14 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const NormA naf{ssqX, ntile, N, 1, N + 1, d, c.rms_eps};
   if (!fuse_f) FE_OTHER(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
   LmArgs la{h->w.lm_head, c.draft_vocab, topk, out->logits, (float *)(ws + L.pmax),
-            (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx)};
+            (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx), inv_temp,
+            uniforms, (float *)(ws + L.cz)};
   int nwg = 0;
   FE_STAGE_RUN(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
                                         d, la, fuse_f ? &naf : nullptr, &nwg, s));
-  FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx, B * N, nwg, topk,
-                    c.draft_vocab, h->w.d2t, out->topk_ids, out->topk_draft, out->topk_probs, s));
+  FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx,
+                      uniforms ? la.cand_z : nullptr, B * N, nwg, topk, c.draft_vocab, h->w.d2t,
+                      out->topk_ids, out->topk_draft, out->topk_probs, s));
   if (out->hidden)
     FE_OTHER(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
                             hipMemcpyDeviceToDevice, s));
@@ -387,8 +392,20 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
 extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *features,
                                       const int32_t *next_tokens, const fe_kv_view *kv,
                                       int32_t topk, const fe_draft_out *out, void *stream) {
+  return fe_draft_sample(h, batch, features, next_tokens, kv, topk, 1.0f, nullptr, out, stream);
+}
+
+extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *features,
+                                     const int32_t *next_tokens, const fe_kv_view *kv,
+                                     int32_t topk, float temperature, const float *uniforms,
+                                     const fe_draft_out *out, void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
+  if (!(temperature > 0.f) || !(temperature < INFINITY))
+    return fail(FE_E_INVALID, "temperature must be positive and finite");
+  const float inv_temp = 1.0f / temperature;
+  if (!(inv_temp < INFINITY)) return fail(FE_E_INVALID, "temperature %g is too small", temperature);
+  if (uniforms && ((uintptr_t)uniforms & 3u)) return fail(FE_E_ALIGN, "uniforms must be 4-byte aligned");
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
   if (topk < 1 || topk > c.max_topk || topk > c.draft_vocab)
     return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
@@ -421,6 +438,8 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   h->have_last = true;
   h->last_batch = batch;
   h->last_topk = topk;
+  h->last_inv_temp = inv_temp;
+  h->last_uniforms = uniforms;
   h->last_features = features;
   h->last_tokens = next_tokens;
   h->last_k.assign(kv->k, kv->k + c.n_layers);
@@ -434,7 +453,8 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
     h->last_out.tree = &h->last_tree;
   }
 
-  if (!h->graph_mode) return enqueue_forward(h, batch, features, next_tokens, kv, topk, out, s);
+  if (!h->graph_mode)
+    return enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms, out, s);
 
   std::vector<uintptr_t> key = {(uintptr_t)batch, (uintptr_t)features, (uintptr_t)next_tokens,
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
@@ -447,7 +467,8 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
                                 (uintptr_t)(out->tree ? out->tree->mask : nullptr),
                                 (uintptr_t)(out->tree ? out->tree->retrieve : nullptr),
                                 (uintptr_t)out->logits, (uintptr_t)out->hidden,
-                                (uintptr_t)h->attn_split};
+                                (uintptr_t)h->attn_split, (uintptr_t)__builtin_bit_cast(uint32_t, inv_temp),
+                                (uintptr_t)uniforms};
   for (int l = 0; l < c.n_layers; ++l) {
     key.push_back((uintptr_t)kv->k[l]);
     key.push_back((uintptr_t)kv->v[l]);
@@ -458,7 +479,8 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
     if (h->graph) { (void)hipGraphDestroy(h->graph); h->graph = nullptr; }
     h->key.clear();
     FE_TRY(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
-    fe_status st = enqueue_forward(h, batch, features, next_tokens, kv, topk, out, h->cap_stream);
+    fe_status st = enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms,
+                                   out, h->cap_stream);
     hipGraph_t g = nullptr;
     hipError_t ec = hipStreamEndCapture(h->cap_stream, &g);
     if (st != FE_OK) { if (g) (void)hipGraphDestroy(g); return st; }
@@ -485,7 +507,8 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
   FE_TRY(hipEventRecord(h->ev_a, s));
   for (int r = 0; r < repeats; ++r) {
     const fe_status st = enqueue_forward(h, h->last_batch, h->last_features, h->last_tokens,
-                                         &h->last_kv, h->last_topk, &h->last_out, s, stage);
+                                         &h->last_kv, h->last_topk, h->last_inv_temp,
+                                         h->last_uniforms, &h->last_out, s, stage);
     if (st != FE_OK) return st;
   }
   FE_TRY(hipEventRecord(h->ev_b, s));

@@ -128,9 +128,12 @@ class Drafter:
 
     def forward(self, di: DeviceInputs, topk: Optional[int] = None, logits=False, hidden=False,
                 out: Optional[Dict[str, object]] = None,
-                tree: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+                tree: Optional[Dict[str, object]] = None, temperature: Optional[float] = None,
+                uniforms=None) -> Dict[str, object]:
         """One drafting pass; with `tree` (from alloc_tree) the Backbone Expansion
-        tree of the pass is built in the same launch sequence."""
+        tree of the pass is built in the same launch sequence.  With a
+        temperature and/or `uniforms` ([B, N, V] float32 on the device) the pass
+        runs through fe_draft_sample (candidates sampled without replacement)."""
         k = int(topk or self.cfg.topk)
         if out is None:
             out = self.alloc_outputs(di.batch, k, logits, hidden)
@@ -142,9 +145,16 @@ class Drafter:
                                               ("tokens", "parents", "depth", "positions", "mask",
                                                "retrieve")])
             self._out.tree = fe.C.pointer(self._fwd_tree)
-        fe.fe_draft_forward(self.handle, di.batch, di.features.data_ptr(),
-                            di.next_tokens.data_ptr(), self.kv_view(di), k, self._out,
-                            self.stream())
+        if temperature is None and uniforms is None:
+            fe.fe_draft_forward(self.handle, di.batch, di.features.data_ptr(),
+                                di.next_tokens.data_ptr(), self.kv_view(di), k, self._out,
+                                self.stream())
+        else:
+            fe.fe_draft_sample(self.handle, di.batch, di.features.data_ptr(),
+                               di.next_tokens.data_ptr(), self.kv_view(di), k,
+                               float(1.0 if temperature is None else temperature),
+                               uniforms.data_ptr() if uniforms is not None else None, self._out,
+                               self.stream())
         return out
 
     def alloc_tree(self, batch: int, topk: int) -> Dict[str, object]:

@@ -19,7 +19,8 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
                 4: "FE_E_WORKSPACE", 5: "FE_E_HIP"}
 
 # Every function include/fe.h declares.
-EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_build_tree",
+EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
+           "fe_build_tree",
            "fe_accept_greedy", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
            "fe_drafter_destroy", "fe_last_error")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
@@ -91,6 +92,10 @@ def lib() -> C.CDLL:
         L.fe_draft_forward.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                        C.POINTER(fe_kv_view), C.c_int32,
                                        C.POINTER(fe_draft_out), C.c_void_p]
+        L.fe_draft_sample.restype = C.c_int
+        L.fe_draft_sample.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                      C.POINTER(fe_kv_view), C.c_int32, C.c_float, C.c_void_p,
+                                      C.POINTER(fe_draft_out), C.c_void_p]
         L.fe_build_tree.restype = C.c_int
         L.fe_build_tree.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
@@ -142,6 +147,14 @@ def fe_draft_forward(h: int, batch: int, features: int, next_tokens: int, kv: fe
     check(lib().fe_draft_forward(C.c_void_p(h), batch, C.c_void_p(features),
                                  C.c_void_p(next_tokens), C.byref(kv), topk, C.byref(out),
                                  C.c_void_p(stream)))
+
+
+def fe_draft_sample(h: int, batch: int, features: int, next_tokens: int, kv: fe_kv_view,
+                    topk: int, temperature: float, uniforms, out: fe_draft_out, stream: int) -> None:
+    check(lib().fe_draft_sample(C.c_void_p(h), batch, C.c_void_p(features),
+                                C.c_void_p(next_tokens), C.byref(kv), topk,
+                                C.c_float(temperature), C.c_void_p(uniforms), C.byref(out),
+                                C.c_void_p(stream)))
 
 
 def fe_build_tree(h: int, batch: int, topk: int, root_tokens: int, topk_ids: int,
