@@ -440,3 +440,142 @@ int feo_kv_update(const feo_config *c, const feo_weights *w, int32_t n_rows, con
   free(f); free(ge); free(x0); free(a);
   return 0;
 }
+
+/* Speculative-sampling acceptance of one drafting cycle at temperature T
+ * (Section 2.4, parallel verification; Section 3 reports temperature 1).
+ * Children drawn without replacement from the level's draft distribution q
+ * (draft_uniforms given: their Gumbel keys fix the order of the draws) are
+ * tested in draw order by recursive rejection sampling: child x is accepted
+ * when u <= p(x) / q(x); on a rejection the target's distribution becomes the
+ * normalised positive part of p - q and x leaves q (which is renormalised).
+ * Children chosen without randomness (draft_uniforms NULL: the top-k list) are
+ * tested in listing order against q = a point mass on x: accepted when
+ * u <= p(x), else x leaves p.  When every child is rejected, or the accepted
+ * node has no children, one more token is drawn from the current p by inverse
+ * CDF in target-id order.  Either way the emitted tokens follow the target's
+ * distributions exactly. */
+int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t draft_vocab,
+                      int32_t target_vocab, const int32_t *tokens, const int32_t *retrieve,
+                      const int32_t *topk_draft, const float *draft_logits, double temperature,
+                      const float *draft_uniforms, const int32_t *d2t, const float *target_probs,
+                      const float *uniforms, int32_t *accept_len, int32_t *accept_path,
+                      int32_t *accepted, double *margin) {
+  if (batch < 0 || n_layers < 1 || n_layers > 63 || topk < 1 || topk > 64 || draft_vocab < topk ||
+      target_vocab < 1)
+    return -1;
+  if (!(temperature > 0.0)) return -1;
+  const int32_t N = n_layers, k = topk, V = draft_vocab, Vt = target_vocab;
+  const int32_t T = 1 + N * k, NL = N * (k - 1) + 1, NU = N * k + 1;
+  double *r = (double *)malloc(sizeof(double) * (size_t)Vt);
+  double *q0 = (double *)malloc(sizeof(double) * (size_t)V);
+  char *gone = (char *)malloc((size_t)V);
+  for (int32_t b = 0; b < batch; ++b) {
+    const int32_t *tok = tokens + (size_t)b * T;
+    const float *u = uniforms + (size_t)b * NU;
+    int32_t path[64], len = 0, node = 0, t = 0;
+    double mg = INFINITY, Z = 0.0;
+    path[0] = 0;
+    for (;;) {
+      /* the target's distribution after the path so far */
+      const float *p = target_probs + ((size_t)b * T + (size_t)node) * Vt;
+      Z = 0.0;
+      for (int32_t x = 0; x < Vt; ++x) { r[x] = (double)p[x]; Z += r[x]; }
+      /* children: the k level-(len+1) nodes under the root or a backbone node */
+      const int32_t lvl = len + 1;
+      const int has_children = lvl <= N && (node == 0 || node == 1 + (lvl - 2) * k);
+      if (!has_children) break;
+      const size_t lrow = (size_t)b * N + (size_t)(lvl - 1);
+      const float *z = draft_logits + lrow * V;
+      const int32_t *cd = topk_draft + lrow * k;
+      /* test order: the draws' order (Gumbel keys, larger first, lower id on
+       * ties), or the listing order for unsampled children */
+      scored ordk[64];
+      for (int32_t rho = 0; rho < k; ++rho) {
+        ordk[rho].id = rho;
+        ordk[rho].z = draft_uniforms
+            ? z[cd[rho]] / temperature + gumbel(draft_uniforms[lrow * V + (size_t)cd[rho]])
+            : -(double)rho;
+      }
+      for (int32_t i = 1; i < k; ++i)   /* insertion sort: keys desc, draft id asc */
+        for (int32_t j = i; j > 0; --j) {
+          const scored a = ordk[j - 1], c = ordk[j];
+          const int swap = c.z > a.z || (c.z == a.z && cd[c.id] < cd[a.id]);
+          if (!swap) break;
+          ordk[j - 1] = c;
+          ordk[j] = a;
+        }
+      /* q_{t+lvl} = softmax(z / T) over the draft vocabulary */
+      double mx = -INFINITY, S = 0.0;
+      for (int32_t v = 0; v < V; ++v) mx = z[v] / temperature > mx ? z[v] / temperature : mx;
+      for (int32_t v = 0; v < V; ++v) { q0[v] = exp(z[v] / temperature - mx); S += q0[v]; }
+      for (int32_t v = 0; v < V; ++v) { q0[v] /= S; gone[v] = 0; }
+      double R = 0.0;  /* q mass of the rejected children */
+      int accepted_child = 0;
+      for (int32_t j = 0; j < k; ++j) {
+        const int32_t rho = ordk[j].id;
+        const int32_t child = 1 + (lvl - 1) * k + rho, vd = cd[rho], x = tok[child];
+        const double qi = draft_uniforms ? q0[vd] / (1.0 - R) : 1.0, pi = r[x] / Z;
+        const double ut = (double)u[t++];
+        const double m = fabs(ut * qi - pi) / (qi > pi ? qi : pi);
+        if (m < mg) mg = m;
+        if (ut * qi <= pi) {
+          node = child;
+          path[++len] = child;
+          accepted_child = 1;
+          break;
+        }
+        if (!draft_uniforms) {   /* q is a point mass on x: x leaves p */
+          Z -= r[x];
+          r[x] = 0.0;
+          continue;
+        }
+        /* p <- (p - q)^+ / Z', q <- q without x */
+        double dec = 0.0;
+        for (int32_t v = 0; v < V; ++v) {
+          if (gone[v]) continue;
+          const int32_t xt = d2t ? d2t[v] : v;
+          const double nv = r[xt] - Z * q0[v] / (1.0 - R);
+          const double nr = nv > 0.0 ? nv : 0.0;
+          dec += r[xt] - nr;
+          r[xt] = nr;
+        }
+        Z -= dec;
+        gone[vd] = 1;
+        R += q0[vd];
+      }
+      if (!accepted_child) break;
+    }
+    /* one token from the current p: inverse CDF in target-id order */
+    const double target = (double)u[NU - 1] * Z;
+    double cum = 0.0;
+    int32_t pick = -1, last = -1;
+    for (int32_t x = 0; x < Vt; ++x) {
+      if (r[x] > 0.0) last = x;
+      const double prev = cum;
+      cum += r[x];
+      if (pick < 0 && cum > target) {
+        pick = x;
+        const double m1 = (target - prev) / Z, m2 = (cum - target) / Z;
+        const double m = m1 < m2 ? m1 : m2;
+        if (m < mg) mg = m;
+      }
+    }
+    if (pick < 0) pick = last;
+    int32_t *acc = accepted + (size_t)b * (N + 1);
+    for (int32_t i = 0; i <= N; ++i) acc[i] = -1;
+    for (int32_t i = 1; i <= len; ++i) acc[i - 1] = tok[path[i]];
+    acc[len] = pick;
+    accept_len[b] = len;
+    /* the first root->leaf path that holds the accepted nodes */
+    const int32_t *ret = retrieve + (size_t)b * NL * (N + 1);
+    accept_path[b] = -1;
+    for (int32_t row = 0; row < NL && accept_path[b] < 0; ++row) {
+      int ok = 1;
+      for (int32_t i = 0; i <= len; ++i) ok &= ret[(size_t)row * (N + 1) + i] == path[i];
+      if (ok) accept_path[b] = row;
+    }
+    if (margin) margin[b] = mg;
+  }
+  free(r); free(q0); free(gone);
+  return 0;
+}

@@ -142,6 +142,29 @@ int feo_kv_update(const feo_config *cfg, const feo_weights *w, int32_t n_rows,
                   const void *features, const int32_t *tokens, const int32_t *positions,
                   double *const *k_out, double *const *v_out);
 
+/*
+ * Speculative-sampling acceptance of one cycle at temperature T (Section 2.4).
+ * For the tree of feo_build_tree (tokens [B, T] target ids, retrieve) with
+ * topk_draft [B, N, k] the children's draft ids, draft_logits [B, N, V] the
+ * raw z of each level (q = softmax(z / T)), draft_uniforms [B, N, V] the
+ * uniforms the candidates were drawn with (feo_draft_sample; NULL for
+ * candidates chosen without randomness), d2t [V] (NULL = identity),
+ * target_probs [B, T, V_t] the target's next-token distribution after each
+ * node's path, and uniforms [B, N*k + 1] in (0, 1): accept test number j uses
+ * uniforms[j], the final draw uses the last one.  Sampled children are tested
+ * in draw order by recursive rejection sampling, unsampled ones in listing
+ * order against a point mass (see fe_oracle.c).  Outputs as
+ * feo_accept_greedy; accept_path is the first retrieve row that holds the
+ * accepted nodes.  margin [B] (optional): the smallest relative distance of a
+ * decision from its threshold.  Returns 0, or -1 on invalid arguments.
+ */
+int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t draft_vocab,
+                      int32_t target_vocab, const int32_t *tokens, const int32_t *retrieve,
+                      const int32_t *topk_draft, const float *draft_logits, double temperature,
+                      const float *draft_uniforms, const int32_t *d2t, const float *target_probs,
+                      const float *uniforms, int32_t *accept_len, int32_t *accept_path,
+                      int32_t *accepted, double *margin);
+
 #ifdef __cplusplus
 }
 #endif

@@ -46,6 +46,7 @@ def lib():
         L.feo_build_tree.restype = C.c_int
         L.feo_accept_greedy.restype = C.c_int
         L.feo_kv_update.restype = C.c_int
+        L.feo_accept_sample.restype = C.c_int
         L.feo_get_threads.restype = C.c_int
         _lib = L
     return _lib
@@ -225,3 +226,36 @@ def kv_update(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.nd
     if rc != 0:
         raise ValueError("oracle kv_update rejected its arguments")
     return ks, vs
+
+
+def accept_sample(n_layers: int, topk: int, tokens, retrieve, topk_draft, draft_logits,
+                  temperature: float, d2t, target_probs, uniforms,
+                  draft_uniforms=None) -> Dict[str, np.ndarray]:
+    """Speculative-sampling acceptance of one cycle (see feo_accept_sample)."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    retrieve = np.ascontiguousarray(retrieve, dtype=np.int32)
+    topk_draft = np.ascontiguousarray(topk_draft, dtype=np.int32)
+    draft_logits = np.ascontiguousarray(draft_logits, dtype=np.float32)
+    target_probs = np.ascontiguousarray(target_probs, dtype=np.float32)
+    uniforms = np.ascontiguousarray(uniforms, dtype=np.float32)
+    B, N, k = tokens.shape[0], int(n_layers), int(topk)
+    V, Vt = draft_logits.shape[-1], target_probs.shape[-1]
+    assert draft_logits.shape == (B, N, V) and target_probs.shape == (B, 1 + N * k, Vt)
+    assert uniforms.shape == (B, N * k + 1) and topk_draft.shape == (B, N, k)
+    d = None if d2t is None else np.ascontiguousarray(d2t, dtype=np.int32)
+    du = None
+    if draft_uniforms is not None:
+        du = np.ascontiguousarray(draft_uniforms, dtype=np.float32)
+        assert du.shape == (B, N, V), du.shape
+    out = dict(accept_len=np.zeros(B, np.int32), accept_path=np.zeros(B, np.int32),
+               accepted=np.zeros((B, N + 1), np.int32), margin=np.zeros(B))
+    rc = lib().feo_accept_sample(C.c_int32(B), C.c_int32(N), C.c_int32(k), C.c_int32(V),
+                                 C.c_int32(Vt), _pi(tokens), _pi(retrieve), _pi(topk_draft),
+                                 _p(draft_logits), C.c_double(temperature),
+                                 _p(du) if du is not None else None,
+                                 _pi(d) if d is not None else None, _p(target_probs),
+                                 _p(uniforms), _pi(out["accept_len"]), _pi(out["accept_path"]),
+                                 _pi(out["accepted"]), _pd(out["margin"]))
+    if rc != 0:
+        raise ValueError("oracle accept_sample rejected its arguments")
+    return out
