@@ -336,6 +336,27 @@ def main():
     torch.cuda.synchronize()
     sms = ev0.elapsed_time(ev1) / args.steps
     log(f"sampled drafting: {sms * 1000:.1f} us/pass")
+    # ... and its speculative-sampling acceptance against synthetic target
+    # distributions over the target vocabulary (one per tree node)
+    sout = dr.alloc_outputs(cfg.batch, cfg.topk, logits=True)
+    stree = dr.alloc_tree(cfg.batch, cfg.topk)
+    dr.forward(di, out=sout, tree=stree, temperature=1.0, uniforms=ud)
+    gen = torch.Generator(device=dr.device).manual_seed(args.seed)
+    tprobs = torch.rand((cfg.batch, 1 + cfg.n_layers * cfg.topk, cfg.target_vocab),
+                        generator=gen, device=dr.device)
+    tprobs /= tprobs.sum(-1, keepdim=True)
+    ua = torch.rand((cfg.batch, cfg.n_layers * cfg.topk + 1), generator=gen,
+                    device=dr.device).clamp_(2.0 ** -24, 1 - 2.0 ** -24)
+    acc_s = dr.accept_sample(stree, sout["topk_draft"], sout["logits"], tprobs, ua,
+                             temperature=1.0, draft_uniforms=ud)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(50):
+        dr.accept_sample(stree, sout["topk_draft"], sout["logits"], tprobs, ua, temperature=1.0,
+                         draft_uniforms=ud, out=acc_s)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    accept_s_us = ev0.elapsed_time(ev1) * 1000.0 / 50
 
     # NEXT-1, the drafter cache update: one cycle's N+1 verified positions,
     # and a whole prefix of max_prefix positions (the prompt's cache, the
@@ -386,7 +407,9 @@ def main():
                                   "us_per_pass": sms * 1000.0,
                                   "drafts_per_s": cfg.batch * 1000.0 / sms,
                                   "uniform_bytes": cfg.batch * cfg.n_layers * cfg.draft_vocab * 4,
-                                  "vs_greedy": ms / sms},
+                                  "vs_greedy": ms / sms,
+                                  "accept_sample_us_per_call": accept_s_us,
+                                  "accept_sample_issue": "eager, from Python"},
         # matrix-core use over the whole pass, against the most that an
         # HBM-bound pass of this arithmetic intensity could reach
         "pass_mfma": {"flops_per_pass": pflops,

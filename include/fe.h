@@ -262,6 +262,48 @@ fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
                        const int32_t *tokens, const int32_t *positions, const int32_t *dst_rows,
                        const fe_kv_cache *cache, void *workspace, size_t ws_bytes, void *stream);
 
+/* Speculative-sampling acceptance of a drafting cycle at temperature T
+ * (Section 2.4, parallel verification, with the sampling of Section 3 at
+ * T > 0), one workgroup per sequence.  Walking from the root, the children of
+ * a node are tested against the target's distribution p there:
+ *  - children drawn by fe_draft_sample (draft_uniforms = the uniforms given to
+ *    it) in the order of their draws (their Gumbel keys), by recursive
+ *    rejection sampling: child x is accepted when u <= p(x) / q(x), with q the
+ *    level's draft distribution softmax(z / T) mapped through d2t; on a
+ *    rejection p becomes the normalised positive part of p - q and x leaves q
+ *    (renormalised);
+ *  - children chosen without randomness (draft_uniforms NULL, e.g. the top-k
+ *    list of fe_draft_forward) in listing order against a point mass: accepted
+ *    when u <= p(x), else x leaves p.
+ * When every child is rejected, or the accepted node has no children, one more
+ * token is drawn from the current p by inverse CDF in target-id order.  The
+ * emitted tokens then follow the target's distributions exactly, whatever the
+ * draft (the speculative-sampling guarantee).
+ *  tokens, retrieve  the tree (fe_build_tree / fe_draft_out.tree), [B, T] and
+ *                    [B, N*(k-1)+1, N+1] int32, T = 1 + N*k
+ *  topk_draft        [B, N, k] int32: the children's draft ids (fe_draft_out)
+ *  draft_logits      [B, N, V] fp32: the raw logits z of the pass (fe_draft_out)
+ *  draft_uniforms    [B, N, V] fp32 or NULL (see above)
+ *  target_probs      [B, T, V_t] fp32: the target's next-token distribution
+ *                    after each node's path, at temperature T (what tree-
+ *                    attention verification yields); rows need not be normalised
+ *  uniforms          [B, N*k + 1] fp32 in (0, 1): accept test number j (in the
+ *                    order the walk makes them) uses uniforms[j], the final
+ *                    draw the last one
+ *  accept_len, accept_path, accepted   as fe_accept_greedy (accept_path: the
+ *                    first retrieve row that holds the accepted nodes)
+ * Uses [B, V_t] floats of the handle's workspace as scratch (calls on one
+ * handle are serialised).  All device pointers 4-byte aligned.  Errors:
+ * FE_E_INVALID (NULL handle or required array, batch outside [0, max_batch],
+ * topk outside [1, max_topk], temperature not positive and finite),
+ * FE_E_ALIGN; nothing is launched on an error. */
+fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk, const int32_t *tokens,
+                           const int32_t *retrieve, const int32_t *topk_draft,
+                           const float *draft_logits, float temperature,
+                           const float *draft_uniforms, const float *target_probs,
+                           const float *uniforms, int32_t *accept_len, int32_t *accept_path,
+                           int32_t *accepted, void *stream);
+
 /* Replays fe_draft_forward through a captured HIP graph when on != 0 (the
  * default is off).  A graph is captured on the first call with a given set of
  * arguments and replayed while they stay the same. */

@@ -504,6 +504,12 @@ int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t dra
           ordk[j - 1] = c;
           ordk[j] = a;
         }
+      if (draft_uniforms)   /* how close the draw order came to a tie */
+        for (int32_t j = 1; j < k; ++j) {
+          const double sc = fabs(ordk[j].z) > 1.0 ? fabs(ordk[j].z) : 1.0;
+          const double m = (ordk[j - 1].z - ordk[j].z) / sc;
+          if (m < mg) mg = m;
+        }
       /* q_{t+lvl} = softmax(z / T) over the draft vocabulary */
       double mx = -INFINITY, S = 0.0;
       for (int32_t v = 0; v < V; ++v) mx = z[v] / temperature > mx ? z[v] / temperature : mx;

@@ -308,6 +308,18 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
                          const int32_t *target_next, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s);
 
+// Speculative-sampling acceptance at temperature 1/inv_temp of B trees (N
+// levels, k per level): topk_draft [B, N, k] draft ids of the children,
+// draft_logits [B, N, V], draft_uniforms [B, N, V] or NULL (unsampled
+// children), target_probs [B, 1+N*k, Vt], uniforms [B, N*k+1]; resid
+// [B, Vt] fp32 scratch.  Outputs as accept_greedy.
+hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
+                         const int32_t *retrieve, const int32_t *topk_draft,
+                         const float *draft_logits, float inv_temp, const float *draft_uniforms,
+                         const int32_t *d2t, const float *target_probs, const float *uniforms,
+                         float *resid, int32_t *accept_len, int32_t *accept_path,
+                         int32_t *accepted, hipStream_t s);
+
 // Global top-k of every row from the tile candidates (by key); softmax
 // statistics merge.  With cand_z (sampled candidates) the k winners are
 // listed by z / T (larger first, lower id on ties), else in key order.

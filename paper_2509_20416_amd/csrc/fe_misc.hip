@@ -350,6 +350,199 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Speculative-sampling acceptance at temperature T (Section 2.4), one
+// workgroup per sequence walking its tree from the root.  At a node with
+// children the target's distribution p (copied to the row's scratch r with
+// its sum Z) is tested against the children: sampled children in draw order
+// (their Gumbel keys, recomputed from the drafting uniforms) by recursive
+// rejection sampling (accept when u * q_i(x) <= r(x) / Z; on a rejection
+// r <- (r - Z q_i)^+ over the draft vocabulary, which is where q lives, and x
+// leaves q), unsampled ones in listing order against point masses (accept
+// when u <= r(x) / Z, else r(x) <- 0).  The last uniform draws one token from
+// r by inverse CDF in target-id order: per-thread contiguous slices, their
+// sums scanned in order.  Every decision is taken on block-reduced values,
+// so control flow is uniform across the workgroup.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float block_sum256(float v, float *red) {
+  v = group_sum<64>(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+__device__ __forceinline__ float block_max256(float v, float *red) {
+  v = group_max<64>(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__global__ __launch_bounds__(256) void k_accept_sample(
+    int N, int k, int V, int Vt, const int32_t *__restrict__ tokens,
+    const int32_t *__restrict__ retrieve, const int32_t *__restrict__ topk_draft,
+    const float *__restrict__ draft_logits, float inv_temp,
+    const float *__restrict__ draft_uniforms, const int32_t *__restrict__ d2t,
+    const float *__restrict__ target_probs, const float *__restrict__ uniforms, float *resid,
+    int32_t *accept_len, int32_t *accept_path, int32_t *accepted) {
+  __shared__ float red[4];
+  __shared__ float s_scan[256];
+  __shared__ int s_path[kMaxLayers + 1];
+  __shared__ int s_pick;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int T = 1 + N * k, NU = N * k + 1, NL = N * (k - 1) + 1;
+  const int32_t *tok = tokens + (size_t)b * T;
+  const float *u = uniforms + (size_t)b * NU;
+  float *r = resid + (size_t)b * Vt;
+  int node = 0, len = 0, t = 0;
+  float Z = 0.f;
+  if (tid == 0) s_path[0] = 0;
+  for (;;) {
+    const float *p = target_probs + ((size_t)b * T + node) * Vt;
+    float zs = 0.f;
+    for (int x = tid; x < Vt; x += 256) {
+      const float v = p[x];
+      r[x] = v;
+      zs += v;
+    }
+    Z = block_sum256(zs, red);  // its barriers also order the copy before later reads
+    const int lvl = len + 1;
+    const bool has_children = lvl <= N && (node == 0 || node == 1 + (lvl - 2) * k);
+    if (!has_children) break;
+    const size_t lrow = (size_t)b * N + (lvl - 1);
+    const float *z = draft_logits + lrow * V;
+    const int32_t *cd = topk_draft + lrow * k;
+    // test order (every thread the same): draw order by key, or listing order
+    int ord[kMaxTopk];
+    float key[kMaxTopk];
+    for (int j = 0; j < k; ++j) {
+      ord[j] = j;
+      const int vd = min(max(cd[j], 0), V - 1);
+      key[j] = draft_uniforms ? z[vd] * inv_temp - logf(-logf(draft_uniforms[lrow * V + vd]))
+                              : -(float)j;
+    }
+    for (int i = 1; i < k; ++i)
+      for (int j = i; j > 0; --j) {
+        const int a = ord[j - 1], c = ord[j];
+        const bool swap = key[c] > key[a] || (key[c] == key[a] && cd[c] < cd[a]);
+        if (!swap) break;
+        ord[j - 1] = c;
+        ord[j] = a;
+      }
+    // q = softmax(z / T) statistics over the draft vocabulary
+    float mx = -INFINITY;
+    for (int v = tid; v < V; v += 256) mx = fmaxf(mx, z[v] * inv_temp);
+    mx = block_max256(mx, red);
+    float se = 0.f;
+    for (int v = tid; v < V; v += 256) se += expf(z[v] * inv_temp - mx);
+    const float S = block_sum256(se, red);
+    float R = 0.f;  // q mass of the rejected children
+    int gone[kMaxTopk];
+    int ngone = 0;
+    bool took = false;
+    for (int j = 0; j < k; ++j) {
+      const int rho = ord[j];
+      const int child = 1 + (lvl - 1) * k + rho;
+      const int vd = min(max(cd[rho], 0), V - 1);
+      const int x = tok[child];
+      const float q0v = expf(z[vd] * inv_temp - mx) / S;
+      const float qi = draft_uniforms ? q0v / (1.f - R) : 1.f;
+      const float rx = (x >= 0 && x < Vt) ? r[x] : 0.f;
+      const float ut = u[t++];
+      __syncthreads();  // every thread has read r[x] before it changes
+      if (ut * qi <= rx / Z) {
+        node = child;
+        ++len;
+        if (tid == 0) s_path[len] = child;
+        took = true;
+        break;
+      }
+      if (!draft_uniforms) {  // point mass on x: x leaves p
+        if (tid == 0 && x >= 0 && x < Vt) r[x] = 0.f;
+        Z -= rx;
+        __syncthreads();
+        continue;
+      }
+      const float scale = Z / (1.f - R);
+      float dec = 0.f;
+      for (int v = tid; v < V; v += 256) {
+        bool out = false;
+        for (int g = 0; g < ngone; ++g) out |= gone[g] == v;
+        if (out) continue;
+        const int xt = d2t ? d2t[v] : v;
+        if (xt < 0 || xt >= Vt) continue;
+        const float old = r[xt];
+        const float nr = fmaxf(old - scale * (expf(z[v] * inv_temp - mx) / S), 0.f);
+        r[xt] = nr;
+        dec += old - nr;
+      }
+      Z -= block_sum256(dec, red);
+      gone[ngone++] = vd;
+      R += q0v;
+    }
+    if (!took) break;
+  }
+  // one token from r: inverse CDF over target ids, contiguous per-thread slices
+  const int C = (Vt + 255) / 256, x0 = min(tid * C, Vt), x1 = min(x0 + C, Vt);
+  float cs = 0.f;
+  int lastnz = -1;
+  for (int x = x0; x < x1; ++x) {
+    cs += r[x];
+    if (r[x] > 0.f) lastnz = x;
+  }
+  s_scan[tid] = cs;
+  if (tid == 0) s_pick = -1;
+  __syncthreads();
+  float pre = 0.f;
+  for (int i = 0; i < tid; ++i) pre += s_scan[i];
+  const float target = u[NU - 1] * Z;
+  if (pre <= target && target < pre + cs) {
+    float cum = pre;
+    int pick = x1 - 1;
+    for (int x = x0; x < x1; ++x) {
+      cum += r[x];
+      if (cum > target) {
+        pick = x;
+        break;
+      }
+    }
+    s_pick = pick;  // the slices' ranges [pre, pre + cs) tile the line: one thread only
+  }
+  const float lastf = block_max256((float)lastnz, red);  // also orders s_pick
+  int pick = s_pick;
+  if (pick < 0) pick = (int)lastf;  // target at or past the total (rounding)
+  if (tid <= N) {
+    int32_t *acc = accepted + (size_t)b * (N + 1);
+    acc[tid] = tid < len ? tok[s_path[tid + 1]] : (tid == len ? pick : -1);
+  }
+  if (tid == 0) {
+    accept_len[b] = len;
+    const int32_t *ret = retrieve + (size_t)b * NL * (N + 1);
+    int row = -1;
+    for (int w = 0; w < NL && row < 0; ++w) {
+      bool ok = true;
+      for (int i = 0; i <= len; ++i) ok &= ret[(size_t)w * (N + 1) + i] == s_path[i];
+      if (ok) row = w;
+    }
+    accept_path[b] = row;
+  }
+}
+
+hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
+                         const int32_t *retrieve, const int32_t *topk_draft,
+                         const float *draft_logits, float inv_temp, const float *draft_uniforms,
+                         const int32_t *d2t, const float *target_probs, const float *uniforms,
+                         float *resid, int32_t *accept_len, int32_t *accept_path,
+                         int32_t *accepted, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (k > kMaxTopk || N > kMaxLayers || N + 1 > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_accept_sample, dim3(B), dim3(256), 0, s, N, k, V, Vt, tokens, retrieve,
+                     topk_draft, draft_logits, inv_temp, draft_uniforms, d2t, target_probs,
+                     uniforms, resid, accept_len, accept_path, accepted);
+  return hipGetLastError();
+}
+
 __global__ void k_rope_table(float *tab, int npos, int D, double theta) {
   const int half = D / 2;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < npos * half; i += gridDim.x * blockDim.x) {

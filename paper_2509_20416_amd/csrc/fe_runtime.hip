@@ -32,7 +32,7 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
-      psum, cval, cidx, cz, splitk, total;
+      psum, cval, cidx, cz, resid, splitk, total;
   size_t splitk_floats;
   int nchmax, nwg, npos;
 };
@@ -72,6 +72,7 @@ Layout layout_of(const fe_config &c) {
   L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cz = take(B * N * (size_t)L.nwg * kMaxTopk * 4);  // z / T of sampled candidates
+  L.resid = take(B * (size_t)c.target_vocab * 4);    // acceptance: residual target distribution
   // split-K slices of the batched GEMMs with narrow outputs: up to 8 slices of
   // the QKV rows (B * N at most, 256 per launch) over 128-column tiles
   {
@@ -630,6 +631,34 @@ extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *fea
     }
   }
   (void)kvd;
+  return FE_OK;
+}
+
+extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk,
+                                      const int32_t *tokens, const int32_t *retrieve,
+                                      const int32_t *topk_draft, const float *draft_logits,
+                                      float temperature, const float *draft_uniforms,
+                                      const float *target_probs, const float *uniforms,
+                                      int32_t *accept_len, int32_t *accept_path,
+                                      int32_t *accepted, void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const fe_config &c = h->cfg;
+  if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
+  if (topk < 1 || topk > c.max_topk) return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
+  if (!(temperature > 0.f) || !(temperature < INFINITY) || !(1.0f / temperature < INFINITY))
+    return fail(FE_E_INVALID, "temperature must be positive and finite");
+  if (batch == 0) return FE_OK;
+  if (!tokens || !retrieve || !topk_draft || !draft_logits || !target_probs || !uniforms ||
+      !accept_len || !accept_path || !accepted)
+    return fail(FE_E_INVALID, "every acceptance input and output except draft_uniforms is required");
+  const void *ptrs[] = {tokens, retrieve, topk_draft, draft_logits, draft_uniforms, target_probs,
+                        uniforms, accept_len, accept_path, accepted};
+  for (const void *q : ptrs)
+    if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "acceptance arrays must be 4-byte aligned");
+  FE_TRY(accept_sample(batch, c.n_layers, topk, c.draft_vocab, c.target_vocab, tokens, retrieve,
+                       topk_draft, draft_logits, 1.0f / temperature, draft_uniforms, h->w.d2t,
+                       target_probs, uniforms, (float *)(h->ws + h->L.resid), accept_len,
+                       accept_path, accepted, (hipStream_t)stream));
   return FE_OK;
 }
 

@@ -200,6 +200,30 @@ class Drafter:
                             out["accepted"].data_ptr(), self.stream())
         return out
 
+    def accept_sample(self, tree: Dict[str, object], topk_draft, draft_logits, target_probs,
+                      uniforms, temperature: float = 1.0, draft_uniforms=None,
+                      topk: Optional[int] = None, batch: Optional[int] = None,
+                      out: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+        """Speculative-sampling acceptance of one cycle (fe_accept_sample); all
+        arrays on the device (see include/fe.h for shapes)."""
+        import torch
+        k = int(topk or self.cfg.topk)
+        B = int(batch if batch is not None else tree["tokens"].shape[0])
+        N = self.cfg.n_layers
+        dev = tree["tokens"].device
+        if out is None:
+            out = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+                   "accept_path": torch.empty(B, dtype=torch.int32, device=dev),
+                   "accepted": torch.empty(B, N + 1, dtype=torch.int32, device=dev)}
+        fe.fe_accept_sample(self.handle, B, k, tree["tokens"].data_ptr(),
+                            tree["retrieve"].data_ptr(), topk_draft.data_ptr(),
+                            draft_logits.data_ptr(), float(temperature),
+                            draft_uniforms.data_ptr() if draft_uniforms is not None else None,
+                            target_probs.data_ptr(), uniforms.data_ptr(),
+                            out["accept_len"].data_ptr(), out["accept_path"].data_ptr(),
+                            out["accepted"].data_ptr(), self.stream())
+        return out
+
     def kv_update(self, features, tokens, positions, dst_rows, kcache, vcache,
                   chunk_rows: int = 1024, n_rows: Optional[int] = None) -> None:
         """Write the drafter cache rows of verified positions (fe_kv_update):

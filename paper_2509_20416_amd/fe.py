@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
            "fe_build_tree",
-           "fe_accept_greedy", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
+           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
            "fe_drafter_destroy", "fe_last_error")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
@@ -101,6 +101,9 @@ def lib() -> C.CDLL:
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
         L.fe_accept_greedy.restype = C.c_int
         L.fe_accept_greedy.argtypes = [C.c_void_p, C.c_int32, C.c_int32] + [C.c_void_p] * 7
+        L.fe_accept_sample.restype = C.c_int
+        L.fe_accept_sample.argtypes = [C.c_void_p, C.c_int32, C.c_int32] + [C.c_void_p] * 4 + \
+            [C.c_float] + [C.c_void_p] * 7
         L.fe_kv_update_workspace_bytes.restype = C.c_size_t
         L.fe_kv_update_workspace_bytes.argtypes = [C.POINTER(fe_config), C.c_int32]
         L.fe_kv_update.restype = C.c_int
@@ -170,6 +173,19 @@ def fe_accept_greedy(h: int, batch: int, topk: int, tokens: int, retrieve: int, 
                                  C.c_void_p(retrieve), C.c_void_p(target_next),
                                  C.c_void_p(accept_len), C.c_void_p(accept_path),
                                  C.c_void_p(accepted), C.c_void_p(stream)))
+
+
+def fe_accept_sample(h: int, batch: int, topk: int, tokens: int, retrieve: int, topk_draft: int,
+                     draft_logits: int, temperature: float, draft_uniforms, target_probs: int,
+                     uniforms: int, accept_len: int, accept_path: int, accepted: int,
+                     stream: int) -> None:
+    check(lib().fe_accept_sample(C.c_void_p(h), batch, topk, C.c_void_p(tokens),
+                                 C.c_void_p(retrieve), C.c_void_p(topk_draft),
+                                 C.c_void_p(draft_logits), C.c_float(temperature),
+                                 C.c_void_p(draft_uniforms), C.c_void_p(target_probs),
+                                 C.c_void_p(uniforms), C.c_void_p(accept_len),
+                                 C.c_void_p(accept_path), C.c_void_p(accepted),
+                                 C.c_void_p(stream)))
 
 
 def fe_kv_update_workspace_bytes(cfg: fe_config, chunk_rows: int) -> int:

@@ -177,3 +177,26 @@ def test_kv_update_validates_before_enqueue(fe):
                 fe.fe_kv_update(h, 3, 1 << 34, 1 << 35, 1 << 35, 1 << 35, cache, 1 << 36, big, 0)
         finally:
             fe.fe_drafter_destroy(h)
+
+
+def test_accept_sample_validates_before_enqueue(fe):
+    cfg = _cfg(fe)
+    w, keep = _fake_weights(fe, cfg.n_layers)
+    h = fe.fe_drafter_create(cfg, w, 1 << 30, fe.fe_workspace_bytes(cfg))
+    try:
+        a = [1 << 33] * 7            # tokens .. uniforms (device addresses, never touched)
+        o = [(1 << 34) + 256 * i for i in range(3)]
+        call = lambda B, k, T, arr, outs: fe.fe_accept_sample(
+            h, B, k, arr[0], arr[1], arr[2], arr[3], T, arr[4], arr[5], arr[6], *outs, 0)
+        for B, k, T, status in ((2, 8, 1.0, "FE_E_INVALID"), (1, 0, 1.0, "FE_E_INVALID"),
+                                (1, 8, 0.0, "FE_E_INVALID"), (1, 8, float("inf"), "FE_E_INVALID"),
+                                (1, 8, 1e-39, "FE_E_INVALID")):
+            with pytest.raises(fe.FeError, match=status):
+                call(B, k, T, a, o)
+        with pytest.raises(fe.FeError, match="FE_E_INVALID"):
+            call(1, 8, 1.0, a[:5] + [0] + a[6:], o)          # no target distributions
+        with pytest.raises(fe.FeError, match="FE_E_ALIGN"):
+            call(1, 8, 1.0, a[:4] + [(1 << 33) + 2] + a[5:], o)  # misaligned draft uniforms
+        call(0, 8, 1.0, a, o)                                   # empty batch: OK
+    finally:
+        fe.fe_drafter_destroy(h)
