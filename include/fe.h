@@ -276,9 +276,11 @@ fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
  *    list of fe_draft_forward) in listing order against a point mass: accepted
  *    when u <= p(x), else x leaves p.
  * When every child is rejected, or the accepted node has no children, one more
- * token is drawn from the current p by inverse CDF in target-id order.  The
- * emitted tokens then follow the target's distributions exactly, whatever the
- * draft (the speculative-sampling guarantee).
+ * token is drawn from the current p by inverse CDF, enumerating first the
+ * target ids that draft ids map to (in draft-id order), then the others in
+ * increasing order.  The emitted tokens then follow the target's distributions
+ * exactly, whatever the draft (the speculative-sampling guarantee).  d2t must
+ * be one-to-one.
  *  tokens, retrieve  the tree (fe_build_tree / fe_draft_out.tree), [B, T] and
  *                    [B, N*(k-1)+1, N+1] int32, T = 1 + N*k
  *  topk_draft        [B, N, k] int32: the children's draft ids (fe_draft_out)
@@ -292,11 +294,12 @@ fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
  *                    draw the last one
  *  accept_len, accept_path, accepted   as fe_accept_greedy (accept_path: the
  *                    first retrieve row that holds the accepted nodes)
- * Uses [B, V_t] floats of the handle's workspace as scratch (calls on one
- * handle are serialised).  All device pointers 4-byte aligned.  Errors:
+ * The residual distribution lives in on-chip memory: draft_vocab <= 32768
+ * and target_vocab <= 131072.  All device pointers 4-byte aligned.  Errors:
  * FE_E_INVALID (NULL handle or required array, batch outside [0, max_batch],
  * topk outside [1, max_topk], temperature not positive and finite),
- * FE_E_ALIGN; nothing is launched on an error. */
+ * FE_E_UNSUPPORTED (vocabulary sizes), FE_E_ALIGN; nothing is launched on an
+ * error. */
 fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk, const int32_t *tokens,
                            const int32_t *retrieve, const int32_t *topk_draft,
                            const float *draft_logits, float temperature,

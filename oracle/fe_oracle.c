@@ -452,8 +452,9 @@ int feo_kv_update(const feo_config *c, const feo_weights *w, int32_t n_rows, con
  * tested in listing order against q = a point mass on x: accepted when
  * u <= p(x), else x leaves p.  When every child is rejected, or the accepted
  * node has no children, one more token is drawn from the current p by inverse
- * CDF in target-id order.  Either way the emitted tokens follow the target's
- * distributions exactly. */
+ * CDF (target ids that draft ids map to first, in draft-id order, then the
+ * others in increasing order).  Either way the emitted tokens follow the
+ * target's distributions exactly. */
 int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t draft_vocab,
                       int32_t target_vocab, const int32_t *tokens, const int32_t *retrieve,
                       const int32_t *topk_draft, const float *draft_logits, double temperature,
@@ -551,11 +552,19 @@ int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t dra
       }
       if (!accepted_child) break;
     }
-    /* one token from the current p: inverse CDF in target-id order */
+    /* one token from the current p by inverse CDF, enumerating the target ids
+     * in a fixed order: those the draft vocabulary maps to, in draft-id order,
+     * then every other target id in increasing order */
     const double target = (double)u[NU - 1] * Z;
     double cum = 0.0;
     int32_t pick = -1, last = -1;
-    for (int32_t x = 0; x < Vt; ++x) {
+    char *img = (char *)calloc((size_t)Vt, 1);
+    for (int32_t v = 0; v < V; ++v) img[d2t ? d2t[v] : v] = 1;
+    for (int32_t e = 0; e < V + Vt; ++e) {
+      int32_t x;
+      if (e < V) x = d2t ? d2t[e] : e;
+      else if (!img[e - V]) x = e - V;
+      else continue;
       if (r[x] > 0.0) last = x;
       const double prev = cum;
       cum += r[x];
@@ -566,6 +575,7 @@ int feo_accept_sample(int32_t batch, int32_t n_layers, int32_t topk, int32_t dra
         if (m < mg) mg = m;
       }
     }
+    free(img);
     if (pick < 0) pick = last;
     int32_t *acc = accepted + (size_t)b * (N + 1);
     for (int32_t i = 0; i <= N; ++i) acc[i] = -1;

@@ -153,7 +153,9 @@ int feo_kv_update(const feo_config *cfg, const feo_weights *w, int32_t n_rows,
  * node's path, and uniforms [B, N*k + 1] in (0, 1): accept test number j uses
  * uniforms[j], the final draw uses the last one.  Sampled children are tested
  * in draw order by recursive rejection sampling, unsampled ones in listing
- * order against a point mass (see fe_oracle.c).  Outputs as
+ * order against a point mass; the final draw enumerates the target ids that
+ * draft ids map to first, in draft-id order, then the others in increasing
+ * order (see fe_oracle.c).  Outputs as
  * feo_accept_greedy; accept_path is the first retrieve row that holds the
  * accepted nodes.  margin [B] (optional): the smallest relative distance of a
  * decision from its threshold.  Returns 0, or -1 on invalid arguments.

@@ -311,13 +311,16 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
 // Speculative-sampling acceptance at temperature 1/inv_temp of B trees (N
 // levels, k per level): topk_draft [B, N, k] draft ids of the children,
 // draft_logits [B, N, V], draft_uniforms [B, N, V] or NULL (unsampled
-// children), target_probs [B, 1+N*k, Vt], uniforms [B, N*k+1]; resid
-// [B, Vt] fp32 scratch.  Outputs as accept_greedy.
+// children), target_probs [B, 1+N*k, Vt], uniforms [B, N*k+1].  Outputs as
+// accept_greedy.  V <= kAccSampleMaxV, Vt <= kAccSampleMaxVt (LDS residual).
+// img: the bitmask of the target ids that d2t maps to, from accept_img.
+constexpr int kAccSampleMaxV = 32768, kAccSampleMaxVt = 131072;
+hipError_t accept_img(const int32_t *d2t, int V, int Vt, uint32_t *img, hipStream_t s);
 hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
                          const int32_t *retrieve, const int32_t *topk_draft,
                          const float *draft_logits, float inv_temp, const float *draft_uniforms,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
-                         float *resid, int32_t *accept_len, int32_t *accept_path,
+                         const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s);
 
 // Global top-k of every row from the tile candidates (by key); softmax

@@ -352,105 +352,290 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
 
 // ---------------------------------------------------------------------------
 // Speculative-sampling acceptance at temperature T (Section 2.4), one
-// workgroup per sequence walking its tree from the root.  At a node with
-// children the target's distribution p (copied to the row's scratch r with
-// its sum Z) is tested against the children: sampled children in draw order
-// (their Gumbel keys, recomputed from the drafting uniforms) by recursive
-// rejection sampling (accept when u * q_i(x) <= r(x) / Z; on a rejection
-// r <- (r - Z q_i)^+ over the draft vocabulary, which is where q lives, and x
-// leaves q), unsampled ones in listing order against point masses (accept
-// when u <= r(x) / Z, else r(x) <- 0).  The last uniform draws one token from
-// r by inverse CDF in target-id order: per-thread contiguous slices, their
-// sums scanned in order.  Every decision is taken on block-reduced values,
-// so control flow is uniform across the workgroup.
+// 1024-thread workgroup per sequence walking its tree from the root.  The
+// target's distribution p at the current node changes only where the draft
+// distribution q lives, i.e. at the target ids the draft ids map to, so the
+// residual is kept per draft id in LDS (rd[v] = r(d2t[v])) while every other
+// target id keeps p(x) in memory; an LDS bitmask marks the mapped target ids.
+// Sampled children are tested in draw order (their Gumbel keys, recomputed
+// from the drafting uniforms) by recursive rejection sampling (accept when
+// u * q_i(x) <= r(x) / Z; on a rejection rd <- (rd - Z q_i)^+ and x leaves q),
+// unsampled ones in listing order against point masses (accept when
+// u <= r(x) / Z, else rd(x) <- 0).  The last uniform draws one token by
+// inverse CDF: mapped ids first in draft-id order, then the other target ids
+// in increasing order.  Each wave owns a contiguous chunk of the ids and
+// reads it 64 consecutive ids per step (coalesced): one pass per visited node
+// sums p (Z) and the unmapped part of every chunk; chunk sums are added in
+// order, the chunks' ranges tile the line exactly, and the owning wave walks
+// its chunk with wave scans to the drawn id.  Loads are issued kAccBatch at a
+// time.  Every decision is taken on block-reduced values, so control flow is
+// uniform across the workgroup.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float block_sum256(float v, float *red) {
+constexpr int kAccThreads = 1024;
+constexpr int kAccBatch = 32;  // floats per lane in flight in a pass over a target row
+constexpr int kAccMaxV = kAccSampleMaxV;    // draft ids whose residual fits the LDS
+constexpr int kAccMaxVt = kAccSampleMaxVt;  // target ids the LDS bitmask covers
+constexpr int kAccWaves = kAccThreads / 64;
+
+__device__ __forceinline__ float acc_sum(float v, float *red) {
   v = group_sum<64>(v);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  return (red[0] + red[1]) + (red[2] + red[3]);
+  float t = 0.f;
+#pragma unroll
+  for (int w = 0; w < kAccWaves; ++w) t += red[w];
+  return t;
 }
-__device__ __forceinline__ float block_max256(float v, float *red) {
+__device__ __forceinline__ float acc_max(float v, float *red) {
   v = group_max<64>(v);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float t = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kAccWaves; ++w) t = fmaxf(t, red[w]);
+  return t;
+}
+// Inclusive scan over the 64 lanes of a wave (fixed order of additions).
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
 }
 
-__global__ __launch_bounds__(256) void k_accept_sample(
+// The owning wave's walk of its chunk [c0, c1) for the running sum (from
+// `start`) to pass `target`: val(e) per id, W consecutive ids per lane and
+// 64 * W per step, kAccBatch / W steps' loads in flight.  Returns the id, or
+// -1 if rounding kept the running sum at or below target through the chunk.
+template <int W, class Load>
+__device__ int acc_walk(int c0, int c1, float start, float target, const Load &load) {
+  constexpr int NB = kAccBatch / W;
+  const int lane = threadIdx.x & 63;
+  float run = start;
+#pragma unroll 1
+  for (int e = c0; e < c1; e += 64 * W * NB) {
+    float a[NB][W];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) load(e + 64 * W * j + W * lane, a[j]);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      float sl = 0.f;
+#pragma unroll
+      for (int q = 0; q < W; ++q) sl += a[j][q];
+      const float incl = wave_incl_scan(sl);
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(run + incl > target);
+      if (hit) {
+        const int L = __builtin_ctzll(hit);
+        float ex = __shfl_up(incl, 1);
+        if (lane == 0) ex = 0.f;
+        float c = run + ex;
+        int pk = -1;
+#pragma unroll
+        for (int q = 0; q < W; ++q) {   // first q whose running sum passes
+          c += a[j][q];
+          if (pk < 0 && c > target) pk = q;
+        }
+        if (pk < 0) pk = W - 1;
+        return e + 64 * W * j + W * L + __shfl(pk, L);
+      }
+      run += __shfl(incl, 63);
+    }
+  }
+  return -1;
+}
+
+// Bitmask of the target ids that draft ids map to: bit x of img is set when
+// x = d2t[v] for some v (built in LDS by one workgroup, then stored).
+__global__ __launch_bounds__(kAccThreads) void k_build_img(const int32_t *__restrict__ d2t, int V,
+                                                           int Vt, uint32_t *img) {
+  __shared__ uint32_t s_img[kAccMaxVt / 32];
+  const int tid = threadIdx.x, nw = (Vt + 31) / 32;
+  for (int w = tid; w < nw; w += kAccThreads) s_img[w] = 0u;
+  __syncthreads();
+  for (int v = tid; v < V; v += kAccThreads) {
+    const int x = d2t ? d2t[v] : v;
+    if (x >= 0 && x < Vt) atomicOr(&s_img[x >> 5], 1u << (x & 31));
+  }
+  __syncthreads();
+  for (int w = tid; w < nw; w += kAccThreads) img[w] = s_img[w];
+}
+
+// VEC: target rows read four ids per lane (Vt % 4 == 0, 16-byte aligned rows).
+template <bool VEC>
+__global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     int N, int k, int V, int Vt, const int32_t *__restrict__ tokens,
     const int32_t *__restrict__ retrieve, const int32_t *__restrict__ topk_draft,
     const float *__restrict__ draft_logits, float inv_temp,
     const float *__restrict__ draft_uniforms, const int32_t *__restrict__ d2t,
-    const float *__restrict__ target_probs, const float *__restrict__ uniforms, float *resid,
-    int32_t *accept_len, int32_t *accept_path, int32_t *accepted) {
-  __shared__ float red[4];
-  __shared__ float s_scan[256];
+    const float *__restrict__ target_probs, const float *__restrict__ uniforms,
+    const uint32_t *__restrict__ img, int32_t *accept_len, int32_t *accept_path,
+    int32_t *accepted) {
+  constexpr int W = VEC ? 4 : 1;  // target ids per lane per load
+  __shared__ float s_rd[kAccMaxV];
+  __shared__ uint32_t s_img[kAccMaxVt / 32];
+  __shared__ float red[kAccWaves];
   __shared__ int s_path[kMaxLayers + 1];
+  __shared__ int s_cd[kMaxTopk], s_ord[kMaxTopk];
+  __shared__ float s_cn[kAccWaves];
+  __shared__ float s_zc[kMaxTopk], s_key[kMaxTopk], s_uc[kMaxTopk];
   __shared__ int s_pick;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = 1 + N * k, NU = N * k + 1, NL = N * (k - 1) + 1;
   const int32_t *tok = tokens + (size_t)b * T;
   const float *u = uniforms + (size_t)b * NU;
-  float *r = resid + (size_t)b * Vt;
+  auto tgt = [&](int v) { return d2t ? d2t[v] : v; };
+  auto in_img = [&](int x) { return (s_img[x >> 5] >> (x & 31)) & 1u; };
+  constexpr int kZ = (kAccMaxV + kAccThreads - 1) / kAccThreads;  // draft ids per thread
+  // bitmask of the target ids that draft ids map to (k_build_img)
+  {
+    constexpr int kW = kAccMaxVt / 32 / kAccThreads;
+    const int nw = (Vt + 31) / 32;
+    uint32_t m[kW];
+#pragma unroll
+    for (int j = 0; j < kW; ++j) {
+      const int w = tid + j * kAccThreads;
+      m[j] = w < nw ? img[w] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kW; ++j) {
+      const int w = tid + j * kAccThreads;
+      if (w < nw) s_img[w] = m[j];
+    }
+  }
+  __syncthreads();
+  // this wave's contiguous chunk of target ids
+  const int CW = ((Vt + kAccWaves - 1) / kAccWaves + 64 * W - 1) / (64 * W) * (64 * W);
+  const int c0 = min(wave * CW, Vt), c1 = min(c0 + CW, Vt);
   int node = 0, len = 0, t = 0;
   float Z = 0.f;
+  int lastn = -1;  // last unmapped id with mass in this lane's share of the chunk
+  const float *p = target_probs + (size_t)b * T * Vt;
+  // loads W consecutive target ids at x of row p (zeros past the chunk)
+  auto loadp = [&](int x, float *a) {
+    if constexpr (VEC) {
+      f32x4 q = {0.f, 0.f, 0.f, 0.f};
+      if (x < c1) q = *reinterpret_cast<const f32x4 *>(p + x);
+      a[0] = q.x; a[1] = q.y; a[2] = q.z; a[3] = q.w;
+    } else {
+      a[0] = x < c1 ? p[x] : 0.f;
+    }
+  };
   if (tid == 0) s_path[0] = 0;
   for (;;) {
-    const float *p = target_probs + ((size_t)b * T + node) * Vt;
-    float zs = 0.f;
-    for (int x = tid; x < Vt; x += 256) {
-      const float v = p[x];
-      r[x] = v;
-      zs += v;
-    }
-    Z = block_sum256(zs, red);  // its barriers also order the copy before later reads
+    p = target_probs + ((size_t)b * T + node) * Vt;
+    // the draft ids of the next level's children, fetched early (lane j)
     const int lvl = len + 1;
+    const size_t lrow = (size_t)b * N + (lvl - 1);
+    const int cdv = (tid < k && lvl <= N) ? topk_draft[lrow * k + tid] : 0;
+    float zs = 0.f, cn = 0.f;
+    lastn = -1;
+    constexpr int NB = kAccBatch / W;
+#pragma unroll 1
+    for (int e = c0; e < c1; e += 64 * W * NB) {
+      float a[NB][W];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) loadp(e + 64 * W * j + W * lane, a[j]);
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < W; ++q) {
+          const int x = e + 64 * W * j + W * lane + q;
+          zs += a[j][q];
+          if (x < c1 && !in_img(x)) {
+            cn += a[j][q];
+            if (a[j][q] > 0.f) lastn = x;
+          }
+        }
+    }
+    cn = group_sum<64>(cn);
+    if (lane == 0) s_cn[wave] = cn;  // read after the barriers below
+    // rd = p at the mapped ids: the map, then the values, half the ids at a time
+#pragma unroll 1
+    for (int h = 0; h < kZ; h += kZ / 2) {
+      int xs[kZ / 2];
+      float g[kZ / 2];
+#pragma unroll
+      for (int j = 0; j < kZ / 2; ++j) {
+        const int v = tid + (h + j) * kAccThreads;
+        const int x = v < V ? tgt(v) : -1;
+        xs[j] = (x >= 0 && x < Vt) ? x : -1;
+      }
+#pragma unroll
+      for (int j = 0; j < kZ / 2; ++j) g[j] = xs[j] >= 0 ? p[xs[j]] : 0.f;
+#pragma unroll
+      for (int j = 0; j < kZ / 2; ++j) {
+        const int v = tid + (h + j) * kAccThreads;
+        if (v < V) s_rd[v] = g[j];
+      }
+    }
+    Z = acc_sum(zs, red);  // its barriers also publish s_rd
     const bool has_children = lvl <= N && (node == 0 || node == 1 + (lvl - 2) * k);
     if (!has_children) break;
-    const size_t lrow = (size_t)b * N + (lvl - 1);
     const float *z = draft_logits + lrow * V;
-    const int32_t *cd = topk_draft + lrow * k;
-    // test order (every thread the same): draw order by key, or listing order
-    int ord[kMaxTopk];
-    float key[kMaxTopk];
-    for (int j = 0; j < k; ++j) {
-      ord[j] = j;
-      const int vd = min(max(cd[j], 0), V - 1);
-      key[j] = draft_uniforms ? z[vd] * inv_temp - logf(-logf(draft_uniforms[lrow * V + vd]))
-                              : -(float)j;
+    // the children: draft ids, tempered logits, keys and the uniforms of the
+    // tests this level can make (lane j), then their test order (thread 0);
+    // their loads go out with this thread's tempered logits of the level
+    const int cd = min(max(cdv, 0), V - 1);
+    float zc = 0.f, ud = 0.5f, uj = 0.f;
+    if (tid < k) {
+      zc = z[cd];
+      if (draft_uniforms) ud = draft_uniforms[lrow * V + cd];
+      uj = u[t + tid];
     }
-    for (int i = 1; i < k; ++i)
-      for (int j = i; j > 0; --j) {
-        const int a = ord[j - 1], c = ord[j];
-        const bool swap = key[c] > key[a] || (key[c] == key[a] && cd[c] < cd[a]);
-        if (!swap) break;
-        ord[j - 1] = c;
-        ord[j] = a;
-      }
-    // q = softmax(z / T) statistics over the draft vocabulary
+    float zr[kZ];
+#pragma unroll
+    for (int j = 0; j < kZ; ++j) {
+      const int v = tid + j * kAccThreads;
+      zr[j] = v < V ? z[v] * inv_temp : -INFINITY;
+    }
+    if (tid < k) {
+      zc *= inv_temp;
+      s_cd[tid] = cd;
+      s_zc[tid] = zc;
+      s_key[tid] = draft_uniforms ? zc - logf(-logf(ud)) : -(float)tid;
+      s_uc[tid] = uj;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      for (int j = 0; j < k; ++j) s_ord[j] = j;
+      for (int i = 1; i < k; ++i)
+        for (int j = i; j > 0; --j) {
+          const int a = s_ord[j - 1], c = s_ord[j];
+          const bool swap = s_key[c] > s_key[a] || (s_key[c] == s_key[a] && s_cd[c] < s_cd[a]);
+          if (!swap) break;
+          s_ord[j - 1] = c;
+          s_ord[j] = a;
+        }
+    }
+    // q = softmax(z / T) over the draft vocabulary: zr becomes exp(z/T - mx)
     float mx = -INFINITY;
-    for (int v = tid; v < V; v += 256) mx = fmaxf(mx, z[v] * inv_temp);
-    mx = block_max256(mx, red);
+#pragma unroll
+    for (int j = 0; j < kZ; ++j) mx = fmaxf(mx, zr[j]);
+    mx = acc_max(mx, red);  // its barriers also publish s_ord
     float se = 0.f;
-    for (int v = tid; v < V; v += 256) se += expf(z[v] * inv_temp - mx);
-    const float S = block_sum256(se, red);
+#pragma unroll
+    for (int j = 0; j < kZ; ++j) {
+      zr[j] = expf(zr[j] - mx);  // 0 past V
+      se += zr[j];
+    }
+    const float S = acc_sum(se, red);
     float R = 0.f;  // q mass of the rejected children
-    int gone[kMaxTopk];
-    int ngone = 0;
     bool took = false;
     for (int j = 0; j < k; ++j) {
-      const int rho = ord[j];
+      const int rho = s_ord[j];
       const int child = 1 + (lvl - 1) * k + rho;
-      const int vd = min(max(cd[rho], 0), V - 1);
-      const int x = tok[child];
-      const float q0v = expf(z[vd] * inv_temp - mx) / S;
+      const int vd = s_cd[rho];
+      const float q0v = expf(s_zc[rho] - mx) / S;
       const float qi = draft_uniforms ? q0v / (1.f - R) : 1.f;
-      const float rx = (x >= 0 && x < Vt) ? r[x] : 0.f;
-      const float ut = u[t++];
-      __syncthreads();  // every thread has read r[x] before it changes
+      const float rx = s_rd[vd];
+      const float ut = s_uc[j];
+      ++t;
+      __syncthreads();  // every thread has read rd(x) before it changes
       if (ut * qi <= rx / Z) {
         node = child;
         ++len;
@@ -459,59 +644,81 @@ __global__ __launch_bounds__(256) void k_accept_sample(
         break;
       }
       if (!draft_uniforms) {  // point mass on x: x leaves p
-        if (tid == 0 && x >= 0 && x < Vt) r[x] = 0.f;
+        if (tid == 0) s_rd[vd] = 0.f;
         Z -= rx;
         __syncthreads();
         continue;
       }
+      // rd <- (rd - Z q_i)^+.  A rejected x had r(x) / Z < q_i(x), so its rd
+      // is now 0 and stays 0 in later passes: leaving x out of q changes
+      // nothing further but the renormalisation 1 / (1 - R).
       const float scale = Z / (1.f - R);
       float dec = 0.f;
-      for (int v = tid; v < V; v += 256) {
-        bool out = false;
-        for (int g = 0; g < ngone; ++g) out |= gone[g] == v;
-        if (out) continue;
-        const int xt = d2t ? d2t[v] : v;
-        if (xt < 0 || xt >= Vt) continue;
-        const float old = r[xt];
-        const float nr = fmaxf(old - scale * (expf(z[v] * inv_temp - mx) / S), 0.f);
-        r[xt] = nr;
+#pragma unroll
+      for (int jj = 0; jj < kZ; ++jj) {
+        const int v = tid + jj * kAccThreads;
+        if (v >= V) continue;
+        const float old = s_rd[v];
+        const float nr = fmaxf(old - scale * (zr[jj] / S), 0.f);
+        s_rd[v] = nr;
         dec += old - nr;
       }
-      Z -= block_sum256(dec, red);
-      gone[ngone++] = vd;
+      Z -= acc_sum(dec, red);
       R += q0v;
     }
     if (!took) break;
   }
-  // one token from r: inverse CDF over target ids, contiguous per-thread slices
-  const int C = (Vt + 255) / 256, x0 = min(tid * C, Vt), x1 = min(x0 + C, Vt);
-  float cs = 0.f;
-  int lastnz = -1;
-  for (int x = x0; x < x1; ++x) {
-    cs += r[x];
-    if (r[x] > 0.f) lastnz = x;
+  // one token from the current p: mapped ids in draft-id order, then the rest;
+  // chunk sums added in order (the same float expression for a chunk's end
+  // and the next chunk's start), the owning wave walks its chunk
+  const int CV = ((V + kAccWaves - 1) / kAccWaves + 63) / 64 * 64;
+  const int d0 = min(wave * CV, V), d1 = min(d0 + CV, V);
+  float ci = 0.f;
+  int lasti = -1;
+  for (int v = d0 + lane; v < d1; v += 64) {
+    ci += s_rd[v];
+    if (s_rd[v] > 0.f) lasti = v;
   }
-  s_scan[tid] = cs;
+  ci = group_sum<64>(ci);
+  __syncthreads();
+  if (lane == 0) red[wave] = ci;
   if (tid == 0) s_pick = -1;
   __syncthreads();
-  float pre = 0.f;
-  for (int i = 0; i < tid; ++i) pre += s_scan[i];
   const float target = u[NU - 1] * Z;
-  if (pre <= target && target < pre + cs) {
-    float cum = pre;
-    int pick = x1 - 1;
-    for (int x = x0; x < x1; ++x) {
-      cum += r[x];
-      if (cum > target) {
-        pick = x;
-        break;
-      }
-    }
-    s_pick = pick;  // the slices' ranges [pre, pre + cs) tile the line: one thread only
+  float Mimg = 0.f, wi = 0.f, wn = 0.f;
+  for (int w = 0; w < kAccWaves; ++w) {
+    if (w == wave) wi = Mimg;
+    Mimg += red[w];
   }
-  const float lastf = block_max256((float)lastnz, red);  // also orders s_pick
+  if (target < Mimg) {
+    if (wi <= target && target < wi + red[wave]) {
+      const int e = acc_walk<1>(d0, d1, wi, target, [&](int v, float *a) {
+        a[0] = v < d1 ? s_rd[v] : 0.f;
+      });
+      if (lane == 0) s_pick = tgt(e >= 0 ? e : d1 - 1);
+    }
+  } else {
+    const float t2 = target - Mimg;
+    float tn = 0.f;
+    for (int w = 0; w < kAccWaves; ++w) {
+      if (w == wave) wn = tn;
+      tn += s_cn[w];
+    }
+    if (wn <= t2 && t2 < wn + s_cn[wave]) {
+      const int e = acc_walk<W>(c0, c1, wn, t2, [&](int x, float *a) {
+        loadp(x, a);
+#pragma unroll
+        for (int q = 0; q < W; ++q)
+          if (x + q >= c1 || in_img(x + q)) a[q] = 0.f;
+      });
+      const int ln = (int)group_max<64>((float)lastn);
+      if (lane == 0) s_pick = e >= 0 ? e : ln;
+    }
+  }
+  const int lo = (int)acc_max((float)lastn, red);   // its barriers publish s_pick
+  const int li = (int)acc_max((float)lasti, red);
   int pick = s_pick;
-  if (pick < 0) pick = (int)lastf;  // target at or past the total (rounding)
+  if (pick < 0) pick = lo >= 0 ? lo : (li >= 0 ? tgt(li) : -1);  // past the total (rounding)
   if (tid <= N) {
     int32_t *acc = accepted + (size_t)b * (N + 1);
     acc[tid] = tid < len ? tok[s_path[tid + 1]] : (tid == len ? pick : -1);
@@ -529,17 +736,29 @@ __global__ __launch_bounds__(256) void k_accept_sample(
   }
 }
 
+hipError_t accept_img(const int32_t *d2t, int V, int Vt, uint32_t *img, hipStream_t s) {
+  if (V > kAccMaxV || Vt > kAccMaxVt) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_build_img, dim3(1), dim3(kAccThreads), 0, s, d2t, V, Vt, img);
+  return hipGetLastError();
+}
+
 hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
                          const int32_t *retrieve, const int32_t *topk_draft,
                          const float *draft_logits, float inv_temp, const float *draft_uniforms,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
-                         float *resid, int32_t *accept_len, int32_t *accept_path,
+                         const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s) {
   if (B <= 0) return hipSuccess;
-  if (k > kMaxTopk || N > kMaxLayers || N + 1 > 256) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_accept_sample, dim3(B), dim3(256), 0, s, N, k, V, Vt, tokens, retrieve,
-                     topk_draft, draft_logits, inv_temp, draft_uniforms, d2t, target_probs,
-                     uniforms, resid, accept_len, accept_path, accepted);
+  if (k > kMaxTopk || N > kMaxLayers || V > kAccMaxV || Vt > kAccMaxVt) return hipErrorInvalidValue;
+  const bool vec = Vt % 4 == 0 && ((uintptr_t)target_probs & 15u) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_accept_sample<true>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
+                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_uniforms, d2t,
+                       target_probs, uniforms, img, accept_len, accept_path, accepted);
+  else
+    hipLaunchKernelGGL(k_accept_sample<false>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
+                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_uniforms, d2t,
+                       target_probs, uniforms, img, accept_len, accept_path, accepted);
   return hipGetLastError();
 }
 

@@ -32,7 +32,7 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
-      psum, cval, cidx, cz, resid, splitk, total;
+      psum, cval, cidx, cz, img, splitk, total;
   size_t splitk_floats;
   int nchmax, nwg, npos;
 };
@@ -72,7 +72,7 @@ Layout layout_of(const fe_config &c) {
   L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cz = take(B * N * (size_t)L.nwg * kMaxTopk * 4);  // z / T of sampled candidates
-  L.resid = take(B * (size_t)c.target_vocab * 4);    // acceptance: residual target distribution
+  L.img = take(((size_t)c.target_vocab + 31) / 32 * 4);  // target ids that d2t reaches
   // split-K slices of the batched GEMMs with narrow outputs: up to 8 slices of
   // the QKV rows (B * N at most, 256 per launch) over 128-column tiles
   {
@@ -150,6 +150,7 @@ struct fe_drafter {
   bool graph_mode = false;
   int attn_split = 0;  // 64-key chunks per attention work unit (0 = automatic)
   bool table_ready = false;  // rotary table built (first pass on the handle)
+  bool img_ready = false;    // bitmask of d2t's image built (first sampling acceptance)
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
   hipGraph_t graph = nullptr;
@@ -647,6 +648,9 @@ extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk
   if (topk < 1 || topk > c.max_topk) return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
   if (!(temperature > 0.f) || !(temperature < INFINITY) || !(1.0f / temperature < INFINITY))
     return fail(FE_E_INVALID, "temperature must be positive and finite");
+  if (c.draft_vocab > kAccSampleMaxV || c.target_vocab > kAccSampleMaxVt)
+    return fail(FE_E_UNSUPPORTED, "sampling acceptance needs draft_vocab <= %d and target_vocab <= %d",
+                kAccSampleMaxV, kAccSampleMaxVt);
   if (batch == 0) return FE_OK;
   if (!tokens || !retrieve || !topk_draft || !draft_logits || !target_probs || !uniforms ||
       !accept_len || !accept_path || !accepted)
@@ -655,10 +659,15 @@ extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk
                         uniforms, accept_len, accept_path, accepted};
   for (const void *q : ptrs)
     if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "acceptance arrays must be 4-byte aligned");
+  uint32_t *img = (uint32_t *)(h->ws + h->L.img);
+  if (!h->img_ready) {
+    FE_TRY(accept_img(h->w.d2t, c.draft_vocab, c.target_vocab, img, (hipStream_t)stream));
+    h->img_ready = true;
+  }
   FE_TRY(accept_sample(batch, c.n_layers, topk, c.draft_vocab, c.target_vocab, tokens, retrieve,
                        topk_draft, draft_logits, 1.0f / temperature, draft_uniforms, h->w.d2t,
-                       target_probs, uniforms, (float *)(h->ws + h->L.resid), accept_len,
-                       accept_path, accepted, (hipStream_t)stream));
+                       target_probs, uniforms, img, accept_len, accept_path, accepted,
+                       (hipStream_t)stream));
   return FE_OK;
 }
 
