@@ -368,10 +368,24 @@ __device__ __forceinline__ void wg_barrier() {
 }
 __device__ __forceinline__ int ring_slot(int row, int piece) { return row * 8 + (piece ^ ((row >> 1) & 7)); }
 
+// Epilogues with kSliced = true cover many row blocks (and groups) in one
+// launch: grid z enumerates them and slice() moves A, M and the epilogue's
+// outputs to block z before anything else runs.
+template <class E, class = void> struct SlicedEpi { static constexpr bool value = false; };
+template <class E> struct SlicedEpi<E, decltype((void)E::kSliced)> {
+  static constexpr bool value = E::kSliced;
+};
+
 template <typename T, int NTW, int WN, int S, class Epi>
 __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
                                                   int M, int K, Epi epi, float *__restrict__ splitp,
                                                   int ldp) {
+  if constexpr (SlicedEpi<Epi>::value) {
+    const T *a = A;
+    epi.slice(blockIdx.z, 64 * (4 / WN), a, M);
+    A = a;
+    if (M <= 0) return;  // the whole workgroup: past the last row block
+  }
   constexpr int E = Elt<T>::kPer16B;  // elements per 16-byte piece
   constexpr int KC = 8 * E;           // elements of K per chunk
   constexpr int WM = 4 / WN;
@@ -752,6 +766,77 @@ template <typename T> struct EpiKvCache {
   }
 };
 
+// Row-block slices of the cache update's GEMMs (bf16, many rows per launch).
+// Fusion FC: EpiStore with the embedding gather of the block's own rows.
+struct TileStore : EpiStore<bf16_t> {
+  static constexpr bool kSliced = true;
+  int lda;
+  __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
+    const int m0 = z * mrows;
+    A += (size_t)m0 * lda;
+    M = min(mrows, M - m0);
+    out += (size_t)m0 * ldo;
+    if (embed) {
+      tokens += m0;
+      gather_out += (size_t)m0 * ld_gather;
+      B = M;
+    }
+  }
+};
+// Input FC into fp32 rows.
+struct TileF32 {
+  static constexpr bool kRowStream = true, kSplitK = false, kSliced = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
+  const bf16_t *w;
+  int ldw, nvcols;
+  float *out;
+  long ldo;
+  int lda;
+  __device__ const bf16_t *wrow(int c) const { return w + (size_t)c * ldw; }
+  __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
+    const int m0 = z * mrows;
+    A += (size_t)m0 * lda;
+    M = min(mrows, M - m0);
+    out += (size_t)m0 * ldo;
+  }
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
+    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
+      const int m = idx / span, c = idx % span;
+      if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = tile[m * ldt + c];
+    }
+  }
+};
+// K/V cache rows of every layer: slice z = layer * row blocks + block, A
+// holds the layers' normalised rows a_layer_stride elements apart.
+struct KvGroupArgs {
+  int nlayers, nblocks, lda;
+  long a_layer_stride;
+  KvCacheArgs layer[kMaxLayers];
+};
+struct TileKv {
+  static constexpr bool kRowStream = true, kSplitK = false, kSliced = true;
+  using Pre = NoPre;
+  __device__ Pre prefetch(int, int, int) const { return {}; }
+  static constexpr int kMidNtw = 0, kMidNtwMin = 1;
+  EpiKvCache<bf16_t> cur;
+  int nvcols;
+  const KvGroupArgs *g;  // device copy of the per-layer arguments
+  __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
+    const int l = z / g->nblocks, m0 = (z % g->nblocks) * mrows;
+    cur.a = g->layer[l];
+    cur.a.positions += m0;
+    cur.a.dst_rows += m0;
+    A += l * g->a_layer_stride + (size_t)m0 * g->lda;
+    M = min(mrows, M - m0);
+  }
+  __device__ const bf16_t *wrow(int c) const { return cur.wrow(c); }
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &p) const {
+    cur.finish(tile, ldt, M, c0, span, p);
+  }
+};
+
 template <typename T> struct EpiSwiglu {
   static constexpr bool kRowStream = true, kSplitK = false;
   using Pre = NoPre;
@@ -1094,6 +1179,70 @@ hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs
   }
   EpiKvCache<float> e{a, nv};
   return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, a.d, e, nullptr, s, ss);
+}
+
+// Many rows at once (bf16): 128 x 64 output tiles, grid z over 128-row
+// blocks (and layers), no split of K.
+constexpr int kTileNtw = 2, kTileWn = 2, kTileStages = 3, kTileRows = 64 * (4 / kTileWn),
+              kTileCols = 16 * kTileNtw * kTileWn;
+
+hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, int ncols, void *out,
+                           int ldo, const void *embed, const int32_t *tokens, int vocab,
+                           void *gather_out, int ld_gather, int d, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  TileStore e;
+  static_cast<EpiStore<bf16_t> &>(e) = EpiStore<bf16_t>{(const bf16_t *)W, K, ncols, (bf16_t *)out,
+                                                        ldo, (const bf16_t *)embed, tokens, vocab,
+                                                        (bf16_t *)gather_out, ld_gather, d, M};
+  e.lda = lda;
+  const dim3 grid((ncols + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
+  hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileStore>), grid, dim3(256),
+                     0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
+  return hipGetLastError();
+}
+
+hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
+                           long ldo, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  const TileF32 e{(const bf16_t *)W, K, ncols, out, ldo, lda};
+  const dim3 grid((ncols + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
+  hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileF32>), grid, dim3(256),
+                     0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
+  return hipGetLastError();
+}
+
+size_t kv_group_args_bytes() { return sizeof(KvGroupArgs); }
+
+__global__ void k_put_kv_args(KvGroupArgs a, KvGroupArgs *dst) {
+  static_assert(sizeof(KvGroupArgs) % 4 == 0, "copied as 32-bit words");
+  const uint32_t *src = reinterpret_cast<const uint32_t *>(&a);
+  uint32_t *d = reinterpret_cast<uint32_t *>(dst);
+  for (int i = threadIdx.x; i < (int)(sizeof(KvGroupArgs) / 4); i += blockDim.x) d[i] = src[i];
+}
+
+hipError_t gemm_kv_rows(const void *A, int lda, long a_layer_stride, int M, int nlayers,
+                        const KvCacheArgs *layers, KvGroupArgs *dev_args, hipStream_t s) {
+  if (M <= 0 || nlayers <= 0) return hipSuccess;
+  if (nlayers > kMaxLayers) return hipErrorInvalidValue;
+  KvGroupArgs h{};
+  h.nlayers = nlayers;
+  h.nblocks = (M + kTileRows - 1) / kTileRows;
+  h.lda = lda;
+  h.a_layer_stride = a_layer_stride;
+  for (int l = 0; l < nlayers; ++l) h.layer[l] = layers[l];
+  // the arguments travel as a kernel argument (captured at launch) into
+  // device memory, where the GEMM's workgroups read their layer's part
+  hipLaunchKernelGGL(k_put_kv_args, dim3(1), dim3(64), 0, s, h, dev_args);
+  const hipError_t ec = hipGetLastError();
+  if (ec != hipSuccess) return ec;
+  TileKv e{};
+  e.cur = EpiKvCache<bf16_t>{layers[0], 2 * layers[0].Hkv * layers[0].D};
+  e.nvcols = e.cur.nvcols;
+  e.g = dev_args;
+  const dim3 grid((e.nvcols + kTileCols - 1) / kTileCols, 1, h.nblocks * nlayers);
+  hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileKv>), grid, dim3(256), 0,
+                     s, (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, e, nullptr, 0);
+  return hipGetLastError();
 }
 
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,

@@ -249,6 +249,22 @@ struct KvCacheArgs {
 hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs &a,
                         hipStream_t s, const SplitScratch *ss = nullptr);
 
+// Many-row bf16 GEMMs of the cache update: 128 x 64 output tiles over a 2-D
+// grid (row blocks in grid z), K unsplit.  gemm_store_rows / gemm_resid_rows
+// behave as gemm_store / gemm_resid (no residual, sums of squares or gain
+// copies); gemm_kv_rows runs every layer's K/V projection at once: A holds
+// layer l's normalised rows at A + l * a_layer_stride, and dev_args is device
+// memory for the per-layer arguments (copied there on the stream first).
+struct KvGroupArgs;
+hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, int ncols, void *out,
+                           int ldo, const void *embed, const int32_t *tokens, int vocab,
+                           void *gather_out, int ld_gather, int d, hipStream_t s);
+hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
+                           long ldo, hipStream_t s);
+hipError_t gemm_kv_rows(const void *A, int lda, long a_layer_stride, int M, int nlayers,
+                        const KvCacheArgs *layers, KvGroupArgs *dev_args, hipStream_t s);
+size_t kv_group_args_bytes();
+
 // s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,
                        const void *w_gate, const void *w_up, int I, void *s_out, int lds,

@@ -87,19 +87,25 @@ Layout layout_of(const fe_config &c) {
 
 // Workspace of fe_kv_update for chunks of C rows: the fused inputs, x_0 in
 // fp32, its per-layer RMSNorm, and split-K slices for the 256-row launches.
+// Chunks of at least kTiledRows rows (bf16) take the 2-D tiled GEMMs, with
+// every layer's normalised rows side by side and one launch for all layers.
+constexpr int kTiledRows = 128;
+
 struct UpdLayout {
-  size_t cat, X, an, splitk, total;
+  size_t cat, X, an, kvargs, splitk, total;
   size_t splitk_floats;
 };
 
 UpdLayout upd_layout_of(const fe_config &c, size_t C) {
   UpdLayout U{};
   const size_t d = c.hidden, es = es_of(c), kvd = (size_t)c.n_kv_heads * c.head_dim;
+  const size_t nan_ = (c.dtype == FE_BF16 && C >= (size_t)kTiledRows) ? c.n_layers : 1;
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
   U.cat = take(C * 2 * d * es);
   U.X = take(C * d * 4);
-  U.an = take(C * d * es);
+  U.an = take(nan_ * C * d * es);
+  U.kvargs = take(kv_group_args_bytes());
   const size_t rows = std::min<size_t>(kGemmMaxRows, C);
   const size_t cols = (std::max<size_t>(2 * kvd, d) + 127) / 128 * 128;
   U.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
@@ -604,6 +610,26 @@ extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *fea
   const SplitScratch ss{(float *)(ws + U.splitk), U.splitk_floats};
   for (int r0 = 0; r0 < n_rows; r0 += C) {
     const int Mc = std::min(C, n_rows - r0);
+    if (dt && Mc >= kTiledRows) {
+      // many rows: one launch per stage over 128 x 64 output tiles, and one
+      // K/V launch for every layer (matrix-core bound from a few hundred rows)
+      FE_TRY(gemm_store_rows((const char *)features + (size_t)r0 * F * d * es, F * d, Mc, F * d,
+                             h->w.w_fuse, d, cat, 2 * d, h->w.embed, tokens + r0, c.target_vocab,
+                             cat + (size_t)d * es, 2 * d, d, s));
+      FE_TRY(gemm_resid_rows(cat, 2 * d, Mc, 2 * d, h->w.w_in, d, X, d, s));
+      KvCacheArgs la[kMaxLayers];
+      for (int l = 0; l < c.n_layers; ++l) {
+        const fe_layer_weights &lw = h->layers[l];
+        FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an + (size_t)l * C * d * es, d,
+                            c.rms_eps, s));
+        la[l] = KvCacheArgs{lw.wk, lw.wv, d, c.head_dim, c.n_kv_heads, positions + r0,
+                            dst_rows + r0, (long)cache->rows, c.max_prefix,
+                            (const float *)(h->ws + h->L.rope), cache->k[l], cache->v[l]};
+      }
+      FE_TRY(gemm_kv_rows(an, d, (long)C * d, Mc, c.n_layers, la,
+                          (KvGroupArgs *)(ws + U.kvargs), s));
+      continue;
+    }
     // stage by stage over the chunk, so that each weight matrix is read by
     // consecutive launches
     for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {

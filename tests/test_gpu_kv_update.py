@@ -100,14 +100,15 @@ def _run(cfg, up, chunk_rows, sample=None, seed=0):
 
 CASES = [
     # (config, accepted per sequence, chunk rows): the row-streaming path
-    # (<= 4 rows), one batched launch, several 256-row launches with a ragged
-    # tail, and several chunks
+    # (<= 4 rows), one batched launch, the tiled many-row GEMMs (bf16 chunks
+    # of 128 rows or more), several 256-row launches, and several chunks
     (C.SMALL_GQA_BF16, [1], 1024),
     (C.SMALL_GQA_BF16, [2, 1, 1], 1024),
     (C.SMALL_GQA_BF16, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
     (C.SMALL_GQA_F32, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
-    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 1024),
-    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 100),
+    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 1024),   # 2-D tiled GEMMs, ragged row block
+    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 100),    # 100-row chunks: the 256-row launches
+    (C.SMALL_GQA_BF16, [40] * 8 + [7], 200),          # tiled chunks of 200 and 127 rows
     (C.TINY_F32_B1, [3] * 100 + [1], 40),
 ]
 
