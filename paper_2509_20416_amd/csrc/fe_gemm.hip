@@ -737,30 +737,51 @@ template <typename T> struct EpiKvCache {
     if (c < kvd) return (const T *)a.wk + (size_t)((c / a.D) * a.D + rope_dim(c % a.D, a.D)) * a.d;
     return (const T *)a.wv + (size_t)(c - kvd) * a.d;
   }
+  // Elements go KB at a time: every load (row destination, position, rotary
+  // factors) of the batch is issued before its stores, which the compiler
+  // could not move loads across.
+  static constexpr int KB = 8;
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     const int kvd = a.Hkv * a.D, D = a.D;
     const float qnan = __int_as_float(0x7fc00000);
-    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
-      const int m = idx / span, c = idx % span, vc = c0 + c;
-      if (vc >= nvcols) continue;
-      const long dst = a.dst_rows[m];
-      if (dst < 0 || dst >= a.cache_rows) continue;  // nowhere to write
-      const int pos = a.positions[m];
-      const bool bad = pos < 0 || pos >= a.pos_limit;
-      const float val = tile[m * ldt + c];
-      if (vc < kvd) {
-        const int h = vc / D, cc = vc % D, dd = rope_dim(cc, D);
-        float o = qnan;
-        if (!bad) {
-          const float pv = tile[m * ldt + (c ^ 8)];
-          const int pm = 8 * (cc >> 4) + (cc & 7);
-          const float c_ = a.rope[((size_t)pos * (D / 2) + pm) * 2];
-          const float s_ = a.rope[((size_t)pos * (D / 2) + pm) * 2 + 1];
-          o = (cc & 8) ? (val * c_ + pv * s_) : (val * c_ - pv * s_);
+    const int n = M * span;
+    for (int i0 = threadIdx.x; i0 < n; i0 += KB * blockDim.x) {
+      int m[KB], pos[KB];
+      long dst[KB];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const int idx = min(i0 + j * (int)blockDim.x, n - 1);
+        m[j] = idx / span;
+        dst[j] = a.dst_rows[m[j]];
+        pos[j] = a.positions[m[j]];
+      }
+      float cs[KB], sn[KB];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const int idx = min(i0 + j * (int)blockDim.x, n - 1);
+        const int cc = (c0 + idx % span) % D;
+        const int pm = 8 * (cc >> 4) + (cc & 7);
+        const int pc = min(max(pos[j], 0), a.pos_limit - 1);
+        cs[j] = a.rope[((size_t)pc * (D / 2) + pm) * 2];
+        sn[j] = a.rope[((size_t)pc * (D / 2) + pm) * 2 + 1];
+      }
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const int idx = i0 + j * (int)blockDim.x;
+        if (idx >= n) break;
+        const int c = idx % span, vc = c0 + c;
+        if (vc >= nvcols) continue;
+        if (dst[j] < 0 || dst[j] >= a.cache_rows) continue;  // nowhere to write
+        const bool bad = pos[j] < 0 || pos[j] >= a.pos_limit;
+        const float val = tile[m[j] * ldt + c];
+        if (vc < kvd) {
+          const int h = vc / D, cc = vc % D, dd = rope_dim(cc, D);
+          const float pv = tile[m[j] * ldt + (c ^ 8)];
+          const float o = bad ? qnan : ((cc & 8) ? (val * cs[j] + pv * sn[j]) : (val * cs[j] - pv * sn[j]));
+          ((T *)a.k_cache)[(size_t)dst[j] * kvd + (size_t)h * D + dd] = Elt<T>::from_f(o);
+        } else {
+          ((T *)a.v_cache)[(size_t)dst[j] * kvd + (vc - kvd)] = Elt<T>::from_f(bad ? qnan : val);
         }
-        ((T *)a.k_cache)[(size_t)dst * kvd + (size_t)h * D + dd] = Elt<T>::from_f(o);
-      } else {
-        ((T *)a.v_cache)[(size_t)dst * kvd + (vc - kvd)] = Elt<T>::from_f(bad ? qnan : val);
       }
     }
   }

@@ -84,6 +84,7 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // candidates its lanes hold (k rounds of butterfly max over ordering keys, no
 // block barrier), then wave 0 selects the top-k of the 4k wave winners and
 // writes them.
+template <bool SAMPLED>
 __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
                                                     const float *__restrict__ psum,
                                                     const float *__restrict__ cval,
@@ -143,8 +144,8 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
   S = group_sum<64>(S);
   if (lane == 0) sv[wave] = S;
   // sampled candidates: their z / T, loaded beside the keys
-  float czv[CAP];
-  if (cz) {
+  float czv[SAMPLED ? CAP : 1];
+  if constexpr (SAMPLED) {
 #pragma unroll
     for (int j = 0; j < CAP; ++j) {
       const int c = min(tid + 256 * j, ncand - 1);
@@ -160,27 +161,32 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
     float zb = -INFINITY;
 #pragma unroll
     for (int j = 0; j < CAP; ++j) {
-      if (cz && key[j] == best && best != kNoKey) zb = czv[j];
+      if constexpr (SAMPLED) {
+        if (key[j] == best && best != kNoKey) zb = czv[j];
+      }
       key[j] = key[j] == best ? kNoKey : key[j];
     }
-    if (cz) zb = group_max<64>(zb);  // one lane held the winner
+    if constexpr (SAMPLED) zb = group_max<64>(zb);  // one lane held the winner
     if (lane == 0) {
       s_key[wave][r] = best;
-      s_z[wave][r] = zb;
+      if constexpr (SAMPLED) s_z[wave][r] = zb;
     }
   }
   __syncthreads();
   if (wave == 0) {
     const float Ssum = (sv[0] + sv[1]) + (sv[2] + sv[3]);
     uint64_t k = lane < 4 * topk ? s_key[lane / topk][lane % topk] : kNoKey;
-    const float kz = lane < 4 * topk ? s_z[lane / topk][lane % topk] : -INFINITY;
+    const float kz = SAMPLED && lane < 4 * topk ? s_z[lane / topk][lane % topk] : -INFINITY;
     uint64_t mine = kNoKey;
     float mz = -INFINITY;
     for (int r = 0; r < topk; ++r) {
       const uint64_t best = wave_max_u64(k);
       // the lane holding the winner (keys are distinct) gives its z / T
-      const uint64_t hit = __builtin_amdgcn_ballot_w64(k == best && best != kNoKey);
-      const float bz = hit ? __shfl(kz, __builtin_ctzll(hit)) : -INFINITY;
+      float bz = -INFINITY;
+      if constexpr (SAMPLED) {
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(k == best && best != kNoKey);
+        bz = hit ? __shfl(kz, __builtin_ctzll(hit)) : -INFINITY;
+      }
       k = k == best ? kNoKey : k;
       if (lane == r) {
         mine = best;
@@ -189,12 +195,12 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
     }
     const int i = topk_key_id(mine);
     const bool valid = lane < topk && mine != kNoKey && i >= 0 && i < V;  // none left (NaN row): -1
-    const float z = cz ? mz : topk_key_value(mine);
+    const float z = SAMPLED ? mz : topk_key_value(mine);
     // listing position: key order, or for sampled candidates the order of z / T
     // (larger first, lower id on ties, NaN after numbers, invalid entries last
     // in lane order): the rank of the lane's ordering key among the winners
     int pos = lane;
-    if (cz) {
+    if constexpr (SAMPLED) {
       const uint64_t zk = valid ? topk_key(z, i) : kNoKey;
       pos = 0;
       for (int t = 0; t < topk; ++t) {
@@ -217,8 +223,12 @@ hipError_t topk_merge(const float *part_max, const float *part_sum, const float 
                       int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
                       hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, s, part_max, part_sum, cand_val,
-                     cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
+  if (cand_z)
+    hipLaunchKernelGGL(k_topk_merge<true>, dim3(rows), dim3(256), 0, s, part_max, part_sum,
+                       cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
+  else
+    hipLaunchKernelGGL(k_topk_merge<false>, dim3(rows), dim3(256), 0, s, part_max, part_sum,
+                       cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
   return hipGetLastError();
 }
 
