@@ -309,7 +309,7 @@ __device__ __forceinline__ void ring_dma16(const void *src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory");
 }
 
-template <int D, int GH, int DEPTH>
+template <int D, int GH, int DEPTH, int NCX>
 __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
                                                  const bf16_t *__restrict__ Vc,
                                                  const int32_t *__restrict__ cu,
@@ -319,8 +319,10 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
                                                  float *__restrict__ part, int nch, int nch_ld,
                                                  int cpw, bf16_t *__restrict__ out, int Hq,
                                                  int Hkv, const float *__restrict__ rope,
-                                                 int cascade, int nseq, int persist) {
+                                                 int cascade, int nseq, int persist,
+                                                 int csplit) {
   static_assert(D == 64 || D == 128, "head dims 64 and 128");
+  static_assert(NCX <= kMaxLayers, "cascade keys per layer");
   constexpr int NKC = D / 32;          // 32-dim steps of QK^T
   constexpr int NDT = D / 16;          // 16-dim tiles of the value product
   constexpr int VPR = D / 8;           // 16-byte pieces per K or V row
@@ -346,14 +348,14 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
 
   // One piece of work: prefix chunks [ch0, ch0 + nchunk) (kAttnChunk keys
   // each) of sequence b for the query heads of column col (KV head c, head
-  // group hg), plus the cascade keys when ch0 == 0.  The result goes to the
-  // output when `whole`, else to partial slot `slot`; npieces > 0 (given to
-  // the first piece of a segment) is stored as the segment's partial count.
+  // group hg), plus the (at most NCX) cascade keys when casc.  The result goes
+  // to the output when `whole`, else to partial slot `slot`; npieces > 0
+  // (given to the first piece of a segment) is stored as the segment's
+  // partial count.
   auto unit = [&](const int b, const int col, const int ch0, const int nchunk, const int slot,
-                  const bool whole, const int npieces) {
+                  const bool whole, const int npieces, const bool casc) {
   const int c = col / ngrp, hg = col % ngrp;
   const int h0 = c * G + hg * GH;
-  const bool casc = ch0 == 0;
 
   // Loads that do not depend on the prefix bounds go first, so their latency
   // overlaps the read of cu: q (B-operand layout), and in chunk 0 the cascade
@@ -370,14 +372,14 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
   // cascade step: lane l < D/2 holds the rotary pair (m, m + D/2), m = l
   const int m2 = min(lane, HD - 1);
   const bool cact = lane < HD;
-  float kj[kMaxLayers][2], vj[kMaxLayers][2], qc[GH][2];
+  float kj[NCX][2], vj[NCX][2], qc[GH][2];
   if (casc) {
 #pragma unroll
     for (int gh = 0; gh < GH; ++gh)
 #pragma unroll
       for (int e = 0; e < 2; ++e) qc[gh][e] = q[((size_t)b * Hq + h0 + gh) * D + m2 + e * HD];
 #pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) {
+    for (int j = 0; j < NCX; ++j) {
       const size_t off = (((size_t)b * nctx + min(j, nctx - 1)) * Hkv + c) * D + m2;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
@@ -398,10 +400,10 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
 #pragma unroll
     for (int w = 0; w < 4; ++w)
       rq[kc][w] = *reinterpret_cast<const f32x4 *>(rope + ((size_t)pos_q * HD + 32 * kc + 8 * g) * 2 + 4 * w);
-  float2 rcj[kMaxLayers], rcq;
+  float2 rcj[NCX], rcq;
   if (casc) {
 #pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j)
+    for (int j = 0; j < NCX; ++j)
       rcj[j] = *reinterpret_cast<const float2 *>(rope + ((size_t)(cascade ? P + min(j, nctx - 1) : P) * HD + m2) * 2);
     rcq = *reinterpret_cast<const float2 *>(rope + ((size_t)pos_q * HD + m2) * 2);
   }
@@ -580,28 +582,28 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
   if (casc) {
     // rotate-half on the pair (m, m + D/2); all nctx-bound work is masked rather
     // than branched, so the reductions of different keys and heads interleave
-    float kr2[kMaxLayers][2];
+    float kr2[NCX][2];
 #pragma unroll
-    for (int j = 0; j < kMaxLayers; ++j) {
+    for (int j = 0; j < NCX; ++j) {
       kr2[j][0] = kj[j][0] * rcj[j].x - kj[j][1] * rcj[j].y;
       kr2[j][1] = kj[j][1] * rcj[j].x + kj[j][0] * rcj[j].y;
     }
     constexpr int HB = GH < 4 ? GH : 4;  // heads per batch of reductions
 #pragma unroll
     for (int g0 = 0; g0 < GH; g0 += HB) {
-    float sj[HB][kMaxLayers];
+    float sj[HB][NCX];
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) {
       const float qa = qc[g0 + hb][0], qb = qc[g0 + hb][1];
       const float q0 = cact ? (qa * rcq.x - qb * rcq.y) * qscale : 0.f;
       const float q1 = cact ? (qb * rcq.x + qa * rcq.y) * qscale : 0.f;
 #pragma unroll
-      for (int j = 0; j < kMaxLayers; ++j) sj[hb][j] = q0 * kr2[j][0] + q1 * kr2[j][1];
+      for (int j = 0; j < NCX; ++j) sj[hb][j] = q0 * kr2[j][0] + q1 * kr2[j][1];
     }
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
-      for (int j = 0; j < kMaxLayers; ++j) {
+      for (int j = 0; j < NCX; ++j) {
         const float t = group_sum<64>(sj[hb][j]);
         sj[hb][j] = j < nctx ? t : -INFINITY;
       }
@@ -610,10 +612,10 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
       const int gh = g0 + hb;
       float mc = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < kMaxLayers; ++j) mc = fmaxf(mc, sj[hb][j]);
+      for (int j = 0; j < NCX; ++j) mc = fmaxf(mc, sj[hb][j]);
       float L = 0.f, o[2] = {0.f, 0.f};
 #pragma unroll
-      for (int j = 0; j < kMaxLayers; ++j) {
+      for (int j = 0; j < NCX; ++j) {
         const float pj = sexp2(sj[hb][j], mc);
         L += pj;
 #pragma unroll
@@ -676,7 +678,15 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     const int b = blockIdx.z, col = blockIdx.x, ch = blockIdx.y;
     const int P = cu[b + 1] - cu[b];
     const int nv = max(1, min((P + span - 1) / span, nch));
-    if (ch < nv) unit(b, col, ch * cpw, cpw, ch, nv == 1, 0);
+    if (csplit) {
+      // the cascade keys as a unit of their own (grid y = nch), off the
+      // prefix units' critical path; every sequence leaves nv + 1 partials,
+      // the cascade's last
+      if (ch == nch) unit(b, col, 0, 0, nv, false, 0, true);
+      else if (ch < nv) unit(b, col, ch * cpw, cpw, ch, false, 0, false);
+      return;
+    }
+    if (ch < nv) unit(b, col, ch * cpw, cpw, ch, nv == 1, 0, ch == 0);
     return;
   }
   // Persistent: a grid of resident waves.  The chunks of all (sequence, column)
@@ -733,7 +743,7 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     const long S = x - ch0;
     const int slot = (int)(starts(x) - starts(S));
     const int np = ch0 == 0 ? (int)(starts(S + nch_b - 1) - starts(S)) + 1 : 0;
-    unit(b, col, ch0, n, slot, false, np);
+    unit(b, col, ch0, n, slot, false, np, ch0 == 0);
     x += n;
   }
 }
@@ -742,7 +752,7 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
 // ---- chunk merge (second launch) -------------------------------------------------
 // A sequence whose prefix spans several workgroups leaves one partial per
 // workgroup: o (scaled to that workgroup's max), max and sum per head.  This
-// launch combines them in chunk order, 16 per round trip.  Sequences that fit
+// launch combines them in chunk order, 32 per round trip.  Sequences that fit
 // one workgroup wrote their rows directly and are skipped.  Keeping the merge in
 // its own launch means no workgroup ever waits on another: the kernel boundary
 // publishes the partials once, where per-workgroup device-scope fences would
@@ -751,19 +761,20 @@ template <typename T, bool LOG2>
 __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ part, int nch_ld,
                                                     const int32_t *__restrict__ cu, int span,
                                                     int nwg, T *__restrict__ out, int Hq, int D,
-                                                    int counted) {
+                                                    int counted, int csplit) {
   const int b = blockIdx.y;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= Hq * D / 2) return;
   const int h = (2 * idx) / D, e = (2 * idx) % D;
   // partials of (b, h): one per span (sequences within one span wrote their
-  // rows directly), or as counted by the persistent attention
+  // rows directly) and, with csplit, the cascade keys' one after them, or as
+  // counted by the persistent attention
   int nv;
   if (counted) {
     nv = (int)part[(size_t)gridDim.y * Hq * nch_ld * (D + 2) + (size_t)b * Hq + h];
   } else {
     const int P = cu[b + 1] - cu[b];
-    nv = max(1, min((P + span - 1) / span, nwg));
+    nv = max(1, min((P + span - 1) / span, nwg)) + csplit;
     if (nv == 1) return;
   }
   const float *po = part + ((size_t)b * Hq + h) * nch_ld * D + e;
@@ -772,24 +783,25 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ pa
     return m == -INFINITY ? 0.f : (LOG2 ? __builtin_amdgcn_exp2f(m - M) : expf(m - M));
   };
   float M = -INFINITY, L = 0.f, ax = 0.f, ay = 0.f;
-  for (int c0 = 0; c0 < nv; c0 += 16) {
-    float2 ov[16], ml[16];
+  constexpr int R = 32;  // partials per round trip
+  for (int c0 = 0; c0 < nv; c0 += R) {
+    float2 ov[R], ml[R];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
+    for (int u = 0; u < R; ++u) {
       const int k = min(c0 + u, nv - 1);
       ov[u] = *reinterpret_cast<const float2 *>(po + (size_t)k * D);
       ml[u] = *reinterpret_cast<const float2 *>(pml + 2 * k);
     }
     float Mn = M;
 #pragma unroll
-    for (int u = 0; u < 16; ++u)
+    for (int u = 0; u < R; ++u)
       if (c0 + u < nv) Mn = fmaxf(Mn, ml[u].x);
     const float rr = ex(M, Mn);
     L *= rr;
     ax *= rr;
     ay *= rr;
 #pragma unroll
-    for (int u = 0; u < 16; ++u)
+    for (int u = 0; u < R; ++u)
       if (c0 + u < nv) {
         const float w = ex(ml[u].x, Mn);
         L += w * ml[u].y;
@@ -841,7 +853,8 @@ template <int D>
 static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, const float *q,
                              const float *knew, const float *vnew, int nctx, float *part, int nch,
                              int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
-                             const float *rope, int cascade, int *persisted, hipStream_t s) {
+                             const float *rope, int cascade, int *persisted, int *csplit,
+                             hipStream_t s) {
   const int G = Hq / Hkv;
   // query heads per wave (the MFMA tiles have 16 columns; more than 8 heads
   // would spill the cascade step's registers)
@@ -852,16 +865,23 @@ static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, co
   const int waves = resident_waves();
   const int persist = B <= 256 && (long)B * ncols * nwg > waves ? 1 : 0;
   *persisted = persist;
-  const dim3 grid = persist ? dim3(waves) : dim3(ncols, nwg, B);
+  // a launch whose partials are merged anyway gives the cascade keys units of
+  // their own (one more partial slot per sequence)
+  const int split = !persist && nwg > 1 ? 1 : 0;
+  *csplit = split;
+  const dim3 grid = persist ? dim3(waves) : dim3(ncols, nwg + split, B);
   // a span of at most 4 stages is requested whole by the ring's prologue
   const bool short_span = cpw * (kAttnChunk / 16) <= 4;
-#define FE_ATTN(GHV, DEP)                                                                        \
-  hipLaunchKernelGGL((k_attn_mma<D, GHV, DEP>), grid, dim3(64), 0, s, (const bf16_t *)K,         \
+#define FE_ATTN(GHV, DEP, NCXV)                                                                  \
+  hipLaunchKernelGGL((k_attn_mma<D, GHV, DEP, NCXV>), grid, dim3(64), 0, s, (const bf16_t *)K,   \
                      (const bf16_t *)V, cu, q, knew, vnew, nctx, part, nwg, nch_ld, cpw,         \
-                     (bf16_t *)out, Hq, Hkv, rope, cascade, B, persist)
+                     (bf16_t *)out, Hq, Hkv, rope, cascade, B, persist, split)
+#define FE_ATTN_NCX(GHV, DEP)                                                                    \
+  if (nctx <= 8) FE_ATTN(GHV, DEP, 8);                                                           \
+  else FE_ATTN(GHV, DEP, kMaxLayers)
 #define FE_ATTN_GH(GHV)                                                                          \
-  if (short_span) FE_ATTN(GHV, 5);                                                               \
-  else FE_ATTN(GHV, 4)
+  if (short_span) { FE_ATTN_NCX(GHV, 5); }                                                       \
+  else { FE_ATTN_NCX(GHV, 4); }
   switch (GH) {
     case 8: FE_ATTN_GH(8); break;
     case 4: FE_ATTN_GH(4); break;
@@ -869,6 +889,7 @@ static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, co
     default: FE_ATTN_GH(1); break;
   }
 #undef FE_ATTN_GH
+#undef FE_ATTN_NCX
 #undef FE_ATTN
   return hipGetLastError();
 }
@@ -891,12 +912,13 @@ hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, co
   if (B <= 0) return hipSuccess;
   if (cpw < 1) cpw = 1;
   hipError_t e;
-  int persisted = 0;
+  int persisted = 0, csplit = 0;
+  if (nctx < 1 || nctx > kMaxLayers) return hipErrorInvalidValue;
   if (dt)
     e = D == 128 ? attn_mma_t<128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                   Hq, Hkv, rope, cascade, &persisted, s)
+                                   Hq, Hkv, rope, cascade, &persisted, &csplit, s)
                  : attn_mma_t<64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                  Hq, Hkv, rope, cascade, &persisted, s);
+                                  Hq, Hkv, rope, cascade, &persisted, &csplit, s);
   else
     e = D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
                                       B, Hq, Hkv, s)
@@ -908,10 +930,10 @@ hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, co
   const dim3 grid((Hq * D / 2 + 255) / 256, B);
   if (dt)
     hipLaunchKernelGGL((k_attn_merge<bf16_t, true>), grid, dim3(256), 0, s, part, nch_ld, cu,
-                       kAttnChunk * cpw, nwg, (bf16_t *)out, Hq, D, persisted);
+                       kAttnChunk * cpw, nwg, (bf16_t *)out, Hq, D, persisted, csplit);
   else
     hipLaunchKernelGGL((k_attn_merge<float, false>), grid, dim3(256), 0, s, part, nch_ld, cu,
-                       kAttnChunk * cpw, nwg, (float *)out, Hq, D, 0);
+                       kAttnChunk * cpw, nwg, (float *)out, Hq, D, 0, 0);
   return hipGetLastError();
 }
 

@@ -130,6 +130,15 @@ __device__ __forceinline__ void accum_staged(const T *__restrict__ A, int lda, c
   }
 }
 
+// Epilogues with kSliced = true cover many row blocks (and groups) in one
+// launch: a grid dimension (z for k_gemm_mid, y for k_gemm) enumerates them
+// and slice() moves A, M and the epilogue's outputs to its block before
+// anything else runs.
+template <class E, class = void> struct SlicedEpi { static constexpr bool value = false; };
+template <class E> struct SlicedEpi<E, decltype((void)E::kSliced)> {
+  static constexpr bool value = E::kSliced;
+};
+
 // ---------------------------------------------------------------------------
 // The GEMM body: WN x WK waves; wave (wn, wk) owns NT 16-column tiles and the
 // wk-th share of K.  Partial tiles are summed over wk in LDS in a fixed order
@@ -150,6 +159,12 @@ __global__ __launch_bounds__(64 * WK * WN) void k_gemm(const T *__restrict__ A, 
   __shared__ float s_inv[16];
   float(*red)[MT * 16][LDT] = reinterpret_cast<float(*)[MT * 16][LDT]>(smem);
 
+  if constexpr (SlicedEpi<Epi>::value) {  // grid y: the epilogue's slices
+    const T *a = A;
+    epi.slice(blockIdx.y, MT * 16, a, M);
+    A = a;
+    if (M <= 0) return;
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wn = wave % WN, wk = wave / WN;
   const int r = lane & 15, g = lane >> 4;
@@ -367,14 +382,6 @@ __device__ __forceinline__ void wg_barrier() {
   asm volatile("" ::: "memory");
 }
 __device__ __forceinline__ int ring_slot(int row, int piece) { return row * 8 + (piece ^ ((row >> 1) & 7)); }
-
-// Epilogues with kSliced = true cover many row blocks (and groups) in one
-// launch: grid z enumerates them and slice() moves A, M and the epilogue's
-// outputs to block z before anything else runs.
-template <class E, class = void> struct SlicedEpi { static constexpr bool value = false; };
-template <class E> struct SlicedEpi<E, decltype((void)E::kSliced)> {
-  static constexpr bool value = E::kSliced;
-};
 
 template <typename T, int NTW, int WN, int S, class Epi>
 __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
@@ -830,11 +837,15 @@ struct TileF32 {
   }
 };
 // K/V cache rows of every layer: slice z = layer * row blocks + block, A
-// holds the layers' normalised rows a_layer_stride elements apart.
-struct KvGroupArgs {
-  int nlayers, nblocks, lda;
+// holds the layers' normalised rows a_layer_stride elements apart.  The layers
+// differ only in their weights and caches; those pointers travel in the kernel
+// arguments and a slice picks its layer's with an unrolled select (a uniform
+// choice: no indexed copy of the arguments).
+struct KvGroup {
+  int nblocks, lda;
   long a_layer_stride;
-  KvCacheArgs layer[kMaxLayers];
+  const void *wk[kMaxLayers], *wv[kMaxLayers];
+  void *kc[kMaxLayers], *vc[kMaxLayers];
 };
 struct TileKv {
   static constexpr bool kRowStream = true, kSplitK = false, kSliced = true;
@@ -843,13 +854,20 @@ struct TileKv {
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   EpiKvCache<bf16_t> cur;
   int nvcols;
-  const KvGroupArgs *g;  // device copy of the per-layer arguments
+  KvGroup g;
   __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
-    const int l = z / g->nblocks, m0 = (z % g->nblocks) * mrows;
-    cur.a = g->layer[l];
+    const int l = z / g.nblocks, m0 = (z % g.nblocks) * mrows;
+#pragma unroll
+    for (int q = 0; q < kMaxLayers; ++q)
+      if (q == l) {
+        cur.a.wk = g.wk[q];
+        cur.a.wv = g.wv[q];
+        cur.a.k_cache = g.kc[q];
+        cur.a.v_cache = g.vc[q];
+      }
     cur.a.positions += m0;
     cur.a.dst_rows += m0;
-    A += l * g->a_layer_stride + (size_t)m0 * g->lda;
+    A += l * g.a_layer_stride + (size_t)m0 * g.lda;
     M = min(mrows, M - m0);
   }
   __device__ const bf16_t *wrow(int c) const { return cur.wrow(c); }
@@ -1232,35 +1250,41 @@ hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, 
   return hipGetLastError();
 }
 
-size_t kv_group_args_bytes() { return sizeof(KvGroupArgs); }
-
-__global__ void k_put_kv_args(KvGroupArgs a, KvGroupArgs *dst) {
-  static_assert(sizeof(KvGroupArgs) % 4 == 0, "copied as 32-bit words");
-  const uint32_t *src = reinterpret_cast<const uint32_t *>(&a);
-  uint32_t *d = reinterpret_cast<uint32_t *>(dst);
-  for (int i = threadIdx.x; i < (int)(sizeof(KvGroupArgs) / 4); i += blockDim.x) d[i] = src[i];
-}
-
 hipError_t gemm_kv_rows(const void *A, int lda, long a_layer_stride, int M, int nlayers,
-                        const KvCacheArgs *layers, KvGroupArgs *dev_args, hipStream_t s) {
+                        const KvCacheArgs *layers, const NormA *na, hipStream_t s) {
   if (M <= 0 || nlayers <= 0) return hipSuccess;
-  if (nlayers > kMaxLayers) return hipErrorInvalidValue;
-  KvGroupArgs h{};
-  h.nlayers = nlayers;
-  h.nblocks = (M + kTileRows - 1) / kTileRows;
-  h.lda = lda;
-  h.a_layer_stride = a_layer_stride;
-  for (int l = 0; l < nlayers; ++l) h.layer[l] = layers[l];
-  // the arguments travel as a kernel argument (captured at launch) into
-  // device memory, where the GEMM's workgroups read their layer's part
-  hipLaunchKernelGGL(k_put_kv_args, dim3(1), dim3(64), 0, s, h, dev_args);
-  const hipError_t ec = hipGetLastError();
-  if (ec != hipSuccess) return ec;
+  if (nlayers > kMaxLayers || (na && M > 16)) return hipErrorInvalidValue;
   TileKv e{};
   e.cur = EpiKvCache<bf16_t>{layers[0], 2 * layers[0].Hkv * layers[0].D};
   e.nvcols = e.cur.nvcols;
-  e.g = dev_args;
-  const dim3 grid((e.nvcols + kTileCols - 1) / kTileCols, 1, h.nblocks * nlayers);
+  e.g.lda = lda;
+  e.g.a_layer_stride = a_layer_stride;
+  for (int l = 0; l < nlayers; ++l) {
+    e.g.wk[l] = layers[l].wk;
+    e.g.wv[l] = layers[l].wv;
+    e.g.kc[l] = layers[l].k_cache;
+    e.g.vc[l] = layers[l].v_cache;
+  }
+  if (na) {
+    // up to 16 rows, A = gamma * x per layer and the rows' sums of squares:
+    // 16-column workgroups with K split over their four waves, grid y = layer
+    e.g.nblocks = 1;
+    const dim3 grid((e.nvcols + 15) / 16, nlayers);
+    hipLaunchKernelGGL((k_gemm<bf16_t, 1, 1, 4, 1, true, TileKv>), grid, dim3(256), 0, s,
+                       (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, *na, e);
+    return hipGetLastError();
+  }
+  e.g.nblocks = (M + kTileRows - 1) / kTileRows;
+  if (M < kTileRows) {
+    // one row block: the weights are the work, so narrower column tiles give
+    // every compute unit a share of them
+    constexpr int cols = 16 * 1 * kTileWn;
+    const dim3 grid((e.nvcols + cols - 1) / cols, 1, e.g.nblocks * nlayers);
+    hipLaunchKernelGGL((k_gemm_mid<bf16_t, 1, kTileWn, kTileStages, TileKv>), grid, dim3(256), 0, s,
+                       (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, e, nullptr, 0);
+    return hipGetLastError();
+  }
+  const dim3 grid((e.nvcols + kTileCols - 1) / kTileCols, 1, e.g.nblocks * nlayers);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileKv>), grid, dim3(256), 0,
                      s, (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, e, nullptr, 0);
   return hipGetLastError();

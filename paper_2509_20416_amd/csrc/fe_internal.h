@@ -252,18 +252,18 @@ hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs
 // Many-row bf16 GEMMs of the cache update: 128 x 64 output tiles over a 2-D
 // grid (row blocks in grid z), K unsplit.  gemm_store_rows / gemm_resid_rows
 // behave as gemm_store / gemm_resid (no residual, sums of squares or gain
-// copies); gemm_kv_rows runs every layer's K/V projection at once: A holds
-// layer l's normalised rows at A + l * a_layer_stride, and dev_args is device
-// memory for the per-layer arguments (copied there on the stream first).
-struct KvGroupArgs;
+// copies).
 hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, int ncols, void *out,
                            int ldo, const void *embed, const int32_t *tokens, int vocab,
                            void *gather_out, int ld_gather, int d, hipStream_t s);
 hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
                            long ldo, hipStream_t s);
+// Every layer's K/V projection into its cache in one launch (bf16): layer l's
+// normalised rows at A + l * a_layer_stride.  With na (M <= 16) A holds
+// gamma * x per layer and the rows' 1/rms come from na's sums of squares;
+// otherwise 128-row tiles (32 columns wide below 128 rows, 64 from there on).
 hipError_t gemm_kv_rows(const void *A, int lda, long a_layer_stride, int M, int nlayers,
-                        const KvCacheArgs *layers, KvGroupArgs *dev_args, hipStream_t s);
-size_t kv_group_args_bytes();
+                        const KvCacheArgs *layers, const NormA *na, hipStream_t s);
 
 // s_out[m, c] = silu(A W_gate^T)[m,c] * (A W_up^T)[m,c]
 hipError_t gemm_swiglu(int dt, const void *A, int lda, const ARows &arows, int M, int K,

@@ -43,7 +43,9 @@ Layout layout_of(const fe_config &c) {
   Layout L{};
   const size_t B = c.max_batch, N = c.n_layers, d = c.hidden, es = es_of(c);
   const size_t Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, I = c.intermediate;
-  L.nchmax = c.max_prefix > 0 ? (c.max_prefix + kAttnChunk - 1) / kAttnChunk : 1;
+  // partial slots per (sequence, head): one per prefix chunk, one for the
+  // cascade keys when they run as a unit of their own
+  L.nchmax = (c.max_prefix > 0 ? (c.max_prefix + kAttnChunk - 1) / kAttnChunk : 1) + 1;
   L.nwg = lmhead_tiles(c.draft_vocab);
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
@@ -86,26 +88,30 @@ Layout layout_of(const fe_config &c) {
 }
 
 // Workspace of fe_kv_update for chunks of C rows: the fused inputs, x_0 in
-// fp32, its per-layer RMSNorm, and split-K slices for the 256-row launches.
-// Chunks of at least kTiledRows rows (bf16) take the 2-D tiled GEMMs, with
-// every layer's normalised rows side by side and one launch for all layers.
-constexpr int kTiledRows = 128;
+// fp32, its per-layer RMSNorm (bf16: every layer's rows side by side, for the
+// one K/V launch over all layers), the rows' sums of squares for the fused
+// norm of chunks up to kFusedRows rows, and split-K slices for the 256-row
+// launches.  Chunks of more rows than one such launch takes (bf16) run the
+// fusion and input FCs as 2-D tiled GEMMs; below that the split-K launches
+// are faster (measured on the 8B shapes: 192 rows 205 against 278 us, 256
+// rows 219 against 287 us).
+constexpr int kTiledRows = kGemmMaxRows + 1, kFusedRows = 16;
 
 struct UpdLayout {
-  size_t cat, X, an, kvargs, splitk, total;
+  size_t cat, X, an, ssq, splitk, total;
   size_t splitk_floats;
 };
 
 UpdLayout upd_layout_of(const fe_config &c, size_t C) {
   UpdLayout U{};
   const size_t d = c.hidden, es = es_of(c), kvd = (size_t)c.n_kv_heads * c.head_dim;
-  const size_t nan_ = (c.dtype == FE_BF16 && C >= (size_t)kTiledRows) ? c.n_layers : 1;
+  const size_t nan_ = c.dtype == FE_BF16 ? c.n_layers : 1;  // bf16: every layer's rows
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
   U.cat = take(C * 2 * d * es);
   U.X = take(C * d * 4);
   U.an = take(nan_ * C * d * es);
-  U.kvargs = take(kv_group_args_bytes());
+  U.ssq = take(std::min<size_t>(kFusedRows, C) * (d / 16) * 4);
   const size_t rows = std::min<size_t>(kGemmMaxRows, C);
   const size_t cols = (std::max<size_t>(2 * kvd, d) + 127) / 128 * 128;
   U.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
@@ -608,41 +614,70 @@ extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *fea
   char *cat = ws + U.cat, *an = ws + U.an;
   float *X = (float *)(ws + U.X);
   const SplitScratch ss{(float *)(ws + U.splitk), U.splitk_floats};
+  // bf16: every layer's K/V projection in one launch
+  auto layer_args = [&](int r0, KvCacheArgs *la) {
+    for (int l = 0; l < c.n_layers; ++l) {
+      const fe_layer_weights &lw = h->layers[l];
+      la[l] = KvCacheArgs{lw.wk, lw.wv, d, c.head_dim, c.n_kv_heads, positions + r0,
+                          dst_rows + r0, (long)cache->rows, c.max_prefix,
+                          (const float *)(h->ws + h->L.rope), cache->k[l], cache->v[l]};
+    }
+  };
   for (int r0 = 0; r0 < n_rows; r0 += C) {
     const int Mc = std::min(C, n_rows - r0);
+    if (dt && Mc <= kFusedRows) {
+      // few rows: the input FC also writes gamma_l * x_0 for every layer and
+      // the rows' sums of squares, and the K/V launch applies 1/rms
+      FE_TRY(gemm_store(dt, (const char *)features + (size_t)r0 * F * d * es, F * d, Mc, F * d,
+                        h->w.w_fuse, d, cat, 2 * d, h->w.embed, tokens + r0, c.target_vocab,
+                        cat + (size_t)d * es, 2 * d, d, Mc, s, &ss));
+      GainCopies gc{};
+      gc.n = c.n_layers;
+      for (int l = 0; l < c.n_layers; ++l) {
+        gc.gamma[l] = h->layers[l].attn_norm;
+        gc.dst[l] = an + (size_t)l * C * d * es;
+        gc.ld[l] = d;
+      }
+      float *ssq = (float *)(ws + U.ssq);
+      FE_TRY(gemm_resid(dt, cat, 2 * d, Mc, 2 * d, h->w.w_in, d, X, d, nullptr, 0, ssq, 1, 0, &gc,
+                        s, &ss));
+      KvCacheArgs la[kMaxLayers];
+      layer_args(r0, la);
+      const NormA na{ssq, d / 16, 1, 0, 1, d, c.rms_eps};
+      FE_TRY(gemm_kv_rows(an, d, (long)C * d, Mc, c.n_layers, la, &na, s));
+      continue;
+    }
     if (dt && Mc >= kTiledRows) {
-      // many rows: one launch per stage over 128 x 64 output tiles, and one
-      // K/V launch for every layer (matrix-core bound from a few hundred rows)
+      // many rows: one launch per stage over 128 x 64 output tiles
+      // (matrix-core bound from a few hundred rows)
       FE_TRY(gemm_store_rows((const char *)features + (size_t)r0 * F * d * es, F * d, Mc, F * d,
                              h->w.w_fuse, d, cat, 2 * d, h->w.embed, tokens + r0, c.target_vocab,
                              cat + (size_t)d * es, 2 * d, d, s));
       FE_TRY(gemm_resid_rows(cat, 2 * d, Mc, 2 * d, h->w.w_in, d, X, d, s));
-      KvCacheArgs la[kMaxLayers];
-      for (int l = 0; l < c.n_layers; ++l) {
-        const fe_layer_weights &lw = h->layers[l];
-        FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an + (size_t)l * C * d * es, d,
-                            c.rms_eps, s));
-        la[l] = KvCacheArgs{lw.wk, lw.wv, d, c.head_dim, c.n_kv_heads, positions + r0,
-                            dst_rows + r0, (long)cache->rows, c.max_prefix,
-                            (const float *)(h->ws + h->L.rope), cache->k[l], cache->v[l]};
+    } else {
+      // stage by stage over the chunk, so that each weight matrix is read by
+      // consecutive launches
+      for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+        const int Ms = std::min(kGemmMaxRows, Mc - s0);
+        FE_TRY(gemm_store(dt, (const char *)features + (size_t)(r0 + s0) * F * d * es, F * d, Ms,
+                          F * d, h->w.w_fuse, d, cat + (size_t)s0 * 2 * d * es, 2 * d, h->w.embed,
+                          tokens + r0 + s0, c.target_vocab, cat + ((size_t)s0 * 2 * d + d) * es,
+                          2 * d, d, Ms, s, &ss));
       }
-      FE_TRY(gemm_kv_rows(an, d, (long)C * d, Mc, c.n_layers, la,
-                          (KvGroupArgs *)(ws + U.kvargs), s));
+      for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+        const int Ms = std::min(kGemmMaxRows, Mc - s0);
+        FE_TRY(gemm_resid(dt, cat + (size_t)s0 * 2 * d * es, 2 * d, Ms, 2 * d, h->w.w_in, d,
+                          X + (size_t)s0 * d, d, nullptr, 0, nullptr, 1, 0, nullptr, s, &ss));
+      }
+    }
+    if (dt) {
+      for (int l = 0; l < c.n_layers; ++l)
+        FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, h->layers[l].attn_norm,
+                            an + (size_t)l * C * d * es, d, c.rms_eps, s));
+      KvCacheArgs la[kMaxLayers];
+      layer_args(r0, la);
+      FE_TRY(gemm_kv_rows(an, d, (long)C * d, Mc, c.n_layers, la, nullptr, s));
       continue;
-    }
-    // stage by stage over the chunk, so that each weight matrix is read by
-    // consecutive launches
-    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
-      const int Ms = std::min(kGemmMaxRows, Mc - s0);
-      FE_TRY(gemm_store(dt, (const char *)features + (size_t)(r0 + s0) * F * d * es, F * d, Ms, F * d,
-                        h->w.w_fuse, d, cat + (size_t)s0 * 2 * d * es, 2 * d, h->w.embed,
-                        tokens + r0 + s0, c.target_vocab, cat + ((size_t)s0 * 2 * d + d) * es, 2 * d,
-                        d, Ms, s, &ss));
-    }
-    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
-      const int Ms = std::min(kGemmMaxRows, Mc - s0);
-      FE_TRY(gemm_resid(dt, cat + (size_t)s0 * 2 * d * es, 2 * d, Ms, 2 * d, h->w.w_in, d,
-                        X + (size_t)s0 * d, d, nullptr, 0, nullptr, 1, 0, nullptr, s, &ss));
     }
     for (int l = 0; l < c.n_layers; ++l) {
       const fe_layer_weights &lw = h->layers[l];

@@ -99,16 +99,24 @@ def _run(cfg, up, chunk_rows, sample=None, seed=0):
 
 
 CASES = [
-    # (config, accepted per sequence, chunk rows): the row-streaming path
-    # (<= 4 rows), one batched launch, the tiled many-row GEMMs (bf16 chunks
-    # of 128 rows or more), several 256-row launches, and several chunks
+    # (config, accepted per sequence, chunk rows).  bf16: chunks of up to 16
+    # rows fuse the norm into one K/V launch for every layer (the input FC
+    # writes the per-layer gamma * x_0 copies); above that one K/V launch over
+    # 128-row blocks (32-column tiles below 128 rows, 64 from there on), and
+    # the FCs as 256-row launches or, above 256 rows, 2-D tiled GEMMs.  fp32:
+    # per-layer launches (row streaming up to 4 rows, 256-row launches above)
     (C.SMALL_GQA_BF16, [1], 1024),
     (C.SMALL_GQA_BF16, [2, 1, 1], 1024),
+    (C.SMALL_GQA_BF16, [6], 1024),
+    (C.SMALL_MHA_BF16_D128, [3] * 5 + [1], 1024),     # 16 rows: the fused limit
+    (C.SMALL_GQA_BF16, [5] * 7 + [2], 9),             # fused chunks of 9 rows and a ragged 1
     (C.SMALL_GQA_BF16, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
     (C.SMALL_GQA_F32, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
+    (C.SMALL_GQA_F32, [2, 1, 1], 1024),
     (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 1024),   # 2-D tiled GEMMs, ragged row block
-    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 100),    # 100-row chunks: the 256-row launches
-    (C.SMALL_GQA_BF16, [40] * 8 + [7], 200),          # tiled chunks of 200 and 127 rows
+    (C.SMALL_MHA_BF16_D128, [50] * 6 + [13], 100),    # chunks of 100 and 13 rows
+    (C.SMALL_GQA_BF16, [40] * 8 + [7], 300),          # a tiled chunk of 300 rows, then 27
+    (C.SMALL_GQA_BF16, [40] * 8 + [7], 200),          # 200 rows (64-column K/V tiles), then 127
     (C.TINY_F32_B1, [3] * 100 + [1], 40),
 ]
 
@@ -134,6 +142,15 @@ def test_kv_update_full_size_sampled():
     up = make_update_rows(cfg, acc, plens, capacity=8192, seed=5)
     sample = [0, 1, 7, 100, 129, 255]
     _run(cfg, up, 1024, sample=sample)
+
+
+def test_kv_update_full_size_b1_cycle():
+    """The 8B shapes at batch 1: the N+1 = 6 positions one cycle accepts at
+    most, every row through the oracle (the fused-norm path)."""
+    cfg = C.LLAMA8B_BF16_B1
+    acc = np.array([cfg.n_layers + 1], np.int32)
+    up = make_update_rows(cfg, acc, np.array([1000], np.int32), capacity=1024, seed=6)
+    _run(cfg, up, 1024)
 
 
 def test_kv_update_out_of_range_rows():
