@@ -212,11 +212,14 @@ hipError_t gemm_store(int dt, const void *A, int lda, int M, int K, const void *
 // out[m, c] = (resid ? resid[m, c] : 0) + sum_k A[m,k] W[c,k]   (fp32 out/resid).
 // When ssq is not null, also writes the sum of squares of every output row over
 // each 16-column tile t to ssq[(m * ssq_rs + ssq_off) * (ncols/16) + t]; when
-// gains is not null, also writes its gain copies of every output row.
+// gains is not null, also writes its gain copies of every output row.  With
+// norm_eps >= 0 the copies are RMS-normalised, gamma * v / sqrt(mean(v^2) +
+// norm_eps), written by a row pass that also sums the split-K slices (ssq is
+// then ignored; ncols <= 8192, a multiple of 4).
 hipError_t gemm_resid(int dt, const void *A, int lda, int M, int K, const void *W, int ncols,
                       float *out, long ldo, const float *resid, long ldr, float *ssq, int ssq_rs,
                       int ssq_off, const GainCopies *gains, hipStream_t s,
-                      const SplitScratch *ss = nullptr);
+                      const SplitScratch *ss = nullptr, float norm_eps = -1.f);
 
 struct QkvArgs {
   const void *wq, *wk, *wv;

@@ -302,14 +302,18 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
                     next_tokens, c.target_vocab, (char *)cat + (size_t)d * esz, 2 * d, d, B, s, &ss));
   // x_0 = FC(concat(g_t, e_{t+1}))  (Eq. 1)
   // Fused RMSNorm (up to 16 rows per GEMM): every producer of a residual row
-  // also writes gamma * row for the later GEMMs that normalise it.
+  // also writes gamma * row for the later GEMMs that normalise it.  Above 16
+  // sequences the producers' split-K row pass writes the normalised rows
+  // themselves (rows_norm), for every consumer, and no RMSNorm launch remains.
   const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
   const bool parallel = c.cascade_ctx == FE_CTX_PARALLEL;  // every layer reads x_0
   char *AQ = ws + L.AQ, *AM = ws + L.AM, *AF = ws + L.AF;
   const size_t aq_layer = (size_t)c.max_batch * N * d * esz;  // bytes per layer block of AQ
   auto nctx_of = [&](int l) { return cascade ? l : 1; };
-  auto fuse_q = [&](int l) { return B * nctx_of(l) <= 16; };
-  const bool fuse_m = B <= 16, fuse_f = B * N <= 16;
+  const bool rows_norm = B > 16 && d <= 8192;
+  const float norm_eps = rows_norm ? c.rms_eps : -1.f;
+  auto fuse_q = [&](int l) { return rows_norm || B * nctx_of(l) <= 16; };
+  const bool fuse_m = rows_norm || B <= 16, fuse_f = rows_norm || B * N <= 16;
   // copies of x_j (j = 0 from the input FC, j = i from layer i's down projection)
   auto x_copies = [&](int j) {
     GainCopies gc{};
@@ -331,7 +335,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   };
   const GainCopies gc_x0 = x_copies(0);
   FE_STAGE_RUN(FE_STAGE_INPUT, gemm_resid(dt, cat, 2 * d, B, 2 * d, h->w.w_in, d, X, xrow, nullptr,
-                                      0, ssqX, N + 1, 0, &gc_x0, s, &ss));
+                                      0, rows_norm ? nullptr : ssqX, N + 1, 0, &gc_x0, s, &ss,
+                                      norm_eps));
 
   for (int i = 1; i <= N; ++i) {
     const fe_layer_weights &lw = h->layers[i - 1];
@@ -344,7 +349,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     if (fuse_q(i)) {
       const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
       FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, AQ + (size_t)(i - 1) * aq_layer, d, ARows{nctx, j0, N},
-                                      B * nctx, qa, &na1, s, &ss));
+                                      B * nctx, qa, rows_norm ? nullptr : &na1, s, &ss));
     } else {
       FE_OTHER(rmsnorm_rows(dt, X, B * nctx, nctx, j0, xrow, d, lw.attn_norm, an, d, c.rms_eps, s));
       FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s, &ss));
@@ -362,12 +367,13 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
       gc_p.ld[0] = d;
     }
     FE_STAGE_RUN(FE_STAGE_OPROJ, gemm_resid(dt, ao, qd, B, qd, lw.wo, d, Xp, d,
-                                        X + (size_t)src * d, xrow, ssqP, 1, 0, &gc_p, s, &ss));
+                                        X + (size_t)src * d, xrow, rows_norm ? nullptr : ssqP, 1,
+                                        0, &gc_p, s, &ss, norm_eps));
     // SwiGLU MLP on RMSNorm(x'), residual into x_i
     if (fuse_m) {
       const NormA na2{ssqP, ntile, 1, 0, 1, d, c.rms_eps};
       FE_STAGE_RUN(FE_STAGE_GATEUP, gemm_swiglu(dt, AM, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
-                                            sbuf, I, &na2, s));
+                                            sbuf, I, rows_norm ? nullptr : &na2, s));
     } else {
       FE_OTHER(rmsnorm_rows(dt, Xp, B, 1, 0, d, 0, lw.mlp_norm, bn, d, c.rms_eps, s));
       FE_STAGE_RUN(FE_STAGE_GATEUP, gemm_swiglu(dt, bn, d, kDenseRows, B, d, lw.w_gate, lw.w_up, I,
@@ -375,7 +381,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     }
     const GainCopies gc_xi = x_copies(i);
     FE_STAGE_RUN(FE_STAGE_DOWN, gemm_resid(dt, sbuf, I, B, I, lw.w_down, d, X + (size_t)i * d, xrow,
-                                       Xp, d, ssqX, N + 1, i, &gc_xi, s, &ss));
+                                       Xp, d, rows_norm ? nullptr : ssqX, N + 1, i, &gc_xi, s, &ss,
+                                       norm_eps));
   }
 
   // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
@@ -386,7 +393,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
             uniforms, (float *)(ws + L.cz)};
   int nwg = 0;
   FE_STAGE_RUN(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
-                                        d, la, fuse_f ? &naf : nullptr, &nwg, s));
+                                        d, la, fuse_f && !rows_norm ? &naf : nullptr, &nwg, s));
   FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx,
                       uniforms ? la.cand_z : nullptr, B * N, nwg, topk, c.draft_vocab, h->w.d2t,
                       out->topk_ids, out->topk_draft, out->topk_probs, s));

@@ -148,7 +148,16 @@ def test_attention_split_parity(cfg, split):
                                                         name="small_gqa_bf16_b36"),
                                  # parallel heads over 12 x 3 rows (normalisation unfused)
                                  C.SMALL_GQA_BF16.with_(batch=12, cascade_ctx="parallel",
-                                                        name="small_gqa_bf16_b12_parallel")],
+                                                        name="small_gqa_bf16_b12_parallel"),
+                                 # more than 16 sequences: the residual GEMMs' row pass
+                                 # writes the normalised rows of every consumer (fp32 and
+                                 # bf16; cascade, parallel and self contexts)
+                                 C.SMALL_GQA_F32.with_(batch=20, prefix=(0, 300),
+                                                       name="small_gqa_f32_b20"),
+                                 C.SMALL_GQA_BF16.with_(batch=20, cascade_ctx="parallel",
+                                                        name="small_gqa_bf16_b20_parallel"),
+                                 C.SMALL_GQA_BF16.with_(batch=20, cascade_ctx="self",
+                                                        name="small_gqa_bf16_b20_self")],
                          ids=lambda c: c.name)
 def test_batched_rows_parity(cfg):
     _run(cfg, seed=5)
