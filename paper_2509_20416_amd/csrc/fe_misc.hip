@@ -84,7 +84,7 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // candidates its lanes hold (k rounds of butterfly max over ordering keys, no
 // block barrier), then wave 0 selects the top-k of the 4k wave winners and
 // writes them.
-template <bool SAMPLED>
+template <bool SAMPLED, int CAP>
 __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
                                                     const float *__restrict__ psum,
                                                     const float *__restrict__ cval,
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
                                                     int topk, int V, const int32_t *__restrict__ d2t,
                                                     int32_t *ids, int32_t *draft_ids,
                                                     float *probs) {
-  constexpr int CAP = kMergeMaxCand / 256;
+  static_assert(256 * CAP <= kMergeMaxCand, "candidates per thread");
   __shared__ float sv[4];
   __shared__ uint64_t s_key[4][kMaxTopk];
   __shared__ float s_z[4][kMaxTopk];
@@ -223,12 +223,21 @@ hipError_t topk_merge(const float *part_max, const float *part_sum, const float 
                       int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
                       hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (cand_z)
-    hipLaunchKernelGGL(k_topk_merge<true>, dim3(rows), dim3(256), 0, s, part_max, part_sum,
-                       cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
-  else
-    hipLaunchKernelGGL(k_topk_merge<false>, dim3(rows), dim3(256), 0, s, part_max, part_sum,
-                       cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs);
+  const long ncand = (long)nwg * topk;
+  if (ncand > kMergeMaxCand) return hipErrorInvalidValue;
+  // candidates per thread: the fewest registers that hold the row (the k
+  // selection rounds scan all of them)
+#define FE_MERGE(SV, CAPV)                                                                         \
+  hipLaunchKernelGGL((k_topk_merge<SV, CAPV>), dim3(rows), dim3(256), 0, s, part_max, part_sum,    \
+                     cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs)
+#define FE_MERGE_CAP(SV)                                     \
+  if (ncand <= 256 * 8) FE_MERGE(SV, 8);                     \
+  else if (ncand <= 256 * 16) FE_MERGE(SV, 16);              \
+  else FE_MERGE(SV, kMergeMaxCand / 256)
+  if (cand_z) { FE_MERGE_CAP(true); }
+  else { FE_MERGE_CAP(false); }
+#undef FE_MERGE_CAP
+#undef FE_MERGE
   return hipGetLastError();
 }
 
