@@ -342,13 +342,25 @@ hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *toke
                          const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s);
 
+// The pass's draft tree, written by the top-k merge itself: rows are
+// (sequence, level) pairs, N levels per sequence; the arrays as build_tree
+// writes them (tokens == nullptr: no tree).
+struct TreeRows {
+  int N = 0;
+  const int32_t *root = nullptr, *cu_prefix = nullptr;
+  int32_t *tokens = nullptr, *parents = nullptr, *depth = nullptr, *positions = nullptr;
+  uint8_t *mask = nullptr;
+  int32_t *retrieve = nullptr;
+};
+
 // Global top-k of every row from the tile candidates (by key); softmax
 // statistics merge.  With cand_z (sampled candidates) the k winners are
-// listed by z / T (larger first, lower id on ties), else in key order.
+// listed by z / T (larger first, lower id on ties), else in key order.  With
+// tree, also the Backbone Expansion tree of the rows' sequences.
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
                       const int32_t *cand_idx, const float *cand_z, int rows, int nwg, int topk,
                       int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
-                      hipStream_t s);
+                      hipStream_t s, const TreeRows *tree = nullptr);
 
 // Backbone Expansion tree of every sequence; P_b from prefix_lens, or from
 // cu_prefix when prefix_lens is NULL.

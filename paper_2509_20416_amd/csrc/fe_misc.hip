@@ -84,6 +84,9 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // candidates its lanes hold (k rounds of butterfly max over ordering keys, no
 // block barrier), then wave 0 selects the top-k of the 4k wave winners and
 // writes them.
+__device__ void tree_structure(int b, int N, int k, int P, int32_t *parents, int32_t *depth,
+                               int32_t *positions, uint8_t *mask, int32_t *retrieve);
+
 template <bool SAMPLED, int CAP>
 __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pmax,
                                                     const float *__restrict__ psum,
@@ -92,12 +95,21 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
                                                     const float *__restrict__ cz, int nwg,
                                                     int topk, int V, const int32_t *__restrict__ d2t,
                                                     int32_t *ids, int32_t *draft_ids,
-                                                    float *probs) {
+                                                    float *probs, TreeRows tr) {
   static_assert(256 * CAP <= kMergeMaxCand, "candidates per thread");
   __shared__ float sv[4];
   __shared__ uint64_t s_key[4][kMaxTopk];
   __shared__ float s_z[4][kMaxTopk];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the tree of sequence b (rows b*N .. b*N+N-1 are its levels): the level-1
+  // row's workgroup writes its root and structure, every row its level's nodes
+  const int tb = tr.tokens ? row / tr.N : 0, tl = tr.tokens ? row % tr.N : 0;
+  const int tT = 1 + tr.N * topk;
+  if (tr.tokens && tl == 0) {
+    if (tid == 0) tr.tokens[(size_t)tb * tT] = tr.root[tb];
+    tree_structure(tb, tr.N, topk, tr.cu_prefix[tb + 1] - tr.cu_prefix[tb], tr.parents, tr.depth,
+                   tr.positions, tr.mask, tr.retrieve);
+  }
   const float *pm = pmax + (size_t)row * nwg;
   const float *ps = psum + (size_t)row * nwg;
   // every candidate of the row into registers (thread t holds t, t+256, ...):
@@ -211,7 +223,9 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
     }
     if (lane < topk) {
       const size_t o = (size_t)row * topk + pos;
-      ids[o] = valid ? (d2t ? d2t[i] : i) : -1;
+      const int32_t id = valid ? (d2t ? d2t[i] : i) : -1;
+      ids[o] = id;
+      if (tr.tokens) tr.tokens[(size_t)tb * tT + 1 + tl * topk + pos] = id;
       if (draft_ids) draft_ids[o] = valid ? i : -1;
       probs[o] = valid ? expf(z - mu) / Ssum : __int_as_float(0x7fc00000);
     }
@@ -221,7 +235,9 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float *__restrict__ pm
 hipError_t topk_merge(const float *part_max, const float *part_sum, const float *cand_val,
                       const int32_t *cand_idx, const float *cand_z, int rows, int nwg, int topk,
                       int V, const int32_t *d2t, int32_t *ids, int32_t *draft_ids, float *probs,
-                      hipStream_t s) {
+                      hipStream_t s, const TreeRows *tree) {
+  const TreeRows tr = tree ? *tree : TreeRows{};
+  if (tr.tokens && (tr.N < 1 || rows % tr.N)) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
   const long ncand = (long)nwg * topk;
   if (ncand > kMergeMaxCand) return hipErrorInvalidValue;
@@ -229,7 +245,7 @@ hipError_t topk_merge(const float *part_max, const float *part_sum, const float 
   // selection rounds scan all of them)
 #define FE_MERGE(SV, CAPV)                                                                         \
   hipLaunchKernelGGL((k_topk_merge<SV, CAPV>), dim3(rows), dim3(256), 0, s, part_max, part_sum,    \
-                     cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs)
+                     cand_val, cand_idx, cand_z, nwg, topk, V, d2t, ids, draft_ids, probs, tr)
 #define FE_MERGE_CAP(SV)                                     \
   if (ncand <= 256 * 8) FE_MERGE(SV, 8);                     \
   else if (ncand <= 256 * 16) FE_MERGE(SV, 16);              \
@@ -250,26 +266,18 @@ hipError_t topk_merge(const float *part_max, const float *part_sum, const float 
 // itself.  Leaves are the side branches (rho != 0) and the level-N backbone
 // node.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_build_tree(int N, int k,
-                                                    const int32_t *__restrict__ root_tokens,
-                                                    const int32_t *__restrict__ topk_ids,
-                                                    const int32_t *__restrict__ prefix_lens,
-                                                    const int32_t *__restrict__ cu_prefix,
-                                                    int32_t *tokens, int32_t *parents,
-                                                    int32_t *depth, int32_t *positions,
-                                                    uint8_t *mask, int32_t *retrieve) {
-  const int b = blockIdx.x, T = 1 + N * k, NL = N * (k - 1) + 1;
-  const int P = prefix_lens ? prefix_lens[b] : cu_prefix[b + 1] - cu_prefix[b];
+// Everything of sequence b's tree except the tokens (closed form in N, k and
+// the prefix length P), spread over the calling workgroup's threads.
+__device__ void tree_structure(int b, int N, int k, int P, int32_t *parents, int32_t *depth,
+                               int32_t *positions, uint8_t *mask, int32_t *retrieve) {
+  const int T = 1 + N * k, NL = N * (k - 1) + 1;
   for (int n = threadIdx.x; n < T; n += blockDim.x) {
-    int lvl = 0, tok = root_tokens[b], par = -1;
+    int lvl = 0, par = -1;
     if (n > 0) {
       lvl = 1 + (n - 1) / k;
-      const int rho = (n - 1) % k;
-      tok = topk_ids[((size_t)b * N + (lvl - 1)) * k + rho];
       par = (lvl == 1) ? 0 : 1 + (lvl - 2) * k;
     }
     const size_t o = (size_t)b * T + n;
-    tokens[o] = tok;
     parents[o] = par;
     depth[o] = lvl;
     positions[o] = P + lvl;
@@ -300,6 +308,27 @@ __global__ __launch_bounds__(256) void k_build_tree(int N, int k,
     row[lvl] = 1 + (lvl - 1) * k + rho;
     for (int t = lvl + 1; t <= N; ++t) row[t] = -1;
   }
+}
+
+__global__ __launch_bounds__(256) void k_build_tree(int N, int k,
+                                                    const int32_t *__restrict__ root_tokens,
+                                                    const int32_t *__restrict__ topk_ids,
+                                                    const int32_t *__restrict__ prefix_lens,
+                                                    const int32_t *__restrict__ cu_prefix,
+                                                    int32_t *tokens, int32_t *parents,
+                                                    int32_t *depth, int32_t *positions,
+                                                    uint8_t *mask, int32_t *retrieve) {
+  const int b = blockIdx.x, T = 1 + N * k;
+  const int P = prefix_lens ? prefix_lens[b] : cu_prefix[b + 1] - cu_prefix[b];
+  for (int n = threadIdx.x; n < T; n += blockDim.x) {
+    int tok = root_tokens[b];
+    if (n > 0) {
+      const int lvl = 1 + (n - 1) / k, rho = (n - 1) % k;
+      tok = topk_ids[((size_t)b * N + (lvl - 1)) * k + rho];
+    }
+    tokens[(size_t)b * T + n] = tok;
+  }
+  tree_structure(b, N, k, P, parents, depth, positions, mask, retrieve);
 }
 
 hipError_t build_tree(int B, int N, int k, const int32_t *root_tokens, const int32_t *topk_ids,

@@ -394,17 +394,21 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   int nwg = 0;
   FE_STAGE_RUN(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
                                         d, la, fuse_f && !rows_norm ? &naf : nullptr, &nwg, s));
+  // with the Backbone Expansion tree of this pass (root = next token) written
+  // by the same launch
+  TreeRows tr{};
+  if (out->tree) {
+    const fe_tree_out *t = out->tree;
+    tr = TreeRows{N, next_tokens, kv->cu_prefix, t->tokens, t->parents, t->depth, t->positions,
+                  t->mask, t->retrieve};
+  }
   FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx,
                       uniforms ? la.cand_z : nullptr, B * N, nwg, topk, c.draft_vocab, h->w.d2t,
-                      out->topk_ids, out->topk_draft, out->topk_probs, s));
+                      out->topk_ids, out->topk_draft, out->topk_probs, s,
+                      out->tree ? &tr : nullptr));
   if (out->hidden)
     FE_OTHER(hipMemcpyAsync(out->hidden, X, (size_t)B * (N + 1) * d * sizeof(float),
                             hipMemcpyDeviceToDevice, s));
-  if (out->tree) {  // Backbone Expansion tree of this pass: root = next token
-    const fe_tree_out *t = out->tree;
-    FE_OTHER(build_tree(B, N, topk, next_tokens, out->topk_ids, nullptr, kv->cu_prefix, t->tokens,
-                        t->parents, t->depth, t->positions, t->mask, t->retrieve, s));
-  }
   return FE_OK;
 }
 
