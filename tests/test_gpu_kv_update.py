@@ -110,6 +110,7 @@ CASES = [
     (C.SMALL_GQA_BF16, [6], 1024),
     (C.SMALL_MHA_BF16_D128, [3] * 5 + [1], 1024),     # 16 rows: the fused limit
     (C.SMALL_GQA_BF16, [5] * 7 + [2], 9),             # fused chunks of 9 rows and a ragged 1
+    (C.SMALL_GQA_BF16.with_(n_layers=10, name="small_gqa_bf16_n10"), [6], 1024),  # 10 layers' copies
     (C.SMALL_GQA_BF16, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
     (C.SMALL_GQA_F32, [4, 6, 1, 3, 5, 2, 7, 9], 1024),
     (C.SMALL_GQA_F32, [2, 1, 1], 1024),

@@ -125,6 +125,19 @@ def test_small_parity(cfg, ctx):
         assert rep["decided"] >= rep["ranks"] // 2, rep
 
 
+# A deep cascade (N = 10): layers 9 and 10 attend to more than 8 cascade keys
+# (the 16-key bound of the attention's cascade loops), every producer writes
+# up to 11 normalised copies; batch 3 with the cascade keys in units of their
+# own, and batch 20 with the residual row pass.
+@pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16.with_(n_layers=10, name="small_gqa_bf16_n10"),
+                                 C.SMALL_GQA_BF16.with_(n_layers=10, batch=20, prefix=(0, 300),
+                                                        name="small_gqa_bf16_b20_n10")],
+                         ids=lambda c: c.name)
+def test_deep_cascade_parity(cfg):
+    plens = np.array([0, 700, 65], np.int32) if cfg.batch == 3 else None
+    _run(cfg, seed=7, prefix_lens=plens)
+
+
 # Attention work split: 1 chunk per workgroup (every 128-key chunk its own
 # partial, merged by the second launch), 2 and 3 (the sub-chunk loop with a
 # ragged last workgroup), 8 (one workgroup per sequence, no merge launch).
