@@ -471,20 +471,26 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
       }
       wg_barrier();
     }
+    // every fragment of the chunk is read before the first product (the ring
+    // holds all MROWS rows, so the reads need no guard and are in flight
+    // together); only the products skip the wave's dead row tiles
+    u32x4 bf[2][NTW], af[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      u32x4 bf[NTW];
 #pragma unroll
       for (int f = 0; f < NTW; ++f)
-        bf[f] = *reinterpret_cast<const u32x4 *>(st + ABYTES + ring_slot(ncol0 + f * 16 + r, ks * 4 + g) * 16);
+        bf[ks][f] = *reinterpret_cast<const u32x4 *>(st + ABYTES + ring_slot(ncol0 + f * 16 + r, ks * 4 + g) * 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (i < mtiles) {
-          const u32x4 af = *reinterpret_cast<const u32x4 *>(st + ring_slot(mrow0 + i * 16 + r, ks * 4 + g) * 16);
-#pragma unroll
-          for (int f = 0; f < NTW; ++f) mma16<T>(acc[i][f], af, bf[f]);
-        }
+        af[ks][i] = *reinterpret_cast<const u32x4 *>(st + ring_slot(mrow0 + i * 16 + r, ks * 4 + g) * 16);
     }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < mtiles)
+#pragma unroll
+          for (int f = 0; f < NTW; ++f) mma16<T>(acc[i][f], af[ks][i], bf[ks][f]);
   }
   wait_vmcnt<0>();  // the chunks fetched past the end land before the ring is reused or freed
   if (splitp) {  // split K: this slice's fp32 sums, reduced (and finished) by a second launch
