@@ -99,6 +99,21 @@ SMALL_MHA_BF16_D128 = DrafterConfig(
     rope_theta=10000.0, dtype="bf16", batch=2, prefix=(1, 300), topk=3)
 
 
+# Grouped-query layouts the small shapes above do not reach: 8 query heads per
+# KV head (the 70B-shaped grouping, head dim 128) and 2 per KV head.
+SMALL_GQA8_BF16_D128 = DrafterConfig(
+    name="small_gqa8_bf16_d128", hidden=512, n_q_heads=16, n_kv_heads=2, head_dim=128,
+    intermediate=1088, n_layers=3, draft_vocab=1504, target_vocab=3001,
+    rope_theta=500000.0, dtype="bf16", batch=3, prefix=(0, 700), topk=4)
+
+SMALL_GQA2_BF16 = DrafterConfig(
+    name="small_gqa2_bf16", hidden=256, n_q_heads=8, n_kv_heads=4, head_dim=64,
+    intermediate=704, n_layers=3, draft_vocab=1024, target_vocab=2048,
+    rope_theta=10000.0, dtype="bf16", batch=2, prefix=(1, 400), topk=4)
+
+SMALL_GQA2_F32 = SMALL_GQA2_BF16.with_(name="small_gqa2_f32", dtype="f32")
+
+
 def prefix_range(cfg: DrafterConfig) -> Tuple[int, int]:
     if isinstance(cfg.prefix, int):
         return cfg.prefix, cfg.prefix

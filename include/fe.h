@@ -109,7 +109,9 @@ typedef struct {
                                 [sum_b P_b, H_kv, D], keys ALREADY rotary-embedded */
   const void *const *v;      /* HOST array [n_layers], each [sum_b P_b, H_kv, D] */
   const int32_t *cu_prefix;  /* device [B+1]: sequence b owns rows cu[b]..cu[b+1]-1 */
-  int32_t max_prefix;        /* HOST bound: every P_b <= max_prefix <= cfg.max_prefix */
+  int32_t max_prefix;        /* HOST bound: every P_b <= max_prefix <= cfg.max_prefix.  On the
+                                device, a sequence whose P_b lies outside [0, max_prefix] reads
+                                no cache row and its outputs are NaN (ids -1) */
 } fe_kv_view;
 
 typedef struct fe_tree_out fe_tree_out;
@@ -343,6 +345,21 @@ typedef enum {
  * unspecified until the next fe_draft_forward. */
 fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                         float *ms_per_launch, int32_t *launches);
+
+/* Test export, host only (no device work, no handle): the work pieces of the
+ * persistent bf16 attention for a batch whose prefix lengths are
+ * prefix_lens[0..batch) (HOST array), `ncols` (KV head, head group) columns
+ * per sequence, `nch_ld` partial slots per (sequence, head) and `waves`
+ * resident waves, from the same split arithmetic the kernel runs.  Row p of
+ * `pieces` (HOST, [max_pieces, 7] int32) is (wave, sequence, column, first
+ * 64-key chunk, chunks, partial slot, pieces of the segment if this is its
+ * first piece else 0); *n_pieces gets the total (rows past max_pieces are not
+ * written; `pieces` may be NULL when max_pieces is 0).  A P_b outside
+ * [0, pmax] counts as an empty prefix.  Errors: FE_E_INVALID for NULL arrays,
+ * batch outside [1, 256] or non-positive sizes. */
+fe_status fe_test_attn_split(const int32_t *prefix_lens, int32_t batch, int32_t ncols,
+                             int32_t nch_ld, int32_t pmax, int32_t waves, int32_t *pieces,
+                             int32_t max_pieces, int32_t *n_pieces);
 
 void fe_drafter_destroy(fe_drafter *h);
 

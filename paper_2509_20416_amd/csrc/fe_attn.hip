@@ -53,7 +53,7 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
                                               const float *__restrict__ vnew, int nctx,
                                               float *__restrict__ part, int nch, int nch_ld,
                                               int cpw,
-                                              T *__restrict__ out, int Hq, int Hkv) {
+                                              T *__restrict__ out, int Hq, int Hkv, int pmax) {
   constexpr int RL = D * (int)sizeof(T) / 16;  // lanes per key row
   constexpr int KPL = 64 / RL;                  // key rows per load instruction
   constexpr int DPL = 16 / (int)sizeof(T);      // dims per lane
@@ -68,7 +68,8 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   // heads fastest: the workgroups that run side by side read neighbouring
   // head segments of the same token rows
   const int ch = blockIdx.y, c = blockIdx.x / ngrp, hg = blockIdx.x % ngrp, b = blockIdx.z;
-  const int start = cu[b], P = cu[b + 1] - start;
+  bool bad;
+  const int start = cu[b], P = attn_prefix(cu, b, pmax, bad);
   const int span = kAttnChunk * cpw;  // prefix keys per workgroup
   const int nv = max(1, min((P + span - 1) / span, nch));
   if (ch >= nv) return;  // chunk beyond this sequence's prefix
@@ -242,6 +243,11 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
       acc += sw * g;
       L += sw * gl;
     }
+    if (bad) {  // P_b outside [0, pmax]: the sequence's output is NaN
+      acc = __int_as_float(0x7fc00000);
+      L = whole ? 1.f : acc;
+      M = 0.f;
+    }
     if (whole) {
       out[(size_t)b * Hq * D + (size_t)(h0 + gh) * D + e] = Elt<T>::from_f(acc / L);
     } else {
@@ -320,7 +326,7 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
                                                  int cpw, bf16_t *__restrict__ out, int Hq,
                                                  int Hkv, const float *__restrict__ rope,
                                                  int cascade, int nseq, int persist,
-                                                 int csplit) {
+                                                 int csplit, int pmax) {
   static_assert(D == 64 || D == 128, "head dims 64 and 128");
   static_assert(NCX <= kMaxLayers, "cascade keys per layer");
   constexpr int NKC = D / 32;          // 32-dim steps of QK^T
@@ -389,7 +395,8 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     }
   }
 
-  const int start = cu[b], P = cu[b + 1] - start;
+  bool bad;
+  const int start = cu[b], P = attn_prefix(cu, b, pmax, bad);
   // rotary coefficients (Section 2.1's decoder layers use RoPE; the cached
   // prefix keys are stored rotated): the query sits at the last cascade
   // position, cascade key j at P + j (one position, P, per layer otherwise).
@@ -644,6 +651,11 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     sc = sexp2(mc, M);
     L = l * sp + s_lc[rr] * sc;
   }
+  if (bad) {  // P_b outside [0, pmax]: the sequence's output is NaN
+    M = 0.f;
+    L = __int_as_float(0x7fc00000);
+    sp = L;
+  }
   if (npieces > 0 && g == 0 && r < GH)
     part_ml[(size_t)nseq * Hq * nch_ld * 2 + (size_t)b * Hq + h0 + r] = (float)npieces;
   if (r >= GH) return;  // padding columns of the MFMA tiles
@@ -676,7 +688,8 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     // heads fastest so the workgroups that run side by side read neighbouring
     // head segments of the same token rows; partial slot = span index
     const int b = blockIdx.z, col = blockIdx.x, ch = blockIdx.y;
-    const int P = cu[b + 1] - cu[b];
+    bool bad;
+    const int P = attn_prefix(cu, b, pmax, bad);
     const int nv = max(1, min((P + span - 1) / span, nch));
     if (csplit) {
       // the cascade keys as a unit of their own (grid y = nch), off the
@@ -689,22 +702,20 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     if (ch < nv) unit(b, col, ch * cpw, cpw, ch, nv == 1, 0, ch == 0);
     return;
   }
-  // Persistent: a grid of resident waves.  The chunks of all (sequence, column)
-  // segments, numbered sequence by sequence, column by column, are cut into W
-  // equal contiguous ranges, one per wave, so the waves finish together however
-  // ragged the sequences are (W = the grid, or the chunk count if smaller).  A
-  // range crossing segments does one piece per segment.  Range w starts at
-  // chunk floor(T w / W), so the pieces of the segment at [S, S + n) are
-  // numbered by the range starts they contain: piece at x has partial slot
-  // starts(x) - starts(S), starts(y) = #{w >= 1 : floor(T w / W) <= y}.  Up to 256
-  // sequences (4 per lane).
+  // Persistent: a grid of resident waves, each taking one range of the
+  // equal-chunk split (AttnSplit; W = the grid, or the chunk count if
+  // smaller), so the waves finish together however ragged the sequences are.
+  // Up to 256 sequences (4 per lane).
   int ucnt[4], uend[4];  // chunks of sequence lane + 64 i (all columns), running total
   int run = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int b = lane + 64 * i;
     int n = 0;
-    if (b < nseq) n = max(1, min((cu[b + 1] - cu[b] + kAttnChunk - 1) / kAttnChunk, nch_ld)) * ncols;
+    if (b < nseq) {
+      bool bad;
+      n = attn_seg_chunks(attn_prefix(cu, b, pmax, bad), nch_ld) * ncols;
+    }
     // inclusive scan over the wave, then add the totals of earlier blocks
     int x = n;
 #pragma unroll
@@ -716,13 +727,10 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     uend[i] = run + x;
     run += __shfl(x, 63, 64);
   }
-  const long total = run;
-  const long W = min((long)gridDim.x, total);
-  if ((long)blockIdx.x >= W) return;
-  // boundaries in [1, y]: w >= 1 with T w < (y + 1) W
-  auto starts = [&](long y) { return min(W - 1, ((y + 1) * W + total - 1) / total - 1); };
-  int x = (int)(total * blockIdx.x / W);
-  const int xe = (int)(total * (blockIdx.x + 1) / W);
+  const AttnSplit eq{run, min((long)gridDim.x, (long)run)};
+  if ((long)blockIdx.x >= eq.W) return;
+  int x = eq.begin(blockIdx.x);
+  const int xe = eq.begin(blockIdx.x + 1);
   while (x < xe) {
     // sequence b: the number of sequences whose chunks all come before x
     int b = 0;
@@ -737,12 +745,8 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
         cnt = n;
       }
     }
-    const int nch_b = cnt / ncols, off = x - first;
-    const int col = off / nch_b, ch0 = off % nch_b;
-    const int n = min(nch_b - ch0, xe - x);
-    const long S = x - ch0;
-    const int slot = (int)(starts(x) - starts(S));
-    const int np = ch0 == 0 ? (int)(starts(S + nch_b - 1) - starts(S)) + 1 : 0;
+    int col, ch0, n, slot, np;
+    eq.piece(x, xe, first, cnt, ncols, col, ch0, n, slot, np);
     unit(b, col, ch0, n, slot, false, np, ch0 == 0);
     x += n;
   }
@@ -761,7 +765,7 @@ template <typename T, bool LOG2>
 __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ part, int nch_ld,
                                                     const int32_t *__restrict__ cu, int span,
                                                     int nwg, T *__restrict__ out, int Hq, int D,
-                                                    int counted, int csplit) {
+                                                    int counted, int csplit, int pmax) {
   const int b = blockIdx.y;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= Hq * D / 2) return;
@@ -773,7 +777,8 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ pa
   if (counted) {
     nv = (int)part[(size_t)gridDim.y * Hq * nch_ld * (D + 2) + (size_t)b * Hq + h];
   } else {
-    const int P = cu[b + 1] - cu[b];
+    bool bad;
+    const int P = attn_prefix(cu, b, pmax, bad);
     nv = max(1, min((P + span - 1) / span, nwg)) + csplit;
     if (nv == 1) return;
   }
@@ -818,7 +823,7 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ pa
 template <typename T, int D>
 static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const float *q,
                          const float *knew, const float *vnew, int nctx, float *part, int nch,
-                         int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
+                         int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int pmax,
                          hipStream_t s) {
   const int G = Hq / Hkv;
   const int GH = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
@@ -826,7 +831,7 @@ static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const 
   const dim3 grid(Hkv * (G / GH), nwg, B);
 #define FE_ATTN(GHV)                                                                            \
   hipLaunchKernelGGL((k_attn<T, D, GHV>), grid, dim3(256), 0, s, (const T *)K, (const T *)V, cu, \
-                     q, knew, vnew, nctx, part, nwg, nch_ld, cpw, (T *)out, Hq, Hkv)
+                     q, knew, vnew, nctx, part, nwg, nch_ld, cpw, (T *)out, Hq, Hkv, pmax)
   if (GH == 4) FE_ATTN(4);
   else if (GH == 2) FE_ATTN(2);
   else FE_ATTN(1);
@@ -853,8 +858,8 @@ template <int D>
 static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, const float *q,
                              const float *knew, const float *vnew, int nctx, float *part, int nch,
                              int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
-                             const float *rope, int cascade, int *persisted, int *csplit,
-                             hipStream_t s) {
+                             const float *rope, int cascade, int pmax, int *persisted,
+                             int *csplit, hipStream_t s) {
   const int G = Hq / Hkv;
   // query heads per wave (the MFMA tiles have 16 columns; more than 8 heads
   // would spill the cascade step's registers)
@@ -875,7 +880,7 @@ static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, co
 #define FE_ATTN(GHV, DEP, NCXV)                                                                  \
   hipLaunchKernelGGL((k_attn_mma<D, GHV, DEP, NCXV>), grid, dim3(64), 0, s, (const bf16_t *)K,   \
                      (const bf16_t *)V, cu, q, knew, vnew, nctx, part, nwg, nch_ld, cpw,         \
-                     (bf16_t *)out, Hq, Hkv, rope, cascade, B, persist, split)
+                     (bf16_t *)out, Hq, Hkv, rope, cascade, B, persist, split, pmax)
 #define FE_ATTN_NCX(GHV, DEP)                                                                    \
   if (nctx <= 8) FE_ATTN(GHV, DEP, 8);                                                           \
   else FE_ATTN(GHV, DEP, kMaxLayers)
@@ -908,7 +913,7 @@ int attention_cpw(int B, int Hkv, int ngroups, int nch) {
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
                      const float *knew, const float *vnew, int nctx, float *part, int nch,
                      int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int D,
-                     const float *rope, int cascade, hipStream_t s) {
+                     const float *rope, int cascade, int pmax, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   if (cpw < 1) cpw = 1;
   hipError_t e;
@@ -916,24 +921,24 @@ hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, co
   if (nctx < 1 || nctx > kMaxLayers) return hipErrorInvalidValue;
   if (dt)
     e = D == 128 ? attn_mma_t<128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                   Hq, Hkv, rope, cascade, &persisted, &csplit, s)
+                                   Hq, Hkv, rope, cascade, pmax, &persisted, &csplit, s)
                  : attn_mma_t<64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out, B,
-                                  Hq, Hkv, rope, cascade, &persisted, &csplit, s);
+                                  Hq, Hkv, rope, cascade, pmax, &persisted, &csplit, s);
   else
     e = D == 128 ? attn_t<float, 128>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
-                                      B, Hq, Hkv, s)
+                                      B, Hq, Hkv, pmax, s)
                  : attn_t<float, 64>(K, V, cu, q, knew, vnew, nctx, part, nch, nch_ld, cpw, out,
-                                     B, Hq, Hkv, s);
+                                     B, Hq, Hkv, pmax, s);
   if (e != hipSuccess) return e;
   const int nwg = nch < 1 ? 1 : (nch + cpw - 1) / cpw;
   if (nwg == 1 && !persisted) return hipSuccess;  // every sequence fits one workgroup
   const dim3 grid((Hq * D / 2 + 255) / 256, B);
   if (dt)
     hipLaunchKernelGGL((k_attn_merge<bf16_t, true>), grid, dim3(256), 0, s, part, nch_ld, cu,
-                       kAttnChunk * cpw, nwg, (bf16_t *)out, Hq, D, persisted, csplit);
+                       kAttnChunk * cpw, nwg, (bf16_t *)out, Hq, D, persisted, csplit, pmax);
   else
     hipLaunchKernelGGL((k_attn_merge<float, false>), grid, dim3(256), 0, s, part, nch_ld, cu,
-                       kAttnChunk * cpw, nwg, (float *)out, Hq, D, 0, 0);
+                       kAttnChunk * cpw, nwg, (float *)out, Hq, D, 0, 0, pmax);
   return hipGetLastError();
 }
 

@@ -158,6 +158,54 @@ constexpr int kMergeMaxCand = 256 * 32;
 constexpr int kGemmMaxRows = 256;
 constexpr int kMaxTopk = 16;
 
+// Prefix length of sequence b as the attention kernels use it: P_b from the
+// packed offsets, or 0 with bad = true when it lies outside [0, pmax] (the
+// caller's bound on every P_b).  A bad sequence reads no cache row and its
+// attention output is NaN.
+__host__ __device__ inline int attn_prefix(const int32_t *cu, int b, int pmax, bool &bad) {
+  const int P = cu[b + 1] - cu[b];
+  bad = P < 0 || P > pmax;
+  return bad ? 0 : P;
+}
+
+// Equal-chunk split of the persistent attention.  The 64-key chunks of all
+// (sequence, column) segments, numbered sequence by sequence and column by
+// column (total of them), are cut into W contiguous ranges, range w starting at
+// chunk floor(total * w / W).  A range crossing segments does one piece per
+// segment.  The pieces of the segment at [S, S + n) are numbered by the range
+// starts they contain: the piece at chunk x takes partial slot
+// starts(x) - starts(S), where starts(y) counts the w >= 1 whose range begins
+// at or before y.
+struct AttnSplit {
+  long total, W;
+  __host__ __device__ long starts(long y) const {
+    const long v = ((y + 1) * W + total - 1) / total - 1;
+    return v < W - 1 ? v : W - 1;
+  }
+  __host__ __device__ int begin(long w) const { return (int)(total * w / W); }
+  // The piece of range [.., xe) that starts at chunk x, inside the segment of
+  // sequence b whose chunks (all columns) are [first, first + cnt), ncols
+  // columns of cnt / ncols chunks each: its column, first chunk, chunk count,
+  // partial slot, and (first piece of a column's segment only, else 0) the
+  // number of pieces of that segment.
+  __host__ __device__ void piece(int x, int xe, int first, int cnt, int ncols, int &col, int &ch0,
+                                 int &n, int &slot, int &npieces) const {
+    const int nch_b = cnt / ncols, off = x - first;
+    col = off / nch_b;
+    ch0 = off % nch_b;
+    n = nch_b - ch0 < xe - x ? nch_b - ch0 : xe - x;
+    const long S = (long)x - ch0;
+    slot = (int)(starts(x) - starts(S));
+    npieces = ch0 == 0 ? (int)(starts(S + nch_b - 1) - starts(S)) + 1 : 0;
+  }
+};
+// Chunks of one (sequence, column) segment: at least one (the cascade keys of
+// an empty prefix), at most nch_ld.
+__host__ __device__ inline int attn_seg_chunks(int P, int nch_ld) {
+  const int n = (P + kAttnChunk - 1) / kAttnChunk;
+  return n < 1 ? 1 : (n > nch_ld ? nch_ld : n);
+}
+
 // Row m of a GEMM's A operand is row (m / per) * outer + j0 + m % per of its buffer.
 struct ARows {
   int per, j0, outer;
@@ -297,7 +345,8 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
                         hipStream_t s);
 
 // Attention of the query rows q [B, Hq, D] over the prefix cache (chunks
-// 0..nch-1 of kAttnChunk keys; keys beyond are not read) and the nctx cascade
+// 0..nch-1 of kAttnChunk keys; keys beyond are not read; a sequence whose P_b
+// lies outside [0, pmax] reads no cache row and gets NaN rows) and the nctx cascade
 // keys/values knew/vnew [B, nctx, Hkv, D] -> out [B, Hq*D] (storage type).
 // bf16: q and the cascade keys arrive unrotated and are rotated here with the
 // table `rope` (cascade != 0: cascade row j at position P + j, else P); fp32:
@@ -310,7 +359,7 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
                      const float *q, const float *knew, const float *vnew, int nctx,
                      float *part, int nch, int nch_ld, int cpw, void *out, int B, int Hq,
-                     int Hkv, int D, const float *rope, int cascade, hipStream_t s);
+                     int Hkv, int D, const float *rope, int cascade, int pmax, hipStream_t s);
 // kAttnChunk-key chunks per attention work unit for a launch of B sequences
 // over nch = ceil(max_prefix / kAttnChunk) chunks
 int attention_cpw(int B, int Hkv, int ngroups, int nch);

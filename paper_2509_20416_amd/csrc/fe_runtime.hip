@@ -357,7 +357,8 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     // attention over the layer's prefix cache plus the cascade keys
     FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
                                       vnew, nctx, part, nch, nch_ld, cpw, ao, B, Hq, Hkv, D,
-                                      (const float *)(ws + L.rope), cascade ? 1 : 0, s));
+                                      (const float *)(ws + L.rope), cascade ? 1 : 0,
+                                      kv->max_prefix, s));
     // x' = x_{i-1} + W_o o
     GainCopies gc_p{};
     if (fuse_m) {
@@ -542,6 +543,50 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
   FE_TRY(hipEventElapsedTime(&ms, h->ev_a, h->ev_b));
   *ms_per_launch = ms / (float)(repeats * per_pass);
   *launches = per_pass;
+  return FE_OK;
+}
+
+// Test export (host only, no device work): the pieces the persistent bf16
+// attention's waves take for the given prefix lengths, from the same split
+// arithmetic the kernel runs (AttnSplit, attn_prefix, attn_seg_chunks).
+extern "C" fe_status fe_test_attn_split(const int32_t *prefix_lens, int32_t batch, int32_t ncols,
+                                        int32_t nch_ld, int32_t pmax, int32_t waves,
+                                        int32_t *pieces, int32_t max_pieces, int32_t *n_pieces) {
+  if (!prefix_lens || (!pieces && max_pieces > 0) || !n_pieces || batch < 1 || batch > 256 || ncols < 1 ||
+      nch_ld < 1 || waves < 1 || max_pieces < 0)
+    return fail(FE_E_INVALID, "bad arguments");
+  std::vector<int32_t> cu(batch + 1, 0);
+  for (int b = 0; b < batch; ++b) cu[b + 1] = cu[b] + prefix_lens[b];
+  std::vector<long> uend(batch);
+  std::vector<int> ucnt(batch);
+  long run = 0;
+  for (int b = 0; b < batch; ++b) {
+    bool bad;
+    ucnt[b] = attn_seg_chunks(attn_prefix(cu.data(), b, pmax, bad), nch_ld) * ncols;
+    run += ucnt[b];
+    uend[b] = run;
+  }
+  const AttnSplit eq{run, std::min<long>(waves, run)};
+  int np_out = 0;
+  for (long w = 0; w < eq.W; ++w) {
+    int x = eq.begin(w);
+    const int xe = eq.begin(w + 1);
+    while (x < xe) {
+      int b = 0;
+      while (b < batch && uend[b] <= x) ++b;  // sequences wholly before chunk x
+      if (b >= batch) return fail(FE_E_INVALID, "split walked past the last sequence");
+      int col, ch0, n, slot, np;
+      eq.piece(x, xe, (int)(uend[b] - ucnt[b]), ucnt[b], ncols, col, ch0, n, slot, np);
+      if (np_out < max_pieces) {
+        int32_t *r = pieces + (size_t)np_out * 7;
+        r[0] = (int32_t)w; r[1] = b; r[2] = col; r[3] = ch0; r[4] = n; r[5] = slot; r[6] = np;
+      }
+      ++np_out;
+      if (n < 1) return fail(FE_E_INVALID, "empty piece");
+      x += n;
+    }
+  }
+  *n_pieces = np_out;
   return FE_OK;
 }
 

@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
            "fe_build_tree",
            "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
-           "fe_drafter_destroy", "fe_last_error")
+           "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
 
@@ -116,6 +116,9 @@ def lib() -> C.CDLL:
         L.fe_time_stage.restype = C.c_int
         L.fe_time_stage.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
                                     C.POINTER(C.c_float), C.POINTER(C.c_int32)]
+        L.fe_test_attn_split.restype = C.c_int
+        L.fe_test_attn_split.argtypes = [C.c_void_p] + [C.c_int32] * 5 + [C.c_void_p, C.c_int32,
+                                                                         C.c_void_p]
         L.fe_drafter_destroy.restype = None
         L.fe_drafter_destroy.argtypes = [C.c_void_p]
         L.fe_last_error.restype = C.c_char_p
@@ -219,3 +222,17 @@ def fe_time_stage(h: int, stage: int, repeats: int, stream: int):
 
 def fe_drafter_destroy(h: int) -> None:
     lib().fe_drafter_destroy(C.c_void_p(h))
+
+
+def fe_test_attn_split(prefix_lens, ncols: int, nch_ld: int, pmax: int, waves: int):
+    """Pieces [n, 7] (wave, sequence, column, first chunk, chunks, slot, pieces of
+    the segment or 0) of the persistent attention's split, computed on the host."""
+    import numpy as np
+    pl = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+    n = C.c_int32()
+    check(lib().fe_test_attn_split(pl.ctypes.data, len(pl), ncols, nch_ld, pmax, waves, None, 0,
+                                   C.byref(n)))
+    out = np.zeros((max(1, n.value), 7), np.int32)
+    check(lib().fe_test_attn_split(pl.ctypes.data, len(pl), ncols, nch_ld, pmax, waves,
+                                   out.ctypes.data, n.value, C.byref(n)))
+    return out[:n.value]

@@ -110,7 +110,10 @@ def test_accept_greedy_bit_exact(N, k, B):
 
 
 # --- small shapes: several tiles, ragged chunks, ragged batch, P = 0 -----------------------
-SMALL = [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128, C.TINY_F32_B1]
+SMALL = [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128, C.TINY_F32_B1,
+         # 8 query heads per KV head (the attention variant only the 70B shape uses
+         # at full size) and 2 per KV head, bf16 and fp32
+         C.SMALL_GQA8_BF16_D128, C.SMALL_GQA2_BF16, C.SMALL_GQA2_F32]
 
 
 @pytest.mark.parametrize("ctx", ["cascade", "self", "parallel"])
@@ -120,6 +123,8 @@ def test_small_parity(cfg, ctx):
     plens = None
     if cfg.batch == 3:
         plens = np.array([0, 700, 65], np.int32)   # empty prefix, several chunks, ragged tail
+    elif cfg.batch == 2 and cfg.head_dim == 64:
+        plens = np.array([400, 1], np.int32)
     rep, _, _ = _run(cfg, seed=1, prefix_lens=plens)
     if cfg.dtype == "f32":
         assert rep["decided"] >= rep["ranks"] // 2, rep
@@ -142,7 +147,8 @@ def test_deep_cascade_parity(cfg):
 # partial, merged by the second launch), 2 and 3 (the sub-chunk loop with a
 # ragged last workgroup), 8 (one workgroup per sequence, no merge launch).
 @pytest.mark.parametrize("split", [1, 2, 3, 8])
-@pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128],
+@pytest.mark.parametrize("cfg", [C.SMALL_GQA_BF16, C.SMALL_GQA_F32, C.SMALL_MHA_BF16_D128,
+                                 C.SMALL_GQA8_BF16_D128, C.SMALL_GQA2_BF16],
                          ids=lambda c: c.name)
 def test_attention_split_parity(cfg, split):
     plens = np.array([0, 700, 65], np.int32) if cfg.batch == 3 else np.array([300, 129], np.int32)
@@ -183,7 +189,12 @@ def test_batched_rows_parity(cfg):
 @pytest.mark.parametrize("graph", [False, True])
 @pytest.mark.parametrize("cfg,split", [
     (C.SMALL_GQA_BF16.with_(batch=36, prefix=(0, 3000), name="small_gqa_bf16_b36_p3000"), None),
-    (C.SMALL_MHA_BF16_D128.with_(batch=24, prefix=(0, 2000), name="small_mha_bf16_d128_b24"), 2)],
+    (C.SMALL_MHA_BF16_D128.with_(batch=24, prefix=(0, 2000), name="small_mha_bf16_d128_b24"), 2),
+    (C.SMALL_GQA8_BF16_D128.with_(batch=40, prefix=(0, 3000), name="small_gqa8_bf16_d128_b40"),
+     None),
+    (C.SMALL_GQA8_BF16_D128.with_(batch=24, prefix=(0, 2000), cascade_ctx="self",
+                                  name="small_gqa8_bf16_d128_b24_self"), 2),
+    (C.SMALL_GQA2_BF16.with_(batch=48, prefix=(0, 4000), name="small_gqa2_bf16_b48"), None)],
     ids=lambda v: v.name if hasattr(v, "name") else str(v))
 def test_attention_queue_parity(cfg, split, graph):
     _run(cfg, seed=6, attn_split=split, graph=graph)
@@ -280,6 +291,35 @@ def test_invalid_token_poisons_only_its_sequence():
     dr.close()
 
 
+@pytest.mark.parametrize("cfg,plens,pmax", [
+    (C.SMALL_GQA_BF16, [0, 700, 65], 100),                       # one unit per span
+    (C.SMALL_GQA_F32, [0, 700, 65], 100),
+    (C.SMALL_GQA_BF16.with_(batch=36, prefix=(0, 3000), name="small_gqa_bf16_b36_p3000"),
+     None, 1500)],                                                # persistent waves
+    ids=["bf16", "f32", "bf16_persistent"])
+def test_prefix_above_bound_poisons_only_its_sequence(cfg, plens, pmax):
+    """A P_b above the view's max_prefix (a contract violation the host cannot
+    see) reads no cache row: that sequence's states from x_1 on are NaN, and
+    every other sequence is unchanged, bit for bit."""
+    import torch
+    from paper_2509_20416_amd import Drafter
+    w = make_weights(cfg, 8)
+    inp = make_inputs(cfg, 8, None if plens is None else np.array(plens, np.int32))
+    P = np.asarray(inp.prefix_lens)
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(P.max()))
+    ref = {n: t.cpu().numpy() for n, t in dr.forward(dr.upload_inputs(inp), hidden=True).items()}
+    out = {n: t.cpu().numpy()
+           for n, t in dr.forward(dr.upload_inputs(inp, max_prefix=pmax), hidden=True).items()}
+    torch.cuda.synchronize()
+    bad = P > pmax
+    assert bad.any() and not bad.all()
+    assert np.isnan(out["hidden"][bad][:, 1:]).all()
+    np.testing.assert_array_equal(out["hidden"][bad][:, 0], ref["hidden"][bad][:, 0])
+    for n in ("hidden", "topk_ids", "topk_probs", "topk_draft"):
+        np.testing.assert_array_equal(out[n][~bad], ref[n][~bad], err_msg=n)
+    dr.close()
+
+
 # --- paper-shaped workloads at full size, in the configuration the bench times -----------
 @pytest.mark.timeout(900)
 def test_llama8b_b1_full():
@@ -299,14 +339,54 @@ def test_vicuna13b_b1_full():
 
 @pytest.mark.timeout(1200)
 def test_llama70b_b1_full():
-    _run(C.LLAMA70B_BF16_B1, seed=0, graph=True, with_debug=False)
+    """Element-wise cascade states and logits at the 70B shapes (8 query heads per
+    KV head, head dim 128, P = 4096)."""
+    _run(C.LLAMA70B_BF16_B1, seed=0, graph=True)
 
 
 @pytest.mark.timeout(1200)
-def test_llama8b_b32_ragged_sampled():
-    """Batch 32, P_b ~ U[256, 8192]: oracle on the shortest and the longest sequence."""
-    from fe_synth import make_prefix_lens
-    cfg = C.LLAMA8B_BF16_B32
-    plens = make_prefix_lens(cfg, 0)
-    sample = [int(np.argmin(plens)), int(np.argmax(plens))]
-    _run(cfg, seed=0, graph=True, sample=sample)
+def test_llama8b_b32_ragged_all():
+    """Batch 32, P_b ~ U[256, 8192], N = 7: every sequence against the oracle."""
+    _run(C.LLAMA8B_BF16_B32, seed=0, graph=True)
+
+
+def _planted_lm_head(cfg, w, ref_hidden, b, base_ids, top=None):
+    """LM-head rows planted so that every level of sequence b has a top-k with wide,
+    known gaps: for level l the k rows s_rho * u_l, with u_l the dual basis of the
+    N final-normalised cascade states of b (u_l . hn_j = 1 if j = l else 0), so a
+    planted row scores s_rho at its own level and about 0 at the others.  Returns
+    the planted draft ids [N, k] in rank order."""
+    from fe_synth import to_f64
+    N, k = cfg.n_layers, cfg.topk
+    g = to_f64(w.final_norm, cfg.dtype)
+    hs = ref_hidden[b, 1:N + 1]
+    hn = g * hs / np.sqrt(np.mean(hs * hs, axis=1, keepdims=True) + cfg.rms_eps)   # [N, d]
+    U = np.linalg.pinv(hn)                                                          # [d, N]
+    top = top if top is not None else 2.0 * k + 14.0
+    scale = top - 2.0 * np.arange(k)                  # gaps of 2, lowest well above random logits
+    ids = np.asarray(base_ids, np.int64).reshape(N, k)
+    rows = (scale[None, :, None] * U.T[:, None, :]).reshape(N * k, -1).astype(np.float32)
+    if cfg.dtype == "bf16":
+        bits = rows.view(np.uint32)
+        w.lm_head[ids.reshape(-1)] = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16).astype(np.uint16)
+    else:
+        w.lm_head[ids.reshape(-1)] = rows
+    return ids
+
+
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("cfg", [C.LLAMA8B_BF16_B1, C.LLAMA70B_BF16_B1], ids=lambda c: c.name)
+def test_planted_topk_full_size(cfg):
+    """At the full 8B / 70B shapes, in graph mode: every level of the sequence gets a
+    planted top-k, so every one of the N * k ranks is decided by the oracle and must
+    match through the 500-tile LM head and the top-k merge."""
+    from oracle import feo
+    w = make_weights(cfg, 0)
+    inp = make_inputs(cfg, 0)
+    ref = feo.draft_forward(cfg, w, inp, want_logits=False)
+    rng = np.random.default_rng(11)
+    ids = _planted_lm_head(cfg, w, ref["hidden"], 0,
+                           rng.choice(cfg.draft_vocab, cfg.n_layers * cfg.topk, replace=False))
+    rep, res, _ = _run(cfg, seed=0, graph=True, weights=w, inputs=inp)
+    assert rep["decided"] == rep["ranks"] == cfg.n_layers * cfg.topk, rep
+    np.testing.assert_array_equal(res["topk_draft"][0], ids)
