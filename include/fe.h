@@ -264,6 +264,27 @@ fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
                        const int32_t *tokens, const int32_t *positions, const int32_t *dst_rows,
                        const fe_kv_cache *cache, void *workspace, size_t ws_bytes, void *stream);
 
+/* Bytes of the device array fe_kv_update_noalloc works in (8 MiB per GPU). */
+#define FE_KV_UPDATE_SCRATCH_BYTES (8 << 20)
+
+/* fe_kv_update for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same computation, rows and errors, but its workspace is a file-scope device
+ * array of FE_KV_UPDATE_SCRATCH_BYTES bytes inside the library, one per GPU,
+ * held until the process ends, instead of a caller buffer.  The rows are
+ * processed in chunks of the most rows that fit it, exactly as fe_kv_update
+ * does with a workspace of that size (so the two give bitwise equal caches).
+ * The call allocates nothing: no hipMalloc, no hipFree; its first call on a
+ * device looks up that device's array address (hipGetSymbolAddress).
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on one
+ * GPU, on any streams or handles, race and must be serialised by the caller.
+ * Errors as fe_kv_update, without the workspace ones, plus FE_E_UNSUPPORTED
+ * when one row of the config needs more than the array holds. */
+fe_status fe_kv_update_noalloc(fe_drafter *h, int32_t n_rows, const void *features,
+                               const int32_t *tokens, const int32_t *positions,
+                               const int32_t *dst_rows, const fe_kv_cache *cache, void *stream);
+
 /* Speculative-sampling acceptance of a drafting cycle at temperature T
  * (Section 2.4, parallel verification, with the sampling of Section 3 at
  * T > 0), one workgroup per sequence.  Walking from the root, the children of

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -621,10 +622,11 @@ extern "C" size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chu
 // Drafter cache rows of verified positions (Section 2.4 update step, cascade
 // context): x_0 of every row as in the pass (Eq. 1), then per layer its
 // RMSNorm and the rotated K / V projections, scattered into the caches.
-extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
-                                  const int32_t *tokens, const int32_t *positions,
-                                  const int32_t *dst_rows, const fe_kv_cache *cache,
-                                  void *workspace, size_t ws_bytes, void *stream) {
+namespace {
+fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
+                         const int32_t *tokens, const int32_t *positions,
+                         const int32_t *dst_rows, const fe_kv_cache *cache, void *workspace,
+                         size_t ws_bytes, void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (c.cascade_ctx == FE_CTX_SELF)
@@ -750,6 +752,52 @@ extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *fea
   }
   (void)kvd;
   return FE_OK;
+}
+}  // namespace
+
+extern "C" fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
+                                  const int32_t *tokens, const int32_t *positions,
+                                  const int32_t *dst_rows, const fe_kv_cache *cache,
+                                  void *workspace, size_t ws_bytes, void *stream) {
+  return kv_update_impl(h, n_rows, features, tokens, positions, dst_rows, cache, workspace,
+                        ws_bytes, stream);
+}
+
+// Workspace of fe_kv_update_noalloc: a file-scope device array, one copy per
+// GPU, held until the process ends.  Host code never passes the array's name
+// to a kernel or a copy: it stands for a host-side symbol, not a device
+// address; the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[FE_KV_UPDATE_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+void *g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+std::once_flag g_scratch_once[kMaxDevices];
+}  // namespace
+
+extern "C" fe_status fe_kv_update_noalloc(fe_drafter *h, int32_t n_rows, const void *features,
+                                          const int32_t *tokens, const int32_t *positions,
+                                          const int32_t *dst_rows, const fe_kv_cache *cache,
+                                          void *stream) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  const size_t one_row = upd_layout_of(h->cfg, 1).total;
+  if (one_row > (size_t)FE_KV_UPDATE_SCRATCH_BYTES)
+    return fail(FE_E_UNSUPPORTED,
+                "one row of this config needs %zu bytes of workspace, above the %d bytes of "
+                "fe_kv_update_noalloc's device array; use fe_kv_update", one_row,
+                (int)FE_KV_UPDATE_SCRATCH_BYTES);
+  int dev = 0;
+  FE_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(FE_E_INVALID, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::call_once(g_scratch_once[dev], [dev] {
+    g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+  });
+  if (g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev])
+    return fail(FE_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                hipGetErrorString(g_scratch_err[dev]));
+  return kv_update_impl(h, n_rows, features, tokens, positions, dst_rows, cache,
+                        g_scratch_ptr[dev], (size_t)FE_KV_UPDATE_SCRATCH_BYTES, stream);
 }
 
 extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk,

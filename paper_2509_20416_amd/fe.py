@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
            "fe_build_tree",
-           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
+           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
            "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
 
@@ -109,6 +109,9 @@ def lib() -> C.CDLL:
         L.fe_kv_update.restype = C.c_int
         L.fe_kv_update.argtypes = [C.c_void_p, C.c_int32] + [C.c_void_p] * 4 + \
             [C.POINTER(fe_kv_cache), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.fe_kv_update_noalloc.restype = C.c_int
+        L.fe_kv_update_noalloc.argtypes = [C.c_void_p, C.c_int32] + [C.c_void_p] * 4 + \
+            [C.POINTER(fe_kv_cache), C.c_void_p]
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
         L.fe_set_attention_split.restype = C.c_int
@@ -201,6 +204,16 @@ def fe_kv_update(h: int, n_rows: int, features: int, tokens: int, positions: int
                              C.c_void_p(tokens), C.c_void_p(positions), C.c_void_p(dst_rows),
                              C.byref(cache), C.c_void_p(workspace), C.c_size_t(ws_bytes),
                              C.c_void_p(stream)))
+
+
+FE_KV_UPDATE_SCRATCH_BYTES = 8 << 20   # include/fe.h
+
+
+def fe_kv_update_noalloc(h: int, n_rows: int, features: int, tokens: int, positions: int,
+                         dst_rows: int, cache: fe_kv_cache, stream: int) -> None:
+    check(lib().fe_kv_update_noalloc(C.c_void_p(h), int(n_rows), C.c_void_p(features),
+                                     C.c_void_p(tokens), C.c_void_p(positions),
+                                     C.c_void_p(dst_rows), C.byref(cache), C.c_void_p(stream)))
 
 
 def fe_set_graph_mode(h: int, on: bool) -> None:
