@@ -114,6 +114,26 @@ SMALL_GQA2_BF16 = DrafterConfig(
 SMALL_GQA2_F32 = SMALL_GQA2_BF16.with_(name="small_gqa2_f32", dtype="f32")
 
 
+# Batch-1 shapes whose widths are multiples of 512 (d, 3d, 2d, H_q * D, I), as
+# the persistent batch-1 pass needs: GQA with head dim 64, 8 query heads per KV
+# head with head dim 128, and multi-head attention with head dim 128 and the
+# deepest cascade the persistent pass takes (8 layers).
+SMALL_PASS_GQA = DrafterConfig(
+    name="small_pass_gqa", hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=64,
+    intermediate=1536, n_layers=3, draft_vocab=2000, target_vocab=5003,
+    rope_theta=500000.0, dtype="bf16", batch=1, prefix=700, topk=5)
+
+SMALL_PASS_GQA8 = DrafterConfig(
+    name="small_pass_gqa8", hidden=1024, n_q_heads=16, n_kv_heads=2, head_dim=128,
+    intermediate=2048, n_layers=4, draft_vocab=3008, target_vocab=7001,
+    rope_theta=500000.0, dtype="bf16", batch=1, prefix=300, topk=8)
+
+SMALL_PASS_MHA_N8 = DrafterConfig(
+    name="small_pass_mha_n8", hidden=1024, n_q_heads=8, n_kv_heads=8, head_dim=128,
+    intermediate=2560, n_layers=8, draft_vocab=1504, target_vocab=1504,
+    rope_theta=10000.0, dtype="bf16", batch=1, prefix=129, topk=3)
+
+
 def prefix_range(cfg: DrafterConfig) -> Tuple[int, int]:
     if isinstance(cfg.prefix, int):
         return cfg.prefix, cfg.prefix

@@ -344,6 +344,27 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
  * [0, 65536]. */
 fe_status fe_set_attention_split(fe_drafter *h, int32_t chunks_per_workgroup);
 
+/* How a batch-1 pass is launched.  Mode 1 (the default, and the only mode
+ * available): every stage is its own launch.  Mode 0 would run, when the shape
+ * allows (bf16, batch 1, greedy top-k, n_layers <= 8, the fusion/input/hidden/
+ * intermediate/H_q*D widths multiples of 512), the stages between two
+ * attention launches as ONE launch of resident workgroups, one per compute
+ * unit, passing results to each other through tagged words in the workspace;
+ * it is switched off in this build (its first device run faulted, the cause is
+ * not found) and asking for it returns FE_E_UNSUPPORTED.  Errors:
+ * FE_E_INVALID for a NULL handle or another mode, FE_E_UNSUPPORTED for mode 0. */
+fe_status fe_set_pass_mode(fe_drafter *h, int32_t mode);
+
+/* Waits for `stream`, then reports and clears the persistent pass's status
+ * word: 0 when every wait of every persistent launch so far completed; bit 0
+ * set when a workgroup gave up waiting for another's results (a bounded
+ * wait; the kernel still ended normally, but that pass's outputs are
+ * unspecified), which happens only when the workgroups of one launch cannot
+ * all be resident at once (the launch uses one per compute unit).  Bit 16 is
+ * set when the most recent pass on the handle ran as persistent launches.
+ * Errors: FE_E_INVALID for NULL arguments, FE_E_HIP. */
+fe_status fe_pass_status(fe_drafter *h, void *stream, int32_t *status);
+
 /* Stages of the pass whose kernel launches can be timed with HIP events. */
 typedef enum {
   FE_STAGE_FUSE = 0,     /* g_t = FC(l, m, h) and the embedding gather (one launch) */
@@ -353,11 +374,14 @@ typedef enum {
   FE_STAGE_OPROJ = 4,    /* per layer: output projection + residual */
   FE_STAGE_GATEUP = 5,   /* per layer: gate/up projections + SwiGLU */
   FE_STAGE_DOWN = 6,     /* per layer: down projection + residual */
-  FE_STAGE_LMHEAD = 7    /* LM head on all N states + tile softmax statistics and top-k */
+  FE_STAGE_LMHEAD = 7,   /* LM head on all N states + tile softmax statistics and top-k */
+  FE_STAGE_PASS = 8      /* the whole pass as fe_draft_forward runs it (one "launch" = one pass) */
 } fe_stage;
 
 /* Kernel timing for roofline measurements: replays every launch of `stage`
- * from the most recent fe_draft_forward on this handle, `repeats` times back to
+ * (stages 0..7 in their one-launch-per-stage form; FE_STAGE_PASS: the whole
+ * pass as fe_draft_forward launches it) from the most recent fe_draft_forward
+ * on this handle, `repeats` times back to
  * back on `stream`, between two HIP events recorded on that stream, waits for
  * them, and writes the mean duration of one launch (ms) to *ms_per_launch and
  * the number of launches of the stage in one pass to *launches.  The buffers

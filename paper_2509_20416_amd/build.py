@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfe.so")
-SOURCES = ["fe_gemm.hip", "fe_attn.hip", "fe_misc.hip", "fe_runtime.hip"]
+SOURCES = ["fe_gemm.hip", "fe_attn.hip", "fe_misc.hip", "fe_pass.hip", "fe_runtime.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -402,6 +402,68 @@ struct TreeRows {
   int32_t *retrieve = nullptr;
 };
 
+// ---- persistent batch-1 pass (fe_pass.hip) -----------------------------------
+// Between two attention launches the stages of a batch-1 pass run inside one
+// launch of resident workgroups (one per compute unit) that hand results to
+// each other as tagged 64-bit words (payload + the pass's tag).
+constexpr int kSegMaxStages = 4;    // stages per launch
+constexpr int kSegMaxRows = 8;      // activation rows of a stage (cascade layers)
+constexpr int kSegMaxCopies = 9;    // normalised copies one produced row feeds
+constexpr int kSegMaxWg = 256;      // workgroups (compute units) at most
+constexpr int kSegRedFloats = 2048; // row partial sums of one stage: rows * 2
+constexpr int kSegResRows = 64;     // residual rows a workgroup keeps (d <= 64 * 256)
+constexpr int kSegLmMaxCols = 128;  // LM-head rows (vocabulary entries) per workgroup
+// sync words in the workspace (uint32, 128 bytes apart)
+constexpr int kSegEpochWord = 0, kSegDepartWord = 32, kSegStatusWord = 64, kSegSyncWords = 96;
+constexpr uint32_t kSegStatusTimeout = 1u;  // a poll gave up (results unspecified)
+constexpr uint32_t kSegStatusPersistent = 1u << 16;  // the last pass ran as persistent launches
+// The persistent launches are switched off: their first device run faulted and
+// the access at fault is not found.  fe_set_pass_mode(0) is refused.
+constexpr bool kSegEnabled = false;
+enum SegKind : int { kSegFuse = 0, kSegInput, kSegQkv, kSegO, kSegGu, kSegDown, kSegLm };
+enum SegSrcKind : int { kSrcPlain = 0, kSrcTagged = 1, kSrcEmbed = 2 };
+// elements [e0, e0 + n) of input row m: plain bf16 at p (element 0 of the
+// part), tagged words at p (two bf16 each), or the embedding-table row of
+// token tok[0] (NaN when it lies outside [0, vocab))
+struct SegSrc {
+  const void *p;
+  const int32_t *tok;
+  int kind, m, e0, n, vocab;
+};
+struct SegStage {
+  int kind, C, K, mr, gran;
+  const bf16_t *w0, *w1, *w2;  // Q/K/V: rows split at split1, split2; gate/up: even/odd rows
+  int split1, split2, qrow;
+  int nsrc;
+  SegSrc src[kSegMaxRows + 1];
+  const uint64_t *ssq[kSegMaxRows];  // tagged per-workgroup sums of squares of input row m, or null
+  uint64_t *out_t;                   // tagged outputs (fusion: g_t; gate/up: SwiGLU; LM: candidates)
+  float *x_out;                      // plain fp32 output row (input FC, down; Q/K/V: q)
+  float *k_out, *v_out;              // Q/K/V: k, v rows [mr, H_kv * D]
+  const float *resid;                // O projection: the residual row
+  uint64_t *ssq_out;                 // tagged sums of squares of the output row
+  int ncopy;                         // gamma_q * row copies for later normalised GEMVs
+  const bf16_t *gamma[kSegMaxCopies];
+  uint64_t *copy_t[kSegMaxCopies];
+};
+struct SegArgs {
+  SegStage st[kSegMaxStages];
+  int nst, nwg, d, V, topk, last;
+  float eps;
+  uint32_t *sync;
+  const uint64_t *cand_t;  // LM-head candidates (the last stage's out_t), merged when last
+  const int32_t *d2t;
+  int32_t *ids, *draft_ids;
+  float *probs, *logits;
+  TreeRows tree;
+};
+int seg_variant(int xbytes);  // workgroup shape for the largest activation block (-1: none)
+int seg_waves(int variant);
+hipError_t seg_occupancy(int variant, int *blocks_per_cu);
+hipError_t seg_launch(int variant, const SegArgs &a, hipStream_t s);
+hipError_t seg_zero(uint64_t *words, size_t n, hipStream_t s);
+
+
 // Global top-k of every row from the tile candidates (by key); softmax
 // statistics merge.  With cand_z (sampled candidates) the k winners are
 // listed by z / T (larger first, lower id on ties), else in key order.  With

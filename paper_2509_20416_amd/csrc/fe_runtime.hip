@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -29,13 +30,21 @@ fe_status fail(fe_status st, const char *fmt, ...) {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+#define FE_TRY(x)                                                           \
+  do {                                                                      \
+    hipError_t e_ = (x);                                                    \
+    if (e_ != hipSuccess) return fail(FE_E_HIP, "%s: %s", #x, hipGetErrorString(e_)); \
+  } while (0)
+
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
-      psum, cval, cidx, cz, img, splitk, total;
+      psum, cval, cidx, cz, img, splitk, tagged, total;
   size_t splitk_floats;
   int nchmax, nwg, npos;
+  // tagged words of the persistent batch-1 pass (offsets in words from `tagged`)
+  size_t t_sync, t_g, t_ssq, t_ssqp, t_copy, t_xp, t_s, t_cand, t_words;
 };
 
 int es_of(const fe_config &c) { return c.dtype == FE_BF16 ? 2 : 4; }
@@ -76,6 +85,23 @@ Layout layout_of(const fe_config &c) {
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cz = take(B * N * (size_t)L.nwg * kMaxTopk * 4);  // z / T of sampled candidates
   L.img = take(((size_t)c.target_vocab + 31) / 32 * 4);  // target ids that d2t reaches
+  // the persistent batch-1 pass: sync words, g_t, sums of squares of x_j and
+  // x'_i per workgroup, normalised copies of x_j for every consumer (QKV of
+  // layer l, or the LM head), of x'_i, the SwiGLU rows, LM-head candidates
+  {
+    size_t w = 0;
+    auto words = [&](size_t n) { size_t at = w; w += (n + 31) / 32 * 32; return at; };
+    L.t_sync = words(kSegSyncWords / 2 + 1);
+    L.t_g = words(d / 2);
+    L.t_ssq = words((N + 1) * (size_t)kSegMaxWg);
+    L.t_ssqp = words(N * (size_t)kSegMaxWg);
+    L.t_copy = words((N + 1) * (N + 1) * (d / 2));
+    L.t_xp = words(N * (d / 2));
+    L.t_s = words(N * (I / 2));
+    L.t_cand = words(N * (size_t)kSegMaxWg * (2 + 2 * kMaxTopk));
+    L.t_words = w;
+    L.tagged = take(w * 8);
+  }
   // split-K slices of the batched GEMMs with narrow outputs: up to 8 slices of
   // the QKV rows (B * N at most, 256 per launch) over 128-column tiles
   {
@@ -163,6 +189,10 @@ struct fe_drafter {
   bool graph_mode = false;
   int attn_split = 0;  // 64-key chunks per attention work unit (0 = automatic)
   bool table_ready = false;  // rotary table built (first pass on the handle)
+  int pass_mode = 1;          // 1: one launch per stage (0, persistent launches, is switched off)
+  bool seg_ready = false;     // tagged words zeroed (first persistent pass on the handle)
+  int seg_nwg = 0, seg_var = -2;  // workgroups (compute units) and variant of the persistent pass
+  bool last_seg = false;      // the most recent pass ran as persistent launches
   bool img_ready = false;    // bitmask of d2t's image built (first sampling acceptance)
   // graph cache: key = every argument of the last captured call
   std::vector<uintptr_t> key;
@@ -235,6 +265,31 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on) {
   return FE_OK;
 }
 
+fe_status fe_set_pass_mode(fe_drafter *h, int32_t mode) {
+  if (!h) return fail(FE_E_INVALID, "handle is NULL");
+  if (mode != 0 && mode != 1) return fail(FE_E_INVALID, "pass mode %d is not 0 or 1", mode);
+  // The persistent launches faulted the device on their first run and the
+  // access at fault has not been found; until it is, they are not launched.
+  if (mode == 0 && !kSegEnabled)
+    return fail(FE_E_UNSUPPORTED, "the persistent batch-1 pass (mode 0) is switched off");
+  h->pass_mode = mode;
+  return FE_OK;
+}
+
+fe_status fe_pass_status(fe_drafter *h, void *stream, int32_t *status) {
+  if (!h || !status) return fail(FE_E_INVALID, "handle or status is NULL");
+  *status = h->last_seg ? (int32_t)kSegStatusPersistent : 0;
+  if (!h->seg_ready) return FE_OK;  // no persistent pass has run
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t *word = (uint32_t *)(h->ws + h->L.tagged) + kSegStatusWord;
+  uint32_t v = 0;
+  FE_TRY(hipStreamSynchronize(s));
+  FE_TRY(hipMemcpy(&v, word, sizeof v, hipMemcpyDeviceToHost));
+  if (v) FE_TRY(hipMemset(word, 0, sizeof v));
+  *status |= (int32_t)v;
+  return FE_OK;
+}
+
 fe_status fe_set_attention_split(fe_drafter *h, int32_t chunks_per_workgroup) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   if (chunks_per_workgroup < 0 || chunks_per_workgroup > (1 << 16))
@@ -257,11 +312,6 @@ void fe_drafter_destroy(fe_drafter *h) {
 
 namespace {
 
-#define FE_TRY(x)                                                           \
-  do {                                                                      \
-    hipError_t e_ = (x);                                                    \
-    if (e_ != hipSuccess) return fail(FE_E_HIP, "%s: %s", #x, hipGetErrorString(e_)); \
-  } while (0)
 
 // With only_stage >= 0, a pass launches just the kernels of that stage (used
 // to time them); every other launch is skipped.
@@ -414,6 +464,263 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   return FE_OK;
 }
 
+// Can the persistent batch-1 pass run this call?  (Otherwise the pass runs as
+// one launch per stage.)  Sets h->seg_var / h->seg_nwg on first use.
+bool seg_supported(fe_drafter *h, int B, float inv_temp, const float *uniforms, int topk) {
+  const fe_config &c = h->cfg;
+  if (!kSegEnabled || h->pass_mode != 0 || B != 1 || uniforms || inv_temp != 1.f || c.dtype != FE_BF16) return false;
+  const long d = c.hidden, N = c.n_layers, I = c.intermediate, qd = (long)c.n_q_heads * c.head_dim;
+  const long kvd = (long)c.n_kv_heads * c.head_dim, F = c.n_feat_levels, V = c.draft_vocab;
+  if (N > kSegMaxRows || topk > kMaxTopk) return false;
+  for (long K : {F * d, 2 * d, d, qd, I})
+    if (K % 512) return false;
+  if (h->seg_var == -2) {
+    int dev = 0, cus = 0;
+    h->seg_var = -1;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus >= 1 && cus <= kSegMaxWg) {
+      const long xbytes = std::max({F * d, 2 * d, N * d, qd, d, I}) * 2;
+      const int var = seg_variant((int)xbytes);
+      int occ = 0;
+      if (var >= 0 && seg_occupancy(var, &occ) == hipSuccess && occ >= 1) {
+        h->seg_var = var;
+        h->seg_nwg = cus;
+      }
+    }
+    (void)hipGetLastError();
+  }
+  if (h->seg_var < 0) return false;
+  const long nwg = h->seg_nwg;
+  auto per_wg = [&](long C, long gran) { return (C / gran + nwg - 1) / nwg * gran; };
+  if (d % 2 || per_wg(d, 2) > kSegResRows) return false;               // residual rows
+  if (per_wg(V, 1) > kSegLmMaxCols || N * per_wg(V, 1) > kSegRedFloats / 2) return false;
+  if (N * per_wg(qd + 2 * kvd, 1) > kSegRedFloats / 2) return false;
+  if (per_wg(2 * I, 4) > kSegRedFloats / 2 || per_wg(F * d, 1) > kSegRedFloats / 2) return false;
+  return true;
+}
+
+// The batch-1 pass as N + 1 persistent launches between the N attention
+// launches: [fusion FC, input FC, Q/K/V of layer 1], attention 1, then per
+// layer [O, gate/up + SwiGLU, down, Q/K/V of the next layer], attention, and
+// finally [O, gate/up, down of layer N, LM head + top-k merge + tree].
+fe_status enqueue_forward_seg(fe_drafter *h, const void *features, const int32_t *next_tokens,
+                              const fe_kv_view *kv, int topk, const fe_draft_out *out,
+                              hipStream_t s) {
+  const fe_config &c = h->cfg;
+  const Layout &L = h->L;
+  const int d = c.hidden, N = c.n_layers, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
+  const int I = c.intermediate, qd = Hq * D, kvd = Hkv * D, F = c.n_feat_levels;
+  char *ws = h->ws;
+  uint64_t *T = (uint64_t *)(ws + L.tagged);
+  uint32_t *sync = (uint32_t *)(T + L.t_sync);
+  float *X = (float *)(ws + L.X), *q = (float *)(ws + L.q);
+  float *knew = (float *)(ws + L.knew), *vnew = (float *)(ws + L.vnew);
+  float *part = (float *)(ws + L.part);
+  const bf16_t *ao = (const bf16_t *)(ws + L.ao);
+  const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
+  const bool parallel = c.cascade_ctx == FE_CTX_PARALLEL;
+  const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
+  const int cpw = h->attn_split > 0 ? h->attn_split : attention_cpw(1, Hkv, 1, nch);
+  auto copy_of = [&](int j, int l) { return T + L.t_copy + ((size_t)j * (N + 1) + l) * (d / 2); };
+  auto ssq_of = [&](int j) { return T + L.t_ssq + (size_t)j * kSegMaxWg; };
+  auto ssqp_of = [&](int i) { return T + L.t_ssqp + (size_t)(i - 1) * kSegMaxWg; };
+  auto xp_of = [&](int i) { return T + L.t_xp + (size_t)(i - 1) * (d / 2); };
+  auto s_of = [&](int i) { return T + L.t_s + (size_t)(i - 1) * (I / 2); };
+  auto nctx_of = [&](int l) { return cascade ? l : 1; };
+  const bf16_t *const *dummy = nullptr;
+  (void)dummy;
+
+  SegArgs base{};
+  base.nwg = h->seg_nwg;
+  base.d = d;
+  base.V = c.draft_vocab;
+  base.topk = topk;
+  base.eps = c.rms_eps;
+  base.sync = sync;
+  base.cand_t = T + L.t_cand;
+  base.d2t = h->w.d2t;
+  base.ids = out->topk_ids;
+  base.draft_ids = out->topk_draft;
+  base.probs = out->topk_probs;
+  base.logits = out->logits;
+  if (out->tree) {
+    const fe_tree_out *t = out->tree;
+    base.tree = TreeRows{N, next_tokens, kv->cu_prefix, t->tokens, t->parents, t->depth,
+                         t->positions, t->mask, t->retrieve};
+  }
+  auto src = [](const void *p, int kind, int m, int e0, int n) {
+    SegSrc r{};
+    r.p = p;
+    r.kind = kind;
+    r.m = m;
+    r.e0 = e0;
+    r.n = n;
+    return r;
+  };
+  // normalised copies of x_j for its consumers: the Q/K/V GEMVs of the layers
+  // that read it and (j >= 1) the LM head
+  auto copies_x = [&](SegStage &st, int j) {
+    st.ncopy = 0;
+    for (int l = j + 1; l <= N; ++l) {
+      const bool uses = cascade ? true : parallel ? j == 0 : l == j + 1;
+      if (!uses) continue;
+      st.gamma[st.ncopy] = (const bf16_t *)h->layers[l - 1].attn_norm;
+      st.copy_t[st.ncopy] = copy_of(j, l);
+      ++st.ncopy;
+    }
+    if (j >= 1) {
+      st.gamma[st.ncopy] = (const bf16_t *)h->w.final_norm;
+      st.copy_t[st.ncopy] = copy_of(j, 0);
+      ++st.ncopy;
+    }
+  };
+  auto qkv = [&](int l) {
+    const fe_layer_weights &lw = h->layers[l - 1];
+    SegStage st{};
+    st.kind = kSegQkv;
+    st.C = qd + 2 * kvd;
+    st.K = d;
+    st.mr = nctx_of(l);
+    st.gran = 1;
+    st.w0 = (const bf16_t *)lw.wq;
+    st.w1 = (const bf16_t *)lw.wk;
+    st.w2 = (const bf16_t *)lw.wv;
+    st.split1 = qd;
+    st.split2 = qd + kvd;
+    st.qrow = st.mr - 1;
+    st.nsrc = st.mr;
+    for (int t = 0; t < st.mr; ++t) {
+      const int j = cascade ? t : parallel ? 0 : l - 1;
+      st.src[t] = src(copy_of(j, l), kSrcTagged, t, 0, d);
+      st.ssq[t] = ssq_of(j);
+    }
+    st.x_out = q;
+    st.k_out = knew;
+    st.v_out = vnew;
+    return st;
+  };
+  auto oproj = [&](int i) {
+    const fe_layer_weights &lw = h->layers[i - 1];
+    SegStage st{};
+    st.kind = kSegO;
+    st.C = d;
+    st.K = qd;
+    st.mr = 1;
+    st.gran = 2;
+    st.w0 = (const bf16_t *)lw.wo;
+    st.nsrc = 1;
+    st.src[0] = src(ao, kSrcPlain, 0, 0, qd);
+    st.resid = X + (size_t)(parallel ? 0 : i - 1) * d;
+    st.ssq_out = ssqp_of(i);
+    st.ncopy = 1;
+    st.gamma[0] = (const bf16_t *)lw.mlp_norm;
+    st.copy_t[0] = xp_of(i);
+    return st;
+  };
+  auto gateup = [&](int i) {
+    const fe_layer_weights &lw = h->layers[i - 1];
+    SegStage st{};
+    st.kind = kSegGu;
+    st.C = 2 * I;
+    st.K = d;
+    st.mr = 1;
+    st.gran = 4;
+    st.w0 = (const bf16_t *)lw.w_gate;
+    st.w1 = (const bf16_t *)lw.w_up;
+    st.nsrc = 1;
+    st.src[0] = src(xp_of(i), kSrcTagged, 0, 0, d);
+    st.ssq[0] = ssqp_of(i);
+    st.out_t = s_of(i);
+    return st;
+  };
+  auto down = [&](int i) {
+    const fe_layer_weights &lw = h->layers[i - 1];
+    SegStage st{};
+    st.kind = kSegDown;
+    st.C = d;
+    st.K = I;
+    st.mr = 1;
+    st.gran = 2;
+    st.w0 = (const bf16_t *)lw.w_down;
+    st.nsrc = 1;
+    st.src[0] = src(s_of(i), kSrcTagged, 0, 0, I);
+    st.x_out = X + (size_t)i * d;
+    st.ssq_out = ssq_of(i);
+    copies_x(st, i);
+    return st;
+  };
+  auto attn = [&](int l) -> fe_status {
+    FE_TRY(attention(1, kv->k[l - 1], kv->v[l - 1], kv->cu_prefix, q, knew, vnew, nctx_of(l),
+                     part, nch, L.nchmax, cpw, (void *)ao, 1, Hq, Hkv, D,
+                     (const float *)(ws + L.rope), cascade ? 1 : 0, kv->max_prefix, s));
+    return FE_OK;
+  };
+  auto launch = [&](std::initializer_list<SegStage> stages, int last) -> fe_status {
+    SegArgs a = base;
+    a.nst = 0;
+    for (const SegStage &st : stages) a.st[a.nst++] = st;
+    a.last = last;
+    FE_TRY(seg_launch(h->seg_var, a, s));
+    return FE_OK;
+  };
+
+  // [g_t = FC(l, m, h); x_0 = FC(g_t, e_{t+1}) (Eq. 1); Q/K/V of layer 1]
+  SegStage fuse{};
+  fuse.kind = kSegFuse;
+  fuse.C = d;
+  fuse.K = F * d;
+  fuse.mr = 1;
+  fuse.gran = 2;
+  fuse.w0 = (const bf16_t *)h->w.w_fuse;
+  fuse.nsrc = 1;
+  fuse.src[0] = src(features, kSrcPlain, 0, 0, F * d);
+  fuse.out_t = T + L.t_g;
+  SegStage input{};
+  input.kind = kSegInput;
+  input.C = d;
+  input.K = 2 * d;
+  input.mr = 1;
+  input.gran = 2;
+  input.w0 = (const bf16_t *)h->w.w_in;
+  input.nsrc = 2;
+  input.src[0] = src(T + L.t_g, kSrcTagged, 0, 0, d);
+  input.src[1] = src(h->w.embed, kSrcEmbed, 0, d, d);
+  input.src[1].tok = next_tokens;
+  input.src[1].vocab = c.target_vocab;
+  input.x_out = X;
+  input.ssq_out = ssq_of(0);
+  copies_x(input, 0);
+  fe_status st = launch({fuse, input, qkv(1)}, 0);
+  if (st != FE_OK) return st;
+  for (int i = 1; i <= N; ++i) {
+    if ((st = attn(i)) != FE_OK) return st;
+    if (i < N) {
+      st = launch({oproj(i), gateup(i), down(i), qkv(i + 1)}, 0);
+    } else {
+      SegStage lm{};
+      lm.kind = kSegLm;
+      lm.C = c.draft_vocab;
+      lm.K = d;
+      lm.mr = N;
+      lm.gran = 1;
+      lm.w0 = (const bf16_t *)h->w.lm_head;
+      lm.nsrc = N;
+      for (int t = 0; t < N; ++t) {
+        lm.src[t] = src(copy_of(t + 1, 0), kSrcTagged, t, 0, d);
+        lm.ssq[t] = ssq_of(t + 1);
+      }
+      lm.out_t = T + L.t_cand;
+      st = launch({oproj(i), gateup(i), down(i), lm}, 1);
+    }
+    if (st != FE_OK) return st;
+  }
+  if (out->hidden)
+    FE_TRY(hipMemcpyAsync(out->hidden, X, (size_t)(N + 1) * d * sizeof(float),
+                          hipMemcpyDeviceToDevice, s));
+  return FE_OK;
+}
+
 }  // namespace
 
 extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *features,
@@ -480,8 +787,18 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
     h->last_out.tree = &h->last_tree;
   }
 
-  if (!h->graph_mode)
-    return enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms, out, s);
+  const bool seg = seg_supported(h, batch, inv_temp, uniforms, topk);
+  h->last_seg = seg;
+  if (seg && !h->seg_ready) {  // tagged words start at tag 0, below every pass's tag
+    FE_TRY(seg_zero((uint64_t *)(h->ws + h->L.tagged), h->L.t_words, s));
+    h->seg_ready = true;
+  }
+  auto enqueue = [&](hipStream_t st) {
+    return seg ? enqueue_forward_seg(h, features, next_tokens, kv, topk, out, st)
+               : enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms,
+                                 out, st);
+  };
+  if (!h->graph_mode) return enqueue(s);
 
   std::vector<uintptr_t> key = {(uintptr_t)batch, (uintptr_t)features, (uintptr_t)next_tokens,
                                 (uintptr_t)kv->cu_prefix, (uintptr_t)kv->max_prefix,
@@ -495,7 +812,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
                                 (uintptr_t)(out->tree ? out->tree->retrieve : nullptr),
                                 (uintptr_t)out->logits, (uintptr_t)out->hidden,
                                 (uintptr_t)h->attn_split, (uintptr_t)__builtin_bit_cast(uint32_t, inv_temp),
-                                (uintptr_t)uniforms};
+                                (uintptr_t)uniforms, (uintptr_t)seg};
   for (int l = 0; l < c.n_layers; ++l) {
     key.push_back((uintptr_t)kv->k[l]);
     key.push_back((uintptr_t)kv->v[l]);
@@ -506,8 +823,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
     if (h->graph) { (void)hipGraphDestroy(h->graph); h->graph = nullptr; }
     h->key.clear();
     FE_TRY(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
-    fe_status st = enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms,
-                                   out, h->cap_stream);
+    fe_status st = enqueue(h->cap_stream);
     hipGraph_t g = nullptr;
     hipError_t ec = hipStreamEndCapture(h->cap_stream, &g);
     if (st != FE_OK) { if (g) (void)hipGraphDestroy(g); return st; }
@@ -523,19 +839,25 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
 extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                                    float *ms_per_launch, int32_t *launches) {
   if (!h || !ms_per_launch || !launches) return fail(FE_E_INVALID, "bad arguments");
-  if (stage < FE_STAGE_FUSE || stage > FE_STAGE_LMHEAD) return fail(FE_E_INVALID, "unknown stage %d", stage);
+  if (stage < FE_STAGE_FUSE || stage > FE_STAGE_PASS) return fail(FE_E_INVALID, "unknown stage %d", stage);
   if (repeats < 1) return fail(FE_E_INVALID, "repeats must be >= 1");
   if (!h->have_last) return fail(FE_E_INVALID, "no fe_draft_forward call to replay yet");
   const int N = h->cfg.n_layers;
-  const int per_pass = (stage == FE_STAGE_FUSE || stage == FE_STAGE_INPUT || stage == FE_STAGE_LMHEAD) ? 1 : N;
+  const int per_pass = (stage == FE_STAGE_FUSE || stage == FE_STAGE_INPUT || stage == FE_STAGE_LMHEAD ||
+                        stage == FE_STAGE_PASS) ? 1 : N;
+  const bool seg = stage == FE_STAGE_PASS &&
+                   seg_supported(h, h->last_batch, h->last_inv_temp, h->last_uniforms, h->last_topk);
   hipStream_t s = (hipStream_t)stream;
   if (!h->ev_a) FE_TRY(hipEventCreate(&h->ev_a));
   if (!h->ev_b) FE_TRY(hipEventCreate(&h->ev_b));
   FE_TRY(hipEventRecord(h->ev_a, s));
   for (int r = 0; r < repeats; ++r) {
-    const fe_status st = enqueue_forward(h, h->last_batch, h->last_features, h->last_tokens,
-                                         &h->last_kv, h->last_topk, h->last_inv_temp,
-                                         h->last_uniforms, &h->last_out, s, stage);
+    const fe_status st =
+        seg ? enqueue_forward_seg(h, h->last_features, h->last_tokens, &h->last_kv, h->last_topk,
+                                  &h->last_out, s)
+            : enqueue_forward(h, h->last_batch, h->last_features, h->last_tokens, &h->last_kv,
+                              h->last_topk, h->last_inv_temp, h->last_uniforms, &h->last_out, s,
+                              stage == FE_STAGE_PASS ? -1 : stage);
     if (st != FE_OK) return st;
   }
   FE_TRY(hipEventRecord(h->ev_b, s));

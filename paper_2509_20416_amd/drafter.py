@@ -91,6 +91,15 @@ class Drafter:
         """64-key prefix chunks per attention work unit; 0 = automatic."""
         fe.fe_set_attention_split(self.handle, chunks_per_workgroup)
 
+    def set_pass_mode(self, mode: int) -> None:
+        """0: persistent launches for batch-1 passes when the shape allows; 1: one launch per stage."""
+        fe.fe_set_pass_mode(self.handle, mode)
+
+    def pass_status(self) -> int:
+        """Waits for the stream; bit 0: a persistent pass gave up waiting (outputs
+        unspecified), bit 16: the last pass ran as persistent launches."""
+        return fe.fe_pass_status(self.handle, self.stream())
+
     def upload_inputs(self, inp, max_prefix: Optional[int] = None) -> DeviceInputs:
         torch = _torch()
         dev, dt = self.device, self.cfg.dtype

@@ -21,9 +21,9 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
            "fe_build_tree",
-           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage",
+           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_set_pass_mode", "fe_pass_status",
            "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split")
-FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7)
+FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7, pass_=8)
 
 
 class fe_config(C.Structure):
@@ -114,6 +114,10 @@ def lib() -> C.CDLL:
             [C.POINTER(fe_kv_cache), C.c_void_p]
         L.fe_set_graph_mode.restype = C.c_int
         L.fe_set_graph_mode.argtypes = [C.c_void_p, C.c_int32]
+        L.fe_set_pass_mode.restype = C.c_int
+        L.fe_set_pass_mode.argtypes = [C.c_void_p, C.c_int32]
+        L.fe_pass_status.restype = C.c_int
+        L.fe_pass_status.argtypes = [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32)]
         L.fe_set_attention_split.restype = C.c_int
         L.fe_set_attention_split.argtypes = [C.c_void_p, C.c_int32]
         L.fe_time_stage.restype = C.c_int
@@ -218,6 +222,16 @@ def fe_kv_update_noalloc(h: int, n_rows: int, features: int, tokens: int, positi
 
 def fe_set_graph_mode(h: int, on: bool) -> None:
     check(lib().fe_set_graph_mode(C.c_void_p(h), 1 if on else 0))
+
+
+def fe_set_pass_mode(h: int, mode: int) -> None:
+    check(lib().fe_set_pass_mode(C.c_void_p(h), int(mode)))
+
+
+def fe_pass_status(h: int, stream: int) -> int:
+    v = C.c_int32()
+    check(lib().fe_pass_status(C.c_void_p(h), C.c_void_p(stream), C.byref(v)))
+    return int(v.value)
 
 
 def fe_set_attention_split(h: int, chunks_per_workgroup: int) -> None:

@@ -19,7 +19,7 @@ def log(*a):
 
 def run_case(cfg, seed=0, prefix_lens=None, topk=None, sample=None, graph=False,
              with_debug=True, weights=None, inputs=None, feo=None, check_tree_struct=True,
-             attn_split=None):
+             attn_split=None, pass_mode=None):
     import torch
     from paper_2509_20416_amd import Drafter
     if feo is None:
@@ -36,15 +36,21 @@ def run_case(cfg, seed=0, prefix_lens=None, topk=None, sample=None, graph=False,
                  graph=graph)
     if attn_split is not None:
         dr.set_attention_split(attn_split)
+    if pass_mode is not None:
+        dr.set_pass_mode(pass_mode)
     di = dr.upload_inputs(inp)
     out = dr.forward(di, k)                                   # the benchmarked configuration
     tree = dr.build_tree(di, out["topk_ids"], k)
     torch.cuda.synchronize()
+    status = dr.pass_status()
+    assert status & 1 == 0, f"persistent pass gave up waiting (status {status:#x})"
+    persistent = bool(status & (1 << 16))
     res = {n: t.cpu().numpy() for n, t in out.items()}
     tr = {n: t.cpu().numpy() for n, t in tree.items()}
     if with_debug:
         dbg = dr.forward(di, k, logits=True, hidden=True)
         torch.cuda.synchronize()
+        assert dr.pass_status() & 1 == 0
         dbg = {n: t.cpu().numpy() for n, t in dbg.items()}
         for n in ("topk_ids", "topk_probs", "topk_draft"):   # debug outputs change nothing
             np.testing.assert_array_equal(dbg[n], res[n], err_msg=n)
@@ -56,7 +62,7 @@ def run_case(cfg, seed=0, prefix_lens=None, topk=None, sample=None, graph=False,
     log(f"{cfg.name}: oracle on {len(idx)} sequence(s) in {time.time() - t1:.1f}s")
     tol = TOL[cfg.dtype]
     N = cfg.n_layers
-    report = {}
+    report = {"persistent": persistent}
     if with_debug:
         report["hidden_err"] = assert_rows_close("hidden", dbg["hidden"][idx], ref["hidden"], tol)
         report["logit_err"] = assert_rows_close("logits", dbg["logits"][idx], ref["logits"], tol)
