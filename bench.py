@@ -70,6 +70,18 @@ def gemm_source_sha1():
     return h.hexdigest()
 
 
+def kernel_source_sha1():
+    """Digest of every kernel source of the library (a counter summary is valid
+    only for the kernels it was taken from)."""
+    import glob
+    import hashlib
+    h = hashlib.sha1()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2509_20416_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def read_traffic():
     """HBM bytes per gate/up launch from the committed rocprofv3 counter summary
     (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel factor); None when the
@@ -89,6 +101,72 @@ def read_traffic():
         return float(vals["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def read_pass_traffic(name):
+    """HBM bytes of one whole pass (FETCH_SIZE + WRITE_SIZE over every launch of
+    one eager pass, scaled by the copy-kernel factors) from the committed
+    counter summary of that workload; None when missing or taken from other
+    kernel sources than these."""
+    vals = {}
+    try:
+        for line in open(os.path.join(ROOT, "profiles", f"traffic_pass_{name}.txt")):
+            if ":" in line and not line.startswith(("#", " ", "|")):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    except OSError:
+        return None
+    if vals.get("source_sha1") != kernel_source_sha1():
+        log(f"pass traffic summary of {name} was taken from other kernel sources; reporting null")
+        return None
+    try:
+        return float(vals["traffic_bytes_per_pass"])
+    except (KeyError, ValueError):
+        return None
+
+
+def read_mfma_counters(name):
+    """Matrix-core FLOPs counted by rocprofv3 (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512)
+    for one pass and one max_prefix-row cache update of the workload, from the
+    committed counter summary; None when missing or taken from other kernel
+    sources than these."""
+    vals = {}
+    try:
+        for line in open(os.path.join(ROOT, "profiles", f"mfma_{name}.txt")):
+            if ":" in line and not line.startswith(("#", " ", "|")):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    except OSError:
+        return None
+    if vals.get("source_sha1") != kernel_source_sha1():
+        log(f"MFMA counter summary of {name} was taken from other kernel sources; reporting null")
+        return None
+    try:
+        return {"pass_flops": float(vals["pass_counter_mfma_flops"]),
+                "kv_update_rows": int(vals["kv_update_rows"]),
+                "kv_update_flops": float(vals["kv_update_counter_mfma_flops"]),
+                "kv_update_busy": float(vals["kv_update_mfma_busy"]),
+                "file": f"profiles/mfma_{name}.txt"}
+    except (KeyError, ValueError):
+        return None
+
+
+def counter_mfma(ctr, ms, peak):
+    """The pass's matrix-core rate from counted FLOPs over the measured pass time."""
+    if ctr is None:
+        return None
+    return {"flops_per_pass": ctr["pass_flops"],
+            "TFLOPs": ctr["pass_flops"] / (ms * 1e-3) / 1e12,
+            "frac": ctr["pass_flops"] / (ms * 1e-3) / 1e12 / peak, "source": ctr["file"]}
+
+
+def counter_update(ctr, upd, peak):
+    """A cache update's matrix-core use from the counter summary (same row count only)."""
+    if ctr is None or ctr["kv_update_rows"] != upd["rows"]:
+        return None
+    return {"flops": ctr["kv_update_flops"], "flops_vs_algorithmic": ctr["kv_update_flops"] / upd["flops"],
+            "frac": ctr["kv_update_flops"] / (upd["us_per_call"] * 1e-6) / 1e12 / peak,
+            "mfma_busy": ctr["kv_update_busy"], "source": ctr["file"]}
 
 
 def cpu_baseline(cfg, w, inp, budget_s):
@@ -175,6 +253,77 @@ def time_kv_update(dr, cfg, positions, reps=20, warmup=3, chunk_rows=1024):
             "issue": "eager, from Python"}
 
 
+def device_weights(cfg, seed, device):
+    """Seeded synthetic weights drawn on the device (timing of the larger
+    configurations only; parity uses fe_synth.make_weights): the same shapes and
+    distributions -- N(0, 0.02) matrices, 1 + N(0, 0.02) gains, a sorted random
+    draft->target map -- from torch's device generator, so a 10 GB weight set
+    takes milliseconds instead of a minute of host time."""
+    import numpy as np
+    import torch
+    from fe_synth.gen import LayerWeights, Weights, int_rng
+    g = torch.Generator(device=device).manual_seed(int(seed))
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    d, I, D = cfg.hidden, cfg.intermediate, cfg.head_dim
+    qd, kvd = cfg.n_q_heads * D, cfg.n_kv_heads * D
+
+    def lin(*shape):
+        return (torch.randn(shape, generator=g, device=device) * 0.02).to(tdt)
+
+    def gain():
+        return (1.0 + torch.randn((d,), generator=g, device=device) * 0.02).to(tdt)
+
+    layers = [LayerWeights(attn_norm=gain(), wq=lin(qd, d), wk=lin(kvd, d), wv=lin(kvd, d),
+                           wo=lin(d, qd), mlp_norm=gain(), w_gate=lin(I, d), w_up=lin(I, d),
+                           w_down=lin(d, I)) for _ in range(cfg.n_layers)]
+    if cfg.draft_vocab == cfg.target_vocab:
+        d2t = np.arange(cfg.draft_vocab, dtype=np.int32)
+    else:
+        d2t = np.sort(int_rng("d2t", seed).choice(cfg.target_vocab, size=cfg.draft_vocab,
+                                                  replace=False)).astype(np.int32)
+    return Weights(w_fuse=lin(d, cfg.n_feat_levels * d), w_in=lin(d, 2 * d),
+                   embed=lin(cfg.target_vocab, d), final_norm=gain(),
+                   lm_head=lin(cfg.draft_vocab, d), d2t=d2t, layers=layers)
+
+
+def time_config(name, seed, steps, warmup):
+    """One more configuration (tiny, 13B-, 70B-shaped): passes (forward + tree,
+    graph replays) timed like the primary workload, weights drawn on the device."""
+    import numpy as np
+    import torch
+    from fe_synth import NAMED, make_inputs
+    from paper_2509_20416_amd import Drafter
+    cfg = NAMED[name]
+    inp = make_inputs(cfg, seed)
+    plens = np.asarray(inp.prefix_lens)
+    w = device_weights(cfg, seed, "cuda")
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=True)
+    del w
+    di = dr.upload_inputs(inp)
+    out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
+    tree = dr.alloc_tree(cfg.batch, cfg.topk)
+    for _ in range(warmup):
+        dr.forward(di, out=out, tree=tree)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        dr.forward(di, out=out, tree=tree)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    dr.close()
+    pbytes = pass_bytes(cfg, plens)
+    log(f"{name}: {ms * 1000:.1f} us/pass")
+    return {"batch": cfg.batch, "dtype": cfg.dtype, "hidden": cfg.hidden,
+            "cascade_layers": cfg.n_layers, "prefix": int(plens.max()), "topk": cfg.topk,
+            "steps": steps, "us_per_pass": ms * 1000.0, "drafts_per_s": cfg.batch * 1000.0 / ms,
+            "bytes_per_pass": pbytes,
+            "hbm_frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "weights": "seeded, drawn on the device"}
+
+
 def time_second(name, seed, steps, warmup):
     """The other half of the metric (by default the batch-32 workload): passes
     (forward + tree, graph replays) timed the same way as the primary one."""
@@ -208,8 +357,11 @@ def time_second(name, seed, steps, warmup):
     dr.close()
     pbytes, pflops = pass_bytes(cfg, plens), pass_flops(cfg, plens)
     peak = MFMA_PEAK_TFS[cfg.dtype]
+    ctr = read_mfma_counters(name)
     log(f"{name}: {ms * 1000:.1f} us/pass")
     return {"workload": name, "batch": cfg.batch, "steps": steps, "warmup": warmup,
+            "traffic_per_pass": read_pass_traffic(name),
+            "counter_mfma": counter_mfma(ctr, ms, peak),
             "us_per_pass": ms * 1000.0, "drafts_per_s": cfg.batch * 1000.0 / ms,
             "hbm_frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "mfma_frac": pflops / (ms * 1e-3) / 1e12 / peak,
@@ -231,6 +383,16 @@ def main():
     ap.add_argument("--second", default="llama8b_bf16_b32",
                     help="second workload timed in the same run and reported in its own "
                          "object ('' = none; the batch-32 half of the metric by default)")
+    ap.add_argument("--configs", default="tiny_fp32_b1,vicuna13b_bf16_b1,llama70b_bf16_b1",
+                    help="further workloads timed in the same run ('' = none)")
+    ap.add_argument("--device-weights", action="store_true",
+                    help="draw the workload's weights on the device (seeded; for timing the large "
+                         "configurations without a minute of host-side generation; implies "
+                         "--no-cpu-baseline)")
+    ap.add_argument("--counter-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: two eager passes and two cache updates of "
+                         "max_prefix rows, separated by fill kernels, then a plain 512 MiB "
+                         "device copy as the counter scale reference; prints what ran")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: a few eager passes, one round of the gate/up "
                          "launches, then a plain 512 MiB device copy as the counter scale "
@@ -248,12 +410,12 @@ def main():
 
     cfg = NAMED[args.workload]
     t0 = time.time()
-    w = make_weights(cfg, args.seed)
+    w = device_weights(cfg, args.seed, "cuda") if args.device_weights else make_weights(cfg, args.seed)
     inp = make_inputs(cfg, args.seed)
     log(f"{cfg.name}: inputs generated in {time.time() - t0:.1f}s")
     plens = np.asarray(inp.prefix_lens)
-    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()),
-                 graph=not (args.eager or args.traffic_probe))
+    probe = args.traffic_probe or args.counter_probe
+    dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=not (args.eager or probe))
     di = dr.upload_inputs(inp)
     out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
     tree = dr.alloc_tree(cfg.batch, cfg.topk)
@@ -276,6 +438,31 @@ def main():
                           "gateup_algorithmic_bytes": gateup_bytes(cfg, cfg.batch),
                           "copy_bytes_read": copy_bytes, "copy_bytes_written": copy_bytes}),
               flush=True)
+        dr.close()
+        return
+    if args.counter_probe:
+        # segments: [pass][fill][pass][fill][update][fill][update][fill][copy]
+        marker = torch.zeros(1, device=dr.device)
+        P = int(plens.max())
+        for i in range(2):
+            step()
+            marker.fill_(float(i + 1))
+        upd_pos = np.arange(P)
+        for i in range(2):
+            time_kv_update(dr, cfg, upd_pos, reps=1, warmup=0)
+            marker.fill_(float(i + 3))
+        torch.cuda.synchronize()
+        copy_bytes = 512 << 20
+        src = torch.ones(copy_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        uflops, ubytes = kv_update_cost(cfg, P)
+        print(json.dumps({"counter_probe": cfg.name, "passes": 2, "pass_bytes": pass_bytes(cfg, plens),
+                          "pass_flops": pass_flops(cfg, plens), "kv_update_rows": P,
+                          "kv_update_calls": 2, "kv_update_flops": uflops,
+                          "kv_update_bytes": ubytes, "copy_bytes": copy_bytes}), flush=True)
         dr.close()
         return
     for _ in range(args.warmup):
@@ -372,6 +559,10 @@ def main():
     gbytes = gateup_bytes(cfg, B)
     achieved = gbytes / (gu_avg * 1e-3) / 1e9
     traffic = read_traffic()
+    pass_traffic = read_pass_traffic(cfg.name)
+    ctr = read_mfma_counters(cfg.name)
+    if ctr is not None:
+        upd_prefill["counter"] = counter_update(ctr, upd_prefill, MFMA_PEAK_TFS[cfg.dtype])
     pbytes = pass_bytes(cfg, plens)
     pflops = pass_flops(cfg, plens)
     res = {
@@ -390,14 +581,21 @@ def main():
                    "target_vocab": cfg.target_vocab, "prefix": cfg.prefix, "topk": cfg.topk,
                    "tree_nodes": cfg.tree_nodes, "cascade_ctx": cfg.cascade_ctx,
                    "graph": not args.eager},
-        "roofline": {"kernel": "gate/up projections + SwiGLU (one per cascade layer)",
-                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "bytes_per_launch": gbytes,
-                     "avg_launch_ms": gu_avg, "launches_timed": n_timed},
-        "pass_roofline": {"bytes_per_pass": pbytes,
-                          "achieved_GBs": pbytes / (ms * 1e-3) / 1e9,
-                          "frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        # the whole pass as the unit: every weight and each layer's prefix K/V
+        # once, over the time of one graph replay (all of its launches)
+        "roofline": {"kernel": "whole drafting pass (one graph replay)",
+                     "bound": "hbm", "achieved": pbytes / (ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": pass_traffic, "bytes_per_pass": pbytes,
+                     "avg_pass_ms": ms},
+        # the dominant kernel alone
+        "roofline_dominant_kernel": {
+            "kernel": "gate/up projections + SwiGLU (one per cascade layer)",
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic, "bytes_per_launch": gbytes,
+            "avg_launch_ms": gu_avg, "launches_timed": n_timed},
         # host-issued launches back to back: the rate is bound by the Python
         # call, the kernel itself is a few microseconds
         "next_accept_greedy": {"us_per_call": accept_us, "batch": B,
@@ -417,7 +615,9 @@ def main():
                       "peak_TFLOPs": MFMA_PEAK_TFS[cfg.dtype],
                       "frac": pflops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFS[cfg.dtype],
                       "ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3
-                                          / MFMA_PEAK_TFS[cfg.dtype])},
+                                          / MFMA_PEAK_TFS[cfg.dtype]),
+                      # FLOPs the matrix cores executed (padding included), counted
+                      "counter": counter_mfma(ctr, ms, MFMA_PEAK_TFS[cfg.dtype])},
     }
     dr.close()
     # NEXT-4, the ablation without the cascade: every layer reads x_0 (same
@@ -450,7 +650,12 @@ def main():
     if args.second and args.second != cfg.name:
         res["second_workload"] = time_second(args.second, args.seed, max(10, args.steps // 4),
                                              max(3, args.warmup // 4))
-    if not args.no_cpu_baseline:
+    if args.configs:
+        res["other_configs"] = {}
+        for name in [n for n in args.configs.split(",") if n and n != cfg.name]:
+            res["other_configs"][name] = time_config(name, args.seed, max(20, args.steps // 2),
+                                                     max(3, args.warmup // 4))
+    if not (args.no_cpu_baseline or args.device_weights):
         log("timing the oracle on the host cores ...")
         res["cpu_baseline"] = cpu_baseline(cfg, w, inp, args.cpu_budget)
     print(json.dumps(res), flush=True)

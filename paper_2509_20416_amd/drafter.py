@@ -49,7 +49,9 @@ class Drafter:
         self.device = torch.device(device)
         dev = self.device
         dt = cfg.dtype
-        up = lambda a: to_device(a, dt, dev)
+        # host arrays are copied in; device tensors (already in the storage
+        # dtype) are used as they are
+        up = lambda a: a.to(dev) if isinstance(a, torch.Tensor) else to_device(a, dt, dev)
         self.w = {n: up(getattr(weights, n)) for n in ("w_fuse", "w_in", "embed", "final_norm",
                                                        "lm_head")}
         self.w["d2t"] = to_device(np.asarray(weights.d2t, dtype=np.int32), "i32", dev)
