@@ -45,8 +45,12 @@ static int g_threads = 1;
 void feo_set_threads(int n) { g_threads = n < 1 ? 1 : n; }
 int feo_get_threads(void) { return g_threads; }
 
+/* Storage code of prefix rows the oracle assembles itself (fp64). */
+enum { KV_F64 = 2 };
+
 /* Exact widening of one stored element. */
 static double widen(const void *p, int32_t dtype, size_t i) {
+  if (dtype == KV_F64) return ((const double *)p)[i];
   if (dtype == FEO_BF16) {
     uint32_t bits = (uint32_t)((const uint16_t *)p)[i] << 16;
     float f;
@@ -149,9 +153,13 @@ static double silu(double u) { return u / (1.0 + exp(-u)); }
  * xs[0..i-1] are the cascade states produced so far (x_0 = fused input);
  * writes x_i into xs[i].  Under FEO_CTX_PARALLEL (the ablation of Section 3.2
  * that replaces the series by parallel heads) every layer reads x_0 instead:
- * x_i = L_i(x_0), attending to its prefix plus x_0 at position P. */
+ * x_i = L_i(x_0), attending to its prefix plus x_0 at position P.  The prefix
+ * keys/values are rows prefix_off .. prefix_off + P - 1 of kc / vc, stored as
+ * kv_dtype (FEO_F32, FEO_BF16 or KV_F64).  k_own / v_own (optional, [H_kv*D]):
+ * the layer's rotated key and value of its own input x_src. */
 static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, double *xs,
-                          const void *kc, const void *vc, int64_t prefix_off, int32_t P) {
+                          const void *kc, const void *vc, int32_t kv_dtype, int64_t prefix_off,
+                          int32_t P, double *k_own, double *v_own) {
   const int32_t d = c->hidden, D = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads;
   const int32_t G = Hq / Hkv, I = c->intermediate;
   const int32_t qd = Hq * D, kvd = Hkv * D;
@@ -175,6 +183,8 @@ static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, do
     if (j == src) {
       matvec(L->wq, c->dtype, qd, d, a, q);
       for (int32_t h = 0; h < Hq; ++h) feo_rope(q + (size_t)h * D, D, pos, c->rope_theta);
+      if (k_own) memcpy(k_own, kn + (size_t)t * kvd, sizeof(double) * (size_t)kvd);
+      if (v_own) memcpy(v_own, vn + (size_t)t * kvd, sizeof(double) * (size_t)kvd);
     }
   }
 
@@ -188,8 +198,8 @@ static void cascade_layer(const feo_config *c, const feo_layer *L, int32_t i, do
     for (int32_t t = 0; t < P; ++t)
       for (int32_t e = 0; e < D; ++e) {
         const size_t src = ((size_t)(prefix_off + t) * Hkv + ch) * D + e;
-        K[(size_t)t * D + e] = widen(kc, c->dtype, src);
-        V[(size_t)t * D + e] = widen(vc, c->dtype, src);
+        K[(size_t)t * D + e] = widen(kc, kv_dtype, src);
+        V[(size_t)t * D + e] = widen(vc, kv_dtype, src);
       }
     for (int32_t t = 0; t < nctx; ++t)
       for (int32_t e = 0; e < D; ++e) {
@@ -278,7 +288,8 @@ int feo_draft_sample(const feo_config *c, const feo_weights *w, int32_t batch,
     fused_input(c, w, features, b, next_tok[b], f, ge, xs);
     /* h_i = L_i(h_{i-1}) (Eq. 1-2) */
     for (int32_t i = 1; i <= N; ++i)
-      cascade_layer(c, &w->layers[i - 1], i, xs, kcache[i - 1], vcache[i - 1], prefix_off, P);
+      cascade_layer(c, &w->layers[i - 1], i, xs, kcache[i - 1], vcache[i - 1], c->dtype, prefix_off,
+                    P, NULL, NULL);
     if (hidden) memcpy(hidden + (size_t)b * (N + 1) * d, xs, sizeof(double) * (size_t)(N + 1) * d);
 
     /* q_{t+i} = softmax(LMHead(RMSNorm(h_i)) / T) and its k candidates
@@ -438,6 +449,67 @@ int feo_kv_update(const feo_config *c, const feo_weights *w, int32_t n_rows, con
     }
   }
   free(f); free(ge); free(x0); free(a);
+  return 0;
+}
+
+/* Drafter cache rows under FEO_CTX_SELF (Section 2.4 update step, read under
+ * the self context of Eq. 2: layer i's context is its prefix plus its own
+ * input).  The row of layer i at position p is layer i's key and value of its
+ * own input x_{i-1}(p) -- what the pass at prefix p attends to as that input
+ * -- so filling it means running the pass itself at every new position, one
+ * position after the other: row m at position p = positions[m] goes to cache
+ * row r = dst_rows[m], its sequence's row of position j < p being cache row
+ * r - (p - j): the row an earlier row of this call wrote there (its fp64
+ * result), else that row of kcache / vcache (storage precision, keys
+ * rotated).  For row m, x_0 is the fused input (Eq. 1); layer i takes x_{i-1},
+ * emits its key and value at position p as row m's output and computes x_i
+ * over the prefix rows 0..p-1 plus its own. */
+int feo_kv_update_self(const feo_config *c, const feo_weights *w, int32_t n_rows,
+                       const void *features, const int32_t *tokens, const int32_t *positions,
+                       const int32_t *dst_rows, const void *const *kcache,
+                       const void *const *vcache, int64_t cache_rows, double *const *k_out,
+                       double *const *v_out) {
+  if (!c || !w || n_rows < 0 || c->n_layers < 1 || c->cascade_ctx != FEO_CTX_SELF) return -1;
+  if (c->n_q_heads % c->n_kv_heads != 0 || c->head_dim % 2 != 0 || cache_rows < 0) return -1;
+  const int32_t d = c->hidden, F = c->n_feat_levels, N = c->n_layers;
+  const int32_t kvd = c->n_kv_heads * c->head_dim;
+  for (int32_t m = 0; m < n_rows; ++m) {
+    if (tokens[m] < 0 || tokens[m] >= c->target_vocab || positions[m] < 0) return -1;
+    if (dst_rows[m] < positions[m] || dst_rows[m] >= cache_rows) return -1;
+  }
+  double *xs = (double *)malloc(sizeof(double) * (size_t)(N + 1) * d);
+  double *f = (double *)malloc(sizeof(double) * (size_t)F * d);
+  double *ge = (double *)malloc(sizeof(double) * (size_t)2 * d);
+  for (int32_t m = 0; m < n_rows; ++m) {
+    const int32_t p = positions[m];
+    const int64_t r0 = (int64_t)dst_rows[m] - p;  /* cache row of position 0 */
+    double *pk = (double *)malloc(sizeof(double) * ((size_t)p * kvd + 1));
+    double *pv = (double *)malloc(sizeof(double) * ((size_t)p * kvd + 1));
+    fused_input(c, w, features, (size_t)m, tokens[m], f, ge, xs);
+    for (int32_t i = 1; i <= N; ++i) {
+      /* layer i's rows of positions 0..p-1 */
+      for (int32_t j = 0; j < p; ++j) {
+        const int64_t row = r0 + j;
+        int32_t from = -1;  /* the last earlier row of this call written there */
+        for (int32_t e = 0; e < m; ++e)
+          if (dst_rows[e] == row) from = e;
+        for (int32_t x = 0; x < kvd; ++x) {
+          if (from >= 0) {
+            pk[(size_t)j * kvd + x] = k_out[i - 1][(size_t)from * kvd + x];
+            pv[(size_t)j * kvd + x] = v_out[i - 1][(size_t)from * kvd + x];
+          } else {
+            pk[(size_t)j * kvd + x] = widen(kcache[i - 1], c->dtype, (size_t)row * kvd + x);
+            pv[(size_t)j * kvd + x] = widen(vcache[i - 1], c->dtype, (size_t)row * kvd + x);
+          }
+        }
+      }
+      cascade_layer(c, &w->layers[i - 1], i, xs, pk, pv, KV_F64, 0, p,
+                    k_out[i - 1] + (size_t)m * kvd, v_out[i - 1] + (size_t)m * kvd);
+    }
+    free(pk);
+    free(pv);
+  }
+  free(xs); free(f); free(ge);
   return 0;
 }
 

@@ -143,6 +143,27 @@ int feo_kv_update(const feo_config *cfg, const feo_weights *w, int32_t n_rows,
                   double *const *k_out, double *const *v_out);
 
 /*
+ * Drafter KV-cache rows under FEO_CTX_SELF (Section 2.4 update step, read
+ * under the self context).  Layer i's row at position p is its rotated key and
+ * value of its own input x_{i-1}(p), the state the pass at prefix p computes,
+ * so the rows are produced by running the pass at each new position in turn
+ * (a multi-position prefill of the N layers).  Row m (features, tokens as in
+ * feo_kv_update) sits at position positions[m] and is written at cache row
+ * dst_rows[m]; its sequence's row of position j < p is cache row
+ * dst_rows[m] - (positions[m] - j), taken from an earlier row of this call
+ * that wrote it (fp64) or else from kcache / vcache ([n_layers] pointers, each
+ * [cache_rows, H_kv, D] in cfg->dtype, keys rotated).  Outputs as
+ * feo_kv_update.  Returns 0, or -1 on invalid arguments (not FEO_CTX_SELF, a
+ * token outside [0, target_vocab), a negative position, dst_rows[m] outside
+ * [positions[m], cache_rows)).
+ */
+int feo_kv_update_self(const feo_config *cfg, const feo_weights *w, int32_t n_rows,
+                       const void *features, const int32_t *tokens, const int32_t *positions,
+                       const int32_t *dst_rows, const void *const *kcache,
+                       const void *const *vcache, int64_t cache_rows, double *const *k_out,
+                       double *const *v_out);
+
+/*
  * Speculative-sampling acceptance of one cycle at temperature T (Section 2.4).
  * For the tree of feo_build_tree (tokens [B, T] target ids, retrieve) with
  * topk_draft [B, N, k] the children's draft ids, draft_logits [B, N, V] the

@@ -46,6 +46,7 @@ def lib():
         L.feo_build_tree.restype = C.c_int
         L.feo_accept_greedy.restype = C.c_int
         L.feo_kv_update.restype = C.c_int
+        L.feo_kv_update_self.restype = C.c_int
         L.feo_accept_sample.restype = C.c_int
         L.feo_get_threads.restype = C.c_int
         _lib = L
@@ -225,6 +226,42 @@ def kv_update(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.nd
                              _pi(positions), kp, vp)
     if rc != 0:
         raise ValueError("oracle kv_update rejected its arguments")
+    return ks, vs
+
+
+def kv_update_self(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.ndarray,
+                   dst_rows: np.ndarray, kcache, vcache):
+    """Per-layer cache rows under the self context (see feo_kv_update_self in
+    fe_oracle.h): the pass run at each new position in turn.  kcache / vcache:
+    per-layer [rows, H_kv, D] caches in storage precision (bf16 as uint16 bit
+    patterns) holding the rows written before the call.  Returns (k, v): lists
+    over layers of [M, H_kv, D] float64, keys rotated (the rows to write at
+    dst_rows)."""
+    features = np.ascontiguousarray(features)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    positions = np.ascontiguousarray(positions, dtype=np.int32)
+    dst_rows = np.ascontiguousarray(dst_rows, dtype=np.int32)
+    M, N = len(tokens), cfg.n_layers
+    assert features.shape[0] == M and len(positions) == M and len(dst_rows) == M
+    kc = [np.ascontiguousarray(a) for a in kcache]
+    vc = [np.ascontiguousarray(a) for a in vcache]
+    rows = kc[0].shape[0]
+    sdt = np.uint16 if cfg.dtype == "bf16" else np.float32
+    for a in kc + vc:
+        assert a.dtype == sdt and a.shape == (rows, cfg.n_kv_heads, cfg.head_dim)
+    W, _keep = _weights(w, N)
+    ks = [np.zeros((M, cfg.n_kv_heads, cfg.head_dim)) for _ in range(N)]
+    vs = [np.zeros((M, cfg.n_kv_heads, cfg.head_dim)) for _ in range(N)]
+    kp = (C.POINTER(C.c_double) * N)(*[_pd(a) for a in ks])
+    vp = (C.POINTER(C.c_double) * N)(*[_pd(a) for a in vs])
+    kcp = (C.c_void_p * N)(*[a.ctypes.data for a in kc])
+    vcp = (C.c_void_p * N)(*[a.ctypes.data for a in vc])
+    cfgc = make_config(cfg)
+    rc = lib().feo_kv_update_self(C.byref(cfgc), C.byref(W), C.c_int32(M), _p(features),
+                                  _pi(tokens), _pi(positions), _pi(dst_rows), kcp, vcp,
+                                  C.c_int64(rows), kp, vp)
+    if rc != 0:
+        raise ValueError("oracle kv_update_self rejected its arguments")
     return ks, vs
 
 
