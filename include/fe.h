@@ -235,18 +235,30 @@ typedef struct {
  * weight matrix serve more rows per read. */
 size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chunk_rows);
 
-/* Drafter cache update after verification (Section 2.4's update step; the
- * rows are read under FE_CTX_CASCADE, and FE_CTX_PARALLEL keys the same rows;
- * FE_CTX_SELF is not accepted).  Row m is
- * a verified position: the target's features there, features[m] (n_feat_levels
- * * d, as for fe_draft_forward), and the token after it, tokens[m].  With
- * x_0(m) = FC(concat(FC(features[m]), e_{tokens[m]})) (Eq. 1), every layer i
- * writes, at cache row dst_rows[m],
- *   k = RoPE(W_k^i RMSNorm(x_0(m); attn_norm_i), positions[m])   (rotated)
- *   v = W_v^i RMSNorm(x_0(m); attn_norm_i)
- * in the storage dtype: the projections the pass applies to its own cascade
- * entry x_0, so a later pass over the grown prefix reads the row as a cached
- * key/value.  Nothing else in the caches is written.
+/* Drafter cache update after verification (Section 2.4's update step).  Row m
+ * is a verified position: the target's features there, features[m]
+ * (n_feat_levels * d, as for fe_draft_forward), and the token after it,
+ * tokens[m], with x_0(m) = FC(concat(FC(features[m]), e_{tokens[m]})) (Eq. 1).
+ * What a layer keys depends on the context (Section 2.1, Eq. 2):
+ *  FE_CTX_CASCADE / FE_CTX_PARALLEL: every layer i writes, at cache row
+ *   dst_rows[m],
+ *     k = RoPE(W_k^i RMSNorm(x_0(m); attn_norm_i), positions[m])   (rotated)
+ *     v = W_v^i RMSNorm(x_0(m); attn_norm_i)
+ *   the projections the pass applies to its own cascade entry x_0.
+ *  FE_CTX_SELF: layer i's row is its key and value of its own input
+ *   x_{i-1}(m), the state the pass at prefix positions[m] computes, so the
+ *   update runs the N layers over the new rows (a multi-position prefill):
+ *   layer by layer, each row attends to its sequence's rows of positions
+ *   0 .. p-1, which sit at cache rows dst_rows[m] - p .. dst_rows[m] - 1
+ *   (p = positions[m]; the rows this call writes included), plus its own key.
+ *   Rows are taken in chunks (as many as the workspace holds): within a chunk
+ *   every row sees the others' rows of the same layer, across chunks the
+ *   earlier chunk's rows of every layer; rows of one sequence must therefore
+ *   come in increasing position order, and no row may need a row of a later
+ *   one.  A row whose rows of position 0 would lie before cache row 0 gets
+ *   NaN state from its first attention on.
+ * Rows are written in the storage dtype, so a later pass over the grown prefix
+ * reads them as cached keys/values; nothing else in the caches is written.
  *  features  [n_rows, n_feat_levels*d] dtype, 16-byte aligned
  *  tokens, positions, dst_rows  [n_rows] int32, 4-byte aligned
  *  workspace caller-owned device memory, 256-byte aligned, at least
@@ -257,9 +269,9 @@ size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chunk_rows);
  * [0, cache->rows) is not written; a position outside [0, cfg.max_prefix) or a
  * token outside [0, target_vocab) writes NaN rows.  Rows that share a
  * destination race.  Errors: FE_E_INVALID (NULL handle, cache or array,
- * n_rows < 0, cfg.max_prefix == 0), FE_E_UNSUPPORTED (FE_CTX_SELF),
- * FE_E_ALIGN, FE_E_WORKSPACE (workspace NULL or below one row); nothing is
- * launched on an error.  n_rows == 0 is a no-op. */
+ * n_rows < 0, cfg.max_prefix == 0), FE_E_ALIGN, FE_E_WORKSPACE (workspace
+ * NULL or below one row); nothing is launched on an error.  n_rows == 0 is a
+ * no-op. */
 fe_status fe_kv_update(fe_drafter *h, int32_t n_rows, const void *features,
                        const int32_t *tokens, const int32_t *positions, const int32_t *dst_rows,
                        const fe_kv_cache *cache, void *workspace, size_t ws_bytes, void *stream);

@@ -47,7 +47,7 @@ template <typename T> __device__ __forceinline__ float piece_at(const u32x4 &w, 
 
 template <typename T, int D, int GH>
 __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T *__restrict__ Vc,
-                                              const int32_t *__restrict__ cu,
+                                              Seqs cu,
                                               const float *__restrict__ q,
                                               const float *__restrict__ knew,
                                               const float *__restrict__ vnew, int nctx,
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
   // head segments of the same token rows
   const int ch = blockIdx.y, c = blockIdx.x / ngrp, hg = blockIdx.x % ngrp, b = blockIdx.z;
   bool bad;
-  const int start = cu[b], P = attn_prefix(cu, b, pmax, bad);
+  const int start = cu.start(b), P = attn_prefix(cu, b, pmax, bad);
   const int span = kAttnChunk * cpw;  // prefix keys per workgroup
   const int nv = max(1, min((P + span - 1) / span, nch));
   if (ch >= nv) return;  // chunk beyond this sequence's prefix
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) void k_attn(const T *__restrict__ Kc, const T 
 template <int D, int GH, int DEPTH, int NCX>
 __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
                                                  const bf16_t *__restrict__ Vc,
-                                                 const int32_t *__restrict__ cu,
+                                                 Seqs cu,
                                                  const float *__restrict__ q,
                                                  const float *__restrict__ knew,
                                                  const float *__restrict__ vnew, int nctx,
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     const int c = col / ngrp, hg = col % ngrp;
     const int h0 = c * G + hg * GH;
     bool bad;
-    const int start = cu[b], P = attn_prefix(cu, b, pmax, bad);
+    const int start = cu.start(b), P = attn_prefix(cu, b, pmax, bad);
     const size_t row0 = (size_t)b * Hq + h0;
     attn_unit<D, GH, DEPTH, NCX>(
         Kc + ((size_t)start * Hkv + c) * D, Vc + ((size_t)start * Hkv + c) * D, (size_t)Hkv * D,
@@ -410,7 +410,7 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
 // write back the L2 once per workgroup.  LOG2: maxima in log2 units.
 template <typename T, bool LOG2>
 __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ part, int nch_ld,
-                                                    const int32_t *__restrict__ cu, int span,
+                                                    Seqs cu, int span,
                                                     int nwg, T *__restrict__ out, int Hq, int D,
                                                     int counted, int csplit, int pmax) {
   const int b = blockIdx.y;
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ pa
 }
 
 template <typename T, int D>
-static hipError_t attn_t(const void *K, const void *V, const int32_t *cu, const float *q,
+static hipError_t attn_t(const void *K, const void *V, Seqs cu, const float *q,
                          const float *knew, const float *vnew, int nctx, float *part, int nch,
                          int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int pmax,
                          hipStream_t s) {
@@ -502,7 +502,7 @@ static int resident_waves() {
 }
 
 template <int D>
-static hipError_t attn_mma_t(const void *K, const void *V, const int32_t *cu, const float *q,
+static hipError_t attn_mma_t(const void *K, const void *V, Seqs cu, const float *q,
                              const float *knew, const float *vnew, int nctx, float *part, int nch,
                              int nch_ld, int cpw, void *out, int B, int Hq, int Hkv,
                              const float *rope, int cascade, int pmax, int *persisted,
@@ -557,7 +557,7 @@ int attention_cpw(int B, int Hkv, int ngroups, int nch) {
   return cpw < 1 ? 1 : (int)cpw;
 }
 
-hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu, const float *q,
+hipError_t attention(int dt, const void *K, const void *V, Seqs cu, const float *q,
                      const float *knew, const float *vnew, int nctx, float *part, int nch,
                      int nch_ld, int cpw, void *out, int B, int Hq, int Hkv, int D,
                      const float *rope, int cascade, int pmax, hipStream_t s) {

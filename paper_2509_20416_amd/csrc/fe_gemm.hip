@@ -795,7 +795,7 @@ template <typename T> struct EpiQkv {
           continue;
         }
         const float pv = tile[m * ldt + (c ^ 8)];
-        const int P = a.cu_prefix[b + 1] - a.cu_prefix[b];
+        const int P = a.seqs.end(b) - a.seqs.start(b);
         const int pos = min(a.cascade ? P + j : P, a.rope_npos - 1);
         const int pm = 8 * (cc >> 4) + (cc & 7);
         const float c_ = a.rope[((size_t)pos * (D / 2) + pm) * 2];

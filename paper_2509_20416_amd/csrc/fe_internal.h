@@ -158,12 +158,23 @@ constexpr int kMergeMaxCand = 256 * 32;
 constexpr int kGemmMaxRows = 256;
 constexpr int kMaxTopk = 16;
 
-// Prefix length of sequence b as the attention kernels use it: P_b from the
-// packed offsets, or 0 with bad = true when it lies outside [0, pmax] (the
-// caller's bound on every P_b).  A bad sequence reads no cache row and its
-// attention output is NaN.
-__host__ __device__ inline int attn_prefix(const int32_t *cu, int b, int pmax, bool &bad) {
-  const int P = cu[b + 1] - cu[b];
+// Where each query's prefix rows sit in the cache: packed, one sequence after
+// the other ([B+1] offsets, rows p[b] .. p[b+1] - 1), or one (start, end) pair
+// per query ([2B], rows p[2b] .. p[2b+1] - 1; the ranges may overlap, as the
+// queries of a multi-position prefill share their sequence's rows).
+struct Seqs {
+  const int32_t *p;
+  int pairs;
+  __host__ __device__ int start(int b) const { return pairs ? p[2 * b] : p[b]; }
+  __host__ __device__ int end(int b) const { return pairs ? p[2 * b + 1] : p[b + 1]; }
+};
+
+// Prefix length of query b as the attention kernels use it: P_b from its
+// rows, or 0 with bad = true when it lies outside [0, pmax] (the caller's
+// bound on every P_b).  A bad query reads no cache row and its attention
+// output is NaN.
+__host__ __device__ inline int attn_prefix(Seqs cu, int b, int pmax, bool &bad) {
+  const int P = cu.end(b) - cu.start(b);
   bad = P < 0 || P > pmax;
   return bad ? 0 : P;
 }
@@ -273,7 +284,7 @@ struct QkvArgs {
   const void *wq, *wk, *wv;
   int d, D, Hq, Hkv;
   int nctx, j0, cascade;     // rows are (b, t) with t < nctx, cascade state j = j0 + t
-  const int32_t *cu_prefix;  // [B+1]
+  Seqs seqs;                 // prefix rows of each sequence (P_b, the position)
   const float *rope;         // [rope_npos, D/2, 2]: cos, sin of pos * theta^(-2m/D)
   int rope_npos;
   float *q_out;              // [B, Hq, D]       (row t == nctx-1 only)
@@ -356,7 +367,7 @@ hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long 
 // (B*Hq*(nch_ld*(D+2) + 1) floats, nch_ld >= nch = chunks of the longest
 // prefix) holds the partials of sequences that span several units (and, for
 // the equal shares, the partial count per head), merged by a second launch.
-hipError_t attention(int dt, const void *K, const void *V, const int32_t *cu_prefix,
+hipError_t attention(int dt, const void *K, const void *V, Seqs seqs,
                      const float *q, const float *knew, const float *vnew, int nctx,
                      float *part, int nch, int nch_ld, int cpw, void *out, int B, int Hq,
                      int Hkv, int D, const float *rope, int cascade, int pmax, hipStream_t s);
@@ -367,6 +378,15 @@ int attention_cpw(int B, int Hkv, int ngroups, int nch);
 // Rotary table: tab[(p * D/2 + m) * 2 + {0,1}] = cos, sin of p * theta^(-2m/D),
 // formed in double precision and rounded to fp32, for p < npos.
 hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s);
+
+// Multi-position prefill (self context): each new row's prefix rows as Seqs
+// pairs, and the rows' K/V written into the cache (see fe_misc.hip).
+hipError_t prefill_ranges(const int32_t *positions, const int32_t *dst_rows, int M,
+                          long cache_rows, int pos_limit, int pmax, int32_t *ranges, hipStream_t s);
+hipError_t kv_scatter(int dt, const float *knew, const float *vnew, int M, int Hkv, int D,
+                      const int32_t *positions, const int32_t *dst_rows, long cache_rows,
+                      int pos_limit, const float *rope, int rotated, void *kc, void *vc,
+                      hipStream_t s);
 
 // Greedy acceptance over the trees of B sequences (N levels, k per level):
 // tokens/target_next [B, 1+N*k], retrieve [B, N*(k-1)+1, N+1] -> accept_len [B],

@@ -777,6 +777,81 @@ __global__ void k_rope_table(float *tab, int npos, int D, double theta) {
   }
 }
 
+// ---- multi-position prefill under the self context --------------------------
+// Prefix rows of each new row m: its sequence's rows of positions 0..p-1, at
+// cache rows dst - p .. dst - 1 (pairs for Seqs).  A row whose position or
+// cache rows are out of range gets an empty range marked bad (length pmax + 1),
+// so its attention output, and everything after it, is NaN.
+__global__ void k_prefill_ranges(const int32_t *__restrict__ positions,
+                                 const int32_t *__restrict__ dst_rows, int M, long cache_rows,
+                                 int pos_limit, int pmax, int32_t *__restrict__ ranges) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  const int p = positions[m], r = dst_rows[m];
+  const bool ok = p >= 0 && p < pos_limit && p <= pmax && r - p >= 0 && r < cache_rows;
+  ranges[2 * m] = ok ? r - p : 0;
+  ranges[2 * m + 1] = ok ? r : pmax + 1;
+}
+
+// Row m's key (rotated at positions[m] unless `rotated`) and value into cache
+// row dst_rows[m] in the storage type; rows outside [0, cache_rows) are not
+// written, positions outside [0, pos_limit) give NaN rows.  One workgroup per
+// row, rotate-half pairs (e, e + D/2).
+template <typename T>
+__global__ __launch_bounds__(256) void k_kv_scatter(const float *__restrict__ knew,
+                                                    const float *__restrict__ vnew, int Hkv, int D,
+                                                    const int32_t *__restrict__ positions,
+                                                    const int32_t *__restrict__ dst_rows,
+                                                    long cache_rows, int pos_limit,
+                                                    const float *__restrict__ rope, int rotated,
+                                                    T *__restrict__ kc, T *__restrict__ vc) {
+  const int m = blockIdx.x, kvd = Hkv * D, half = D / 2;
+  const long r = dst_rows[m];
+  if (r < 0 || r >= cache_rows) return;
+  const int p = positions[m];
+  const bool bad = p < 0 || p >= pos_limit;
+  const float qnan = __int_as_float(0x7fc00000);
+  const float *kr = knew + (size_t)m * kvd, *vr = vnew + (size_t)m * kvd;
+  for (int i = threadIdx.x; i < Hkv * half; i += blockDim.x) {
+    const int h = i / half, e = i % half, o0 = h * D + e, o1 = o0 + half;
+    float k0 = kr[o0], k1 = kr[o1];
+    if (!rotated && !bad) {
+      const float cs = rope[((size_t)p * half + e) * 2], sn = rope[((size_t)p * half + e) * 2 + 1];
+      const float a = k0 * cs - k1 * sn, b = k1 * cs + k0 * sn;
+      k0 = a;
+      k1 = b;
+    }
+    kc[(size_t)r * kvd + o0] = Elt<T>::from_f(bad ? qnan : k0);
+    kc[(size_t)r * kvd + o1] = Elt<T>::from_f(bad ? qnan : k1);
+    vc[(size_t)r * kvd + o0] = Elt<T>::from_f(bad ? qnan : vr[o0]);
+    vc[(size_t)r * kvd + o1] = Elt<T>::from_f(bad ? qnan : vr[o1]);
+  }
+}
+
+hipError_t prefill_ranges(const int32_t *positions, const int32_t *dst_rows, int M,
+                          long cache_rows, int pos_limit, int pmax, int32_t *ranges, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_prefill_ranges, dim3((M + 255) / 256), dim3(256), 0, s, positions, dst_rows,
+                     M, cache_rows, pos_limit, pmax, ranges);
+  return hipGetLastError();
+}
+
+hipError_t kv_scatter(int dt, const float *knew, const float *vnew, int M, int Hkv, int D,
+                      const int32_t *positions, const int32_t *dst_rows, long cache_rows,
+                      int pos_limit, const float *rope, int rotated, void *kc, void *vc,
+                      hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (dt)
+    hipLaunchKernelGGL((k_kv_scatter<bf16_t>), dim3(M), dim3(256), 0, s, knew, vnew, Hkv, D,
+                       positions, dst_rows, cache_rows, pos_limit, rope, rotated, (bf16_t *)kc,
+                       (bf16_t *)vc);
+  else
+    hipLaunchKernelGGL((k_kv_scatter<float>), dim3(M), dim3(256), 0, s, knew, vnew, Hkv, D,
+                       positions, dst_rows, cache_rows, pos_limit, rope, rotated, (float *)kc,
+                       (float *)vc);
+  return hipGetLastError();
+}
+
 hipError_t rope_table(float *tab, int npos, int D, double theta, hipStream_t s) {
   const long n = (long)npos * (D / 2);
   const int grid = (int)((n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048);

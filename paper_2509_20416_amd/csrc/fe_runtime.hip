@@ -127,6 +127,11 @@ constexpr int kTiledRows = kGemmMaxRows + 1, kFusedRows = 16;
 struct UpdLayout {
   size_t cat, X, an, ssq, splitk, total;
   size_t splitk_floats;
+  // self context: the layers' row state of a prefill step (q, own K/V,
+  // attention output, x', SwiGLU rows, prefix ranges, attention partials of
+  // one 256-row slice)
+  size_t q, knew, vnew, ao, Xp, sb, ranges, part;
+  int nch_ld;
 };
 
 UpdLayout upd_layout_of(const fe_config &c, size_t C) {
@@ -140,9 +145,23 @@ UpdLayout upd_layout_of(const fe_config &c, size_t C) {
   U.an = take(nan_ * C * d * es);
   U.ssq = take(std::min<size_t>(kFusedRows, C) * (d / 16) * 4);
   const size_t rows = std::min<size_t>(kGemmMaxRows, C);
-  const size_t cols = (std::max<size_t>(2 * kvd, d) + 127) / 128 * 128;
+  const bool self = c.cascade_ctx == FE_CTX_SELF;
+  const size_t qd = (size_t)c.n_q_heads * c.head_dim;
+  const size_t cols = (std::max<size_t>(self ? qd + 2 * kvd : 2 * kvd, d) + 127) / 128 * 128;
   U.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
   U.splitk = take(U.splitk_floats * 4);
+  if (self) {
+    const size_t D = c.head_dim;
+    U.nch_ld = (c.max_prefix + kAttnChunk - 1) / kAttnChunk + 1;
+    U.q = take(C * qd * 4);
+    U.knew = take(C * kvd * 4);
+    U.vnew = take(C * kvd * 4);
+    U.ao = take(C * qd * es);
+    U.Xp = take(C * d * 4);
+    U.sb = take(C * (size_t)c.intermediate * es);
+    U.ranges = take(C * 2 * 4);
+    U.part = take(rows * c.n_q_heads * ((size_t)U.nch_ld * (D + 2) + 1) * 4);
+  }
   U.total = o;
   return U;
 }
@@ -395,7 +414,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     const int nctx = nctx_of(i), j0 = cascade ? 0 : src;
     // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
     // separate pass otherwise
-    QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, kv->cu_prefix,
+    QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, nctx, j0, cascade ? 1 : 0, Seqs{kv->cu_prefix, 0},
                (const float *)(ws + L.rope), L.npos, q, knew, vnew, dt ? 0 : 1};
     if (fuse_q(i)) {
       const NormA na1{ssqX, ntile, nctx, j0, N + 1, d, c.rms_eps};
@@ -406,7 +425,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
       FE_STAGE_RUN(FE_STAGE_QKV, gemm_qkv(dt, an, d, kDenseRows, B * nctx, qa, nullptr, s, &ss));
     }
     // attention over the layer's prefix cache plus the cascade keys
-    FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], kv->cu_prefix, q, knew,
+    FE_STAGE_RUN(FE_STAGE_ATTN, attention(dt, kv->k[i - 1], kv->v[i - 1], Seqs{kv->cu_prefix, 0}, q, knew,
                                       vnew, nctx, part, nch, nch_ld, cpw, ao, B, Hq, Hkv, D,
                                       (const float *)(ws + L.rope), cascade ? 1 : 0,
                                       kv->max_prefix, s));
@@ -651,7 +670,7 @@ fe_status enqueue_forward_seg(fe_drafter *h, const void *features, const int32_t
     return st;
   };
   auto attn = [&](int l) -> fe_status {
-    FE_TRY(attention(1, kv->k[l - 1], kv->v[l - 1], kv->cu_prefix, q, knew, vnew, nctx_of(l),
+    FE_TRY(attention(1, kv->k[l - 1], kv->v[l - 1], Seqs{kv->cu_prefix, 0}, q, knew, vnew, nctx_of(l),
                      part, nch, L.nchmax, cpw, (void *)ao, 1, Hq, Hkv, D,
                      (const float *)(ws + L.rope), cascade ? 1 : 0, kv->max_prefix, s));
     return FE_OK;
@@ -885,7 +904,7 @@ extern "C" fe_status fe_test_attn_split(const int32_t *prefix_lens, int32_t batc
   long run = 0;
   for (int b = 0; b < batch; ++b) {
     bool bad;
-    ucnt[b] = attn_seg_chunks(attn_prefix(cu.data(), b, pmax, bad), nch_ld) * ncols;
+    ucnt[b] = attn_seg_chunks(attn_prefix(Seqs{cu.data(), 0}, b, pmax, bad), nch_ld) * ncols;
     run += ucnt[b];
     uend[b] = run;
   }
@@ -945,14 +964,73 @@ extern "C" size_t fe_kv_update_workspace_bytes(const fe_config *cfg, int32_t chu
 // context): x_0 of every row as in the pass (Eq. 1), then per layer its
 // RMSNorm and the rotated K / V projections, scattered into the caches.
 namespace {
+// The N layers over Mc new rows of the self context, whose x_0 rows are in U.X:
+// layer by layer, every row's Q/K/V, its K/V into the cache, then its attention
+// over its sequence's rows of earlier positions (the rows this step just wrote
+// included) plus its own key, the O projection, the MLP, x_i into U.X.  Rows
+// go in slices of at most kGemmMaxRows per launch.
+fe_status prefill_layers(fe_drafter *h, const UpdLayout &U, char *ws, int Mc,
+                         const int32_t *positions, const int32_t *dst_rows,
+                         const fe_kv_cache *cache, const SplitScratch *ss, hipStream_t s) {
+  const fe_config &c = h->cfg;
+  const int dt = c.dtype == FE_BF16 ? 1 : 0, es = es_of(c);
+  const int d = c.hidden, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, I = c.intermediate;
+  const int qd = Hq * D, kvd = Hkv * D;
+  float *X = (float *)(ws + U.X), *Xp = (float *)(ws + U.Xp);
+  float *q = (float *)(ws + U.q), *knew = (float *)(ws + U.knew), *vnew = (float *)(ws + U.vnew);
+  char *an = ws + U.an, *ao = ws + U.ao, *sb = ws + U.sb;
+  int32_t *ranges = (int32_t *)(ws + U.ranges);
+  float *part = (float *)(ws + U.part);
+  const float *rope = (const float *)(h->ws + h->L.rope);
+  const int pmax = c.max_prefix;
+  const int nch = (pmax + kAttnChunk - 1) / kAttnChunk;
+  FE_TRY(prefill_ranges(positions, dst_rows, Mc, (long)cache->rows, c.max_prefix, pmax, ranges, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const fe_layer_weights &lw = h->layers[l];
+    FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an, d, c.rms_eps, s));
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      const QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, 1, 0, 0, Seqs{ranges + 2 * s0, 1},
+                       rope, h->L.npos, q + (size_t)s0 * qd, knew + (size_t)s0 * kvd,
+                       vnew + (size_t)s0 * kvd, dt ? 0 : 1};
+      FE_TRY(gemm_qkv(dt, an + (size_t)s0 * d * es, d, kDenseRows, Ms, qa, nullptr, s, ss));
+    }
+    // every row's K/V is in the cache before any row's attention reads it
+    FE_TRY(kv_scatter(dt, knew, vnew, Mc, Hkv, D, positions, dst_rows, (long)cache->rows,
+                      c.max_prefix, rope, dt ? 0 : 1, cache->k[l], cache->v[l], s));
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      const int cpw = h->attn_split > 0 ? h->attn_split : attention_cpw(Ms, Hkv, 1, nch);
+      FE_TRY(attention(dt, cache->k[l], cache->v[l], Seqs{ranges + 2 * s0, 1},
+                       q + (size_t)s0 * qd, knew + (size_t)s0 * kvd, vnew + (size_t)s0 * kvd, 1,
+                       part, nch, U.nch_ld, cpw, ao + (size_t)s0 * qd * es, Ms, Hq, Hkv, D, rope,
+                       0, pmax, s));
+    }
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      // x' = x_{i-1} + W_o o
+      FE_TRY(gemm_resid(dt, ao + (size_t)s0 * qd * es, qd, Ms, qd, lw.wo, d, Xp + (size_t)s0 * d,
+                        d, X + (size_t)s0 * d, d, nullptr, 1, 0, nullptr, s, ss));
+    }
+    FE_TRY(rmsnorm_rows(dt, Xp, Mc, 1, 0, d, 0, lw.mlp_norm, an, d, c.rms_eps, s));
+    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+      const int Ms = std::min(kGemmMaxRows, Mc - s0);
+      FE_TRY(gemm_swiglu(dt, an + (size_t)s0 * d * es, d, kDenseRows, Ms, d, lw.w_gate, lw.w_up, I,
+                         sb + (size_t)s0 * I * es, I, nullptr, s));
+      // x_i = x' + W_d s (Eq. 2)
+      FE_TRY(gemm_resid(dt, sb + (size_t)s0 * I * es, I, Ms, I, lw.w_down, d, X + (size_t)s0 * d,
+                        d, Xp + (size_t)s0 * d, d, nullptr, 1, 0, nullptr, s, ss));
+    }
+  }
+  return FE_OK;
+}
+
 fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
                          const int32_t *tokens, const int32_t *positions,
                          const int32_t *dst_rows, const fe_kv_cache *cache, void *workspace,
                          size_t ws_bytes, void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
-  if (c.cascade_ctx == FE_CTX_SELF)
-    return fail(FE_E_UNSUPPORTED, "the cache update is not defined for FE_CTX_SELF");
   if (n_rows < 0) return fail(FE_E_INVALID, "n_rows %d is negative", n_rows);
   if (!cache || !cache->k || !cache->v) return fail(FE_E_INVALID, "cache and its pointer arrays are required");
   if (cache->rows < 0) return fail(FE_E_INVALID, "cache->rows is negative");
@@ -1003,9 +1081,10 @@ fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
                           (const float *)(h->ws + h->L.rope), cache->k[l], cache->v[l]};
     }
   };
+  const bool self = c.cascade_ctx == FE_CTX_SELF;
   for (int r0 = 0; r0 < n_rows; r0 += C) {
     const int Mc = std::min(C, n_rows - r0);
-    if (dt && Mc <= kFusedRows) {
+    if (dt && Mc <= kFusedRows && !self) {
       // few rows: the input FC also writes gamma_l * x_0 for every layer and
       // the rows' sums of squares, and the K/V launch applies 1/rms
       FE_TRY(gemm_store(dt, (const char *)features + (size_t)r0 * F * d * es, F * d, Mc, F * d,
@@ -1049,6 +1128,11 @@ fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
         FE_TRY(gemm_resid(dt, cat + (size_t)s0 * 2 * d * es, 2 * d, Ms, 2 * d, h->w.w_in, d,
                           X + (size_t)s0 * d, d, nullptr, 0, nullptr, 1, 0, nullptr, s, &ss));
       }
+    }
+    if (self) {
+      const fe_status st = prefill_layers(h, U, ws, Mc, positions + r0, dst_rows + r0, cache, &ss, s);
+      if (st != FE_OK) return st;
+      continue;
     }
     if (dt) {
       for (int l = 0; l < c.n_layers; ++l)

@@ -202,12 +202,7 @@ def test_kv_update_errors():
     dev = torch.device("cuda:0")
     args = (to_device(up.features, cfg.dtype, dev), to_device(up.tokens, "i32", dev),
             to_device(up.positions, "i32", dev), to_device(up.dst_rows, "i32", dev))
-    dr = Drafter(cfg.with_(cascade_ctx="self"), w, max_batch=1, max_prefix=4, max_topk=cfg.topk)
     ks, vs = _caches(cfg, 4, dev)
-    with pytest.raises(fe.FeError) as e:
-        dr.kv_update(*args, ks, vs)
-    assert e.value.status == fe.FE_E_UNSUPPORTED
-    dr.close()
     dr = Drafter(cfg, w, max_batch=1, max_prefix=4, max_topk=cfg.topk)
     with pytest.raises(fe.FeError) as e:   # misaligned features
         dr.kv_update(args[0].view(-1)[1:], *args[1:], ks, vs, n_rows=1)
