@@ -213,6 +213,23 @@ def kv_update_cost(cfg, M):
     return 2 * M * per_row_mac, wbytes + rbytes
 
 
+def kv_update_cost_self(cfg, positions):
+    """Algorithmic FLOPs and bytes of one cache update under the self context
+    (the N layers run over the rows): per row the fusion and input FCs and per
+    layer Q/K/V, O, gate/up and down, plus the attention's two contractions
+    over the row's p earlier keys and its own; every weight matrix the layers
+    use read once, each row's features, embedding row and written K/V rows."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    d, F, N, I = cfg.hidden, cfg.n_feat_levels, cfg.n_layers, cfg.intermediate
+    qd, kvd = cfg.n_q_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+    M = len(positions)
+    per_row_mac = F * d * d + 2 * d * d + N * (d * (qd + 2 * kvd) + qd * d + 3 * d * I)
+    attn = sum(N * 4 * qd * (int(p) + 1) for p in positions)
+    wbytes = (F * d * d + 2 * d * d + N * (d * (qd + 2 * kvd) + qd * d + 3 * d * I)) * es
+    rbytes = M * (F * d + d + N * 2 * kvd) * es
+    return 2 * M * per_row_mac + attn, wbytes + rbytes
+
+
 def time_kv_update(dr, cfg, positions, reps=20, warmup=3, chunk_rows=1024):
     """fe_kv_update of len(positions) rows into fresh caches (rows written in
     order), eager launches on the current stream, mean per call."""
@@ -230,8 +247,8 @@ def time_kv_update(dr, cfg, positions, reps=20, warmup=3, chunk_rows=1024):
     dst = to_device(np.arange(M, dtype=np.int32), "i32", dev)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     shape = (M, cfg.n_kv_heads, cfg.head_dim)
-    ks = [torch.empty(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
-    vs = [torch.empty(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
+    ks = [torch.zeros(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
+    vs = [torch.zeros(shape, dtype=tdt, device=dev) for _ in range(cfg.n_layers)]
     for _ in range(warmup):
         dr.kv_update(feats, toks, pos, dst, ks, vs, chunk_rows=chunk_rows)
     torch.cuda.synchronize()
@@ -243,7 +260,10 @@ def time_kv_update(dr, cfg, positions, reps=20, warmup=3, chunk_rows=1024):
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / reps
-    flops, nbytes = kv_update_cost(cfg, M)
+    if cfg.cascade_ctx == "self":
+        flops, nbytes = kv_update_cost_self(cfg, positions)
+    else:
+        flops, nbytes = kv_update_cost(cfg, M)
     tfs = flops / (ms * 1e-3) / 1e12
     peak = MFMA_PEAK_TFS[cfg.dtype]
     return {"rows": M, "us_per_call": ms * 1000.0, "flops": flops, "bytes": nbytes,
@@ -551,6 +571,15 @@ def main():
     P = int(plens.max())
     upd_cycle = time_kv_update(dr, cfg, np.arange(max(0, P - cfg.n_layers - 1), P))
     upd_prefill = time_kv_update(dr, cfg, np.arange(P), reps=10)
+    # ... and under the self context, where the update is a prefill of the N
+    # layers over the rows (same weights, a drafter of its own)
+    sdr = Drafter(cfg.with_(cascade_ctx="self"), w, max_batch=cfg.batch, max_prefix=P,
+                  max_topk=cfg.topk)
+    upd_self_cycle = time_kv_update(sdr, sdr.cfg, np.arange(max(0, P - cfg.n_layers - 1), P))
+    upd_self_prefill = time_kv_update(sdr, sdr.cfg, np.arange(P), reps=5, warmup=1)
+    sdr.close()
+    log(f"self-context update: {upd_self_cycle['us_per_call']:.1f} us cycle, "
+        f"{upd_self_prefill['us_per_call']:.1f} us for {P} rows")
     log(f"kv update: {upd_cycle['rows']} rows {upd_cycle['us_per_call']:.1f} us, "
         f"{upd_prefill['rows']} rows {upd_prefill['us_per_call']:.1f} us "
         f"({upd_prefill['mfma_frac'] * 100:.1f}% of the MFMA peak)")
@@ -600,7 +629,8 @@ def main():
         # call, the kernel itself is a few microseconds
         "next_accept_greedy": {"us_per_call": accept_us, "batch": B,
                                "accept_len_seq0": accept_len0, "issue": "eager, from Python"},
-        "next_kv_update": {"cycle": upd_cycle, "prefill": upd_prefill},
+        "next_kv_update": {"cycle": upd_cycle, "prefill": upd_prefill,
+                           "self_context": {"cycle": upd_self_cycle, "prefill": upd_self_prefill}},
         "next_sampled_drafting": {"temperature": 1.0, "steps": args.steps,
                                   "us_per_pass": sms * 1000.0,
                                   "drafts_per_s": cfg.batch * 1000.0 / sms,

@@ -42,6 +42,12 @@ struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
       psum, cval, cidx, cz, img, splitk, tagged, total;
   size_t splitk_floats;
+  // Layer-private buffers (x', its norms and sums of squares, Q/K/V, attention
+  // partials and output, SwiGLU rows, split-K slices): one lane, or under
+  // FE_CTX_PARALLEL one lane per layer, so that the independent layers can
+  // run side by side; bytes per lane of each.
+  int lanes;
+  size_t Xp_l, ssqP_l, AM_l, an_l, bn_l, q_l, knew_l, vnew_l, part_l, ao_l, s_l, splitk_l;
   int nchmax, nwg, npos;
   // tagged words of the persistent batch-1 pass (offsets in words from `tagged`)
   size_t t_sync, t_g, t_ssq, t_ssqp, t_copy, t_xp, t_s, t_cand, t_words;
@@ -59,26 +65,31 @@ Layout layout_of(const fe_config &c) {
   L.nwg = lmhead_tiles(c.draft_vocab);
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += up256(bytes); return at; };
+  L.lanes = c.cascade_ctx == FE_CTX_PARALLEL ? (int)N : 1;
+  auto lane = [&](size_t bytes, size_t &lane_bytes) {
+    lane_bytes = up256(bytes);
+    return take(lane_bytes * L.lanes);
+  };
   L.cat = take(B * 2 * d * es);
   L.X = take(B * (N + 1) * d * 4);
-  L.Xp = take(B * d * 4);
+  L.Xp = lane(B * d * 4, L.Xp_l);
   L.ssqX = take(B * (N + 1) * (d / 16) * 4);  // sums of squares of x_j per 16-column tile
-  L.ssqP = take(B * (d / 16) * 4);            // ... of x' (post-attention residual)
+  L.ssqP = lane(B * (d / 16) * 4, L.ssqP_l);  // ... of x' (post-attention residual)
   // gamma * x operands of the fused-RMSNorm GEMMs: per layer l the QKV rows
   // (b, j) of x_j, the MLP rows of x', the final-norm rows (b, i-1) of x_i
   L.AQ = take(N * B * N * d * es);
-  L.AM = take(B * d * es);
+  L.AM = lane(B * d * es, L.AM_l);
   L.AF = take(B * N * d * es);
-  L.an = take(B * N * d * es);
-  L.bn = take(B * d * es);
-  L.q = take(B * Hq * D * 4);
-  L.knew = take(B * N * Hkv * D * 4);
-  L.vnew = take(B * N * Hkv * D * 4);
-  L.part = take(B * Hq * ((size_t)L.nchmax * (D + 2) + 1) * 4);  // + partial counts
+  L.an = lane(B * N * d * es, L.an_l);
+  L.bn = lane(B * d * es, L.bn_l);
+  L.q = lane(B * Hq * D * 4, L.q_l);
+  L.knew = lane(B * N * Hkv * D * 4, L.knew_l);
+  L.vnew = lane(B * N * Hkv * D * 4, L.vnew_l);
+  L.part = lane(B * Hq * ((size_t)L.nchmax * (D + 2) + 1) * 4, L.part_l);  // + partial counts
   L.npos = c.max_prefix + c.n_layers;  // positions P_b + j, j < N
   L.rope = take((size_t)L.npos * (D / 2) * 2 * 4);
-  L.ao = take(B * Hq * D * es);
-  L.s = take(B * I * es);
+  L.ao = lane(B * Hq * D * es, L.ao_l);
+  L.s = lane(B * I * es, L.s_l);
   L.pmax = take(B * N * (size_t)L.nwg * 4);
   L.psum = take(B * N * (size_t)L.nwg * 4);
   L.cval = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
@@ -108,7 +119,7 @@ Layout layout_of(const fe_config &c) {
     const size_t rows = std::min<size_t>(256, B * N);
     const size_t cols = (std::max<size_t>((Hq + 2 * Hkv) * D, d) + 127) / 128 * 128;
     L.splitk_floats = rows > 16 ? 8 * rows * cols : 0;
-    L.splitk = take(L.splitk_floats * 4);
+    L.splitk = lane(L.splitk_floats * 4, L.splitk_l);
   }
   L.total = o;
   return L;
@@ -229,6 +240,9 @@ struct fe_drafter {
   fe_draft_out last_out{};
   fe_tree_out last_tree{};
   hipEvent_t ev_a = nullptr, ev_b = nullptr;
+  // FE_CTX_PARALLEL: one stream per layer (default priority), fork and join events
+  hipStream_t side[kMaxLayers] = {};
+  hipEvent_t ev_fork = nullptr, ev_join[kMaxLayers] = {};
 };
 
 extern "C" {
@@ -324,6 +338,11 @@ void fe_drafter_destroy(fe_drafter *h) {
   if (h->exec) (void)hipGraphExecDestroy(h->exec);
   if (h->graph) (void)hipGraphDestroy(h->graph);
   if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
+  for (int i = 0; i < kMaxLayers; ++i) {
+    if (h->side[i]) (void)hipStreamDestroy(h->side[i]);
+    if (h->ev_join[i]) (void)hipEventDestroy(h->ev_join[i]);
+  }
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   delete h;
 }
 
@@ -343,6 +362,18 @@ namespace {
     if (only_stage < 0) FE_TRY(x);   \
   } while (0)
 
+// The per-layer streams and fork/join events of FE_CTX_PARALLEL, created once
+// per handle before the first pass (never while a graph is being captured).
+fe_status ensure_lanes(fe_drafter *h) {
+  if (h->cfg.cascade_ctx != FE_CTX_PARALLEL || h->cfg.n_layers < 2) return FE_OK;
+  if (!h->ev_fork) FE_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
+  for (int i = 0; i < h->cfg.n_layers; ++i) {
+    if (!h->side[i]) FE_TRY(hipStreamCreateWithFlags(&h->side[i], hipStreamNonBlocking));
+    if (!h->ev_join[i]) FE_TRY(hipEventCreateWithFlags(&h->ev_join[i], hipEventDisableTiming));
+  }
+  return FE_OK;
+}
+
 // The whole pass: FCs of Eq. 1, N cascade layers (Eq. 2), LM head + top-k.
 fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int32_t *next_tokens,
                           const fe_kv_view *kv, int topk, float inv_temp, const float *uniforms,
@@ -354,17 +385,15 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   const int I = c.intermediate, qd = Hq * D, F = c.n_feat_levels;
   char *ws = h->ws;
   void *cat = ws + L.cat;
-  float *X = (float *)(ws + L.X), *Xp = (float *)(ws + L.Xp);
-  void *an = ws + L.an, *bn = ws + L.bn, *ao = ws + L.ao, *sbuf = ws + L.s;
-  float *q = (float *)(ws + L.q), *knew = (float *)(ws + L.knew), *vnew = (float *)(ws + L.vnew);
-  float *part = (float *)(ws + L.part);
+  float *X = (float *)(ws + L.X);
+  void *an = ws + L.an;  // lane 0: the final norm's rows after the layers
   const long xrow = (long)(N + 1) * d;  // stride between sequences in X
   const int esz = dt ? 2 : 4;
   const int nch = kv->max_prefix > 0 ? (kv->max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
   const int nch_ld = L.nchmax;
   const int cpw = h->attn_split > 0 ? h->attn_split : attention_cpw(B, Hkv, 1, nch);
   const int ntile = d / 16;
-  float *ssqX = (float *)(ws + L.ssqX), *ssqP = (float *)(ws + L.ssqP);
+  float *ssqX = (float *)(ws + L.ssqX);
 
   // g_t = FC(concat(l, m, h)) -> cat[:, :d]; e_{t+1} -> cat[:, d:]
   const SplitScratch ss{(float *)(ws + L.splitk), L.splitk_floats};
@@ -377,7 +406,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   // themselves (rows_norm), for every consumer, and no RMSNorm launch remains.
   const bool cascade = c.cascade_ctx == FE_CTX_CASCADE;
   const bool parallel = c.cascade_ctx == FE_CTX_PARALLEL;  // every layer reads x_0
-  char *AQ = ws + L.AQ, *AM = ws + L.AM, *AF = ws + L.AF;
+  char *AQ = ws + L.AQ, *AF = ws + L.AF;
   const size_t aq_layer = (size_t)c.max_batch * N * d * esz;  // bytes per layer block of AQ
   auto nctx_of = [&](int l) { return cascade ? l : 1; };
   const bool rows_norm = B > 16 && d <= 8192;
@@ -408,9 +437,33 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
                                       0, rows_norm ? nullptr : ssqX, N + 1, 0, &gc_x0, s, &ss,
                                       norm_eps));
 
+  // Under FE_CTX_PARALLEL the layers are independent (each reads x_0): each
+  // runs on a stream of its own, forked from and joined back into `s`, with
+  // its own buffers, so that their launches overlap (a captured pass holds
+  // them as parallel branches).
+  const bool fork = parallel && only_stage < 0 && N > 1;
+  hipStream_t lane_stream[kMaxLayers];
+  for (int i = 0; i < N; ++i) lane_stream[i] = s;
+  if (fork) {
+    FE_TRY(hipEventRecord(h->ev_fork, s));  // streams and events: ensure_lanes
+    for (int i = 0; i < N; ++i) {
+      FE_TRY(hipStreamWaitEvent(h->side[i], h->ev_fork, 0));
+      lane_stream[i] = h->side[i];
+    }
+  }
   for (int i = 1; i <= N; ++i) {
     const fe_layer_weights &lw = h->layers[i - 1];
     const int src = parallel ? 0 : i - 1;  // the layer's input state
+    hipStream_t s = lane_stream[i - 1];
+    // this layer's private buffers (lane i - 1 under FE_CTX_PARALLEL)
+    const size_t ln = L.lanes > 1 ? (size_t)(i - 1) : 0;
+    float *Xp = (float *)(ws + L.Xp + ln * L.Xp_l), *ssqP = (float *)(ws + L.ssqP + ln * L.ssqP_l);
+    char *AM = ws + L.AM + ln * L.AM_l;
+    void *an = ws + L.an + ln * L.an_l, *bn = ws + L.bn + ln * L.bn_l;
+    float *q = (float *)(ws + L.q + ln * L.q_l), *knew = (float *)(ws + L.knew + ln * L.knew_l);
+    float *vnew = (float *)(ws + L.vnew + ln * L.vnew_l), *part = (float *)(ws + L.part + ln * L.part_l);
+    void *ao = ws + L.ao + ln * L.ao_l, *sbuf = ws + L.s + ln * L.s_l;
+    const SplitScratch ss{(float *)(ws + L.splitk + ln * L.splitk_l), L.splitk_floats};
     const int nctx = nctx_of(i), j0 = cascade ? 0 : src;
     // pre-attention RMSNorm of the context rows: fused for up to 16 rows, a
     // separate pass otherwise
@@ -455,6 +508,11 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
                                        Xp, d, rows_norm ? nullptr : ssqX, N + 1, i, &gc_xi, s, &ss,
                                        norm_eps));
   }
+  if (fork)
+    for (int i = 0; i < N; ++i) {
+      FE_TRY(hipEventRecord(h->ev_join[i], h->side[i]));
+      FE_TRY(hipStreamWaitEvent(s, h->ev_join[i], 0));
+    }
 
   // shared LM head on every h_i (rows b*N + i-1), fused softmax statistics and top-k
   const NormA naf{ssqX, ntile, N, 1, N + 1, d, c.rms_eps};
@@ -785,6 +843,10 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
   if (!h->table_ready) {  // first pass on this handle: the rotary table
     FE_TRY(rope_table((float *)(h->ws + h->L.rope), h->L.npos, c.head_dim, (double)c.rope_theta, s));
     h->table_ready = true;
+  }
+  {
+    const fe_status st = ensure_lanes(h);
+    if (st != FE_OK) return st;
   }
 
   // remember the call for fe_time_stage

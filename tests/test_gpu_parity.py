@@ -327,6 +327,34 @@ def test_prefix_above_bound_poisons_only_its_sequence(cfg, plens, pmax):
     dr.close()
 
 
+@pytest.mark.parametrize("batch", [1, 3, 20])
+def test_parallel_heads_graph_replays_match_eager(batch):
+    """Under FE_CTX_PARALLEL every layer runs on a stream of its own (forked
+    from the caller's stream and joined back; a captured pass holds them as
+    parallel branches): eager passes and graph replays, with eager work
+    between the replays, agree bit for bit, and both match the oracle."""
+    import torch
+    from paper_2509_20416_amd import Drafter
+    cfg = C.SMALL_GQA_BF16.with_(cascade_ctx="parallel", batch=batch,
+                                 name=f"small_gqa_bf16_b{batch}_parallel")
+    rep, _, _ = _run(cfg, seed=5, graph=True)
+    w, inp = make_weights(cfg, 5), make_inputs(cfg, 5)
+    dr = Drafter(cfg, w, max_batch=batch, max_prefix=int(inp.prefix_lens.max()))
+    di = dr.upload_inputs(inp)
+    eager = {n: t.cpu().numpy() for n, t in dr.forward(di, logits=True, hidden=True).items()}
+    dr.set_graph_mode(True)
+    out = dr.alloc_outputs(batch, cfg.topk, logits=True, hidden=True)
+    for r in range(4):
+        for t in out.values():
+            t.zero_()
+        dr.forward(di, out=out)
+        torch.cuda.synchronize()
+        _ = torch.ones(1000, device="cuda").sum().item()
+        for n in eager:
+            np.testing.assert_array_equal(out[n].cpu().numpy(), eager[n], err_msg=f"replay {r} {n}")
+    dr.close()
+
+
 # --- paper-shaped workloads at full size, in the configuration the bench times -----------
 @pytest.mark.timeout(900)
 def test_llama8b_b1_full():
