@@ -257,6 +257,48 @@ int feo_draft_forward(const feo_config *c, const feo_weights *w, int32_t batch,
                           NULL, hidden, logits, topk_draft, topk_ids, topk_probs);
 }
 
+/* Philox4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC 2011): ten rounds of the 4x64 Philox S-box over the
+ * counter, the two-word key bumped by the Weyl constants between rounds.  A
+ * round multiplies counter words 0 and 2 by the two round multipliers and
+ * rebuilds the counter as (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1,
+ * lo(M0 c0)). */
+void feo_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+  uint64_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const unsigned __int128 p0 = (unsigned __int128)M0 * c0, p1 = (unsigned __int128)M1 * c2;
+    const uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+    const uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Uniforms first .. first+n-1 of the draw stream (seed, offset): uniform e is
+ * word e mod 4 of the Philox4x64-10 block at counter (floor(e / 4), offset, 0,
+ * 0) under key (seed, 0), its top 23 bits j mapped to (j + 1/2) / 2^23, which
+ * is exact in float and lies in (0, 1). */
+void feo_philox_uniforms(uint64_t seed, uint64_t offset, uint64_t first, int64_t n, float *out) {
+  const uint64_t key[2] = {seed, 0};
+  for (int64_t i = 0; i < n; ++i) {
+    const uint64_t e = first + (uint64_t)i;
+    const uint64_t ctr[4] = {e >> 2, offset, 0, 0};
+    uint64_t blk[4];
+    feo_philox4x64_10(ctr, key, blk);
+    const uint64_t j = blk[e & 3] >> 41;
+    out[i] = (float)(((double)j + 0.5) / 8388608.0);
+  }
+}
+
 /* -log(-log(u)): a standard Gumbel variate from a uniform u in (0, 1). */
 static double gumbel(float u) { return -log(-log((double)u)); }
 

@@ -164,6 +164,20 @@ int feo_kv_update_self(const feo_config *cfg, const feo_weights *w, int32_t n_ro
                        double *const *v_out);
 
 /*
+ * Counter-based uniforms for stochastic drafting (the randomness of Section
+ * 2.2's sampled candidates, drawn from a seed and an offset instead of a
+ * stored array).  feo_philox4x64_10: one block of the Philox4x64-10 generator
+ * (Salmon et al., SC 2011) for counter ctr and key.  feo_philox_uniforms:
+ * uniforms first .. first+n-1 of the stream (seed, offset); uniform e is word
+ * e mod 4 of the block at counter (e / 4, offset, 0, 0), key (seed, 0), its
+ * top 23 bits j giving (j + 1/2) / 2^23.  Uniform e of a drafting pass is the
+ * one of row b*N + i - 1, draft id v: e = (b*N + i - 1) * V + v, as the
+ * uniforms array of feo_draft_sample is laid out.
+ */
+void feo_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+void feo_philox_uniforms(uint64_t seed, uint64_t offset, uint64_t first, int64_t n, float *out);
+
+/*
  * Speculative-sampling acceptance of one cycle at temperature T (Section 2.4).
  * For the tree of feo_build_tree (tokens [B, T] target ids, retrieve) with
  * topk_draft [B, N, k] the children's draft ids, draft_logits [B, N, V] the

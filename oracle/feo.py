@@ -229,6 +229,26 @@ def kv_update(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.nd
     return ks, vs
 
 
+def philox4x64_10(counter, key) -> np.ndarray:
+    """One Philox4x64-10 block (see feo_philox4x64_10)."""
+    c = np.ascontiguousarray(counter, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, np.uint64)
+    assert c.shape == (4,) and k.shape == (2,)
+    lib().feo_philox4x64_10(C.c_void_p(c.ctypes.data), C.c_void_p(k.ctypes.data),
+                            C.c_void_p(out.ctypes.data))
+    return out
+
+
+def philox_uniforms(seed: int, offset: int, first: int, n: int) -> np.ndarray:
+    """float32 uniforms first .. first+n-1 of the draw stream (seed, offset)
+    (see feo_philox_uniforms)."""
+    out = np.zeros(int(n), np.float32)
+    lib().feo_philox_uniforms(C.c_uint64(int(seed)), C.c_uint64(int(offset)),
+                              C.c_uint64(int(first)), C.c_int64(int(n)), _p(out))
+    return out
+
+
 def kv_update_self(cfg, w, features: np.ndarray, tokens: np.ndarray, positions: np.ndarray,
                    dst_rows: np.ndarray, kcache, vcache):
     """Per-layer cache rows under the self context (see feo_kv_update_self in
