@@ -370,6 +370,22 @@ def time_second(name, seed, steps, warmup):
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / steps
+    # stochastic drafting at this batch: uniforms read from HBM, or drawn in the pass
+    from fe_synth import make_uniforms
+    ud = torch.from_numpy(make_uniforms((cfg.batch, cfg.n_layers, cfg.draft_vocab),
+                                        seed=seed + 1)).to(dr.device)
+    so = torch.tensor([seed + 1, 0], dtype=torch.int64, device=dr.device)
+    samp = {}
+    for name, kw in (("uniforms_array", dict(uniforms=ud)), ("seeded", dict(seed_offset=so))):
+        dr.forward(di, out=out, tree=tree, temperature=1.0, **kw)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(steps):
+            dr.forward(di, out=out, tree=tree, temperature=1.0, **kw)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        samp[name + "_us_per_pass"] = ev0.elapsed_time(ev1) / steps * 1000.0
+    samp["uniform_bytes"] = cfg.batch * cfg.n_layers * cfg.draft_vocab * 4
     # NEXT-1 for this batch: every sequence appends N+1 verified positions
     # (the most one cycle accepts) after its prefix
     upd_pos = np.concatenate([np.arange(p - cfg.n_layers - 1, p) for p in plens])
@@ -386,6 +402,7 @@ def time_second(name, seed, steps, warmup):
             "hbm_frac": pbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "mfma_frac": pflops / (ms * 1e-3) / 1e12 / peak,
             "mfma_ceiling_frac": min(1.0, pflops / pbytes * HBM_PEAK_GBS / 1e3 / peak),
+            "sampled_drafting": samp,
             "next_kv_update_cycle": upd}
 
 
@@ -543,6 +560,19 @@ def main():
     torch.cuda.synchronize()
     sms = ev0.elapsed_time(ev1) / args.steps
     log(f"sampled drafting: {sms * 1000:.1f} us/pass")
+    # ... and with the uniforms drawn inside the pass (counter-based stream,
+    # (seed, offset) in device memory, a new offset per pass)
+    so = torch.tensor([args.seed + 1, 0], dtype=torch.int64, device=dr.device)
+    dr.forward(di, out=out, tree=tree, temperature=1.0, seed_offset=so)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        so[1:].fill_(i)
+        dr.forward(di, out=out, tree=tree, temperature=1.0, seed_offset=so)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    seeded_ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"seeded sampled drafting: {seeded_ms * 1000:.1f} us/pass (offset advanced per pass)")
     # ... and its speculative-sampling acceptance against synthetic target
     # distributions over the target vocabulary (one per tree node)
     sout = dr.alloc_outputs(cfg.batch, cfg.topk, logits=True)
@@ -636,6 +666,10 @@ def main():
                                   "drafts_per_s": cfg.batch * 1000.0 / sms,
                                   "uniform_bytes": cfg.batch * cfg.n_layers * cfg.draft_vocab * 4,
                                   "vs_greedy": ms / sms,
+                                  "seeded_us_per_pass": seeded_ms * 1000.0,
+                                  "seeded_note": "uniforms drawn in the pass (Philox4x64-10); "
+                                                 "the timed loop also launches one fill per pass "
+                                                 "to advance the offset",
                                   "accept_sample_us_per_call": accept_s_us,
                                   "accept_sample_issue": "eager, from Python"},
         # matrix-core use over the whole pass, against the most that an

@@ -188,6 +188,24 @@ fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *features,
                           float temperature, const float *uniforms, const fe_draft_out *out,
                           void *stream);
 
+/* fe_draft_sample with the uniforms drawn inside the pass from a counter-based
+ * generator instead of read from an array (Section 2.2's sampled candidates;
+ * Section 3 evaluates T = 1): uniform e = (b*N + i - 1) * V + v -- the index
+ * the uniforms array of fe_draft_sample would give it -- is word e mod 4 of
+ * the Philox4x64-10 block (Salmon, Moraes, Dror and Shaw, SC 2011) at
+ * counter (e / 4, offset, 0, 0) under key (seed, 0), its top 23 bits j giving
+ * u = (j + 1/2) / 2^23.  seed_offset: device memory holding the two uint64
+ * values (seed, offset), 8-byte aligned, read by the kernels when they run,
+ * so a captured pass (graph mode) replays with whatever the caller wrote
+ * there: advance the offset per cycle to draw fresh candidates.  The pass
+ * reads no [B, N, V] array (28.7 MB at the 8B batch-32 shapes).  Outputs,
+ * tree and errors as fe_draft_sample, plus FE_E_INVALID for a NULL
+ * seed_offset and FE_E_ALIGN for a misaligned one. */
+fe_status fe_draft_sample_seeded(fe_drafter *h, int32_t batch, const void *features,
+                                 const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
+                                 float temperature, const uint64_t *seed_offset,
+                                 const fe_draft_out *out, void *stream);
+
 /* Backbone Expansion tree (Section 2.2) of every sequence in one launch:
  * level 1 hangs the k candidates of q_{t+1} under the root; the most probable
  * extends the backbone, the other k-1 are side branches; every later level hangs
@@ -342,6 +360,20 @@ fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk, const int
                            const float *uniforms, int32_t *accept_len, int32_t *accept_path,
                            int32_t *accepted, void *stream);
 
+/* fe_accept_sample for children drawn by fe_draft_sample_seeded: the drafting
+ * uniforms of the children come from the same counter-based stream (the
+ * (seed, offset) pair in device memory at draft_seed_offset, as given to the
+ * pass) instead of a [B, N, V] array.  Everything else as fe_accept_sample,
+ * plus FE_E_INVALID for a NULL draft_seed_offset and FE_E_ALIGN for a
+ * misaligned one. */
+fe_status fe_accept_sample_seeded(fe_drafter *h, int32_t batch, int32_t topk,
+                                  const int32_t *tokens, const int32_t *retrieve,
+                                  const int32_t *topk_draft, const float *draft_logits,
+                                  float temperature, const uint64_t *draft_seed_offset,
+                                  const float *target_probs, const float *uniforms,
+                                  int32_t *accept_len, int32_t *accept_path, int32_t *accepted,
+                                  void *stream);
+
 /* Replays fe_draft_forward through a captured HIP graph when on != 0 (the
  * default is off).  A graph is captured on the first call with a given set of
  * arguments and replayed while they stay the same. */
@@ -402,6 +434,14 @@ typedef enum {
  * unspecified until the next fe_draft_forward. */
 fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                         float *ms_per_launch, int32_t *launches);
+
+/* Test export (device work on `stream`): uniforms first .. first+n-1 of the
+ * counter-based stream of fe_draft_sample_seeded ((seed, offset) in device
+ * memory at seed_offset) into the device array out [n] fp32, so the generator
+ * can be checked on its own.  Errors: FE_E_INVALID (n < 0, NULL pointers with
+ * n > 0), FE_E_ALIGN, FE_E_HIP. */
+fe_status fe_test_philox_uniforms(const uint64_t *seed_offset, uint64_t first, int64_t n,
+                                  float *out, void *stream);
 
 /* Test export, host only (no device work, no handle): the work pieces of the
  * persistent bf16 attention for a batch whose prefix lengths are

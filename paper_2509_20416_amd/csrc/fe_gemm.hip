@@ -1008,8 +1008,8 @@ template <typename T> struct EpiLm {
   // selection key of tempered logit xt at column col of row m: xt, or
   // xt + Gumbel(u) = xt - log(-log(u)) for sampling without replacement
   __device__ float sel_key(float xt, int m, int col) const {
-    if (!a.uniforms) return xt;
-    const float u = a.uniforms[(size_t)m * nvcols + col];
+    if (!a.draws.on()) return xt;
+    const float u = a.draws.at((uint64_t)m * nvcols + col);
     return xt - logf(-logf(u));
   }
 
@@ -1056,7 +1056,7 @@ template <typename T> struct EpiLm {
       if (j < a.topk) {
         a.cand_val[pb * kMaxTopk + j] = is[j] != 0x7fffffff ? vs[j] : -INFINITY;
         a.cand_idx[pb * kMaxTopk + j] = is[j];
-        if (a.uniforms) a.cand_z[pb * kMaxTopk + j] = zs[j];
+        if (a.draws.on()) a.cand_z[pb * kMaxTopk + j] = zs[j];
       }
   }
 
@@ -1113,12 +1113,12 @@ template <typename T> struct EpiLm {
           zb = key[p] == best ? v[p] : zb;
           key[p] = key[p] == best ? kNoKey : key[p];
         }
-        if (a.uniforms) zb = group_max<64>(zb);
+        if (a.draws.on()) zb = group_max<64>(zb);
         if (lane == 0) {
           const bool got = best != kNoKey;
           a.cand_val[pb * kMaxTopk + r] = got ? topk_key_value(best) : -INFINITY;
           a.cand_idx[pb * kMaxTopk + r] = got ? topk_key_id(best) : 0x7fffffff;
-          if (a.uniforms) a.cand_z[pb * kMaxTopk + r] = got ? zb : -INFINITY;
+          if (a.draws.on()) a.cand_z[pb * kMaxTopk + r] = got ? zb : -INFINITY;
         }
       }
     }

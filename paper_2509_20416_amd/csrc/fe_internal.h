@@ -169,6 +169,46 @@ struct Seqs {
   __host__ __device__ int end(int b) const { return pairs ? p[2 * b + 1] : p[b + 1]; }
 };
 
+// Counter-based uniforms (Philox4x64-10, Salmon, Moraes, Dror and Shaw, SC
+// 2011): uniform e of the stream (seed, offset) is word e mod 4 of the block
+// at counter (e / 4, offset, 0, 0) under key (seed, 0), its top 23 bits j
+// giving (j + 1/2) / 2^23, exact in float and inside (0, 1).  Ten rounds; a
+// round multiplies counter words 0 and 2 by the two round multipliers and
+// rebuilds the counter from the products' halves, the other two words and the
+// key, which the Weyl constants advance between rounds.
+__device__ inline float philox_uniform(uint64_t seed, uint64_t offset, uint64_t e) {
+  constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+  uint64_t c0 = e >> 2, c1 = offset, c2 = 0, c3 = 0, k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const uint64_t hi0 = __umul64hi(M0, c0), lo0 = M0 * c0;
+    const uint64_t hi1 = __umul64hi(M1, c2), lo1 = M1 * c2;
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+  }
+  const int w = (int)(e & 3);
+  const uint64_t x = w == 0 ? c0 : w == 1 ? c1 : w == 2 ? c2 : c3;
+  return ((float)(x >> 41) + 0.5f) * 0x1p-23f;
+}
+
+// The uniforms of stochastic drafting, uniform e = (row) * V + draft id: a
+// stored array (the caller's), or the counter-based stream whose (seed,
+// offset) pair sits in device memory (so a captured pass replays with new
+// values); neither means greedy selection.
+struct Draws {
+  const float *u = nullptr;      // [rows, V] or null
+  const uint64_t *so = nullptr;  // device (seed, offset) or null
+  __host__ __device__ bool on() const { return u != nullptr || so != nullptr; }
+  __device__ float at(uint64_t e) const { return u ? u[e] : philox_uniform(so[0], so[1], e); }
+};
+
 // Prefix length of query b as the attention kernels use it: P_b from its
 // rows, or 0 with bad = true when it lies outside [0, pmax] (the caller's
 // bound on every P_b).  A bad query reads no cache row and its attention
@@ -341,8 +381,8 @@ struct LmArgs {
   float *cand_val;           // [M, nwg, kMaxTopk] selection keys
   int32_t *cand_idx;         // [M, nwg, kMaxTopk]
   float inv_temp;            // 1 / T
-  const float *uniforms;     // optional [M, V] in (0, 1): key = z/T + Gumbel(u), else z/T
-  float *cand_z;             // [M, nwg, kMaxTopk] z / T of each candidate (with uniforms)
+  Draws draws;               // uniforms u in (0, 1): key = z/T + Gumbel(u); none: z/T
+  float *cand_z;             // [M, nwg, kMaxTopk] z / T of each candidate (with draws)
 };
 // LM head tiles with per-tile max, sum of exponentials and top-k candidates.
 // Returns the number of column tiles (nwg) through *nwg_out.
@@ -406,10 +446,14 @@ constexpr int kAccSampleMaxV = 32768, kAccSampleMaxVt = 131072;
 hipError_t accept_img(const int32_t *d2t, int V, int Vt, uint32_t *img, hipStream_t s);
 hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
                          const int32_t *retrieve, const int32_t *topk_draft,
-                         const float *draft_logits, float inv_temp, const float *draft_uniforms,
+                         const float *draft_logits, float inv_temp, Draws draft_draws,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
                          const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s);
+// Uniforms first .. first+n-1 of the counter-based stream ((seed, offset) in
+// device memory) into out (test export of the generator).
+hipError_t philox_fill(const uint64_t *seed_offset, uint64_t first, long n, float *out,
+                       hipStream_t s);
 
 // The pass's draft tree, written by the top-k merge itself: rows are
 // (sequence, level) pairs, N levels per sequence; the arrays as build_tree

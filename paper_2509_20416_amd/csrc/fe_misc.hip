@@ -474,7 +474,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     int N, int k, int V, int Vt, const int32_t *__restrict__ tokens,
     const int32_t *__restrict__ retrieve, const int32_t *__restrict__ topk_draft,
     const float *__restrict__ draft_logits, float inv_temp,
-    const float *__restrict__ draft_uniforms, const int32_t *__restrict__ d2t,
+    Draws draft_draws, const int32_t *__restrict__ d2t,
     const float *__restrict__ target_probs, const float *__restrict__ uniforms,
     const uint32_t *__restrict__ img, int32_t *accept_len, int32_t *accept_path,
     int32_t *accepted) {
@@ -587,7 +587,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     float zc = 0.f, ud = 0.5f, uj = 0.f;
     if (tid < k) {
       zc = z[cd];
-      if (draft_uniforms) ud = draft_uniforms[lrow * V + cd];
+      if (draft_draws.on()) ud = draft_draws.at((uint64_t)lrow * V + cd);
       uj = u[t + tid];
     }
     float zr[kZ];
@@ -600,7 +600,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
       zc *= inv_temp;
       s_cd[tid] = cd;
       s_zc[tid] = zc;
-      s_key[tid] = draft_uniforms ? zc - logf(-logf(ud)) : -(float)tid;
+      s_key[tid] = draft_draws.on() ? zc - logf(-logf(ud)) : -(float)tid;
       s_uc[tid] = uj;
     }
     __syncthreads();
@@ -634,7 +634,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
       const int child = 1 + (lvl - 1) * k + rho;
       const int vd = s_cd[rho];
       const float q0v = expf(s_zc[rho] - mx) / S;
-      const float qi = draft_uniforms ? q0v / (1.f - R) : 1.f;
+      const float qi = draft_draws.on() ? q0v / (1.f - R) : 1.f;
       const float rx = s_rd[vd];
       const float ut = s_uc[j];
       ++t;
@@ -646,7 +646,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
         took = true;
         break;
       }
-      if (!draft_uniforms) {  // point mass on x: x leaves p
+      if (!draft_draws.on()) {  // point mass on x: x leaves p
         if (tid == 0) s_rd[vd] = 0.f;
         Z -= rx;
         __syncthreads();
@@ -747,7 +747,7 @@ hipError_t accept_img(const int32_t *d2t, int V, int Vt, uint32_t *img, hipStrea
 
 hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
                          const int32_t *retrieve, const int32_t *topk_draft,
-                         const float *draft_logits, float inv_temp, const float *draft_uniforms,
+                         const float *draft_logits, float inv_temp, Draws draft_draws,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
                          const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
                          int32_t *accepted, hipStream_t s) {
@@ -756,11 +756,11 @@ hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *toke
   const bool vec = Vt % 4 == 0 && ((uintptr_t)target_probs & 15u) == 0;
   if (vec)
     hipLaunchKernelGGL(k_accept_sample<true>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
-                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_uniforms, d2t,
+                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_draws, d2t,
                        target_probs, uniforms, img, accept_len, accept_path, accepted);
   else
     hipLaunchKernelGGL(k_accept_sample<false>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
-                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_uniforms, d2t,
+                       tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_draws, d2t,
                        target_probs, uniforms, img, accept_len, accept_path, accepted);
   return hipGetLastError();
 }
@@ -849,6 +849,21 @@ hipError_t kv_scatter(int dt, const float *knew, const float *vnew, int M, int H
     hipLaunchKernelGGL((k_kv_scatter<float>), dim3(M), dim3(256), 0, s, knew, vnew, Hkv, D,
                        positions, dst_rows, cache_rows, pos_limit, rope, rotated, (float *)kc,
                        (float *)vc);
+  return hipGetLastError();
+}
+
+__global__ void k_philox_fill(const uint64_t *__restrict__ so, uint64_t first, long n,
+                              float *__restrict__ out) {
+  const Draws dr{nullptr, so};
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    out[i] = dr.at(first + (uint64_t)i);
+}
+
+hipError_t philox_fill(const uint64_t *seed_offset, uint64_t first, long n, float *out,
+                       hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const long blocks = (n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096;
+  hipLaunchKernelGGL(k_philox_fill, dim3((unsigned)blocks), dim3(256), 0, s, seed_offset, first, n, out);
   return hipGetLastError();
 }
 

@@ -232,7 +232,7 @@ struct fe_drafter {
   bool have_last = false;
   int last_batch = 0, last_topk = 0;
   float last_inv_temp = 1.f;
-  const float *last_uniforms = nullptr;
+  Draws last_draws;
   const void *last_features = nullptr;
   const int32_t *last_tokens = nullptr;
   std::vector<const void *> last_k, last_v;
@@ -376,7 +376,7 @@ fe_status ensure_lanes(fe_drafter *h) {
 
 // The whole pass: FCs of Eq. 1, N cascade layers (Eq. 2), LM head + top-k.
 fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int32_t *next_tokens,
-                          const fe_kv_view *kv, int topk, float inv_temp, const float *uniforms,
+                          const fe_kv_view *kv, int topk, float inv_temp, Draws draws,
                           const fe_draft_out *out, hipStream_t s, int only_stage = -1) {
   const fe_config &c = h->cfg;
   const Layout &L = h->L;
@@ -519,7 +519,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
   if (!fuse_f) FE_OTHER(rmsnorm_rows(dt, X, B * N, N, 1, xrow, d, h->w.final_norm, an, d, c.rms_eps, s));
   LmArgs la{h->w.lm_head, c.draft_vocab, topk, out->logits, (float *)(ws + L.pmax),
             (float *)(ws + L.psum), (float *)(ws + L.cval), (int32_t *)(ws + L.cidx), inv_temp,
-            uniforms, (float *)(ws + L.cz)};
+            draws, (float *)(ws + L.cz)};
   int nwg = 0;
   FE_STAGE_RUN(FE_STAGE_LMHEAD, gemm_lmhead(dt, fuse_f ? (const void *)AF : an, d, kDenseRows, B * N,
                                         d, la, fuse_f && !rows_norm ? &naf : nullptr, &nwg, s));
@@ -532,7 +532,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
                   t->mask, t->retrieve};
   }
   FE_OTHER(topk_merge(la.part_max, la.part_sum, la.cand_val, la.cand_idx,
-                      uniforms ? la.cand_z : nullptr, B * N, nwg, topk, c.draft_vocab, h->w.d2t,
+                      draws.on() ? la.cand_z : nullptr, B * N, nwg, topk, c.draft_vocab, h->w.d2t,
                       out->topk_ids, out->topk_draft, out->topk_probs, s,
                       out->tree ? &tr : nullptr));
   if (out->hidden)
@@ -543,9 +543,9 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
 
 // Can the persistent batch-1 pass run this call?  (Otherwise the pass runs as
 // one launch per stage.)  Sets h->seg_var / h->seg_nwg on first use.
-bool seg_supported(fe_drafter *h, int B, float inv_temp, const float *uniforms, int topk) {
+bool seg_supported(fe_drafter *h, int B, float inv_temp, Draws draws, int topk) {
   const fe_config &c = h->cfg;
-  if (!kSegEnabled || h->pass_mode != 0 || B != 1 || uniforms || inv_temp != 1.f || c.dtype != FE_BF16) return false;
+  if (!kSegEnabled || h->pass_mode != 0 || B != 1 || draws.on() || inv_temp != 1.f || c.dtype != FE_BF16) return false;
   const long d = c.hidden, N = c.n_layers, I = c.intermediate, qd = (long)c.n_q_heads * c.head_dim;
   const long kvd = (long)c.n_kv_heads * c.head_dim, F = c.n_feat_levels, V = c.draft_vocab;
   if (N > kSegMaxRows || topk > kMaxTopk) return false;
@@ -806,17 +806,44 @@ extern "C" fe_status fe_draft_forward(fe_drafter *h, int32_t batch, const void *
   return fe_draft_sample(h, batch, features, next_tokens, kv, topk, 1.0f, nullptr, out, stream);
 }
 
+namespace {
+fe_status draft_sample_impl(fe_drafter *h, int32_t batch, const void *features,
+                            const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
+                            float temperature, Draws draws, const fe_draft_out *out, void *stream);
+}  // namespace
+
 extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *features,
                                      const int32_t *next_tokens, const fe_kv_view *kv,
                                      int32_t topk, float temperature, const float *uniforms,
                                      const fe_draft_out *out, void *stream) {
+  if (uniforms && ((uintptr_t)uniforms & 3u)) return fail(FE_E_ALIGN, "uniforms must be 4-byte aligned");
+  Draws dr;
+  dr.u = uniforms;
+  return draft_sample_impl(h, batch, features, next_tokens, kv, topk, temperature, dr, out, stream);
+}
+
+extern "C" fe_status fe_draft_sample_seeded(fe_drafter *h, int32_t batch, const void *features,
+                                            const int32_t *next_tokens, const fe_kv_view *kv,
+                                            int32_t topk, float temperature,
+                                            const uint64_t *seed_offset, const fe_draft_out *out,
+                                            void *stream) {
+  if (!seed_offset) return fail(FE_E_INVALID, "seed_offset is NULL");
+  if ((uintptr_t)seed_offset & 7u) return fail(FE_E_ALIGN, "seed_offset must be 8-byte aligned");
+  Draws dr;
+  dr.so = seed_offset;
+  return draft_sample_impl(h, batch, features, next_tokens, kv, topk, temperature, dr, out, stream);
+}
+
+namespace {
+fe_status draft_sample_impl(fe_drafter *h, int32_t batch, const void *features,
+                            const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
+                            float temperature, Draws draws, const fe_draft_out *out, void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (!(temperature > 0.f) || !(temperature < INFINITY))
     return fail(FE_E_INVALID, "temperature must be positive and finite");
   const float inv_temp = 1.0f / temperature;
   if (!(inv_temp < INFINITY)) return fail(FE_E_INVALID, "temperature %g is too small", temperature);
-  if (uniforms && ((uintptr_t)uniforms & 3u)) return fail(FE_E_ALIGN, "uniforms must be 4-byte aligned");
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
   if (topk < 1 || topk > c.max_topk || topk > c.draft_vocab)
     return fail(FE_E_INVALID, "topk %d outside [1, %d]", topk, c.max_topk);
@@ -854,7 +881,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
   h->last_batch = batch;
   h->last_topk = topk;
   h->last_inv_temp = inv_temp;
-  h->last_uniforms = uniforms;
+  h->last_draws = draws;
   h->last_features = features;
   h->last_tokens = next_tokens;
   h->last_k.assign(kv->k, kv->k + c.n_layers);
@@ -868,7 +895,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
     h->last_out.tree = &h->last_tree;
   }
 
-  const bool seg = seg_supported(h, batch, inv_temp, uniforms, topk);
+  const bool seg = seg_supported(h, batch, inv_temp, draws, topk);
   h->last_seg = seg;
   if (seg && !h->seg_ready) {  // tagged words start at tag 0, below every pass's tag
     FE_TRY(seg_zero((uint64_t *)(h->ws + h->L.tagged), h->L.t_words, s));
@@ -876,7 +903,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
   }
   auto enqueue = [&](hipStream_t st) {
     return seg ? enqueue_forward_seg(h, features, next_tokens, kv, topk, out, st)
-               : enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, uniforms,
+               : enqueue_forward(h, batch, features, next_tokens, kv, topk, inv_temp, draws,
                                  out, st);
   };
   if (!h->graph_mode) return enqueue(s);
@@ -893,7 +920,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
                                 (uintptr_t)(out->tree ? out->tree->retrieve : nullptr),
                                 (uintptr_t)out->logits, (uintptr_t)out->hidden,
                                 (uintptr_t)h->attn_split, (uintptr_t)__builtin_bit_cast(uint32_t, inv_temp),
-                                (uintptr_t)uniforms, (uintptr_t)seg};
+                                (uintptr_t)draws.u, (uintptr_t)draws.so, (uintptr_t)seg};
   for (int l = 0; l < c.n_layers; ++l) {
     key.push_back((uintptr_t)kv->k[l]);
     key.push_back((uintptr_t)kv->v[l]);
@@ -916,6 +943,7 @@ extern "C" fe_status fe_draft_sample(fe_drafter *h, int32_t batch, const void *f
   FE_TRY(hipGraphLaunch(h->exec, s));
   return FE_OK;
 }
+}  // namespace
 
 extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                                    float *ms_per_launch, int32_t *launches) {
@@ -927,7 +955,7 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
   const int per_pass = (stage == FE_STAGE_FUSE || stage == FE_STAGE_INPUT || stage == FE_STAGE_LMHEAD ||
                         stage == FE_STAGE_PASS) ? 1 : N;
   const bool seg = stage == FE_STAGE_PASS &&
-                   seg_supported(h, h->last_batch, h->last_inv_temp, h->last_uniforms, h->last_topk);
+                   seg_supported(h, h->last_batch, h->last_inv_temp, h->last_draws, h->last_topk);
   hipStream_t s = (hipStream_t)stream;
   if (!h->ev_a) FE_TRY(hipEventCreate(&h->ev_a));
   if (!h->ev_b) FE_TRY(hipEventCreate(&h->ev_b));
@@ -937,7 +965,7 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
         seg ? enqueue_forward_seg(h, h->last_features, h->last_tokens, &h->last_kv, h->last_topk,
                                   &h->last_out, s)
             : enqueue_forward(h, h->last_batch, h->last_features, h->last_tokens, &h->last_kv,
-                              h->last_topk, h->last_inv_temp, h->last_uniforms, &h->last_out, s,
+                              h->last_topk, h->last_inv_temp, h->last_draws, &h->last_out, s,
                               stage == FE_STAGE_PASS ? -1 : stage);
     if (st != FE_OK) return st;
   }
@@ -1268,13 +1296,13 @@ extern "C" fe_status fe_kv_update_noalloc(fe_drafter *h, int32_t n_rows, const v
                         g_scratch_ptr[dev], (size_t)FE_KV_UPDATE_SCRATCH_BYTES, stream);
 }
 
-extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk,
-                                      const int32_t *tokens, const int32_t *retrieve,
-                                      const int32_t *topk_draft, const float *draft_logits,
-                                      float temperature, const float *draft_uniforms,
-                                      const float *target_probs, const float *uniforms,
-                                      int32_t *accept_len, int32_t *accept_path,
-                                      int32_t *accepted, void *stream) {
+namespace {
+fe_status accept_sample_impl(fe_drafter *h, int32_t batch, int32_t topk, const int32_t *tokens,
+                             const int32_t *retrieve, const int32_t *topk_draft,
+                             const float *draft_logits, float temperature, Draws draft_draws,
+                             const float *target_probs, const float *uniforms,
+                             int32_t *accept_len, int32_t *accept_path, int32_t *accepted,
+                             void *stream) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
@@ -1288,7 +1316,7 @@ extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk
   if (!tokens || !retrieve || !topk_draft || !draft_logits || !target_probs || !uniforms ||
       !accept_len || !accept_path || !accepted)
     return fail(FE_E_INVALID, "every acceptance input and output except draft_uniforms is required");
-  const void *ptrs[] = {tokens, retrieve, topk_draft, draft_logits, draft_uniforms, target_probs,
+  const void *ptrs[] = {tokens, retrieve, topk_draft, draft_logits, draft_draws.u, target_probs,
                         uniforms, accept_len, accept_path, accepted};
   for (const void *q : ptrs)
     if ((uintptr_t)q & 3u) return fail(FE_E_ALIGN, "acceptance arrays must be 4-byte aligned");
@@ -1298,9 +1326,51 @@ extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk
     h->img_ready = true;
   }
   FE_TRY(accept_sample(batch, c.n_layers, topk, c.draft_vocab, c.target_vocab, tokens, retrieve,
-                       topk_draft, draft_logits, 1.0f / temperature, draft_uniforms, h->w.d2t,
+                       topk_draft, draft_logits, 1.0f / temperature, draft_draws, h->w.d2t,
                        target_probs, uniforms, img, accept_len, accept_path, accepted,
                        (hipStream_t)stream));
+  return FE_OK;
+}
+}  // namespace
+
+extern "C" fe_status fe_accept_sample(fe_drafter *h, int32_t batch, int32_t topk,
+                                      const int32_t *tokens, const int32_t *retrieve,
+                                      const int32_t *topk_draft, const float *draft_logits,
+                                      float temperature, const float *draft_uniforms,
+                                      const float *target_probs, const float *uniforms,
+                                      int32_t *accept_len, int32_t *accept_path,
+                                      int32_t *accepted, void *stream) {
+  Draws dr;
+  dr.u = draft_uniforms;
+  return accept_sample_impl(h, batch, topk, tokens, retrieve, topk_draft, draft_logits,
+                            temperature, dr, target_probs, uniforms, accept_len, accept_path,
+                            accepted, stream);
+}
+
+extern "C" fe_status fe_accept_sample_seeded(fe_drafter *h, int32_t batch, int32_t topk,
+                                             const int32_t *tokens, const int32_t *retrieve,
+                                             const int32_t *topk_draft, const float *draft_logits,
+                                             float temperature, const uint64_t *draft_seed_offset,
+                                             const float *target_probs, const float *uniforms,
+                                             int32_t *accept_len, int32_t *accept_path,
+                                             int32_t *accepted, void *stream) {
+  if (!draft_seed_offset) return fail(FE_E_INVALID, "draft_seed_offset is NULL");
+  if ((uintptr_t)draft_seed_offset & 7u) return fail(FE_E_ALIGN, "draft_seed_offset must be 8-byte aligned");
+  Draws dr;
+  dr.so = draft_seed_offset;
+  return accept_sample_impl(h, batch, topk, tokens, retrieve, topk_draft, draft_logits,
+                            temperature, dr, target_probs, uniforms, accept_len, accept_path,
+                            accepted, stream);
+}
+
+extern "C" fe_status fe_test_philox_uniforms(const uint64_t *seed_offset, uint64_t first,
+                                             int64_t n, float *out, void *stream) {
+  if (n < 0) return fail(FE_E_INVALID, "n is negative");
+  if (n == 0) return FE_OK;
+  if (!seed_offset || !out) return fail(FE_E_INVALID, "seed_offset and out are required");
+  if ((uintptr_t)seed_offset & 7u) return fail(FE_E_ALIGN, "seed_offset must be 8-byte aligned");
+  if ((uintptr_t)out & 3u) return fail(FE_E_ALIGN, "out must be 4-byte aligned");
+  FE_TRY(philox_fill(seed_offset, first, (long)n, out, (hipStream_t)stream));
   return FE_OK;
 }
 

@@ -140,11 +140,13 @@ class Drafter:
     def forward(self, di: DeviceInputs, topk: Optional[int] = None, logits=False, hidden=False,
                 out: Optional[Dict[str, object]] = None,
                 tree: Optional[Dict[str, object]] = None, temperature: Optional[float] = None,
-                uniforms=None) -> Dict[str, object]:
+                uniforms=None, seed_offset=None) -> Dict[str, object]:
         """One drafting pass; with `tree` (from alloc_tree) the Backbone Expansion
         tree of the pass is built in the same launch sequence.  With a
         temperature and/or `uniforms` ([B, N, V] float32 on the device) the pass
-        runs through fe_draft_sample (candidates sampled without replacement)."""
+        runs through fe_draft_sample (candidates sampled without replacement);
+        with `seed_offset` (a device int64/uint64 tensor [2]: seed, offset) through
+        fe_draft_sample_seeded, the uniforms drawn in the pass."""
         k = int(topk or self.cfg.topk)
         if out is None:
             out = self.alloc_outputs(di.batch, k, logits, hidden)
@@ -156,7 +158,12 @@ class Drafter:
                                               ("tokens", "parents", "depth", "positions", "mask",
                                                "retrieve")])
             self._out.tree = fe.C.pointer(self._fwd_tree)
-        if temperature is None and uniforms is None:
+        if seed_offset is not None:
+            fe.fe_draft_sample_seeded(self.handle, di.batch, di.features.data_ptr(),
+                                      di.next_tokens.data_ptr(), self.kv_view(di), k,
+                                      float(1.0 if temperature is None else temperature),
+                                      seed_offset.data_ptr(), self._out, self.stream())
+        elif temperature is None and uniforms is None:
             fe.fe_draft_forward(self.handle, di.batch, di.features.data_ptr(),
                                 di.next_tokens.data_ptr(), self.kv_view(di), k, self._out,
                                 self.stream())
@@ -214,9 +221,12 @@ class Drafter:
     def accept_sample(self, tree: Dict[str, object], topk_draft, draft_logits, target_probs,
                       uniforms, temperature: float = 1.0, draft_uniforms=None,
                       topk: Optional[int] = None, batch: Optional[int] = None,
-                      out: Optional[Dict[str, object]] = None) -> Dict[str, object]:
-        """Speculative-sampling acceptance of one cycle (fe_accept_sample); all
-        arrays on the device (see include/fe.h for shapes)."""
+                      out: Optional[Dict[str, object]] = None,
+                      draft_seed_offset=None) -> Dict[str, object]:
+        """Speculative-sampling acceptance of one cycle (fe_accept_sample, or
+        fe_accept_sample_seeded with `draft_seed_offset`, the device (seed,
+        offset) pair the pass drew with); all arrays on the device (see
+        include/fe.h for shapes)."""
         import torch
         k = int(topk or self.cfg.topk)
         B = int(batch if batch is not None else tree["tokens"].shape[0])
@@ -226,6 +236,15 @@ class Drafter:
             out = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
                    "accept_path": torch.empty(B, dtype=torch.int32, device=dev),
                    "accepted": torch.empty(B, N + 1, dtype=torch.int32, device=dev)}
+        if draft_seed_offset is not None:
+            fe.fe_accept_sample_seeded(self.handle, B, k, tree["tokens"].data_ptr(),
+                                       tree["retrieve"].data_ptr(), topk_draft.data_ptr(),
+                                       draft_logits.data_ptr(), float(temperature),
+                                       draft_seed_offset.data_ptr(), target_probs.data_ptr(),
+                                       uniforms.data_ptr(), out["accept_len"].data_ptr(),
+                                       out["accept_path"].data_ptr(), out["accepted"].data_ptr(),
+                                       self.stream())
+            return out
         fe.fe_accept_sample(self.handle, B, k, tree["tokens"].data_ptr(),
                             tree["retrieve"].data_ptr(), topk_draft.data_ptr(),
                             draft_logits.data_ptr(), float(temperature),

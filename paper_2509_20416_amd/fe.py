@@ -20,9 +20,9 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 
 # Every function include/fe.h declares.
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
-           "fe_build_tree",
-           "fe_accept_greedy", "fe_accept_sample", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_set_pass_mode", "fe_pass_status",
-           "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split")
+           "fe_draft_sample_seeded", "fe_build_tree",
+           "fe_accept_greedy", "fe_accept_sample", "fe_accept_sample_seeded", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_set_pass_mode", "fe_pass_status",
+           "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split", "fe_test_philox_uniforms")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7, pass_=8)
 
 
@@ -96,6 +96,12 @@ def lib() -> C.CDLL:
         L.fe_draft_sample.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                       C.POINTER(fe_kv_view), C.c_int32, C.c_float, C.c_void_p,
                                       C.POINTER(fe_draft_out), C.c_void_p]
+        L.fe_draft_sample_seeded.restype = C.c_int
+        L.fe_draft_sample_seeded.argtypes = L.fe_draft_sample.argtypes
+        L.fe_accept_sample_seeded.restype = C.c_int
+        L.fe_test_philox_uniforms.restype = C.c_int
+        L.fe_test_philox_uniforms.argtypes = [C.c_void_p, C.c_uint64, C.c_int64, C.c_void_p,
+                                              C.c_void_p]
         L.fe_build_tree.restype = C.c_int
         L.fe_build_tree.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
@@ -104,6 +110,7 @@ def lib() -> C.CDLL:
         L.fe_accept_sample.restype = C.c_int
         L.fe_accept_sample.argtypes = [C.c_void_p, C.c_int32, C.c_int32] + [C.c_void_p] * 4 + \
             [C.c_float] + [C.c_void_p] * 7
+        L.fe_accept_sample_seeded.argtypes = L.fe_accept_sample.argtypes
         L.fe_kv_update_workspace_bytes.restype = C.c_size_t
         L.fe_kv_update_workspace_bytes.argtypes = [C.POINTER(fe_config), C.c_int32]
         L.fe_kv_update.restype = C.c_int
@@ -168,6 +175,20 @@ def fe_draft_sample(h: int, batch: int, features: int, next_tokens: int, kv: fe_
                                 C.c_void_p(next_tokens), C.byref(kv), topk,
                                 C.c_float(temperature), C.c_void_p(uniforms), C.byref(out),
                                 C.c_void_p(stream)))
+
+
+def fe_draft_sample_seeded(h: int, batch: int, features: int, next_tokens: int, kv: fe_kv_view,
+                           topk: int, temperature: float, seed_offset: int, out: fe_draft_out,
+                           stream: int) -> None:
+    check(lib().fe_draft_sample_seeded(C.c_void_p(h), batch, C.c_void_p(features),
+                                       C.c_void_p(next_tokens), C.byref(kv), topk,
+                                       C.c_float(temperature), C.c_void_p(seed_offset),
+                                       C.byref(out), C.c_void_p(stream)))
+
+
+def fe_test_philox_uniforms(seed_offset: int, first: int, n: int, out: int, stream: int) -> None:
+    check(lib().fe_test_philox_uniforms(C.c_void_p(seed_offset), C.c_uint64(int(first)),
+                                        C.c_int64(int(n)), C.c_void_p(out), C.c_void_p(stream)))
 
 
 def fe_build_tree(h: int, batch: int, topk: int, root_tokens: int, topk_ids: int,
@@ -263,3 +284,16 @@ def fe_test_attn_split(prefix_lens, ncols: int, nch_ld: int, pmax: int, waves: i
     check(lib().fe_test_attn_split(pl.ctypes.data, len(pl), ncols, nch_ld, pmax, waves,
                                    out.ctypes.data, n.value, C.byref(n)))
     return out[:n.value]
+
+
+def fe_accept_sample_seeded(h: int, batch: int, topk: int, tokens: int, retrieve: int,
+                            topk_draft: int, draft_logits: int, temperature: float,
+                            draft_seed_offset: int, target_probs: int, uniforms: int,
+                            accept_len: int, accept_path: int, accepted: int, stream: int) -> None:
+    check(lib().fe_accept_sample_seeded(C.c_void_p(h), batch, topk, C.c_void_p(tokens),
+                                        C.c_void_p(retrieve), C.c_void_p(topk_draft),
+                                        C.c_void_p(draft_logits), C.c_float(temperature),
+                                        C.c_void_p(draft_seed_offset), C.c_void_p(target_probs),
+                                        C.c_void_p(uniforms), C.c_void_p(accept_len),
+                                        C.c_void_p(accept_path), C.c_void_p(accepted),
+                                        C.c_void_p(stream)))

@@ -33,7 +33,7 @@ def log(*a):
     print("[accept-sample]", *a, flush=True)
 
 
-def _cycle(cfg, B, k, T, sampled, seed):
+def _cycle(cfg, B, k, T, sampled, seed, philox=None):
     """Host arrays of one cycle: draft logits, candidates (drawn or top-k,
     listed most probable first), the tree, target distributions that put part
     of their mass where the draft does, and the uniforms."""
@@ -43,7 +43,10 @@ def _cycle(cfg, B, k, T, sampled, seed):
     w = make_weights(cfg.with_(n_layers=1), 0)
     d2t = w.d2t
     z = (rng.standard_normal((B, N, V)) * 2.5).astype(np.float32)
-    ud = make_uniforms((B, N, V), seed=seed + 1)
+    if philox is None:
+        ud = make_uniforms((B, N, V), seed=seed + 1)
+    else:   # the counter-based stream the seeded pass draws from
+        ud = feo.philox_uniforms(philox[0], philox[1], 0, B * N * V).reshape(B, N, V)
     keys = z / T - (np.log(-np.log(ud.astype(np.float64))) if sampled else 0.0)
     cand = np.argsort(-keys, axis=-1, kind="stable")[..., :k]
     zc = np.take_along_axis(z, cand, -1)
@@ -72,12 +75,12 @@ def _cycle(cfg, B, k, T, sampled, seed):
     return dict(z=z, ud=ud if sampled else None, cand=cand, tree=tree, tp=tp, u=u, d2t=d2t, w=w)
 
 
-def _run(cfg, B, k, T, sampled, seed):
+def _run(cfg, B, k, T, sampled, seed, philox=None):
     import torch
     from oracle import feo
     from paper_2509_20416_amd import Drafter
     cfg = cfg.with_(batch=B, topk=k)
-    cy = _cycle(cfg, B, k, T, sampled, seed)
+    cy = _cycle(cfg, B, k, T, sampled, seed, philox)
     N = cfg.n_layers
     log(f"{cfg.name}: N={N} k={k} B={B} T={T} sampled={sampled} V={cfg.draft_vocab} "
         f"Vt={cfg.target_vocab}")
@@ -86,9 +89,14 @@ def _run(cfg, B, k, T, sampled, seed):
     dev = dr.device
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     tree = {n: t(a) for n, a in cy["tree"].items()}
-    got = dr.accept_sample(tree, t(cy["cand"]), t(cy["z"]), t(cy["tp"]), t(cy["u"]),
-                           temperature=T,
-                           draft_uniforms=t(cy["ud"]) if cy["ud"] is not None else None, topk=k)
+    if philox is None:
+        got = dr.accept_sample(tree, t(cy["cand"]), t(cy["z"]), t(cy["tp"]), t(cy["u"]),
+                               temperature=T,
+                               draft_uniforms=t(cy["ud"]) if cy["ud"] is not None else None, topk=k)
+    else:
+        so = torch.tensor(list(philox), dtype=torch.int64, device=dev)
+        got = dr.accept_sample(tree, t(cy["cand"]), t(cy["z"]), t(cy["tp"]), t(cy["u"]),
+                               temperature=T, draft_seed_offset=so, topk=k)
     torch.cuda.synchronize()
     got = {n: a.cpu().numpy() for n, a in got.items()}
     ref = feo.accept_sample(N, k, cy["tree"]["tokens"], cy["tree"]["retrieve"], cy["cand"], cy["z"],
@@ -134,6 +142,15 @@ CASES = [
                               for c, b, k, t, s in CASES])
 def test_accept_sample_parity(cfg, B, k, T, sampled):
     _run(cfg, B, k, T, sampled, seed=B * 100 + k)
+
+
+@pytest.mark.parametrize("B,k,T", [(32, 5, 1.0), (16, 16, 0.7)])
+def test_accept_sample_seeded_parity(B, k, T):
+    """Children drawn from the counter-based stream (fe_draft_sample_seeded):
+    the acceptance recomputes their uniforms from (seed, offset) in device
+    memory (fe_accept_sample_seeded); the oracle reads the same stream's
+    uniforms from an array."""
+    _run(SMALL_V, B, k, T, True, seed=B * 100 + k + 1, philox=(77, 3))
 
 
 def test_accept_sample_8b_vocabularies():

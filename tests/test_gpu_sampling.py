@@ -68,7 +68,9 @@ def check_sampled(gpu_draft, gpu_probs, z, u, T, ref_draft, tol):
     return decided, exact
 
 
-def _run(cfg, T, seed=1, topk=None, graph=False, prefix_lens=None):
+def _run(cfg, T, seed=1, topk=None, graph=False, prefix_lens=None, philox=None):
+    """philox = (seed, offset): the pass draws its uniforms itself
+    (fe_draft_sample_seeded); the oracle gets the same stream's uniforms."""
     import torch
     from oracle import feo
     from paper_2509_20416_amd import Drafter
@@ -76,14 +78,21 @@ def _run(cfg, T, seed=1, topk=None, graph=False, prefix_lens=None):
     w = make_weights(cfg, seed)
     inp = make_inputs(cfg, seed, prefix_lens)
     B, N, V = len(inp.prefix_lens), cfg.n_layers, cfg.draft_vocab
-    u = make_uniforms((B, N, V), seed=seed + 100)
-    log(f"{cfg.name}: T={T} k={k} B={B} graph={graph}")
+    if philox is None:
+        u = make_uniforms((B, N, V), seed=seed + 100)
+    else:
+        u = feo.philox_uniforms(philox[0], philox[1], 0, B * N * V).reshape(B, N, V)
+    log(f"{cfg.name}: T={T} k={k} B={B} graph={graph} philox={philox}")
     dr = Drafter(cfg, w, max_batch=B, max_prefix=int(inp.prefix_lens.max()),
                  max_topk=max(k, cfg.topk), graph=graph)
     di = dr.upload_inputs(inp)
-    ud = torch.from_numpy(u).cuda()
     tree = dr.alloc_tree(B, k)
-    out = dr.forward(di, k, logits=True, temperature=T, uniforms=ud, tree=tree)
+    if philox is None:
+        ud = torch.from_numpy(u).cuda()
+        out = dr.forward(di, k, logits=True, temperature=T, uniforms=ud, tree=tree)
+    else:
+        so = torch.tensor(list(philox), dtype=torch.int64, device="cuda")
+        out = dr.forward(di, k, logits=True, temperature=T, seed_offset=so, tree=tree)
     torch.cuda.synchronize()
     got = {n: t.cpu().numpy() for n, t in out.items()}
     tr = {n: t.cpu().numpy() for n, t in tree.items()}
@@ -157,4 +166,66 @@ def test_greedy_at_temperature_and_graph_rereads_uniforms():
             torch.cuda.synchronize()
             np.testing.assert_array_equal(out["topk_draft"].cpu().numpy(), eager[j],
                                           err_msg=f"replay {rep} seed {s}")
+    dr.close()
+
+
+# --- counter-based uniforms (fe_draft_sample_seeded) ------------------------------------
+
+@pytest.mark.parametrize("seed,offset,first,n", [(1, 0, 0, 1000), (0x7EEDFACE1234567, 5, 12345, 777),
+                                                 (3, 2**40, 2**41 + 3, 1001)])
+def test_philox_uniforms_match_oracle(seed, offset, first, n):
+    """The device generator equals the oracle's, bit for bit."""
+    import torch
+    from oracle import feo
+    from paper_2509_20416_amd import fe
+    so = torch.tensor([seed, offset], dtype=torch.int64, device="cuda")
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    fe.fe_test_philox_uniforms(so.data_ptr(), first, n, out.data_ptr(),
+                               torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy(), feo.philox_uniforms(seed, offset, first, n))
+
+
+SEEDED = [
+    (C.SMALL_GQA_F32, 1.0, None),
+    (C.SMALL_GQA_BF16, 1.0, None),
+    (C.SMALL_GQA_F32.with_(batch=12, name="small_gqa_f32_b12"), 0.8, 8),
+]
+
+
+@pytest.mark.parametrize("cfg,T,k", SEEDED, ids=[f"{c.name}-T{t}-k{k}" for c, t, k in SEEDED])
+def test_seeded_sampling_parity(cfg, T, k):
+    dec, ex, rows = _run(cfg, T, topk=k, philox=(2024, 7))
+    if cfg.dtype == "f32":
+        assert dec >= rows // 2, (dec, rows)
+
+
+def test_seeded_graph_replays_follow_the_offset():
+    """A captured seeded pass reads (seed, offset) from device memory on every
+    replay: each replay equals the eager pass at that offset, bit for bit, and
+    new offsets draw new candidates."""
+    import torch
+    from paper_2509_20416_amd import Drafter
+    cfg = C.SMALL_GQA_BF16
+    w, inp = make_weights(cfg, 3), make_inputs(cfg, 3)
+    B = len(inp.prefix_lens)
+    dr = Drafter(cfg, w, max_batch=B, max_prefix=int(inp.prefix_lens.max()))
+    di = dr.upload_inputs(inp)
+    so = torch.tensor([99, 0], dtype=torch.int64, device="cuda")
+    eager = []
+    for off in range(3):
+        so[1] = off
+        eager.append(dr.forward(di, temperature=1.0, seed_offset=so)["topk_draft"].cpu().numpy())
+    assert not np.array_equal(eager[0], eager[1])
+    dr.set_graph_mode(True)
+    out = dr.alloc_outputs(B, cfg.topk)
+    for rep in range(2):
+        for off in range(3):
+            so[1] = off
+            out["topk_draft"].zero_()
+            dr.forward(di, out=out, temperature=1.0, seed_offset=so)
+            torch.cuda.synchronize()
+            _ = torch.ones(1000, device="cuda").sum().item()
+            np.testing.assert_array_equal(out["topk_draft"].cpu().numpy(), eager[off],
+                                          err_msg=f"replay {rep} offset {off}")
     dr.close()
