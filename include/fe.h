@@ -435,6 +435,33 @@ typedef enum {
 fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                         float *ms_per_launch, int32_t *launches);
 
+/* Test export (device work on `stream`, synchronised; allocates and frees its
+ * own scratch, so not for production paths): one layer's attention as the
+ * pass runs it (Section 2.1: the GQA attention of a decoder layer over its
+ * prefix cache plus the cascade keys).  Query b, heads 0..Hq-1: keys/values
+ * are the prefix rows cu_prefix[b] .. cu_prefix[b+1]-1 of k_cache / v_cache
+ * ([rows, Hkv, D], storage dtype, keys rotated at their positions) followed by
+ * the nctx rows knew/vnew[b, t] ([B, nctx, Hkv, D] fp32) at positions P_b + t
+ * (cascade != 0) or P_b (cascade == 0, nctx == 1); the query q[b] ([B, Hq, D]
+ * fp32) sits at the last of those positions.  bf16: q and knew unrotated (the
+ * kernel rotates them); fp32: already rotated.  Head h reads KV head
+ * h / (Hq/Hkv).  out [B, Hq, D] in the storage dtype.  chunks_per_workgroup
+ * as fe_set_attention_split (0 = automatic).  Errors: FE_E_INVALID,
+ * FE_E_UNSUPPORTED (head_dim not 64 or 128), FE_E_HIP. */
+fe_status fe_test_attention(int32_t dtype, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                            int32_t head_dim, const void *k_cache, const void *v_cache,
+                            const int32_t *cu_prefix, int32_t max_prefix, const float *q,
+                            const float *knew, const float *vnew, int32_t nctx, int32_t cascade,
+                            double rope_theta, int32_t chunks_per_workgroup, void *out,
+                            void *stream);
+
+/* Test export (device work on `stream`): the standalone RMSNorm launch,
+ * out[r] = gamma * x[r] / sqrt(mean(x[r]^2) + eps) for rows x [rows, d] fp32,
+ * gamma [d] and out [rows, d] in the storage dtype.  Errors: FE_E_INVALID,
+ * FE_E_HIP. */
+fe_status fe_test_rmsnorm(int32_t dtype, const float *x, int32_t rows, int32_t d,
+                          const void *gamma, float eps, void *out, void *stream);
+
 /* Test export (device work on `stream`): uniforms first .. first+n-1 of the
  * counter-based stream of fe_draft_sample_seeded ((seed, offset) in device
  * memory at seed_offset) into the device array out [n] fp32, so the generator

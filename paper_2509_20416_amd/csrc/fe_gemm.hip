@@ -1031,8 +1031,26 @@ template <typename T> struct EpiLm {
       zs[j] = -INFINITY;
       is[j] = 0x7fffffff;
     }
+    // counter-based draws: one generator block per four consecutive columns
+    const bool gen = a.draws.so != nullptr;
+    const uint64_t seed = gen ? a.draws.so[0] : 0, offset = gen ? a.draws.so[1] : 0;
+    uint64_t have = ~0ull;
+    float ub[4] = {0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < nvalid; ++c) {
-      const float x = row[c], xt = x * a.inv_temp, key = sel_key(xt, m, c0 + c);
+      const float x = row[c], xt = x * a.inv_temp;
+      float key = xt;
+      if (gen) {
+        const uint64_t e = (uint64_t)m * nvcols + c0 + c;
+        if ((e >> 2) != have) {
+          have = e >> 2;
+          philox_block(seed, offset, have, ub);
+        }
+        const int w = (int)(e & 3);
+        const float u = w == 0 ? ub[0] : w == 1 ? ub[1] : w == 2 ? ub[2] : ub[3];
+        key = xt - logf(-logf(u));
+      } else {
+        key = sel_key(xt, m, c0 + c);
+      }
       se += expf(xt - mx);
       if (a.logits) a.logits[(size_t)m * nvcols + c0 + c] = x;
 #pragma unroll
@@ -1098,9 +1116,27 @@ template <typename T> struct EpiLm {
         a.part_sum[pb] = se;
       }
       uint64_t key[PER];
+      const uint64_t e0 = (uint64_t)m * nvcols + c0;  // uniform of column c0
+      if (a.draws.so != nullptr && (e0 & 3) == 0) {
+        // counter-based draws, block-aligned tile row: lane q draws block
+        // e0/4 + q (columns 4q .. 4q+3), and lane l takes column l + 64p's
+        // uniform from lane l/4 + 16p, word l & 3
+        float ub[4];
+        philox_block(a.draws.so[0], a.draws.so[1], (e0 >> 2) + lane, ub);
+        const int w = lane & 3;
 #pragma unroll
-      for (int p = 0; p < PER; ++p)
-        key[p] = id[p] != 0x7fffffff ? topk_key(sel_key(v[p], m, id[p]), id[p]) : kNoKey;
+        for (int p = 0; p < PER; ++p) {
+          const int src = (lane >> 2) + 16 * p;
+          const float u0 = __shfl(ub[0], src, 64), u1 = __shfl(ub[1], src, 64);
+          const float u2 = __shfl(ub[2], src, 64), u3 = __shfl(ub[3], src, 64);
+          const float u = w == 0 ? u0 : w == 1 ? u1 : w == 2 ? u2 : u3;
+          key[p] = id[p] != 0x7fffffff ? topk_key(v[p] - logf(-logf(u)), id[p]) : kNoKey;
+        }
+      } else {
+#pragma unroll
+        for (int p = 0; p < PER; ++p)
+          key[p] = id[p] != 0x7fffffff ? topk_key(sel_key(v[p], m, id[p]), id[p]) : kNoKey;
+      }
       for (int r = 0; r < a.topk; ++r) {
         // lane-local best, then wave max of the ordering keys (lower id wins ties)
         uint64_t best = kNoKey;

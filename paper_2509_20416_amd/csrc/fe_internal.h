@@ -176,10 +176,11 @@ struct Seqs {
 // round multiplies counter words 0 and 2 by the two round multipliers and
 // rebuilds the counter from the products' halves, the other two words and the
 // key, which the Weyl constants advance between rounds.
-__device__ inline float philox_uniform(uint64_t seed, uint64_t offset, uint64_t e) {
+// The four uniforms of block `blk` (uniforms 4 blk .. 4 blk + 3) of the stream.
+__device__ inline void philox_block(uint64_t seed, uint64_t offset, uint64_t blk, float u[4]) {
   constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
   constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-  uint64_t c0 = e >> 2, c1 = offset, c2 = 0, c3 = 0, k0 = seed, k1 = 0;
+  uint64_t c0 = blk, c1 = offset, c2 = 0, c3 = 0, k0 = seed, k1 = 0;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r > 0) {
@@ -193,9 +194,16 @@ __device__ inline float philox_uniform(uint64_t seed, uint64_t offset, uint64_t 
     c2 = hi0 ^ c3 ^ k1;
     c3 = lo0;
   }
+  u[0] = ((float)(c0 >> 41) + 0.5f) * 0x1p-23f;
+  u[1] = ((float)(c1 >> 41) + 0.5f) * 0x1p-23f;
+  u[2] = ((float)(c2 >> 41) + 0.5f) * 0x1p-23f;
+  u[3] = ((float)(c3 >> 41) + 0.5f) * 0x1p-23f;
+}
+__device__ inline float philox_uniform(uint64_t seed, uint64_t offset, uint64_t e) {
+  float u[4];
+  philox_block(seed, offset, e >> 2, u);
   const int w = (int)(e & 3);
-  const uint64_t x = w == 0 ? c0 : w == 1 ? c1 : w == 2 ? c2 : c3;
-  return ((float)(x >> 41) + 0.5f) * 0x1p-23f;
+  return w == 0 ? u[0] : w == 1 ? u[1] : w == 2 ? u[2] : u[3];
 }
 
 // The uniforms of stochastic drafting, uniform e = (row) * V + draft id: a

@@ -981,6 +981,56 @@ extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats
 // Test export (host only, no device work): the pieces the persistent bf16
 // attention's waves take for the given prefix lengths, from the same split
 // arithmetic the kernel runs (AttnSplit, attn_prefix, attn_seg_chunks).
+// Test export: one layer's attention exactly as the pass launches it, on
+// caller buffers, with its own (allocated and freed) rotary table and partials.
+extern "C" fe_status fe_test_attention(int32_t dtype, int32_t batch, int32_t n_q_heads,
+                                       int32_t n_kv_heads, int32_t head_dim, const void *k_cache,
+                                       const void *v_cache, const int32_t *cu_prefix,
+                                       int32_t max_prefix, const float *q, const float *knew,
+                                       const float *vnew, int32_t nctx, int32_t cascade,
+                                       double rope_theta, int32_t chunks_per_workgroup, void *out,
+                                       void *stream) {
+  if (dtype != FE_BF16 && dtype != FE_F32) return fail(FE_E_INVALID, "dtype %d", dtype);
+  if (batch < 0 || n_kv_heads < 1 || n_q_heads % n_kv_heads || max_prefix < 0 ||
+      chunks_per_workgroup < 0 || nctx < 1 || nctx > kMaxLayers)
+    return fail(FE_E_INVALID, "bad attention shape");
+  if (head_dim != 64 && head_dim != 128) return fail(FE_E_UNSUPPORTED, "head_dim %d", head_dim);
+  if (batch == 0) return FE_OK;
+  if (!cu_prefix || !q || !knew || !vnew || !out || (max_prefix > 0 && (!k_cache || !v_cache)))
+    return fail(FE_E_INVALID, "attention inputs are required");
+  const int dt = dtype == FE_BF16 ? 1 : 0, D = head_dim, Hq = n_q_heads, Hkv = n_kv_heads;
+  const int nch = max_prefix > 0 ? (max_prefix + kAttnChunk - 1) / kAttnChunk : 0;
+  const int nch_ld = (max_prefix > 0 ? nch : 1) + 1;
+  const int npos = max_prefix + nctx;
+  const int cpw = chunks_per_workgroup > 0 ? chunks_per_workgroup : attention_cpw(batch, Hkv, 1, nch);
+  hipStream_t s = (hipStream_t)stream;
+  float *rope = nullptr, *part = nullptr;
+  const size_t part_floats = (size_t)batch * Hq * ((size_t)nch_ld * (D + 2) + 1);
+  FE_TRY(hipMalloc(&rope, (size_t)npos * (D / 2) * 2 * sizeof(float)));
+  hipError_t e = hipMalloc(&part, part_floats * sizeof(float));
+  if (e == hipSuccess) e = rope_table(rope, npos, D, rope_theta, s);
+  if (e == hipSuccess)
+    e = attention(dt, k_cache, v_cache, Seqs{cu_prefix, 0}, q, knew, vnew, nctx, part, nch, nch_ld,
+                  cpw, out, batch, Hq, Hkv, D, rope, cascade ? 1 : 0, max_prefix, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipFree(part);
+  (void)hipFree(rope);
+  if (e != hipSuccess) return fail(FE_E_HIP, "fe_test_attention: %s", hipGetErrorString(e));
+  return FE_OK;
+}
+
+// Test export: the standalone RMSNorm launch (fp32 rows in, storage dtype out).
+extern "C" fe_status fe_test_rmsnorm(int32_t dtype, const float *x, int32_t rows, int32_t d,
+                                     const void *gamma, float eps, void *out, void *stream) {
+  if (dtype != FE_BF16 && dtype != FE_F32) return fail(FE_E_INVALID, "dtype %d", dtype);
+  if (rows < 0 || d < 4 || d % 4 || d > 8192) return fail(FE_E_INVALID, "bad shape");
+  if (rows == 0) return FE_OK;
+  if (!x || !gamma || !out) return fail(FE_E_INVALID, "inputs are required");
+  FE_TRY(rmsnorm_rows(dtype == FE_BF16 ? 1 : 0, x, rows, 1, 0, d, 0, gamma, out, d, eps,
+                      (hipStream_t)stream));
+  return FE_OK;
+}
+
 extern "C" fe_status fe_test_attn_split(const int32_t *prefix_lens, int32_t batch, int32_t ncols,
                                         int32_t nch_ld, int32_t pmax, int32_t waves,
                                         int32_t *pieces, int32_t max_pieces, int32_t *n_pieces) {

@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "FE_OK", 1: "FE_E_INVALID", 2: "FE_E_UNSUPPORTED", 3: "FE_E_A
 EXPORTS = ("fe_workspace_bytes", "fe_drafter_create", "fe_draft_forward", "fe_draft_sample",
            "fe_draft_sample_seeded", "fe_build_tree",
            "fe_accept_greedy", "fe_accept_sample", "fe_accept_sample_seeded", "fe_kv_update_workspace_bytes", "fe_kv_update", "fe_kv_update_noalloc", "fe_set_graph_mode", "fe_set_attention_split", "fe_time_stage", "fe_set_pass_mode", "fe_pass_status",
-           "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split", "fe_test_philox_uniforms")
+           "fe_drafter_destroy", "fe_last_error", "fe_test_attn_split", "fe_test_philox_uniforms",
+           "fe_test_attention", "fe_test_rmsnorm")
 FE_STAGE = dict(fuse=0, input=1, qkv=2, attn=3, oproj=4, gateup=5, down=6, lmhead=7, pass_=8)
 
 
@@ -102,6 +103,12 @@ def lib() -> C.CDLL:
         L.fe_test_philox_uniforms.restype = C.c_int
         L.fe_test_philox_uniforms.argtypes = [C.c_void_p, C.c_uint64, C.c_int64, C.c_void_p,
                                               C.c_void_p]
+        L.fe_test_attention.restype = C.c_int
+        L.fe_test_attention.argtypes = [C.c_int32] * 5 + [C.c_void_p] * 3 + [C.c_int32] + \
+            [C.c_void_p] * 3 + [C.c_int32, C.c_int32, C.c_double, C.c_int32, C.c_void_p, C.c_void_p]
+        L.fe_test_rmsnorm.restype = C.c_int
+        L.fe_test_rmsnorm.argtypes = [C.c_int32, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                      C.c_float, C.c_void_p, C.c_void_p]
         L.fe_build_tree.restype = C.c_int
         L.fe_build_tree.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.POINTER(fe_tree_out), C.c_void_p]
@@ -297,3 +304,20 @@ def fe_accept_sample_seeded(h: int, batch: int, topk: int, tokens: int, retrieve
                                         C.c_void_p(uniforms), C.c_void_p(accept_len),
                                         C.c_void_p(accept_path), C.c_void_p(accepted),
                                         C.c_void_p(stream)))
+
+
+def fe_test_attention(dtype: int, batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                      k_cache: int, v_cache: int, cu_prefix: int, max_prefix: int, q: int,
+                      knew: int, vnew: int, nctx: int, cascade: int, rope_theta: float,
+                      chunks_per_workgroup: int, out: int, stream: int) -> None:
+    check(lib().fe_test_attention(dtype, batch, n_q_heads, n_kv_heads, head_dim,
+                                  C.c_void_p(k_cache), C.c_void_p(v_cache), C.c_void_p(cu_prefix),
+                                  max_prefix, C.c_void_p(q), C.c_void_p(knew), C.c_void_p(vnew),
+                                  nctx, cascade, float(rope_theta), chunks_per_workgroup,
+                                  C.c_void_p(out), C.c_void_p(stream)))
+
+
+def fe_test_rmsnorm(dtype: int, x: int, rows: int, d: int, gamma: int, eps: float, out: int,
+                    stream: int) -> None:
+    check(lib().fe_test_rmsnorm(dtype, C.c_void_p(x), rows, d, C.c_void_p(gamma), C.c_float(eps),
+                                C.c_void_p(out), C.c_void_p(stream)))
