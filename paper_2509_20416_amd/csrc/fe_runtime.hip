@@ -11,6 +11,8 @@
 #include <new>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "../../include/fe.h"
 #include "fe_internal.h"
 
@@ -37,6 +39,16 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
   } while (0)
 
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// A roctx range over a host scope: the entry points, the pass and its layers
+// show up by name on a rocprofv3 --marker-trace timeline (host time: when the
+// work was enqueued, or captured).
+struct Range {
+  explicit Range(const char *name) { roctxRangePushA(name); }
+  ~Range() { roctxRangePop(); }
+  Range(const Range &) = delete;
+  Range &operator=(const Range &) = delete;
+};
 
 struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
@@ -452,6 +464,7 @@ fe_status enqueue_forward(fe_drafter *h, int B, const void *features, const int3
     }
   }
   for (int i = 1; i <= N; ++i) {
+    const Range range("fe.layer");
     const fe_layer_weights &lw = h->layers[i - 1];
     const int src = parallel ? 0 : i - 1;  // the layer's input state
     hipStream_t s = lane_stream[i - 1];
@@ -838,6 +851,7 @@ namespace {
 fe_status draft_sample_impl(fe_drafter *h, int32_t batch, const void *features,
                             const int32_t *next_tokens, const fe_kv_view *kv, int32_t topk,
                             float temperature, Draws draws, const fe_draft_out *out, void *stream) {
+  const Range range("fe_draft_sample");
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (!(temperature > 0.f) || !(temperature < INFINITY))
@@ -947,6 +961,7 @@ fe_status draft_sample_impl(fe_drafter *h, int32_t batch, const void *features,
 
 extern "C" fe_status fe_time_stage(fe_drafter *h, int32_t stage, int32_t repeats, void *stream,
                                    float *ms_per_launch, int32_t *launches) {
+  const Range range("fe_time_stage");
   if (!h || !ms_per_launch || !launches) return fail(FE_E_INVALID, "bad arguments");
   if (stage < FE_STAGE_FUSE || stage > FE_STAGE_PASS) return fail(FE_E_INVALID, "unknown stage %d", stage);
   if (repeats < 1) return fail(FE_E_INVALID, "repeats must be >= 1");
@@ -1076,6 +1091,7 @@ extern "C" fe_status fe_accept_greedy(fe_drafter *h, int32_t batch, int32_t topk
                                       const int32_t *tokens, const int32_t *retrieve,
                                       const int32_t *target_next, int32_t *accept_len,
                                       int32_t *accept_path, int32_t *accepted, void *stream) {
+  const Range range("fe_accept_greedy");
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
@@ -1126,6 +1142,7 @@ fe_status prefill_layers(fe_drafter *h, const UpdLayout &U, char *ws, int Mc,
   const int nch = (pmax + kAttnChunk - 1) / kAttnChunk;
   FE_TRY(prefill_ranges(positions, dst_rows, Mc, (long)cache->rows, c.max_prefix, pmax, ranges, s));
   for (int l = 0; l < c.n_layers; ++l) {
+    const Range range("fe.prefill_layer");
     const fe_layer_weights &lw = h->layers[l];
     FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an, d, c.rms_eps, s));
     for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
@@ -1169,6 +1186,7 @@ fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
                          const int32_t *tokens, const int32_t *positions,
                          const int32_t *dst_rows, const fe_kv_cache *cache, void *workspace,
                          size_t ws_bytes, void *stream) {
+  const Range range("fe_kv_update");
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (n_rows < 0) return fail(FE_E_INVALID, "n_rows %d is negative", n_rows);
@@ -1353,6 +1371,7 @@ fe_status accept_sample_impl(fe_drafter *h, int32_t batch, int32_t topk, const i
                              const float *target_probs, const float *uniforms,
                              int32_t *accept_len, int32_t *accept_path, int32_t *accepted,
                              void *stream) {
+  const Range range("fe_accept_sample");
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);
@@ -1428,6 +1447,7 @@ extern "C" fe_status fe_build_tree(fe_drafter *h, int32_t batch, int32_t topk,
                                    const int32_t *root_tokens, const int32_t *topk_ids,
                                    const int32_t *prefix_lens, const fe_tree_out *out,
                                    void *stream) {
+  const Range range("fe_build_tree");
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   const fe_config &c = h->cfg;
   if (batch < 0 || batch > c.max_batch) return fail(FE_E_INVALID, "batch %d outside [0, %d]", batch, c.max_batch);

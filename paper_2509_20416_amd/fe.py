@@ -10,7 +10,9 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libfe.so")
+# FE_LIBRARY selects another build of the same library (the host-sanitizer
+# build, for host-only test runs); the default is the in-tree libfe.so.
+LIB_PATH = os.environ.get("FE_LIBRARY") or os.path.join(HERE, "libfe.so")
 
 FE_OK, FE_E_INVALID, FE_E_UNSUPPORTED, FE_E_ALIGN, FE_E_WORKSPACE, FE_E_HIP = range(6)
 FE_F32, FE_BF16 = 0, 1
