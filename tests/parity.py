@@ -17,6 +17,13 @@ import numpy as np
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+# Drift guard of the full-size bf16 workloads: the parity bar above is what
+# bf16 storage of the layer states allows; the full-size passes have measured
+# per-row errors of 5e-3 to 7.3e-3 against the oracle (bf16 unit roundoff is
+# 3.9e-3), so an error above 1e-2 there means the arithmetic has drifted
+# (a lost fp32 accumulation, a norm in bf16) even while parity still holds.
+DRIFT = {"f32": 1e-4, "bf16": 1e-2}
+
 
 def rel_row_err(gpu: np.ndarray, ref: np.ndarray) -> np.ndarray:
     g = gpu.reshape(-1, gpu.shape[-1]).astype(np.float64)

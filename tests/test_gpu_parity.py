@@ -356,33 +356,46 @@ def test_parallel_heads_graph_replays_match_eager(batch):
 
 
 # --- paper-shaped workloads at full size, in the configuration the bench times -----------
+def _drift_guard(rep, cfg):
+    """Full-size errors stay within the drift guard (tests/parity.py DRIFT)."""
+    from tests.parity import DRIFT
+    for n in ("hidden_err", "logit_err"):
+        assert rep[n] <= DRIFT[cfg.dtype], (n, rep[n])
+
+
 @pytest.mark.timeout(900)
 def test_llama8b_b1_full():
-    _run(C.LLAMA8B_BF16_B1, seed=0, graph=True)
+    rep, _, _ = _run(C.LLAMA8B_BF16_B1, seed=0, graph=True)
+    _drift_guard(rep, C.LLAMA8B_BF16_B1)
 
 
 @pytest.mark.timeout(900)
 def test_llama8b_b1_parallel_heads_full():
     """The ablation without the cascade, at the 8B shapes the bench times it on."""
-    _run(C.LLAMA8B_BF16_B1.with_(cascade_ctx="parallel"), seed=0, graph=True)
+    cfg = C.LLAMA8B_BF16_B1.with_(cascade_ctx="parallel")
+    rep, _, _ = _run(cfg, seed=0, graph=True)
+    _drift_guard(rep, cfg)
 
 
 @pytest.mark.timeout(900)
 def test_vicuna13b_b1_full():
-    _run(C.VICUNA13B_BF16_B1, seed=0, graph=True)
+    rep, _, _ = _run(C.VICUNA13B_BF16_B1, seed=0, graph=True)
+    _drift_guard(rep, C.VICUNA13B_BF16_B1)
 
 
 @pytest.mark.timeout(1200)
 def test_llama70b_b1_full():
     """Element-wise cascade states and logits at the 70B shapes (8 query heads per
     KV head, head dim 128, P = 4096)."""
-    _run(C.LLAMA70B_BF16_B1, seed=0, graph=True)
+    rep, _, _ = _run(C.LLAMA70B_BF16_B1, seed=0, graph=True)
+    _drift_guard(rep, C.LLAMA70B_BF16_B1)
 
 
 @pytest.mark.timeout(1200)
 def test_llama8b_b32_ragged_all():
     """Batch 32, P_b ~ U[256, 8192], N = 7: every sequence against the oracle."""
-    _run(C.LLAMA8B_BF16_B32, seed=0, graph=True)
+    rep, _, _ = _run(C.LLAMA8B_BF16_B32, seed=0, graph=True)
+    _drift_guard(rep, C.LLAMA8B_BF16_B32)
 
 
 def _planted_lm_head(cfg, w, ref_hidden, b, base_ids, top=None):
