@@ -549,10 +549,20 @@ static hipError_t attn_mma_t(const void *K, const void *V, Seqs cu, const float 
 // Enough workgroups to keep every CU busy with several at a time until the
 // end (one-wave workgroups, four per CU) and no more: a sequence split over
 // more workgroups only adds set-up work and partials to merge.
+// A launch of at most a few rounds of resident waves (batch 1 at every model
+// shape) instead takes the fewest chunks per unit that keep it to one round
+// and its merge to one round trip (32 partials per head): measured at batch 1,
+// 13B-shaped (40 KV heads, P 2048) 16.3 us per layer against 31.1 with one
+// chunk per unit, 70B-shaped (P 4096) 16.2 against 19.0, 8B-shaped unchanged.
 int attention_cpw(int B, int Hkv, int ngroups, int nch) {
   constexpr long kTargetWorkgroups = 4096;
-  const long cols = (long)B * Hkv * ngroups;
-  long cpw = (cols * nch + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  const long cols = (long)B * Hkv * ngroups, units = cols * nch;
+  long cpw = (units + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  if (units <= kTargetWorkgroups) {
+    const long waves = resident_waves();
+    const long one_round = (units + waves - 1) / waves, one_trip = (nch + 31) / 32;
+    cpw = one_round > one_trip ? one_round : one_trip;
+  }
   if (cpw > nch) cpw = nch;
   return cpw < 1 ? 1 : (int)cpw;
 }
