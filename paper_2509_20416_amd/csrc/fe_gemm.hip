@@ -383,20 +383,23 @@ __device__ __forceinline__ void wg_barrier() {
 }
 __device__ __forceinline__ int ring_slot(int row, int piece) { return row * 8 + (piece ^ ((row >> 1) & 7)); }
 
-template <typename T, int NTW, int WN, int S, class Epi>
+template <typename T, int NTW, int WN, int S, class Epi, int RT = 4>
 __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int lda, ARows arows,
                                                   int M, int K, Epi epi, float *__restrict__ splitp,
                                                   int ldp) {
+  // RT: 16-row tiles per wave (4; 2 when at most 32 rows are live, so that the
+  // ring does not carry duplicated rows of A)
+  static_assert(RT == 4 || RT == 2, "row tiles per wave");
+  constexpr int WM = 4 / WN;
+  constexpr int MROWS = 16 * RT * WM;  // rows this configuration holds
   if constexpr (SlicedEpi<Epi>::value) {
     const T *a = A;
-    epi.slice(blockIdx.z, 64 * (4 / WN), a, M);
+    epi.slice(blockIdx.z, MROWS, a, M);
     A = a;
     if (M <= 0) return;  // the whole workgroup: past the last row block
   }
   constexpr int E = Elt<T>::kPer16B;  // elements per 16-byte piece
   constexpr int KC = 8 * E;           // elements of K per chunk
-  constexpr int WM = 4 / WN;
-  constexpr int MROWS = 64 * WM;      // rows this configuration holds
   constexpr int BN = NTW * WN * 16;
   static_assert(BN % 32 == 0, "weight slots must split evenly over the four waves");
   constexpr int AI = MROWS / 32;      // A load instructions per wave per stage
@@ -448,13 +451,13 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
       lds_dma16(wsrc[j] + min(k + woff[j], K - E), st + ABYTES + (j * 4 + wave) * 1024);
   };
 
-  f32x4 acc[4][NTW];
+  f32x4 acc[RT][NTW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
     for (int f = 0; f < NTW; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int mrow0 = wm * 64, ncol0 = wn * NTW * 16;
-  const int mtiles = min(4, (M - mrow0 + 15) / 16);  // this wave's live 16-row tiles (may be <= 0)
+  const int mrow0 = wm * 16 * RT, ncol0 = wn * NTW * 16;
+  const int mtiles = min(RT, (M - mrow0 + 15) / 16);  // this wave's live 16-row tiles (may be <= 0)
 
 #pragma unroll
   for (int st = 0; st < S - 1; ++st) issue(st);
@@ -474,20 +477,20 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
     // every fragment of the chunk is read before the first product (the ring
     // holds all MROWS rows, so the reads need no guard and are in flight
     // together); only the products skip the wave's dead row tiles
-    u32x4 bf[2][NTW], af[2][4];
+    u32x4 bf[2][NTW], af[2][RT];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
       for (int f = 0; f < NTW; ++f)
         bf[ks][f] = *reinterpret_cast<const u32x4 *>(st + ABYTES + ring_slot(ncol0 + f * 16 + r, ks * 4 + g) * 16);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < RT; ++i)
         af[ks][i] = *reinterpret_cast<const u32x4 *>(st + ring_slot(mrow0 + i * 16 + r, ks * 4 + g) * 16);
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < RT; ++i)
         if (i < mtiles)
 #pragma unroll
           for (int f = 0; f < NTW; ++f) mma16<T>(acc[i][f], af[ks][i], bf[ks][f]);
@@ -496,7 +499,7 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   if (splitp) {  // split K: this slice's fp32 sums, reduced (and finished) by a second launch
     float *dst = splitp + (size_t)blockIdx.y * M * ldp + c0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < RT; ++i)
       if (i < mtiles)
 #pragma unroll
         for (int f = 0; f < NTW; ++f)
@@ -510,7 +513,7 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   wg_barrier();
   float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < RT; ++i)
     if (i < mtiles)
 #pragma unroll
       for (int f = 0; f < NTW; ++f)
@@ -1199,6 +1202,11 @@ struct SplitOut {
   int ldp = 0, ks = 0;
 };
 
+// ring stages of the at-most-32-row configuration: four keep two workgroups
+// per CU (measured at the 8B batch-32 shapes: 1962 us per pass, against 1992
+// with six stages and 1996 with 64-row tiles)
+constexpr int kHalfStages = 4;
+
 template <typename T, int NT, int WKmax, int WN, class Epi>
 static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K, const Epi &epi,
                            const NormA *na, hipStream_t s, const SplitScratch *ss = nullptr,
@@ -1270,13 +1278,18 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
     if ((size_t)ks * M * ldp > ss->floats) ks = 1;
     if (ks > 1) sp = ss->p;
   }
-#define FE_GEMM_MID(NTWV, WNV, SV)                                                                   \
-  hipLaunchKernelGGL((k_gemm_mid<T, NTWV, WNV, SV, Epi>),                                           \
+#define FE_GEMM_MID_RT(NTWV, WNV, SV, RTV)                                                           \
+  hipLaunchKernelGGL((k_gemm_mid<T, NTWV, WNV, SV, Epi, RTV>),                                      \
                      dim3((epi.nvcols + 16 * NTWV * WNV - 1) / (16 * NTWV * WNV), ks), dim3(256), 0,  \
                      s, A, lda, arows, M, K, epi, sp, ldp)
+#define FE_GEMM_MID(NTWV, WNV, SV) FE_GEMM_MID_RT(NTWV, WNV, SV, 4)
+  // at most 32 rows: two 16-row tiles per wave, so the ring carries no
+  // duplicated rows of A, and the stages it frees go to a deeper ring
+  const bool half = wn == 4 && M <= 32;
   if constexpr (Epi::kSplitK) {
     if (sp) {
-      if (wn == 4) FE_GEMM_MID(2, 4, 4);
+      if (wn == 4 && half) FE_GEMM_MID_RT(2, 4, kHalfStages, 2);
+      else if (wn == 4) FE_GEMM_MID(2, 4, 4);
       else if (wn == 2) FE_GEMM_MID(4, 2, 4);
       else FE_GEMM_MID(8, 1, 3);
       const hipError_t e = hipGetLastError();
@@ -1289,7 +1302,10 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
       return hipGetLastError();
     }
   }
-  if (wn == 4) {
+  if (wn == 4 && half) {
+    if (ntw >= 2) FE_GEMM_MID_RT(2, 4, kHalfStages, 2);
+    else FE_GEMM_MID_RT(1, 4, kHalfStages, 2);
+  } else if (wn == 4) {
     if (ntw >= 2) FE_GEMM_MID(2, 4, 4);
     else FE_GEMM_MID(1, 4, 4);
   } else if (wn == 2) {
@@ -1300,6 +1316,7 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
     else FE_GEMM_MID(2, 1, 3);
   }
 #undef FE_GEMM_MID
+#undef FE_GEMM_MID_RT
   return hipGetLastError();
 }
 
