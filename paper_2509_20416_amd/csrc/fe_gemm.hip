@@ -899,7 +899,8 @@ struct TileStore : EpiStore<bf16_t> {
     }
   }
 };
-// Input FC into fp32 rows.
+// Input FC into fp32 rows (out = A W^T), or with `resid` a residual FC
+// (out = resid + A W^T).
 struct TileF32 {
   static constexpr bool kRowStream = true, kSplitK = false, kSliced = true;
   using Pre = NoPre;
@@ -910,17 +911,22 @@ struct TileF32 {
   float *out;
   long ldo;
   int lda;
+  const float *resid = nullptr;
+  long ldr = 0;
   __device__ const bf16_t *wrow(int c) const { return w + (size_t)c * ldw; }
   __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
     const int m0 = z * mrows;
     A += (size_t)m0 * lda;
     M = min(mrows, M - m0);
     out += (size_t)m0 * ldo;
+    if (resid) resid += (size_t)m0 * ldr;
   }
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
-      if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = tile[m * ldt + c];
+      if (c0 + c < nvcols)
+        out[(size_t)m * ldo + c0 + c] =
+            tile[m * ldt + c] + (resid ? resid[(size_t)m * ldr + c0 + c] : 0.f);
     }
   }
 };
@@ -990,6 +996,18 @@ template <typename T> struct EpiSwiglu {
       const int col = (vc >> 5) * 16 + (vc & 15);
       out[(size_t)m * ldo + col] = Elt<T>::from_f(s);
     }
+  }
+};
+
+// Gate/up + SwiGLU over row blocks (the multi-position prefill's MLP).
+struct TileSwiglu : EpiSwiglu<bf16_t> {
+  static constexpr bool kSliced = true;
+  int lda;
+  __device__ void slice(int z, int mrows, const bf16_t *&A, int &M) {
+    const int m0 = z * mrows;
+    A += (size_t)m0 * lda;
+    M = min(mrows, M - m0);
+    out += (size_t)m0 * ldo;
   }
 };
 
@@ -1418,10 +1436,25 @@ hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, 
   return hipGetLastError();
 }
 
-hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
-                           long ldo, hipStream_t s) {
+hipError_t gemm_swiglu_rows(const void *A, int lda, int M, int K, const void *w_gate,
+                            const void *w_up, int I, void *out, int ldo, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  const TileF32 e{(const bf16_t *)W, K, ncols, out, ldo, lda};
+  TileSwiglu e;
+  static_cast<EpiSwiglu<bf16_t> &>(e) = EpiSwiglu<bf16_t>{(const bf16_t *)w_gate, (const bf16_t *)w_up,
+                                                          K, I, 2 * I, (bf16_t *)out, ldo};
+  e.lda = lda;
+  const dim3 grid((2 * I + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
+  hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileSwiglu>), grid,
+                     dim3(256), 0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
+  return hipGetLastError();
+}
+
+hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
+                           long ldo, hipStream_t s, const float *resid, long ldr) {
+  if (M <= 0) return hipSuccess;
+  TileF32 e{(const bf16_t *)W, K, ncols, out, ldo, lda};
+  e.resid = resid;
+  e.ldr = ldr;
   const dim3 grid((ncols + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileF32>), grid, dim3(256),
                      0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);

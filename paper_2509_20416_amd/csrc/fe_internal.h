@@ -367,7 +367,9 @@ hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, 
                            int ldo, const void *embed, const int32_t *tokens, int vocab,
                            void *gather_out, int ld_gather, int d, hipStream_t s);
 hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, int ncols, float *out,
-                           long ldo, hipStream_t s);
+                           long ldo, hipStream_t s, const float *resid = nullptr, long ldr = 0);
+hipError_t gemm_swiglu_rows(const void *A, int lda, int M, int K, const void *w_gate,
+                            const void *w_up, int I, void *out, int ldo, hipStream_t s);
 // Every layer's K/V projection into its cache in one launch (bf16): layer l's
 // normalised rows at A + l * a_layer_stride.  With na (M <= 16) A holds
 // gamma * x per layer and the rows' 1/rms come from na's sums of squares;

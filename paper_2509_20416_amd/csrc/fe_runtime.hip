@@ -1141,11 +1141,20 @@ fe_status prefill_layers(fe_drafter *h, const UpdLayout &U, char *ws, int Mc,
   const int pmax = c.max_prefix;
   const int nch = (pmax + kAttnChunk - 1) / kAttnChunk;
   FE_TRY(prefill_ranges(positions, dst_rows, Mc, (long)cache->rows, c.max_prefix, pmax, ranges, s));
+  // bf16 chunks of more rows than one batched launch takes: every GEMM as one
+  // 2-D tiled launch over all rows (each weight matrix streamed once per chunk)
+  const bool tiled = dt && Mc >= kTiledRows;
   for (int l = 0; l < c.n_layers; ++l) {
     const Range range("fe.prefill_layer");
     const fe_layer_weights &lw = h->layers[l];
     FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, lw.attn_norm, an, d, c.rms_eps, s));
-    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+    if (tiled) {
+      // q, K, V of every row (fp32, unrotated: the attention rotates them)
+      FE_TRY(gemm_resid_rows(an, d, Mc, d, lw.wq, qd, q, qd, s));
+      FE_TRY(gemm_resid_rows(an, d, Mc, d, lw.wk, kvd, knew, kvd, s));
+      FE_TRY(gemm_resid_rows(an, d, Mc, d, lw.wv, kvd, vnew, kvd, s));
+    }
+    for (int s0 = 0; s0 < Mc && !tiled; s0 += kGemmMaxRows) {
       const int Ms = std::min(kGemmMaxRows, Mc - s0);
       const QkvArgs qa{lw.wq, lw.wk, lw.wv, d, D, Hq, Hkv, 1, 0, 0, Seqs{ranges + 2 * s0, 1},
                        rope, h->L.npos, q + (size_t)s0 * qd, knew + (size_t)s0 * kvd,
@@ -1163,14 +1172,21 @@ fe_status prefill_layers(fe_drafter *h, const UpdLayout &U, char *ws, int Mc,
                        part, nch, U.nch_ld, cpw, ao + (size_t)s0 * qd * es, Ms, Hq, Hkv, D, rope,
                        0, pmax, s));
     }
-    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+    if (tiled) {  // x' = x_{i-1} + W_o o
+      FE_TRY(gemm_resid_rows(ao, qd, Mc, qd, lw.wo, d, Xp, d, s, X, d));
+    }
+    for (int s0 = 0; s0 < Mc && !tiled; s0 += kGemmMaxRows) {
       const int Ms = std::min(kGemmMaxRows, Mc - s0);
       // x' = x_{i-1} + W_o o
       FE_TRY(gemm_resid(dt, ao + (size_t)s0 * qd * es, qd, Ms, qd, lw.wo, d, Xp + (size_t)s0 * d,
                         d, X + (size_t)s0 * d, d, nullptr, 1, 0, nullptr, s, ss));
     }
     FE_TRY(rmsnorm_rows(dt, Xp, Mc, 1, 0, d, 0, lw.mlp_norm, an, d, c.rms_eps, s));
-    for (int s0 = 0; s0 < Mc; s0 += kGemmMaxRows) {
+    if (tiled) {  // SwiGLU rows, then x_i = x' + W_d s (Eq. 2)
+      FE_TRY(gemm_swiglu_rows(an, d, Mc, d, lw.w_gate, lw.w_up, I, sb, I, s));
+      FE_TRY(gemm_resid_rows(sb, I, Mc, I, lw.w_down, d, X, d, s, Xp, d));
+    }
+    for (int s0 = 0; s0 < Mc && !tiled; s0 += kGemmMaxRows) {
       const int Ms = std::min(kGemmMaxRows, Mc - s0);
       FE_TRY(gemm_swiglu(dt, an + (size_t)s0 * d * es, d, kDenseRows, Ms, d, lw.w_gate, lw.w_up, I,
                          sb + (size_t)s0 * I * es, I, nullptr, s));
