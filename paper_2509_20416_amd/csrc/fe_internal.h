@@ -453,13 +453,25 @@ hipError_t accept_greedy(int B, int N, int k, const int32_t *tokens, const int32
 // accept_greedy.  V <= kAccSampleMaxV, Vt <= kAccSampleMaxVt (LDS residual).
 // img: the bitmask of the target ids that d2t maps to, from accept_img.
 constexpr int kAccSampleMaxV = 32768, kAccSampleMaxVt = 131072;
+// Workspace of the acceptance's row pre-pass (batches of at most max_batch
+// sequences): per (sequence, node) 16 chunk sums and unmapped sums, 16 last
+// unmapped ids, and p at the V mapped ids.  Used for a single sequence only:
+// measured on the 8B vocabularies, 58 us per call against 64 at batch 1, but
+// 121 against 102 at batch 4 (every node's row is read, not just the visited
+// ones).
+struct AccPre {
+  float *p = nullptr;
+  int max_batch = 0;
+};
+constexpr int kAccPreMaxBatch = 1;
+inline size_t acc_pre_bytes(int B, int T, int V) { return (size_t)B * T * (16 * 3 + (size_t)V) * 4; }
 hipError_t accept_img(const int32_t *d2t, int V, int Vt, uint32_t *img, hipStream_t s);
 hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *tokens,
                          const int32_t *retrieve, const int32_t *topk_draft,
                          const float *draft_logits, float inv_temp, Draws draft_draws,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
                          const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
-                         int32_t *accepted, hipStream_t s);
+                         int32_t *accepted, hipStream_t s, AccPre pre = AccPre{});
 // Uniforms first .. first+n-1 of the counter-based stream ((seed, offset) in
 // device memory) into out (test export of the generator).
 hipError_t philox_fill(const uint64_t *seed_offset, uint64_t first, long n, float *out,

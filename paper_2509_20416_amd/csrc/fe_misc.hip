@@ -468,7 +468,91 @@ __global__ __launch_bounds__(kAccThreads) void k_build_img(const int32_t *__rest
   for (int w = tid; w < nw; w += kAccThreads) img[w] = s_img[w];
 }
 
+// Chunks of a target row as the walk's waves own them: kAccWaves contiguous
+// ranges of CW ids (CW a multiple of 64 W).
+__host__ __device__ inline int acc_chunk_width(int Vt, int W) {
+  return ((Vt + kAccWaves - 1) / kAccWaves + 64 * W - 1) / (64 * W) * (64 * W);
+}
+
+// Few sequences: before the walk, every node's target row is reduced by
+// workgroups of its own instead of by the one walking workgroup when (and if)
+// it gets there.  Row (sequence b, node n), workgroup y < kAccWaves: chunk y's
+// sum of p, its unmapped part (ids no draft id maps to) and its last unmapped
+// id with mass; y >= kAccWaves: p at the mapped ids of draft ids
+// [(y - kAccWaves) * VP, ...) (the walk's residual row, compact).
+constexpr int kAccPreThreads = 256, kAccPreGather = 16;
+template <int W>
+__global__ __launch_bounds__(kAccPreThreads) void k_accept_rows(
+    int Vt, int V, const int32_t *__restrict__ d2t, const float *__restrict__ target_probs,
+    const uint32_t *__restrict__ img, float *__restrict__ agg, int32_t *__restrict__ agg_last,
+    float *__restrict__ gathered) {
+  __shared__ float red[kAccPreThreads / 64];
+  __shared__ int redi[kAccPreThreads / 64];
+  const int row = blockIdx.x, y = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float *p = target_probs + (size_t)row * Vt;
+  if (y >= kAccWaves) {
+    const int VP = (V + kAccPreGather - 1) / kAccPreGather;
+    const int v0 = (y - kAccWaves) * VP, v1 = min(v0 + VP, V);
+    for (int v = v0 + tid; v < v1; v += kAccPreThreads) {
+      const int x = d2t ? d2t[v] : v;
+      gathered[(size_t)row * V + v] = (x >= 0 && x < Vt) ? p[x] : 0.f;
+    }
+    return;
+  }
+  const int CW = acc_chunk_width(Vt, W);
+  const int c0 = min(y * CW, Vt), c1 = min(c0 + CW, Vt);
+  float zs = 0.f, cn = 0.f;
+  int last = -1;
+  for (int x0 = c0 + tid * W; x0 < c1; x0 += kAccPreThreads * W) {
+    float a[W];
+    if constexpr (W == 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4 *>(p + x0);  // W | CW, rows 16-byte aligned
+      a[0] = q.x; a[1] = q.y; a[2] = q.z; a[3] = q.w;
+    } else {
+      a[0] = p[x0];
+    }
+#pragma unroll
+    for (int q = 0; q < W; ++q) {
+      const int x = x0 + q;
+      if (x >= c1) continue;
+      zs += a[q];
+      if (!((img[x >> 5] >> (x & 31)) & 1u)) {
+        cn += a[q];
+        if (a[q] > 0.f) last = x;
+      }
+    }
+  }
+  zs = group_sum<64>(zs);
+  cn = group_sum<64>(cn);
+  last = (int)group_max<64>((float)last);
+  if (lane == 0) {
+    red[wave] = zs;
+    redi[wave] = last;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float z = 0.f;
+    int l = -1;
+    for (int w = 0; w < kAccPreThreads / 64; ++w) {
+      z += red[w];
+      l = max(l, redi[w]);
+    }
+    agg[((size_t)row * kAccWaves + y) * 2] = z;
+    agg_last[(size_t)row * kAccWaves + y] = l;
+  }
+  __syncthreads();
+  if (lane == 0) red[wave] = cn;
+  __syncthreads();
+  if (tid == 0) {
+    float c = 0.f;
+    for (int w = 0; w < kAccPreThreads / 64; ++w) c += red[w];
+    agg[((size_t)row * kAccWaves + y) * 2 + 1] = c;
+  }
+}
+
 // VEC: target rows read four ids per lane (Vt % 4 == 0, 16-byte aligned rows).
+// agg / agg_last / gathered (k_accept_rows, or null): the nodes' rows reduced
+// beforehand; the walk then reads them instead of the target rows.
 template <bool VEC>
 __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     int N, int k, int V, int Vt, const int32_t *__restrict__ tokens,
@@ -477,7 +561,8 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     Draws draft_draws, const int32_t *__restrict__ d2t,
     const float *__restrict__ target_probs, const float *__restrict__ uniforms,
     const uint32_t *__restrict__ img, int32_t *accept_len, int32_t *accept_path,
-    int32_t *accepted) {
+    int32_t *accepted, const float *__restrict__ agg, const int32_t *__restrict__ agg_last,
+    const float *__restrict__ gathered) {
   constexpr int W = VEC ? 4 : 1;  // target ids per lane per load
   __shared__ float s_rd[kAccMaxV];
   __shared__ uint32_t s_img[kAccMaxVt / 32];
@@ -512,7 +597,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
   }
   __syncthreads();
   // this wave's contiguous chunk of target ids
-  const int CW = ((Vt + kAccWaves - 1) / kAccWaves + 64 * W - 1) / (64 * W) * (64 * W);
+  const int CW = acc_chunk_width(Vt, W);
   const int c0 = min(wave * CW, Vt), c1 = min(c0 + CW, Vt);
   int node = 0, len = 0, t = 0;
   float Z = 0.f;
@@ -538,8 +623,18 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
     float zs = 0.f, cn = 0.f;
     lastn = -1;
     constexpr int NB = kAccBatch / W;
+    if (agg) {  // reduced beforehand: chunk sums (summed in chunk order) and rd
+      const size_t r = (size_t)b * T + node;
+      float z = 0.f;
+      for (int w = 0; w < kAccWaves; ++w) z += agg[(r * kAccWaves + w) * 2];
+      if (lane == 0) s_cn[wave] = agg[(r * kAccWaves + wave) * 2 + 1];
+      lastn = agg_last[r * kAccWaves + wave];
+      for (int v = tid; v < V; v += kAccThreads) s_rd[v] = gathered[r * V + v];
+      __syncthreads();
+      Z = z;
+    }
 #pragma unroll 1
-    for (int e = c0; e < c1; e += 64 * W * NB) {
+    for (int e = c0; e < c1 && !agg; e += 64 * W * NB) {
       float a[NB][W];
 #pragma unroll
       for (int j = 0; j < NB; ++j) loadp(e + 64 * W * j + W * lane, a[j]);
@@ -555,11 +650,13 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
           }
         }
     }
+    if (!agg) {
     cn = group_sum<64>(cn);
     if (lane == 0) s_cn[wave] = cn;  // read after the barriers below
+    }
     // rd = p at the mapped ids: the map, then the values, half the ids at a time
 #pragma unroll 1
-    for (int h = 0; h < kZ; h += kZ / 2) {
+    for (int h = 0; h < kZ && !agg; h += kZ / 2) {
       int xs[kZ / 2];
       float g[kZ / 2];
 #pragma unroll
@@ -576,7 +673,7 @@ __global__ __launch_bounds__(kAccThreads) void k_accept_sample(
         if (v < V) s_rd[v] = g[j];
       }
     }
-    Z = acc_sum(zs, red);  // its barriers also publish s_rd
+    if (!agg) Z = acc_sum(zs, red);  // its barriers also publish s_rd
     const bool has_children = lvl <= N && (node == 0 || node == 1 + (lvl - 2) * k);
     if (!has_children) break;
     const float *z = draft_logits + lrow * V;
@@ -750,18 +847,35 @@ hipError_t accept_sample(int B, int N, int k, int V, int Vt, const int32_t *toke
                          const float *draft_logits, float inv_temp, Draws draft_draws,
                          const int32_t *d2t, const float *target_probs, const float *uniforms,
                          const uint32_t *img, int32_t *accept_len, int32_t *accept_path,
-                         int32_t *accepted, hipStream_t s) {
+                         int32_t *accepted, hipStream_t s, AccPre pre) {
   if (B <= 0) return hipSuccess;
   if (k > kMaxTopk || N > kMaxLayers || V > kAccMaxV || Vt > kAccMaxVt) return hipErrorInvalidValue;
   const bool vec = Vt % 4 == 0 && ((uintptr_t)target_probs & 15u) == 0;
+  float *agg = nullptr, *gathered = nullptr;
+  int32_t *agg_last = nullptr;
+  if (pre.p && B <= pre.max_batch) {  // few sequences: reduce every node's row first
+    const int T = 1 + N * k;
+    agg = pre.p;
+    agg_last = (int32_t *)(agg + (size_t)B * T * kAccWaves * 2);
+    gathered = (float *)(agg_last + (size_t)B * T * kAccWaves);
+    const dim3 grid(B * T, kAccWaves + kAccPreGather);
+    if (vec)
+      hipLaunchKernelGGL(k_accept_rows<4>, grid, dim3(kAccPreThreads), 0, s, Vt, V, d2t,
+                         target_probs, img, agg, agg_last, gathered);
+    else
+      hipLaunchKernelGGL(k_accept_rows<1>, grid, dim3(kAccPreThreads), 0, s, Vt, V, d2t,
+                         target_probs, img, agg, agg_last, gathered);
+  }
   if (vec)
     hipLaunchKernelGGL(k_accept_sample<true>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
                        tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_draws, d2t,
-                       target_probs, uniforms, img, accept_len, accept_path, accepted);
+                       target_probs, uniforms, img, accept_len, accept_path, accepted, agg,
+                       agg_last, gathered);
   else
     hipLaunchKernelGGL(k_accept_sample<false>, dim3(B), dim3(kAccThreads), 0, s, N, k, V, Vt,
                        tokens, retrieve, topk_draft, draft_logits, inv_temp, draft_draws, d2t,
-                       target_probs, uniforms, img, accept_len, accept_path, accepted);
+                       target_probs, uniforms, img, accept_len, accept_path, accepted, agg,
+                       agg_last, gathered);
   return hipGetLastError();
 }
 

@@ -54,6 +54,8 @@ struct Layout {
   size_t cat, X, Xp, ssqX, ssqP, AQ, AM, AF, an, bn, q, knew, vnew, part, rope, ao, s, pmax,
       psum, cval, cidx, cz, img, splitk, tagged, total;
   size_t splitk_floats;
+  size_t acc_pre;
+  int acc_pre_batch;
   // Layer-private buffers (x', its norms and sums of squares, Q/K/V, attention
   // partials and output, SwiGLU rows, split-K slices): one lane, or under
   // FE_CTX_PARALLEL one lane per layer, so that the independent layers can
@@ -108,6 +110,9 @@ Layout layout_of(const fe_config &c) {
   L.cidx = take(B * N * (size_t)L.nwg * kMaxTopk * 4);
   L.cz = take(B * N * (size_t)L.nwg * kMaxTopk * 4);  // z / T of sampled candidates
   L.img = take(((size_t)c.target_vocab + 31) / 32 * 4);  // target ids that d2t reaches
+  // the sampling acceptance's row pre-pass for batches of a few sequences
+  L.acc_pre_batch = (int)std::min<size_t>(B, kAccPreMaxBatch);
+  L.acc_pre = take(acc_pre_bytes(L.acc_pre_batch, 1 + (int)N * c.max_topk, c.draft_vocab));
   // the persistent batch-1 pass: sync words, g_t, sums of squares of x_j and
   // x'_i per workgroup, normalised copies of x_j for every consumer (QKV of
   // layer l, or the LM head), of x'_i, the SwiGLU rows, LM-head candidates
@@ -1410,10 +1415,13 @@ fe_status accept_sample_impl(fe_drafter *h, int32_t batch, int32_t topk, const i
     FE_TRY(accept_img(h->w.d2t, c.draft_vocab, c.target_vocab, img, (hipStream_t)stream));
     h->img_ready = true;
   }
+  AccPre pre;
+  pre.p = (float *)(h->ws + h->L.acc_pre);
+  pre.max_batch = h->L.acc_pre_batch;
   FE_TRY(accept_sample(batch, c.n_layers, topk, c.draft_vocab, c.target_vocab, tokens, retrieve,
                        topk_draft, draft_logits, 1.0f / temperature, draft_draws, h->w.d2t,
                        target_probs, uniforms, img, accept_len, accept_path, accepted,
-                       (hipStream_t)stream));
+                       (hipStream_t)stream, pre));
   return FE_OK;
 }
 }  // namespace

@@ -134,6 +134,14 @@ CASES = [
     (SMALL_V, 16, 16, 1.0, True),
     (SMALL_V, 32, 5, 1.0, False),
     (C.TINY_F32_B1.with_(n_layers=6), 8, 4, 1.0, True),   # identity map
+    # one sequence: every node's target row reduced by a pre-pass first
+    (SMALL_V, 1, 5, 1.0, True),
+    (SMALL_V, 1, 4, 1.0, False),
+    (C.TINY_F32_B1.with_(n_layers=6), 1, 4, 1.0, True),
+    (SMALL_V, 2, 5, 1.0, True),
+    (SMALL_V, 4, 16, 0.7, True),
+    (SMALL_V, 3, 5, 1.0, False),
+    (C.TINY_F32_B1.with_(n_layers=6), 4, 3, 1.0, True),
 ]
 
 
@@ -144,7 +152,7 @@ def test_accept_sample_parity(cfg, B, k, T, sampled):
     _run(cfg, B, k, T, sampled, seed=B * 100 + k)
 
 
-@pytest.mark.parametrize("B,k,T", [(32, 5, 1.0), (16, 16, 0.7)])
+@pytest.mark.parametrize("B,k,T", [(32, 5, 1.0), (16, 16, 0.7), (4, 5, 1.0), (1, 5, 1.0)])
 def test_accept_sample_seeded_parity(B, k, T):
     """Children drawn from the counter-based stream (fe_draft_sample_seeded):
     the acceptance recomputes their uniforms from (seed, offset) in device
