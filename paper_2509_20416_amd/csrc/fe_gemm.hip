@@ -523,6 +523,9 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
 }
 
+// split-K slices the reductions sum (k_splitk_finish, k_resid_rows)
+constexpr int kMaxSlices = 8;
+
 // Split-K reduction: sums the ks partial slices of a 16-column span in a fixed
 // order and hands the span to the epilogue, like k_gemm_mid would.  A thread
 // takes 4 adjacent columns of a row and issues all of its slice loads before
@@ -537,13 +540,13 @@ __global__ __launch_bounds__(256) void k_splitk_finish(const float *__restrict__
   for (int q = threadIdx.x; q < M * (BNR / 4); q += 256) {
     const int m = q / (BNR / 4), c = (q % (BNR / 4)) * 4;
     const float *src = splitp + (size_t)m * ldp + c0 + c;
-    f32x4 part[8];
+    f32x4 part[kMaxSlices];
 #pragma unroll
-    for (int y = 0; y < 8; ++y)
+    for (int y = 0; y < kMaxSlices; ++y)
       part[y] = y < ks ? *reinterpret_cast<const f32x4 *>(src + y * slice) : f32x4{0.f, 0.f, 0.f, 0.f};
     f32x4 v = part[0];
 #pragma unroll
-    for (int y = 1; y < 8; ++y) v += part[y];
+    for (int y = 1; y < kMaxSlices; ++y) v += part[y];
 #pragma unroll
     for (int e = 0; e < 4; ++e) tile[m * LDT + c + e] = v[e];
   }
@@ -592,12 +595,12 @@ __global__ __launch_bounds__(kRowThreads) void k_resid_rows(const float *__restr
     const int e = 4 * (tid + kRowThreads * u), ec = min(e, d - 4);
     if (ks > 0) {
       const float *src = splitp + (size_t)m * ldp + ec;
-      f32x4 part[8];
+      f32x4 part[kMaxSlices];
 #pragma unroll
-      for (int y = 0; y < 8; ++y) part[y] = y < ks ? *reinterpret_cast<const f32x4 *>(src + y * slice) : zero;
+      for (int y = 0; y < kMaxSlices; ++y) part[y] = y < ks ? *reinterpret_cast<const f32x4 *>(src + y * slice) : zero;
       f32x4 t = part[0];
 #pragma unroll
-      for (int y = 1; y < 8; ++y) t += part[y];
+      for (int y = 1; y < kMaxSlices; ++y) t += part[y];
       if (resid) t = *reinterpret_cast<const f32x4 *>(resid + (size_t)m * ldr + ec) + t;
       v[u] = t;
     } else {
@@ -1220,6 +1223,10 @@ struct SplitOut {
   int ldp = 0, ks = 0;
 };
 
+// split-K slices of the narrow batched-rows GEMMs (at most 128 rows): up to
+// kSliceCap32 slices, about kSliceWgs workgroups
+constexpr int kSliceCap32 = 8, kSliceWgs = 256;
+
 // ring stages of the at-most-32-row configuration: four keep two workgroups
 // per CU (measured at the 8B batch-32 shapes: 1962 us per pass, against 1992
 // with six stages and 1996 with 64-row tiles)
@@ -1290,7 +1297,8 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
     const int gx = (epi.nvcols + 127) / 128, nchk = (K + KC - 1) / KC;
     // about one workgroup per CU (k_splitk_finish sums at most 8 slices); many
     // rows make each slice heavier and its partial sums larger: fewer slices
-    ks = min(M > 128 ? 4 : 8, max(1, (256 + gx - 1) / gx));
+    ks = min(M > 128 ? 4 : kSliceCap32, max(1, (kSliceWgs + gx - 1) / gx));
+    ks = min(ks, kMaxSlices);
     ks = min(ks, max(1, nchk / 4));  // a few chunks per slice for the ring
     ldp = gx * 128;
     if ((size_t)ks * M * ldp > ss->floats) ks = 1;
