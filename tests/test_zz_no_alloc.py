@@ -50,7 +50,10 @@ def _view(fe, ks, vs):
 # update (fused norm) in the second
 CASES = [(CF.SMALL_GQA_BF16, [200] * 5, [6]),
          (CF.LLAMA8B_BF16_B1, [50, 40, 30], [6]),
-         (CF.SMALL_GQA_F32, [90] * 3, [2, 1])]
+         (CF.SMALL_GQA_F32, [90] * 3, [2, 1]),
+         # the self context: the layers run over the rows (a prefill)
+         (CF.SMALL_GQA_BF16.with_(cascade_ctx="self", name="small_gqa_bf16_self"), [150] * 4, [6]),
+         (CF.LLAMA8B_BF16_B1.with_(cascade_ctx="self", name="llama8b_bf16_self"), [40, 30], [6])]
 
 
 @pytest.mark.parametrize("cfg,acc1,acc2", CASES, ids=[c[0].name for c in CASES])
