@@ -523,6 +523,151 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
   epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
 }
 
+// ---------------------------------------------------------------------------
+// Many rows, matrix-core bound (the cache update's and the prefill's row
+// blocks: bf16, K a multiple of 64): 128 x 128 output tiles, eight waves as 2
+// row groups x 4 column groups of 64 x 32, so two waves share each SIMD.  The
+// ring and its swizzle are k_gemm_mid's; the schedule is software-pipelined
+// over the two 32-wide K steps of a chunk:
+//   read step-1 fragments of chunk c | products of step 0 (read last round)
+//   wait: chunk c+1 landed, every read of chunk c done; barrier
+//   refill chunk c's slot with chunk c+S | read step-0 fragments of chunk c+1
+//   products of step 1
+// so every product's operands were read while other products ran.  Waits are
+// compiler-visible s_waitcnt immediates and the phases are fenced with
+// scheduling barriers: with inline-asm waits the compiler hoisted the barrier
+// (and its lgkmcnt(0)) above the products, serialising LDS latency.  At 1024
+// rows (8B shapes) this runs the fusion GEMM at 34 %, the K/V GEMM of all
+// layers at 33 % of the bf16 peak, against 24 % for k_gemm_mid's tiles.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ constexpr int waitcnt_imm(int vm, int lgkm) {
+  return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (lgkm << 8);
+}
+
+constexpr int kBigRows = 128, kBigCols = 128;
+
+template <int S, class Epi>
+__global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A, int lda, int M, int K,
+                                                   Epi epi) {
+  constexpr int RT = 4, NTW = 2, WN = 4, NW = 8;
+  constexpr int BM = kBigRows, BN = kBigCols, KC = 64;
+  constexpr int ABYTES = BM * 128, STAGE = ABYTES + BN * 128;
+  constexpr int AI = BM / 8 / NW, WI = BN / 8 / NW, CNT = AI + WI;  // 1 KB loads per wave per chunk
+  static_assert(S >= 2 && (S - 1) * CNT <= 63, "vmcnt range");
+  constexpr int LDT = BN + 1, TILE = BM * LDT * 4;
+  constexpr int SMEM = S * STAGE > TILE ? S * STAGE : TILE;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  {
+    const bf16_t *a = A;
+    epi.slice(blockIdx.z, BM, a, M);
+    A = a;
+    if (M <= 0) return;  // the whole workgroup: past the last row block
+  }
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int wm = wave / WN, wn = wave % WN;
+  const int c0 = blockIdx.x * BN;
+  const int nch = K / KC;
+  // the lane's slot in each of its load instructions and the source there
+  // (rows past M repeat row M-1, columns past the end the last column: their
+  // products land in outputs that are never stored)
+  const bf16_t *asrc[AI], *wsrc[WI];
+#pragma unroll
+  for (int j = 0; j < AI; ++j) {
+    const int q = (j * NW + wave) * 64 + lane, row = q >> 3;
+    asrc[j] = A + (size_t)min(row, M - 1) * lda + ((q & 7) ^ ((row >> 1) & 7)) * 8;
+  }
+#pragma unroll
+  for (int j = 0; j < WI; ++j) {
+    const int q = (j * NW + wave) * 64 + lane, n = q >> 3;
+    wsrc[j] = epi.wrow(min(c0 + n, epi.nvcols - 1)) + ((q & 7) ^ ((n >> 1) & 7)) * 8;
+  }
+  // chunk ch into its ring slot (past the end the last chunk is fetched again,
+  // so every wave issues the same count)
+  auto issue = [&](int ch) {
+    char *st = smem + (ch % S) * STAGE;
+    const int k = min(ch, nch - 1) * KC;
+#pragma unroll
+    for (int j = 0; j < AI; ++j) lds_dma16(asrc[j] + k, st + (j * NW + wave) * 1024);
+#pragma unroll
+    for (int j = 0; j < WI; ++j) lds_dma16(wsrc[j] + k, st + ABYTES + (j * NW + wave) * 1024);
+  };
+  f32x4 acc[RT][NTW];
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int f = 0; f < NTW; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int mrow0 = wm * 16 * RT, ncol0 = wn * NTW * 16;
+  u32x4 a0[RT], b0[NTW], a1[RT], b1[NTW];
+  auto frags = [&](const char *st, int ks, u32x4 (&af)[RT], u32x4 (&bf)[NTW]) {
+#pragma unroll
+    for (int f = 0; f < NTW; ++f)
+      bf[f] = *reinterpret_cast<const u32x4 *>(st + ABYTES + ring_slot(ncol0 + f * 16 + r, ks * 4 + g) * 16);
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+      af[i] = *reinterpret_cast<const u32x4 *>(st + ring_slot(mrow0 + i * 16 + r, ks * 4 + g) * 16);
+  };
+  auto products = [&](const u32x4 (&af)[RT], const u32x4 (&bf)[NTW]) {
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int f = 0; f < NTW; ++f) mma16<bf16_t>(acc[i][f], af[i], bf[f]);
+  };
+#pragma unroll
+  for (int st = 0; st < S; ++st) issue(st);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 1) * CNT, 15));  // chunk 0 (this wave's part)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  frags(smem, 0, a0, b0);
+  for (int ch = 0; ch < nch; ++ch) {
+    // the step-0 fragments (read during the last products) are in
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
+    __builtin_amdgcn_sched_barrier(0);
+    frags(smem + (ch % S) * STAGE, 1, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    products(a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    // chunk ch+1 landed (this wave's part) and every read of chunk ch is done;
+    // the barrier extends both to the workgroup
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 2) * CNT, 0));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(ch + S);  // into chunk ch's slot
+    if (ch + 1 < nch) frags(smem + ((ch + 1) % S) * STAGE, 0, a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    products(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // the chunks fetched past the end land before the ring becomes the tile
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+  __syncthreads();
+  float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int f = 0; f < NTW; ++f)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][ncol0 + f * 16 + r] = acc[i][f][v];
+  __syncthreads();
+  epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
+}
+
+// Launch of k_gemm_tile over ncols virtual columns and nz row blocks (of
+// kBigRows): a three-stage ring when the grid is about one workgroup per CU
+// (96 KB of LDS: one workgroup per CU), else two stages, which lets two
+// workgroups share a CU (measured at 1024 rows: fusion and input FC 120 and
+// 78 us with three stages against 134 and 86 with two; the K/V GEMM of five
+// layers 103 us with two stages against 120 with three).
+template <class Epi>
+static hipError_t launch_tile(const bf16_t *A, int lda, int M, int K, const Epi &e, int ncols, int nz,
+                              hipStream_t s) {
+  const dim3 grid((ncols + kBigCols - 1) / kBigCols, 1, nz);
+  if ((long)grid.x * nz <= 288)
+    hipLaunchKernelGGL((k_gemm_tile<3, Epi>), grid, dim3(512), 0, s, A, lda, M, K, e);
+  else
+    hipLaunchKernelGGL((k_gemm_tile<2, Epi>), grid, dim3(512), 0, s, A, lda, M, K, e);
+  return hipGetLastError();
+}
+
 // split-K slices the reductions sum (k_splitk_finish, k_resid_rows)
 constexpr int kMaxSlices = 8;
 
@@ -567,6 +712,17 @@ template <> __device__ __forceinline__ void store4<float>(float *y, const f32x4 
 template <> __device__ __forceinline__ void store4<bf16_t>(bf16_t *y, const f32x4 &v) {
   *reinterpret_cast<u32x2 *>(y) = u32x2{f2bf2(v.x, v.y), f2bf2(v.z, v.w)};
 }
+// Eight adjacent values: one 16-byte store (bf16) or two (fp32).
+template <typename T> __device__ __forceinline__ void store8(T *y, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<u32x4 *>(y) =
+        u32x4{f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7])};
+  } else {
+    *reinterpret_cast<f32x4 *>(y) = f32x4{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4 *>(y + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+}
+__device__ __forceinline__ bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
 template <typename T> __device__ __forceinline__ f32x4 load4(const T *g);
 template <> __device__ __forceinline__ f32x4 load4<float>(const float *g) {
   return *reinterpret_cast<const f32x4 *>(g);
@@ -659,10 +815,26 @@ template <typename T> struct EpiStore {
   T *gather_out;
   int ld_gather, d, B;
   __device__ const T *wrow(int c) const { return w + (size_t)c * ldw; }
+  // a thread per element when that is one round, else per (row, 8 adjacent
+  // columns) with one vector store where aligned
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
-    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
-      const int m = idx / span, c = idx % span;
-      if (c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = Elt<T>::from_f(tile[m * ldt + c]);
+    const int gpr = span >> 3;
+    if (M * span <= (int)blockDim.x) {
+      const int idx = threadIdx.x, m = idx / span, c = idx % span;
+      if (idx < M * span && c0 + c < nvcols) out[(size_t)m * ldo + c0 + c] = Elt<T>::from_f(tile[m * ldt + c]);
+    }
+    for (int idx = threadIdx.x; M * span > (int)blockDim.x && idx < M * gpr; idx += blockDim.x) {
+      const int m = idx / gpr, c = (idx % gpr) * 8;
+      T *y = out + (size_t)m * ldo + c0 + c;
+      const float *t = tile + m * ldt + c;
+      if (c0 + c + 8 <= nvcols && aligned16(y)) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = t[j];
+        store8<T>(y, v);
+      } else {
+        for (int j = 0; j < 8 && c0 + c + j < nvcols; ++j) y[j] = Elt<T>::from_f(t[j]);
+      }
     }
     if (embed) {  // the embedding row e_{t+1} of every sequence, copied next to g_t
       constexpr int E = Elt<T>::kPer16B;
@@ -835,51 +1007,61 @@ template <typename T> struct EpiKvCache {
     if (c < kvd) return (const T *)a.wk + (size_t)((c / a.D) * a.D + rope_dim(c % a.D, a.D)) * a.d;
     return (const T *)a.wv + (size_t)(c - kvd) * a.d;
   }
-  // Elements go KB at a time: every load (row destination, position, rotary
-  // factors) of the batch is issued before its stores, which the compiler
-  // could not move loads across.
-  static constexpr int KB = 8;
+  // A thread per (row, 8 adjacent virtual columns): those are 8 adjacent
+  // dimensions of one head's key (inside one rotary half, paired with the 8
+  // columns 8 away in the same 16-column tile) or of a value row, so each
+  // group is one vector store of the cache row piece.
+  // With at most one element per thread the thread takes one element.
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
     const int kvd = a.Hkv * a.D, D = a.D;
     const float qnan = __int_as_float(0x7fc00000);
-    const int n = M * span;
-    for (int i0 = threadIdx.x; i0 < n; i0 += KB * blockDim.x) {
-      int m[KB], pos[KB];
-      long dst[KB];
-#pragma unroll
-      for (int j = 0; j < KB; ++j) {
-        const int idx = min(i0 + j * (int)blockDim.x, n - 1);
-        m[j] = idx / span;
-        dst[j] = a.dst_rows[m[j]];
-        pos[j] = a.positions[m[j]];
-      }
-      float cs[KB], sn[KB];
-#pragma unroll
-      for (int j = 0; j < KB; ++j) {
-        const int idx = min(i0 + j * (int)blockDim.x, n - 1);
-        const int cc = (c0 + idx % span) % D;
-        const int pm = 8 * (cc >> 4) + (cc & 7);
-        const int pc = min(max(pos[j], 0), a.pos_limit - 1);
-        cs[j] = a.rope[((size_t)pc * (D / 2) + pm) * 2];
-        sn[j] = a.rope[((size_t)pc * (D / 2) + pm) * 2 + 1];
-      }
-#pragma unroll
-      for (int j = 0; j < KB; ++j) {
-        const int idx = i0 + j * (int)blockDim.x;
-        if (idx >= n) break;
-        const int c = idx % span, vc = c0 + c;
-        if (vc >= nvcols) continue;
-        if (dst[j] < 0 || dst[j] >= a.cache_rows) continue;  // nowhere to write
-        const bool bad = pos[j] < 0 || pos[j] >= a.pos_limit;
-        const float val = tile[m[j] * ldt + c];
+    const bool one = M * span <= (int)blockDim.x;
+    const int per = one ? 1 : 8, gpr = span / per;
+    for (int idx = threadIdx.x; idx < M * gpr; idx += blockDim.x) {
+      const int m = idx / gpr, c = (idx % gpr) * per, vc = c0 + c;
+      if (vc >= nvcols) continue;
+      const long dst = a.dst_rows[m];
+      if (dst < 0 || dst >= a.cache_rows) continue;  // nowhere to write
+      const int pos = a.positions[m];
+      const bool bad = pos < 0 || pos >= a.pos_limit;
+      const float *t = tile + m * ldt + c;
+      float o[8];
+      T *y;
+      if (one) {  // a single element
         if (vc < kvd) {
-          const int h = vc / D, cc = vc % D, dd = rope_dim(cc, D);
-          const float pv = tile[m[j] * ldt + (c ^ 8)];
-          const float o = bad ? qnan : ((cc & 8) ? (val * cs[j] + pv * sn[j]) : (val * cs[j] - pv * sn[j]));
-          ((T *)a.k_cache)[(size_t)dst[j] * kvd + (size_t)h * D + dd] = Elt<T>::from_f(o);
+          const int h = vc / D, cc = vc % D;
+          const int pc = min(max(pos, 0), a.pos_limit - 1);
+          const float *rp = a.rope + ((size_t)pc * (D / 2) + 8 * (cc >> 4) + (cc & 7)) * 2;
+          const float pv = tile[m * ldt + (c ^ 8)];
+          const float v = bad ? qnan : ((cc & 8) ? (t[0] * rp[0] + pv * rp[1]) : (t[0] * rp[0] - pv * rp[1]));
+          ((T *)a.k_cache)[(size_t)dst * kvd + (size_t)h * D + rope_dim(cc, D)] = Elt<T>::from_f(v);
         } else {
-          ((T *)a.v_cache)[(size_t)dst[j] * kvd + (vc - kvd)] = Elt<T>::from_f(bad ? qnan : val);
+          ((T *)a.v_cache)[(size_t)dst * kvd + (vc - kvd)] = Elt<T>::from_f(bad ? qnan : t[0]);
         }
+        continue;
+      }
+      if (vc < kvd) {
+        const int h = vc / D, cc = vc % D;
+        const int pc = min(max(pos, 0), a.pos_limit - 1);
+        // rotary pair index 8 (cc >> 4) + j of dims rope_dim(cc, D) + j
+        const float *rp = a.rope + ((size_t)pc * (D / 2) + 8 * (cc >> 4)) * 2;
+        const float *pt = tile + m * ldt + (c ^ 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float cs = rp[2 * j], sn = rp[2 * j + 1];
+          o[j] = bad ? qnan : ((cc & 8) ? (t[j] * cs + pt[j] * sn) : (t[j] * cs - pt[j] * sn));
+        }
+        y = (T *)a.k_cache + (size_t)dst * kvd + (size_t)h * D + rope_dim(cc, D);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = bad ? qnan : t[j];
+        y = (T *)a.v_cache + (size_t)dst * kvd + (vc - kvd);
+      }
+      if (aligned16(y)) {
+        store8<T>(y, o);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = Elt<T>::from_f(o[j]);
       }
     }
   }
@@ -924,12 +1106,21 @@ struct TileF32 {
     out += (size_t)m0 * ldo;
     if (resid) resid += (size_t)m0 * ldr;
   }
+  // a thread per (row, 4 adjacent columns): vector loads and stores where aligned
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
-    for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
-      const int m = idx / span, c = idx % span;
-      if (c0 + c < nvcols)
-        out[(size_t)m * ldo + c0 + c] =
-            tile[m * ldt + c] + (resid ? resid[(size_t)m * ldr + c0 + c] : 0.f);
+    const int gpr = span >> 2;
+    for (int idx = threadIdx.x; idx < M * gpr; idx += blockDim.x) {
+      const int m = idx / gpr, c = (idx % gpr) * 4;
+      float *y = out + (size_t)m * ldo + c0 + c;
+      const float *rr = resid ? resid + (size_t)m * ldr + c0 + c : nullptr;
+      const float *t = tile + m * ldt + c;
+      if (c0 + c + 4 <= nvcols && aligned16(y) && (!rr || aligned16(rr))) {
+        f32x4 v = f32x4{t[0], t[1], t[2], t[3]};
+        if (rr) v += *reinterpret_cast<const f32x4 *>(rr);
+        *reinterpret_cast<f32x4 *>(y) = v;
+      } else {
+        for (int j = 0; j < 4 && c0 + c + j < nvcols; ++j) y[j] = t[j] + (rr ? rr[j] : 0.f);
+      }
     }
   }
 };
@@ -987,17 +1178,36 @@ template <typename T> struct EpiSwiglu {
     const int p = c >> 5, f = (c >> 4) & 1, n = c & 15;
     return (f ? wu : wg) + (size_t)(p * 16 + n) * ldw;
   }
+  // a thread per output when that is one round, else per (row, 8 adjacent
+  // gate columns): 8 adjacent outputs, one vector store where aligned
   __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
-    const int half = span >> 1;
-    for (int idx = threadIdx.x; idx < M * half; idx += blockDim.x) {
-      const int m = idx / half, q = idx % half;
+    const int half = span >> 1, gpr = span >> 4;
+    if (M * half <= (int)blockDim.x) {
+      const int idx = threadIdx.x, m = idx / half, q = idx % half;
       const int c = (q >> 4) * 32 + (q & 15);  // gate column inside the tile
       const int vc = c0 + c;
+      if (idx < M * half && vc < nvcols) {
+        const float gt = tile[m * ldt + c], up = tile[m * ldt + c + 16];
+        const float s = gt / (1.f + expf(-gt)) * up;
+        out[(size_t)m * ldo + (vc >> 5) * 16 + (vc & 15)] = Elt<T>::from_f(s);
+      }
+      return;
+    }
+    for (int idx = threadIdx.x; idx < M * gpr; idx += blockDim.x) {
+      const int m = idx / gpr, q = (idx % gpr) * 8;
+      const int c = (q >> 4) * 32 + (q & 15);  // first gate column inside the tile
+      const int vc = c0 + c;
       if (vc >= nvcols) continue;
-      const float gt = tile[m * ldt + c], up = tile[m * ldt + c + 16];
-      const float s = gt / (1.f + expf(-gt)) * up;
-      const int col = (vc >> 5) * 16 + (vc & 15);
-      out[(size_t)m * ldo + col] = Elt<T>::from_f(s);
+      const float *t = tile + m * ldt + c;
+      float s[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s[j] = t[j] / (1.f + expf(-t[j])) * t[j + 16];
+      T *y = out + (size_t)m * ldo + (vc >> 5) * 16 + (vc & 15);
+      if (vc + 8 <= nvcols && aligned16(y)) {
+        store8<T>(y, s);
+      } else {
+        for (int j = 0; j < 8 && vc + j < nvcols; ++j) y[j] = Elt<T>::from_f(s[j]);
+      }
     }
   }
 };
@@ -1424,10 +1634,12 @@ hipError_t gemm_kvcache(int dt, const void *A, int lda, int M, const KvCacheArgs
   return run_gemm<float, 1, 8, 1>((const float *)A, lda, kDenseRows, M, a.d, e, nullptr, s, ss);
 }
 
-// Many rows at once (bf16): 128 x 64 output tiles, grid z over 128-row
+// Many rows at once (bf16): 128 x 128 output tiles of k_gemm_tile (K a
+// multiple of 64; else k_gemm_mid's 128 x 64 tiles), grid z over 128-row
 // blocks (and layers), no split of K.
 constexpr int kTileNtw = 2, kTileWn = 2, kTileStages = 3, kTileRows = 64 * (4 / kTileWn),
               kTileCols = 16 * kTileNtw * kTileWn;
+static_assert(kTileRows == kBigRows, "both tiled kernels slice 128-row blocks (TileKv's nblocks)");
 
 hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, int ncols, void *out,
                            int ldo, const void *embed, const int32_t *tokens, int vocab,
@@ -1438,6 +1650,7 @@ hipError_t gemm_store_rows(const void *A, int lda, int M, int K, const void *W, 
                                                         ldo, (const bf16_t *)embed, tokens, vocab,
                                                         (bf16_t *)gather_out, ld_gather, d, M};
   e.lda = lda;
+  if (K % 64 == 0) return launch_tile((const bf16_t *)A, lda, M, K, e, ncols, (M + kBigRows - 1) / kBigRows, s);
   const dim3 grid((ncols + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileStore>), grid, dim3(256),
                      0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
@@ -1451,6 +1664,7 @@ hipError_t gemm_swiglu_rows(const void *A, int lda, int M, int K, const void *w_
   static_cast<EpiSwiglu<bf16_t> &>(e) = EpiSwiglu<bf16_t>{(const bf16_t *)w_gate, (const bf16_t *)w_up,
                                                           K, I, 2 * I, (bf16_t *)out, ldo};
   e.lda = lda;
+  if (K % 64 == 0) return launch_tile((const bf16_t *)A, lda, M, K, e, 2 * I, (M + kBigRows - 1) / kBigRows, s);
   const dim3 grid((2 * I + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileSwiglu>), grid,
                      dim3(256), 0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
@@ -1463,6 +1677,7 @@ hipError_t gemm_resid_rows(const void *A, int lda, int M, int K, const void *W, 
   TileF32 e{(const bf16_t *)W, K, ncols, out, ldo, lda};
   e.resid = resid;
   e.ldr = ldr;
+  if (K % 64 == 0) return launch_tile((const bf16_t *)A, lda, M, K, e, ncols, (M + kBigRows - 1) / kBigRows, s);
   const dim3 grid((ncols + kTileCols - 1) / kTileCols, 1, (M + kTileRows - 1) / kTileRows);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileF32>), grid, dim3(256),
                      0, s, (const bf16_t *)A, lda, kDenseRows, M, K, e, nullptr, 0);
@@ -1503,6 +1718,8 @@ hipError_t gemm_kv_rows(const void *A, int lda, long a_layer_stride, int M, int 
                        (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, e, nullptr, 0);
     return hipGetLastError();
   }
+  if (layers[0].d % 64 == 0)
+    return launch_tile((const bf16_t *)A, lda, M, layers[0].d, e, e.nvcols, e.g.nblocks * nlayers, s);
   const dim3 grid((e.nvcols + kTileCols - 1) / kTileCols, 1, e.g.nblocks * nlayers);
   hipLaunchKernelGGL((k_gemm_mid<bf16_t, kTileNtw, kTileWn, kTileStages, TileKv>), grid, dim3(256), 0,
                      s, (const bf16_t *)A, lda, kDenseRows, M, layers[0].d, e, nullptr, 0);

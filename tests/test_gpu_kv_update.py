@@ -145,6 +145,17 @@ def test_kv_update_full_size_sampled():
     _run(cfg, up, 1024, sample=sample)
 
 
+def test_kv_update_full_size_prefill_tiled():
+    """The 8B shapes over 1000 positions in one chunk: the 2-D tiled GEMMs at
+    their full K (12288, 8192, 4096) with a ragged last row block, sampled
+    rows (every row block, both ends of the ragged one) through the oracle."""
+    cfg = C.LLAMA8B_BF16_B1
+    acc = np.array([1000], np.int32)
+    up = make_update_rows(cfg, acc, np.array([20], np.int32), capacity=1024, seed=8)
+    sample = [0, 1, 127, 128, 383, 640, 895, 896, 999]
+    _run(cfg, up, 1024, sample=sample)
+
+
 def test_kv_update_full_size_b1_cycle():
     """The 8B shapes at batch 1: the N+1 = 6 positions one cycle accepts at
     most, every row through the oracle (the fused-norm path)."""
