@@ -546,27 +546,44 @@ __device__ __forceinline__ constexpr int waitcnt_imm(int vm, int lgkm) {
 
 constexpr int kBigRows = 128, kBigCols = 128;
 
-template <int S, class Epi>
-__global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A, int lda, int M, int K,
-                                                   Epi epi) {
-  constexpr int RT = 4, NTW = 2, WN = 4, NW = 8;
-  constexpr int BM = kBigRows, BN = kBigCols, KC = 64;
+// SPLIT: K is split over grid y and each slice's fp32 sums go to splitp
+// (slice y at y * M * ldp, row m at m * ldp) for a second launch that sums them
+// and runs the epilogue; the row blocks of grid z then cover rows
+// arows.row(m) of A directly (no epilogue slicing).
+// RT x NTW 16 x 16 tiles per wave, WM x WN waves (eight): the cache update's
+// 128 x 128 tiles are 4, 2, 2, 4; the 256 x 128 tiles of up to 256 rows (one
+// row block, so the weights are streamed once) are 4, 4, 4, 2.
+template <int RT, int NTW, int WM, int WN, int S, class Epi, bool SPLIT = false>
+__global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A, int lda, ARows arows,
+                                                   int M, int K, Epi epi, float *__restrict__ splitp,
+                                                   int ldp) {
+  constexpr int NW = WM * WN;
+  static_assert(NW == 8, "eight waves");
+  constexpr int BM = 16 * RT * WM, BN = 16 * NTW * WN, KC = 64;
   constexpr int ABYTES = BM * 128, STAGE = ABYTES + BN * 128;
   constexpr int AI = BM / 8 / NW, WI = BN / 8 / NW, CNT = AI + WI;  // 1 KB loads per wave per chunk
   static_assert(S >= 2 && (S - 1) * CNT <= 63, "vmcnt range");
   constexpr int LDT = BN + 1, TILE = BM * LDT * 4;
   constexpr int SMEM = S * STAGE > TILE ? S * STAGE : TILE;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  {
+  int m0 = 0, Mb = M;  // first row of this block, rows in it
+  if constexpr (SPLIT) {
+    m0 = blockIdx.z * BM;
+    Mb = min(BM, M - m0);
+  } else if constexpr (SlicedEpi<Epi>::value) {
     const bf16_t *a = A;
     epi.slice(blockIdx.z, BM, a, M);
     A = a;
-    if (M <= 0) return;  // the whole workgroup: past the last row block
-  }
+    Mb = M;
+  }  // else one row block of at most BM rows
+  if (Mb <= 0) return;  // the whole workgroup: past the last row block
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
   const int wm = wave / WN, wn = wave % WN;
   const int c0 = blockIdx.x * BN;
-  const int nch = K / KC;
+  // this workgroup's chunks of K: [cb, cb + nch)
+  const int nchk = K / KC;
+  const int cb = SPLIT ? (int)((long)nchk * blockIdx.y / gridDim.y) : 0;
+  const int nch = SPLIT ? (int)((long)nchk * (blockIdx.y + 1) / gridDim.y) - cb : nchk;
   // the lane's slot in each of its load instructions and the source there
   // (rows past M repeat row M-1, columns past the end the last column: their
   // products land in outputs that are never stored)
@@ -574,7 +591,7 @@ __global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A,
 #pragma unroll
   for (int j = 0; j < AI; ++j) {
     const int q = (j * NW + wave) * 64 + lane, row = q >> 3;
-    asrc[j] = A + (size_t)min(row, M - 1) * lda + ((q & 7) ^ ((row >> 1) & 7)) * 8;
+    asrc[j] = A + (size_t)arows.row(m0 + min(row, Mb - 1)) * lda + ((q & 7) ^ ((row >> 1) & 7)) * 8;
   }
 #pragma unroll
   for (int j = 0; j < WI; ++j) {
@@ -585,7 +602,7 @@ __global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A,
   // so every wave issues the same count)
   auto issue = [&](int ch) {
     char *st = smem + (ch % S) * STAGE;
-    const int k = min(ch, nch - 1) * KC;
+    const int k = (cb + min(ch, nch - 1)) * KC;
 #pragma unroll
     for (int j = 0; j < AI; ++j) lds_dma16(asrc[j] + k, st + (j * NW + wave) * 1024);
 #pragma unroll
@@ -639,6 +656,19 @@ __global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A,
   }
   // the chunks fetched past the end land before the ring becomes the tile
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+  if constexpr (SPLIT) {
+    float *dst = splitp + ((size_t)blockIdx.y * M + m0) * ldp + c0;
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int f = 0; f < NTW; ++f)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int m = mrow0 + i * 16 + 4 * g + v;
+          if (m < Mb) dst[(size_t)m * ldp + ncol0 + f * 16 + r] = acc[i][f][v];
+        }
+    return;
+  }
   __syncthreads();
   float(*tile)[LDT] = reinterpret_cast<float(*)[LDT]>(smem);
 #pragma unroll
@@ -648,7 +678,7 @@ __global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A,
 #pragma unroll
       for (int v = 0; v < 4; ++v) tile[mrow0 + i * 16 + 4 * g + v][ncol0 + f * 16 + r] = acc[i][f][v];
   __syncthreads();
-  epi.finish(&tile[0][0], LDT, M, c0, BN, typename Epi::Pre{});
+  epi.finish(&tile[0][0], LDT, Mb, c0, BN, typename Epi::Pre{});
 }
 
 // Launch of k_gemm_tile over ncols virtual columns and nz row blocks (of
@@ -662,9 +692,11 @@ static hipError_t launch_tile(const bf16_t *A, int lda, int M, int K, const Epi 
                               hipStream_t s) {
   const dim3 grid((ncols + kBigCols - 1) / kBigCols, 1, nz);
   if ((long)grid.x * nz <= 288)
-    hipLaunchKernelGGL((k_gemm_tile<3, Epi>), grid, dim3(512), 0, s, A, lda, M, K, e);
+    hipLaunchKernelGGL((k_gemm_tile<4, 2, 2, 4, 3, Epi>), grid, dim3(512), 0, s, A, lda, kDenseRows, M,
+                       K, e, nullptr, 0);
   else
-    hipLaunchKernelGGL((k_gemm_tile<2, Epi>), grid, dim3(512), 0, s, A, lda, M, K, e);
+    hipLaunchKernelGGL((k_gemm_tile<4, 2, 2, 4, 2, Epi>), grid, dim3(512), 0, s, A, lda, kDenseRows, M,
+                       K, e, nullptr, 0);
   return hipGetLastError();
 }
 
@@ -1287,6 +1319,7 @@ template <typename T> struct EpiLm {
       }
       se += expf(xt - mx);
       if (a.logits) a.logits[(size_t)m * nvcols + c0 + c] = x;
+      if (!(vs[KL - 1] < key)) continue;  // not in the list: nothing below would change
 #pragma unroll
       for (int j = KL - 1; j >= 1; --j) {
         const bool prev = vs[j - 1] < key, here = vs[j] < key;
@@ -1485,6 +1518,32 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
   // batched rows: all M rows per workgroup, columns split over the grid; the
   // waves split columns as well when the rows do not fill four row groups
   if (M > 256) return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 2 && Epi::kSplitK) {
+    // More than 128 rows (bf16, K a multiple of 64), when the epilogue can
+    // follow a split-K reduction: k_gemm_tile's 256 x 128 tiles (all rows in
+    // one block, so the weights are streamed once), K split so that the grid
+    // is about one workgroup per CU (k_gemm_mid has only one column wave
+    // here); the slices are summed, in a fixed order, by the finish launch.
+    if (M > 128 && K % 64 == 0 && ss != nullptr && ss->p != nullptr) {
+      const int gx = (epi.nvcols + 127) / 128;
+      int ksb = (288 + gx - 1) / gx;
+      ksb = min(ksb, kMaxSlices);
+      ksb = max(1, min(ksb, (K / 64) / 8));  // at least 8 chunks of K per slice
+      const int ldpb = gx * 128;
+      if ((size_t)ksb * M * ldpb <= ss->floats) {
+        hipLaunchKernelGGL((k_gemm_tile<4, 4, 4, 2, 3, Epi, true>), dim3(gx, ksb, 1), dim3(512), 0, s, A,
+                           lda, arows, M, K, epi, ss->p, ldpb);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess || so) {  // the caller sums the slices
+          if (so) *so = SplitOut{ss->p, ldpb, ksb};
+          return e;
+        }
+        hipLaunchKernelGGL((k_splitk_finish<Epi>), dim3((epi.nvcols + 15) / 16), dim3(256), 0, s,
+                           (const float *)ss->p, ldpb, ksb, M, epi);
+        return hipGetLastError();
+      }
+    }
+  }
   const int wn = M <= 64 ? 4 : (M <= 128 ? 2 : 1);
   int tt = Epi::kMidNtw;  // 16-column tiles per workgroup
   if (tt == 0) {
@@ -1747,6 +1806,17 @@ int lmhead_tiles(int V) { return (V + kLmWN * kLmNT * 16 - 1) / (kLmWN * kLmNT *
 hipError_t gemm_lmhead(int dt, const void *A, int lda, const ARows &arows, int M, int K,
                        const LmArgs &a, const NormA *na, int *nwg_out, hipStream_t s) {
   *nwg_out = lmhead_tiles(a.V);
+  if (dt && !na && M > 128 && M <= 256 && K % 64 == 0) {
+    // many rows (batched drafting, B x N of them): every row in one 256 x 128
+    // tile of k_gemm_tile, so the head is streamed once; 128-column tiles
+    // (half as many as lmhead_tiles counts)
+    EpiLm<bf16_t> e{a, K, a.V};
+    const int gx = (a.V + 127) / 128;
+    *nwg_out = gx;
+    hipLaunchKernelGGL((k_gemm_tile<4, 4, 4, 2, 3, EpiLm<bf16_t>>), dim3(gx), dim3(512), 0, s,
+                       (const bf16_t *)A, lda, arows, M, K, e, nullptr, 0);
+    return hipGetLastError();
+  }
   if (dt) {
     EpiLm<bf16_t> e{a, K, a.V};
     return run_gemm<bf16_t, kLmNT, 1, kLmWN>((const bf16_t *)A, lda, arows, M, K, e, na, s);
