@@ -833,7 +833,7 @@ struct NoPre {
   bool ok = false;
 };
 template <typename T> struct EpiStore {
-  static constexpr bool kRowStream = true, kSplitK = true;
+  static constexpr bool kRowStream = true, kSplitK = true, kQkv = false;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
@@ -886,7 +886,7 @@ template <typename T> struct EpiStore {
 };
 
 template <typename T> struct EpiResid {
-  static constexpr bool kRowStream = true, kSplitK = true;
+  static constexpr bool kRowStream = true, kSplitK = true, kQkv = false;
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
   const T *w;
   int ldw, nvcols;
@@ -961,7 +961,7 @@ __device__ __forceinline__ int rope_dim(int cc, int D) {
 }
 
 template <typename T> struct EpiQkv {
-  static constexpr bool kRowStream = true, kSplitK = true;
+  static constexpr bool kRowStream = true, kSplitK = true, kQkv = true;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
@@ -1028,7 +1028,7 @@ template <typename T> struct EpiQkv {
 // the value rows; row m is rotated at positions[m] and stored in the storage
 // type at cache row dst_rows[m].
 template <typename T> struct EpiKvCache {
-  static constexpr bool kRowStream = true, kSplitK = true;
+  static constexpr bool kRowStream = true, kSplitK = true, kQkv = false;
   using Pre = NoPre;
   __device__ Pre prefetch(int, int, int) const { return {}; }
   static constexpr int kMidNtw = 0, kMidNtwMin = 1;
@@ -1466,6 +1466,12 @@ struct SplitOut {
   int ldp = 0, ks = 0;
 };
 
+// batched rows above this go to k_gemm_tile's split-K path when the epilogue
+// allows (measured at batch 32: the Q/K/V GEMM from 32 rows, 15.7 us against
+// 18.4 on k_gemm_mid; the 32-row residual GEMMs stay on k_gemm_mid, whose
+// half-height tiles were 8 % faster there)
+constexpr int kTileSplitMinRows = 32, kTileSplitMinRowsQkv = 16;
+
 // split-K slices of the narrow batched-rows GEMMs (at most 128 rows): up to
 // kSliceCap32 slices, about kSliceWgs workgroups
 constexpr int kSliceCap32 = 8, kSliceWgs = 256;
@@ -1519,20 +1525,28 @@ static hipError_t run_gemm(const T *A, int lda, const ARows &arows, int M, int K
   // waves split columns as well when the rows do not fill four row groups
   if (M > 256) return hipErrorInvalidValue;
   if constexpr (sizeof(T) == 2 && Epi::kSplitK) {
-    // More than 128 rows (bf16, K a multiple of 64), when the epilogue can
-    // follow a split-K reduction: k_gemm_tile's 256 x 128 tiles (all rows in
-    // one block, so the weights are streamed once), K split so that the grid
+    // More than 32 rows (bf16, K a multiple of 64), when the epilogue can
+    // follow a split-K reduction: k_gemm_tile's 256 x 128 tiles (128 x 128 up
+    // to 128 rows; all rows in one block, so the weights are streamed once), K split so that the grid
     // is about one workgroup per CU (k_gemm_mid has only one column wave
     // here); the slices are summed, in a fixed order, by the finish launch.
-    if (M > 128 && K % 64 == 0 && ss != nullptr && ss->p != nullptr) {
+    // The Q/K/V GEMM (6144 columns) aims at fewer slices: six cost more to
+    // write and sum than they save (layers of 160-224 rows at batch 32: 33.5
+    // us per launch with six, 25.3 with four, 30.3 on k_gemm_mid).
+    if (M > (Epi::kQkv ? kTileSplitMinRowsQkv : kTileSplitMinRows) && K % 64 == 0 && ss != nullptr &&
+        ss->p != nullptr) {
       const int gx = (epi.nvcols + 127) / 128;
-      int ksb = (288 + gx - 1) / gx;
+      int ksb = ((Epi::kQkv ? 192 : 288) + gx - 1) / gx;
       ksb = min(ksb, kMaxSlices);
       ksb = max(1, min(ksb, (K / 64) / 8));  // at least 8 chunks of K per slice
       const int ldpb = gx * 128;
       if ((size_t)ksb * M * ldpb <= ss->floats) {
-        hipLaunchKernelGGL((k_gemm_tile<4, 4, 4, 2, 3, Epi, true>), dim3(gx, ksb, 1), dim3(512), 0, s, A,
-                           lda, arows, M, K, epi, ss->p, ldpb);
+        if (M > 128)
+          hipLaunchKernelGGL((k_gemm_tile<4, 4, 4, 2, 3, Epi, true>), dim3(gx, ksb, 1), dim3(512), 0, s,
+                             A, lda, arows, M, K, epi, ss->p, ldpb);
+        else  // 128 x 128 tiles
+          hipLaunchKernelGGL((k_gemm_tile<4, 2, 2, 4, 3, Epi, true>), dim3(gx, ksb, 1), dim3(512), 0, s,
+                             A, lda, arows, M, K, epi, ss->p, ldpb);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess || so) {  // the caller sums the slices
           if (so) *so = SplitOut{ss->p, ldpb, ksb};
