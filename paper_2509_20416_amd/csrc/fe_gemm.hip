@@ -716,6 +716,8 @@ __global__ __launch_bounds__(256) void k_splitk_finish(const float *__restrict__
   const size_t slice = (size_t)M * ldp;
   for (int q = threadIdx.x; q < M * (BNR / 4); q += 256) {
     const int m = q / (BNR / 4), c = (q % (BNR / 4)) * 4;
+    if constexpr (Epi::kQkv)
+      if (!epi.row_used(m, c0)) continue;  // the epilogue never reads this row here
     const float *src = splitp + (size_t)m * ldp + c0 + c;
     f32x4 part[kMaxSlices];
 #pragma unroll
@@ -984,7 +986,15 @@ template <typename T> struct EpiQkv {
     }
     return base + (size_t)row * a.d;
   }
-  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &) const {
+  // only the last context row of a sequence carries a query
+  __device__ bool row_used(int m, int c0) const {
+    return c0 >= a.Hq * a.D || m % a.nctx == a.nctx - 1;
+  }
+  __device__ void finish(float *tile, int ldt, int M, int c0, int span, const Pre &p) const {
+    if (M * span > (int)blockDim.x) {
+      finish8(tile, ldt, M, c0, span);
+      return;
+    }
     const int qd = a.Hq * a.D, kvd = a.Hkv * a.D, D = a.D;
     for (int idx = threadIdx.x; idx < M * span; idx += blockDim.x) {
       const int m = idx / span, c = idx % span;
@@ -1018,6 +1028,54 @@ template <typename T> struct EpiQkv {
       } else {
         vc -= qd + kvd;
         a.v_out[((size_t)b * a.nctx + t) * kvd + vc] = val;
+      }
+    }
+  }
+  // Many rows: a thread per (row, 8 adjacent virtual columns), which are 8
+  // adjacent dimensions of one head's query or key (one rotary half, paired
+  // with the 8 columns 8 away in the same 16-column tile) or of a value row.
+  __device__ void finish8(const float *tile, int ldt, int M, int c0, int span) const {
+    const int qd = a.Hq * a.D, kvd = a.Hkv * a.D, D = a.D;
+    const int gpr = span >> 3;
+    for (int idx = threadIdx.x; idx < M * gpr; idx += blockDim.x) {
+      const int m = idx / gpr, c = (idx % gpr) * 8, vc = c0 + c;
+      if (vc >= nvcols) continue;
+      const int b = m / a.nctx, t = m % a.nctx;
+      const float *tv = tile + m * ldt + c;
+      float o[8];
+      float *y;
+      if (vc < qd + kvd) {
+        const bool isq = vc < qd;
+        if (isq && t != a.nctx - 1) continue;
+        const int lc = isq ? vc : vc - qd;
+        const int h = lc / D, cc = lc % D;
+        if (!a.rotate) {  // attention rotates
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = tv[e];
+        } else {
+          const float *pt = tile + m * ldt + (c ^ 8);
+          const int P = a.seqs.end(b) - a.seqs.start(b);
+          const int pos = min(a.cascade ? P + a.j0 + t : P, a.rope_npos - 1);
+          // rotary pair index 8 (cc >> 4) + e of dims rope_dim(cc, D) + e
+          const float *rp = a.rope + ((size_t)pos * (D / 2) + 8 * (cc >> 4)) * 2;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float cs = rp[2 * e], sn = rp[2 * e + 1];
+            o[e] = (cc & 8) ? (tv[e] * cs + pt[e] * sn) : (tv[e] * cs - pt[e] * sn);
+          }
+        }
+        y = isq ? a.q_out + ((size_t)b * a.Hq + h) * D + rope_dim(cc, D)
+                : a.k_out + (((size_t)b * a.nctx + t) * a.Hkv + h) * D + rope_dim(cc, D);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = tv[e];
+        y = a.v_out + ((size_t)b * a.nctx + t) * kvd + (vc - qd - kvd);
+      }
+      if (aligned16(y)) {
+        store8<float>(y, o);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = o[e];
       }
     }
   }
