@@ -176,7 +176,17 @@ def test_attention_split_parity(cfg, split):
                                  C.SMALL_GQA_BF16.with_(batch=20, cascade_ctx="parallel",
                                                         name="small_gqa_bf16_b20_parallel"),
                                  C.SMALL_GQA_BF16.with_(batch=20, cascade_ctx="self",
-                                                        name="small_gqa_bf16_b20_self")],
+                                                        name="small_gqa_bf16_b20_self"),
+                                 # more than 128 LM-head rows (48 x 3, 60 x 4): every row in
+                                 # one 256-row tile per 128 columns (a ragged last column tile
+                                 # at V = 1040); Q/K/V over 48..240 rows and the fusion and
+                                 # residual GEMMs over more than 32 rows as split-K slices of
+                                 # the eight-wave tiles; K = 1376 (not a multiple of 64) keeps
+                                 # the down projection on the ring GEMM
+                                 C.SMALL_GQA_BF16.with_(batch=48, prefix=(0, 300),
+                                                        name="small_gqa_bf16_b48"),
+                                 C.SMALL_MHA_BF16_D128.with_(batch=60, prefix=(1, 200),
+                                                             name="small_mha_bf16_d128_b60")],
                          ids=lambda c: c.name)
 def test_batched_rows_parity(cfg):
     _run(cfg, seed=5)

@@ -118,6 +118,8 @@ SAMPLED = [
     (C.TINY_F32_B1, 1.0, None),
     # more than 16 LM-head rows: the per-row candidate scan
     (C.SMALL_GQA_F32.with_(batch=12, name="small_gqa_f32_b12"), 1.0, 8),
+    # more than 128 bf16 LM-head rows: the 256-row tiles' epilogue
+    (C.SMALL_GQA_BF16.with_(batch=48, prefix=(0, 300), name="small_gqa_bf16_b48"), 1.0, 8),
 ]
 
 
@@ -190,6 +192,7 @@ SEEDED = [
     (C.SMALL_GQA_F32, 1.0, None),
     (C.SMALL_GQA_BF16, 1.0, None),
     (C.SMALL_GQA_F32.with_(batch=12, name="small_gqa_f32_b12"), 0.8, 8),
+    (C.SMALL_GQA_BF16.with_(batch=48, prefix=(0, 300), name="small_gqa_bf16_b48"), 1.0, 8),
 ]
 
 
