@@ -537,8 +537,9 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const T *__restrict__ A, int l
 // compiler-visible s_waitcnt immediates and the phases are fenced with
 // scheduling barriers: with inline-asm waits the compiler hoisted the barrier
 // (and its lgkmcnt(0)) above the products, serialising LDS latency.  At 1024
-// rows (8B shapes) this runs the fusion GEMM at 34 %, the K/V GEMM of all
-// layers at 33 % of the bf16 peak, against 24 % for k_gemm_mid's tiles.
+// rows (8B shapes, epilogues included) the fusion GEMM runs at 33 %, the
+// input FC at 34 % and the K/V GEMM of all five layers at 24 % of the bf16
+// peak, against 20-29 % for k_gemm_mid's 128 x 64 tiles.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ constexpr int waitcnt_imm(int vm, int lgkm) {
   return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (lgkm << 8);
