@@ -376,7 +376,7 @@ def time_second(name, seed, steps, warmup):
                                         seed=seed + 1)).to(dr.device)
     so = torch.tensor([seed + 1, 0], dtype=torch.int64, device=dr.device)
     samp = {}
-    for name, kw in (("uniforms_array", dict(uniforms=ud)), ("seeded", dict(seed_offset=so))):
+    for source, kw in (("uniforms_array", dict(uniforms=ud)), ("seeded", dict(seed_offset=so))):
         dr.forward(di, out=out, tree=tree, temperature=1.0, **kw)
         torch.cuda.synchronize()
         ev0.record(stream)
@@ -384,7 +384,7 @@ def time_second(name, seed, steps, warmup):
             dr.forward(di, out=out, tree=tree, temperature=1.0, **kw)
         ev1.record(stream)
         torch.cuda.synchronize()
-        samp[name + "_us_per_pass"] = ev0.elapsed_time(ev1) / steps * 1000.0
+        samp[source + "_us_per_pass"] = ev0.elapsed_time(ev1) / steps * 1000.0
     samp["uniform_bytes"] = cfg.batch * cfg.n_layers * cfg.draft_vocab * 4
     # NEXT-1 for this batch: every sequence appends N+1 verified positions
     # (the most one cycle accepts) after its prefix
