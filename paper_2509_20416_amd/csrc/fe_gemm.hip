@@ -24,10 +24,12 @@
 //    Q/K tiles pair rotary halves (dims m and m + D/2) inside one 16-column
 //    tile; gate/up tiles pair gate row c with up row c.
 #include "fe_internal.h"
+#include <type_traits>
 
 namespace fe {
 
 template <typename T> __device__ __forceinline__ void mma16(f32x4 &acc, u32x4 a, u32x4 b);
+template <typename T> struct EpiLm;
 
 template <> __device__ __forceinline__ void mma16<uint16_t>(f32x4 &acc, u32x4 a, u32x4 b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
@@ -564,7 +566,11 @@ __global__ __launch_bounds__(512) void k_gemm_tile(const bf16_t *__restrict__ A,
   constexpr int ABYTES = BM * 128, STAGE = ABYTES + BN * 128;
   constexpr int AI = BM / 8 / NW, WI = BN / 8 / NW, CNT = AI + WI;  // 1 KB loads per wave per chunk
   static_assert(S >= 2 && (S - 1) * CNT <= 63, "vmcnt range");
-  constexpr int LDT = BN + 1, TILE = BM * LDT * 4;
+  // epilogue tile rows 4 floats longer than the span: 16-byte aligned for
+  // the epilogues' vector reads, and the accumulator writes (4 rows x 16
+  // columns per instruction) land on distinct banks; one float longer for
+  // the LM head's scan (a thread per row: consecutive rows on distinct banks)
+  constexpr int LDT = BN + (std::is_same<Epi, EpiLm<bf16_t>>::value ? 1 : 4), TILE = BM * LDT * 4;
   constexpr int SMEM = S * STAGE > TILE ? S * STAGE : TILE;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   int m0 = 0, Mb = M;  // first row of this block, rows in it
@@ -758,6 +764,19 @@ template <typename T> __device__ __forceinline__ void store8(T *y, const float (
   }
 }
 __device__ __forceinline__ bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+// Eight adjacent floats of an epilogue tile row: two 16-byte LDS reads when
+// the tile's row stride is a multiple of 4 floats (the caller's column is a
+// multiple of 8), else eight scalar reads.
+__device__ __forceinline__ void tile8(const float *t, int ldt, float (&v)[8]) {
+  if ((ldt & 3) == 0) {
+    const f32x4 a = *reinterpret_cast<const f32x4 *>(t), b = *reinterpret_cast<const f32x4 *>(t + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = t[j];
+  }
+}
 template <typename T> __device__ __forceinline__ f32x4 load4(const T *g);
 template <> __device__ __forceinline__ f32x4 load4<float>(const float *g) {
   return *reinterpret_cast<const f32x4 *>(g);
@@ -864,8 +883,7 @@ template <typename T> struct EpiStore {
       const float *t = tile + m * ldt + c;
       if (c0 + c + 8 <= nvcols && aligned16(y)) {
         float v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = t[j];
+        tile8(t, ldt, v);
         store8<T>(y, v);
       } else {
         for (int j = 0; j < 8 && c0 + c + j < nvcols; ++j) y[j] = Elt<T>::from_f(t[j]);
@@ -1136,16 +1154,19 @@ template <typename T> struct EpiKvCache {
         const int pc = min(max(pos, 0), a.pos_limit - 1);
         // rotary pair index 8 (cc >> 4) + j of dims rope_dim(cc, D) + j
         const float *rp = a.rope + ((size_t)pc * (D / 2) + 8 * (cc >> 4)) * 2;
-        const float *pt = tile + m * ldt + (c ^ 8);
+        float tv[8], pv[8];
+        tile8(t, ldt, tv);
+        tile8(tile + m * ldt + (c ^ 8), ldt, pv);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float cs = rp[2 * j], sn = rp[2 * j + 1];
-          o[j] = bad ? qnan : ((cc & 8) ? (t[j] * cs + pt[j] * sn) : (t[j] * cs - pt[j] * sn));
+          o[j] = bad ? qnan : ((cc & 8) ? (tv[j] * cs + pv[j] * sn) : (tv[j] * cs - pv[j] * sn));
         }
         y = (T *)a.k_cache + (size_t)dst * kvd + (size_t)h * D + rope_dim(cc, D);
       } else {
+        tile8(t, ldt, o);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) o[j] = bad ? qnan : t[j];
+        for (int j = 0; j < 8; ++j) o[j] = bad ? qnan : o[j];
         y = (T *)a.v_cache + (size_t)dst * kvd + (vc - kvd);
       }
       if (aligned16(y)) {
@@ -1206,7 +1227,7 @@ struct TileF32 {
       const float *rr = resid ? resid + (size_t)m * ldr + c0 + c : nullptr;
       const float *t = tile + m * ldt + c;
       if (c0 + c + 4 <= nvcols && aligned16(y) && (!rr || aligned16(rr))) {
-        f32x4 v = f32x4{t[0], t[1], t[2], t[3]};
+        f32x4 v = (ldt & 3) == 0 ? *reinterpret_cast<const f32x4 *>(t) : f32x4{t[0], t[1], t[2], t[3]};
         if (rr) v += *reinterpret_cast<const f32x4 *>(rr);
         *reinterpret_cast<f32x4 *>(y) = v;
       } else {
@@ -1290,9 +1311,11 @@ template <typename T> struct EpiSwiglu {
       const int vc = c0 + c;
       if (vc >= nvcols) continue;
       const float *t = tile + m * ldt + c;
-      float s[8];
+      float gt[8], up[8], s[8];
+      tile8(t, ldt, gt);
+      tile8(t + 16, ldt, up);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) s[j] = t[j] / (1.f + expf(-t[j])) * t[j + 16];
+      for (int j = 0; j < 8; ++j) s[j] = gt[j] / (1.f + expf(-gt[j])) * up[j];
       T *y = out + (size_t)m * ldo + (vc >> 5) * 16 + (vc & 15);
       if (vc + 8 <= nvcols && aligned16(y)) {
         store8<T>(y, s);

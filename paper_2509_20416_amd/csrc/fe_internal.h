@@ -400,6 +400,16 @@ hipError_t gemm_lmhead(int dt, const void *A, int lda, const ARows &arows, int M
                        const LmArgs &a, const NormA *na, int *nwg_out, hipStream_t s);
 int lmhead_tiles(int V);
 
+// The same RMS of each dense fp32 row x (rows r at X + r * d) under several
+// gains: copy q = gamma[q] * x / rms(x) at out[q] + r * d, storage type.
+struct RmsCopies {
+  int n;
+  const void *gamma[kMaxLayers];
+  void *out[kMaxLayers];
+};
+hipError_t rmsnorm_copies(int dt, const float *X, int rows, const RmsCopies &c, int d, float eps,
+                          hipStream_t s);
+
 // RMSNorm of rows r < rows: source row = X + (r / per)*outer + (j0 + r % per)*inner.
 hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long outer,
                         long inner, const void *gamma, void *out, int d, float eps,

@@ -44,10 +44,12 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float *__restrict__ X, in
   for (int u = 0; u < NV; ++u) {
     const int e = 4 * (tid + 256 * u);
     if (e < d) {
-      y[e] = Elt<T>::from_f(gv[u][0] * (xv[u].x * inv));
-      y[e + 1] = Elt<T>::from_f(gv[u][1] * (xv[u].y * inv));
-      y[e + 2] = Elt<T>::from_f(gv[u][2] * (xv[u].z * inv));
-      y[e + 3] = Elt<T>::from_f(gv[u][3] * (xv[u].w * inv));
+      const float v0 = gv[u][0] * (xv[u].x * inv), v1 = gv[u][1] * (xv[u].y * inv);
+      const float v2 = gv[u][2] * (xv[u].z * inv), v3 = gv[u][3] * (xv[u].w * inv);
+      if constexpr (sizeof(T) == 2)  // four values in one 8-byte store
+        *reinterpret_cast<u32x2 *>(y + e) = u32x2{f2bf2(v0, v1), f2bf2(v2, v3)};
+      else
+        *reinterpret_cast<f32x4 *>(y + e) = f32x4{v0, v1, v2, v3};
     }
   }
 }
@@ -63,6 +65,63 @@ static void launch_rmsnorm(const float *X, int rows, int per, int j0, long outer
   else if (d <= 4096) FE_RMS(4);
   else FE_RMS(8);
 #undef FE_RMS
+}
+
+// One RMS per row, several gains: copy q of row r is gamma_q * x / rms(x) at
+// out_q + r * d (the cache update's per-layer K/V operands from one x_0).
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void k_rmsnorm_copies(const float *__restrict__ X, RmsCopies c,
+                                                        int d, float eps) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const float *x = X + (long)r * d;
+  f32x4 xv[NV];
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int e = 4 * (tid + 256 * u);
+    xv[u] = e < d ? *reinterpret_cast<const f32x4 *>(x + e) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u) ss += xv[u].x * xv[u].x + xv[u].y * xv[u].y + xv[u].z * xv[u].z + xv[u].w * xv[u].w;
+  ss = group_sum<64>(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int e = 4 * (tid + 256 * u);
+    if (e >= d) continue;
+    for (int q = 0; q < c.n; ++q) {
+      const T *g = (const T *)c.gamma[q];
+      T *y = (T *)c.out[q] + (long)r * d + e;
+      float v[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = Elt<T>::to_f(g[e + k]) * (xv[u][k] * inv);
+      if constexpr (sizeof(T) == 2)  // four values in one 8-byte store
+        *reinterpret_cast<u32x2 *>(y) = u32x2{f2bf2(v[0], v[1]), f2bf2(v[2], v[3])};
+      else
+        *reinterpret_cast<f32x4 *>(y) = f32x4{v[0], v[1], v[2], v[3]};
+    }
+  }
+}
+
+hipError_t rmsnorm_copies(int dt, const float *X, int rows, const RmsCopies &c, int d, float eps,
+                          hipStream_t s) {
+  if (rows <= 0 || c.n <= 0) return hipSuccess;
+  if (d > 8192 || d % 4 || c.n > kMaxLayers) return hipErrorInvalidValue;
+#define FE_RMSC(TV, NVV) \
+  hipLaunchKernelGGL((k_rmsnorm_copies<TV, NVV>), dim3(rows), dim3(256), 0, s, X, c, d, eps)
+#define FE_RMSC_T(TV)                \
+  if (d <= 1024) FE_RMSC(TV, 1);     \
+  else if (d <= 2048) FE_RMSC(TV, 2); \
+  else if (d <= 4096) FE_RMSC(TV, 4); \
+  else FE_RMSC(TV, 8)
+  if (dt) { FE_RMSC_T(bf16_t); } else { FE_RMSC_T(float); }
+#undef FE_RMSC_T
+#undef FE_RMSC
+  return hipGetLastError();
 }
 
 hipError_t rmsnorm_rows(int dt, const float *X, int rows, int per, int j0, long outer, long inner,

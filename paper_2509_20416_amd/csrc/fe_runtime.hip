@@ -1314,9 +1314,14 @@ fe_status kv_update_impl(fe_drafter *h, int32_t n_rows, const void *features,
       continue;
     }
     if (dt) {
-      for (int l = 0; l < c.n_layers; ++l)
-        FE_TRY(rmsnorm_rows(dt, X, Mc, 1, 0, d, 0, h->layers[l].attn_norm,
-                            an + (size_t)l * C * d * es, d, c.rms_eps, s));
+      // every layer's normalised rows from one RMS per row (one launch)
+      RmsCopies rc{};
+      rc.n = c.n_layers;
+      for (int l = 0; l < c.n_layers; ++l) {
+        rc.gamma[l] = h->layers[l].attn_norm;
+        rc.out[l] = an + (size_t)l * C * d * es;
+      }
+      FE_TRY(rmsnorm_copies(dt, X, Mc, rc, d, c.rms_eps, s));
       KvCacheArgs la[kMaxLayers];
       layer_args(r0, la);
       FE_TRY(gemm_kv_rows(an, d, (long)C * d, Mc, c.n_layers, la, nullptr, s));
