@@ -306,7 +306,7 @@ def device_weights(cfg, seed, device):
                    lm_head=lin(cfg.draft_vocab, d), d2t=d2t, layers=layers)
 
 
-def time_config(name, seed, steps, warmup):
+def time_config(name, seed, steps, warmup, pass_mode=None):
     """One more configuration (tiny, 13B-, 70B-shaped): passes (forward + tree,
     graph replays) timed like the primary workload, weights drawn on the device."""
     import numpy as np
@@ -319,6 +319,8 @@ def time_config(name, seed, steps, warmup):
     w = device_weights(cfg, seed, "cuda")
     dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=True)
     del w
+    if pass_mode is not None:
+        dr.set_pass_mode(pass_mode)
     di = dr.upload_inputs(inp)
     out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
     tree = dr.alloc_tree(cfg.batch, cfg.topk)
@@ -414,6 +416,9 @@ def main():
     ap.add_argument("--workload", default="llama8b_bf16_b1")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--eager", action="store_true", help="launch kernels one by one, no HIP graph")
+    ap.add_argument("--pass-mode", type=int, default=None, choices=[0, 1],
+                    help="batch-1 pass launches: 0 persistent stage launches, 1 one launch "
+                         "per stage (default: the library's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--prof-repeats", type=int, default=8)
@@ -453,6 +458,8 @@ def main():
     plens = np.asarray(inp.prefix_lens)
     probe = args.traffic_probe or args.counter_probe
     dr = Drafter(cfg, w, max_batch=cfg.batch, max_prefix=int(plens.max()), graph=not (args.eager or probe))
+    if args.pass_mode is not None:
+        dr.set_pass_mode(args.pass_mode)
     di = dr.upload_inputs(inp)
     out = dr.alloc_outputs(cfg.batch, cfg.topk, draft=False)
     tree = dr.alloc_tree(cfg.batch, cfg.topk)
@@ -724,7 +731,7 @@ def main():
         res["other_configs"] = {}
         for name in [n for n in args.configs.split(",") if n and n != cfg.name]:
             res["other_configs"][name] = time_config(name, args.seed, max(20, args.steps // 2),
-                                                     max(3, args.warmup // 4))
+                                                     max(3, args.warmup // 4), args.pass_mode)
     if not (args.no_cpu_baseline or args.device_weights):
         log("timing the oracle on the host cores ...")
         res["cpu_baseline"] = cpu_baseline(cfg, w, inp, args.cpu_budget)

@@ -388,15 +388,15 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on);
  * [0, 65536]. */
 fe_status fe_set_attention_split(fe_drafter *h, int32_t chunks_per_workgroup);
 
-/* How a batch-1 pass is launched.  Mode 1 (the default, and the only mode
- * available): every stage is its own launch.  Mode 0 would run, when the shape
- * allows (bf16, batch 1, greedy top-k, n_layers <= 8, the fusion/input/hidden/
- * intermediate/H_q*D widths multiples of 512), the stages between two
- * attention launches as ONE launch of resident workgroups, one per compute
- * unit, passing results to each other through tagged words in the workspace;
- * it is switched off in this build (its first device run faulted, the cause is
- * not found) and asking for it returns FE_E_UNSUPPORTED.  Errors:
- * FE_E_INVALID for a NULL handle or another mode, FE_E_UNSUPPORTED for mode 0. */
+/* How a batch-1 pass is launched.  Mode 1 (the default): every stage is its
+ * own launch.  Mode 0 runs, when the shape allows (bf16, batch 1, greedy
+ * top-k, n_layers <= 8, the fusion/input/hidden/intermediate/H_q*D widths
+ * multiples of 512), the stages between two attention launches as ONE launch
+ * of resident workgroups, one per compute unit, passing results to each other
+ * through tagged words in the workspace (the pass of Section 2.4 as N + 1
+ * launches besides the N attention launches); other calls still run mode 1.
+ * Errors: FE_E_INVALID for a NULL handle or another mode, FE_E_UNSUPPORTED for
+ * mode 0 in a build that has the persistent launches switched off. */
 fe_status fe_set_pass_mode(fe_drafter *h, int32_t mode);
 
 /* Waits for `stream`, then reports and clears the persistent pass's status

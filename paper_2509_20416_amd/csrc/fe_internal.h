@@ -513,9 +513,9 @@ constexpr int kSegLmMaxCols = 128;  // LM-head rows (vocabulary entries) per wor
 constexpr int kSegEpochWord = 0, kSegDepartWord = 32, kSegStatusWord = 64, kSegSyncWords = 96;
 constexpr uint32_t kSegStatusTimeout = 1u;  // a poll gave up (results unspecified)
 constexpr uint32_t kSegStatusPersistent = 1u << 16;  // the last pass ran as persistent launches
-// The persistent launches are switched off: their first device run faulted and
-// the access at fault is not found.  fe_set_pass_mode(0) is refused.
-constexpr bool kSegEnabled = false;
+// The persistent launches can be switched off here (fe_set_pass_mode(0) is then
+// refused and every pass runs one launch per stage).
+constexpr bool kSegEnabled = true;
 enum SegKind : int { kSegFuse = 0, kSegInput, kSegQkv, kSegO, kSegGu, kSegDown, kSegLm };
 enum SegSrcKind : int { kSrcPlain = 0, kSrcTagged = 1, kSrcEmbed = 2 };
 // elements [e0, e0 + n) of input row m: plain bf16 at p (element 0 of the
@@ -554,7 +554,6 @@ struct SegArgs {
   TreeRows tree;
 };
 int seg_variant(int xbytes);  // workgroup shape for the largest activation block (-1: none)
-int seg_waves(int variant);
 hipError_t seg_occupancy(int variant, int *blocks_per_cu);
 hipError_t seg_launch(int variant, const SegArgs &a, hipStream_t s);
 hipError_t seg_zero(uint64_t *words, size_t n, hipStream_t s);

@@ -9,9 +9,12 @@
 // merge and the draft tree after the last) runs inside ONE launch of resident
 // workgroups, one per compute unit:
 //  * Every wave streams its share of the stage's weight rows in 1 KB pieces
-//    (64 lanes x 16 bytes of one row) through two LDS banks that
-//    direct-to-LDS loads fill.  Those loads have no destination registers, so
-//    no compiler-inserted wait drains them.  The issue cursor runs ahead
+//    (64 lanes x 16 bytes of one row) through two register banks of DEP
+//    pieces: one bank is in flight while the other is consumed, so up to
+//    2 * DEP KB per wave (W waves per compute unit) are on their way from
+//    memory.  Every bank slot issues its load, also past the end of the
+//    stream (it then re-reads the last piece, and nothing consumes it), so the
+//    compiler's own wait counts stay exact.  The issue cursor runs ahead
 //    across stage boundaries: the next stage's first weights are in flight
 //    while a stage's results are published and the next inputs collected.
 //  * A stage's results reach the other workgroups as 64-bit words holding a
@@ -24,6 +27,8 @@
 //    fixed order (deterministic, no atomics on data).
 // Every wait is bounded: a poll that gives up sets a status bit and the
 // kernel runs on to its normal end.
+#include <type_traits>
+
 #include "fe_internal.h"
 #include "fe_tree.h"
 
@@ -55,29 +60,8 @@ __device__ __forceinline__ float dot8(u32x4 w, u32x4 x, float acc) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, w3), __builtin_bit_cast(bf16x2_v, x3), acc, false);
 }
 
-// 1 KB from global memory into LDS: lane l's 16 bytes at base + voff (voff =
-// 16 l, a register never rewritten) to lds + 16 l.  base and lds are
-// wave-uniform (scalar registers); the load is invisible to the compiler, so
-// nothing but the explicit waits below orders it.  M0 has no other user here.
-__device__ __forceinline__ void dma1k(const void *base, uint32_t voff, uint32_t lds) {
-  const uint64_t b = (uint64_t)base;
-  const uint64_t ub = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32) |
-                      __builtin_amdgcn_readfirstlane((uint32_t)b);
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff),
-               "s"((const void *)ub), "s"(__builtin_amdgcn_readfirstlane(lds))
-               : "memory");
-}
-// wait until at most n (0..M) direct-to-LDS loads are in flight
-template <int M> __device__ __forceinline__ void vm_le(int n) {
-  if constexpr (M == 0) {
-    wait_vmcnt<0>();
-  } else {
-    if (n >= M) {
-      wait_vmcnt<M>();
-      return;
-    }
-    vm_le<M - 1>(n);
-  }
+__device__ __forceinline__ u32x4 ld_piece(const bf16_t *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
 }
 __device__ __forceinline__ void wg_sync() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -121,7 +105,8 @@ __device__ __forceinline__ const bf16_t *wrow(const SegStage &s, int r) {
 
 template <int W, int DEP, int XB>
 struct SegLds {
-  unsigned char ring[W][2][DEP][1024];
+  // the stage's input rows; after the last stage, the LM-head candidates of
+  // every workgroup for the merge
   bf16_t x[XB / 2];
   float red[kSegRedFloats];
   union {  // epilogue values; the next stage's partial sums of squares (not at once)
@@ -374,7 +359,8 @@ template <int W, int DEP, int XB>
 __device__ void merge_row(const SegArgs &a, SegLds<W, DEP, XB> &lds, int m, uint32_t tag) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int k = a.topk, nwg = a.nwg, nw = nwg * kMaxStat;
-  uint32_t *buf = reinterpret_cast<uint32_t *>(lds.ring);  // the rings are idle now
+  static_assert(XB >= kSegMaxWg * kMaxStat * 4, "candidate words fit the input rows' space");
+  uint32_t *buf = reinterpret_cast<uint32_t *>(lds.x);  // no stage reads its inputs any more
   poll_words(a.cand_t + (size_t)m * nw, nw, buf, tag, a.sync, &lds.aborted);
   const TreeRows &tr = a.tree;
   if (tr.tokens && m == 0) {
@@ -465,56 +451,66 @@ __global__ __launch_bounds__(64 * W) void k_seg(SegArgs args) {
   if (threadIdx.x == 0) lds.aborted = 0;
   wg_sync();
   const int nst = a.nst;
-  const uint32_t voff = lane * 16;
-  const uint32_t ring0 = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)((__attribute__((address_space(3))) unsigned char *)&lds.ring[sw][0][0][0]));
 
-  // ---- issue cursor: banks never span two stages ----
-  int ist = 0, it = 0, iend = 0, irow = 0, ip = 0, ippr = 1;
-  Rows irw{0, 0};
+  // ---- issue cursor: a bank never spans two stages ----
+  // The wave's pieces of a stage are [it, iend) of the row-major piece list of
+  // its rows.  Within one weight matrix consecutive pieces are 1 KB apart, so
+  // the cursor walks runs of contiguous pieces with one add per piece and only
+  // maps a piece back to its row where a run ends (a gate/up row pair, a
+  // Q/K/V matrix boundary).
+  int ist = 0, it = 0, iend = 0, irun = 0, ippr = 1, ir0 = 0;
+  const char *iptr = reinterpret_cast<const char *>(a.st[0].w0);
+  const char *ilast = iptr;  // last piece issued (first row of stage 0 before any)
+  auto run_init = [&]() {
+    const SegStage &s = a.st[ist];
+    const int r = ir0 + it / ippr;
+    iptr = reinterpret_cast<const char *>(wrow(s, r)) + (size_t)(it % ippr) * (kPieceElems * 2);
+    int rend = s.C;  // first row past this matrix-contiguous run
+    if (s.kind == kSegGu) rend = r + 1;
+    else if (s.kind == kSegQkv) rend = r < s.split1 ? s.split1 : (r < s.split2 ? s.split2 : s.C);
+    irun = min(iend, (rend - ir0) * ippr);
+  };
   auto issue_stage_init = [&]() {
     while (ist < nst) {
       const SegStage &s = a.st[ist];
-      irw = rows_of(s, g, a.nwg);
+      const Rows rw = rows_of(s, g, a.nwg);
+      ir0 = rw.r0;
       ippr = s.K / kPieceElems;
-      const Range q = range_of((irw.r1 - irw.r0) * ippr, ippr, W, sw);
+      const Range q = range_of((rw.r1 - rw.r0) * ippr, ippr, W, sw);
       it = q.t0;
       iend = q.t1;
-      irow = q.t0 / ippr;
-      ip = q.t0 % ippr;
-      if (it < iend) return;
+      if (it < iend) {
+        run_init();
+        return;
+      }
       ++ist;
     }
   };
   issue_stage_init();
-  int cnt[2] = {0, 0};
-  auto issue_bank = [&](int bank) {
+  // Fills a bank with the next pieces of the current stage (at most DEP);
+  // returns how many slots hold pieces.  Every slot issues a load.
+  auto issue_bank = [&](u32x4(&bank)[DEP]) -> int {
     int n = 0;
-    if (ist < nst) {
-      const SegStage &s = a.st[ist];
-      const bf16_t *row = wrow(s, irw.r0 + irow);
+    const bool live = ist < nst;
 #pragma unroll
-      for (int i = 0; i < DEP; ++i) {
-        if (it < iend) {
-          dma1k(row + ip * kPieceElems, voff, ring0 + (bank * DEP + i) * 1024);
-          ++n;
-          ++it;
-          if (++ip == ippr) {
-            ip = 0;
-            ++irow;
-            row = wrow(s, irw.r0 + irow);
-          }
-        }
+    for (int i = 0; i < DEP; ++i) {
+      if (live && it < iend) {
+        ilast = iptr;
+        iptr += kPieceElems * 2;
+        ++n;
+        if (++it == irun && it < iend) run_init();
       }
-      if (it >= iend) {
-        ++ist;
-        issue_stage_init();
-      }
+      bank[i] = ld_piece(reinterpret_cast<const bf16_t *>(ilast) + lane * 8);
     }
-    cnt[bank] = n;
+    if (live && it >= iend) {
+      ++ist;
+      issue_stage_init();
+    }
+    return n;
   };
-  issue_bank(0);
-  issue_bank(1);
+  u32x4 b0[DEP], b1[DEP];
+  int n0 = issue_bank(b0);
+  int n1 = issue_bank(b1);
 
   // ---- consume cursor ----
   int cst = 0, ct = 0, cend = 0, crow = 0, cp = 0, cppr = 1, cK = 0, cmr = 1, frow = 0, RW = 0;
@@ -535,53 +531,46 @@ __global__ __launch_bounds__(64 * W) void k_seg(SegArgs args) {
     fsplit = cp != 0;
   };
   collect(a, a.st[0], lds, tag);
-  wait_vmcnt<0>();
   wg_sync();
   consume_stage_init();
-  float acc[kSegMaxRows];
-#pragma unroll
-  for (int m = 0; m < kSegMaxRows; ++m) acc[m] = 0.f;
-  int cb = 0;
-  while (cst < nst) {
-    if (ct >= cend) {
-      // stage cst is done for this wave: publish it, collect the next inputs
+  // Runs the stage ends this wave has reached (epilogue, next inputs); false
+  // once every stage is done.
+  auto ready = [&]() -> bool {
+    while (ct >= cend) {
       wg_sync();
       epilogue(a, a.st[cst], lds, tag);
       wg_sync();
-      ++cst;
-      if (cst < nst) {
-        collect(a, a.st[cst], lds, tag);
-        // the epilogue's stores were issued after the banks' loads: wait for
-        // everything, so the bank waits below count loads only
-        wait_vmcnt<0>();
-        wg_sync();
-        consume_stage_init();
-      }
-      continue;
+      if (++cst >= nst) return false;
+      collect(a, a.st[cst], lds, tag);
+      wg_sync();
+      consume_stage_init();
     }
-    // the next bank belongs to stage cst (banks are issued stage by stage)
-    vm_le<DEP>(cnt[cb ^ 1]);
-    u32x4 b[DEP];
-    const unsigned char *bp = &lds.ring[sw][cb][0][0] + lane * 16;
+    return true;
+  };
+  float acc[kSegMaxRows];
 #pragma unroll
-    for (int i = 0; i < DEP; ++i) b[i] = *reinterpret_cast<const u32x4 *>(bp + i * 1024);
-    const int n = cnt[cb];
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // read before the bank is refilled
-    issue_bank(cb);
+  for (int m = 0; m < kSegMaxRows; ++m) acc[m] = 0.f;
+  // The n pieces of a bank (all of stage cst) into the row sums; MR rows at
+  // compile time (1: the single-row stages), else cmr <= kSegMaxRows.
+  auto consume_rows = [&](const u32x4(&bank)[DEP], int n, auto mr_tag) {
+    constexpr int MR = decltype(mr_tag)::value;
+    const int mr = MR == 1 ? 1 : cmr;
+    const bf16_t *xl = lds.x + lane * 8;
 #pragma unroll
     for (int i = 0; i < DEP; ++i) {
       if (i < n) {
-        const bf16_t *xp = lds.x + cp * kPieceElems + lane * 8;
+        const bf16_t *xp = xl + cp * kPieceElems;
 #pragma unroll
-        for (int m = 0; m < kSegMaxRows; ++m)
-          if (m < cmr) acc[m] = dot8(b[i], *reinterpret_cast<const u32x4 *>(xp + (size_t)m * cK), acc[m]);
+        for (int m = 0; m < MR; ++m)
+          if (MR == 1 || m < mr)
+            acc[m] = dot8(bank[i], *reinterpret_cast<const u32x4 *>(xp + (size_t)m * cK), acc[m]);
         ++ct;
         const bool row_end = ++cp == cppr;
         if (row_end || ct == cend) {
           const int slot = (crow == frow && fsplit) ? 1 : 0;
 #pragma unroll
-          for (int m = 0; m < kSegMaxRows; ++m) {
-            if (m < cmr) {
+          for (int m = 0; m < MR; ++m) {
+            if (MR == 1 || m < mr) {
               const float v = wave_sum(acc[m]);
               if (lane == 0) lds.red[(m * RW + crow) * 2 + slot] = v;
             }
@@ -592,15 +581,31 @@ __global__ __launch_bounds__(64 * W) void k_seg(SegArgs args) {
             ++crow;
           }
         }
+      } else {
+        // a slot past the stream: its load is waited for here, so that no
+        // path reaches the bank's refill with a load still pending on its
+        // registers (the compiler would otherwise wait before every refill
+        // load, draining the other bank)
+        asm volatile("" ::"v"(bank[i]));
       }
     }
-    cb ^= 1;
+  };
+  auto consume = [&](const u32x4(&bank)[DEP], int n) {
+    if (cmr == 1) consume_rows(bank, n, std::integral_constant<int, 1>{});
+    else consume_rows(bank, n, std::integral_constant<int, kSegMaxRows>{});
+  };
+  // banks alternate: b0, b1, b0, ...; each is refilled as soon as it is consumed
+  for (;;) {
+    if (!ready()) break;
+    consume(b0, n0);
+    n0 = issue_bank(b0);
+    if (!ready()) break;
+    consume(b1, n1);
+    n1 = issue_bank(b1);
   }
-  wait_vmcnt<0>();  // no load into LDS outlives the stream
 
   if (a.last) {
-    // the LM head's rows: row m merged by workgroup m, in the rings (idle once
-    // every wave's loads into them have landed)
+    // the LM head's rows: row m merged by workgroup m
     wg_sync();
     const int mr = a.st[nst - 1].mr;
     for (int m = g; m < mr; m += a.nwg) merge_row(a, lds, m, tag);
@@ -632,10 +637,11 @@ int seg_variant(int xbytes) {
   if (xbytes <= 81920) return 2;
   return -1;
 }
-int seg_waves(int variant) { return variant == 0 ? 12 : 8; }
 
-// (waves, bank depth, activation bytes) per variant, sized to 160 KB of LDS
-#define FE_SEG_VARIANTS(X) X(0, 12, 4, 40960) X(1, 8, 4, 65536) X(2, 8, 3, 81920)
+// (waves, bank depth, activation bytes) per variant
+#ifndef FE_SEG_VARIANTS
+#define FE_SEG_VARIANTS(X) X(0, 12, 8, 40960) X(1, 12, 8, 65536) X(2, 12, 8, 81920)
+#endif
 
 hipError_t seg_occupancy(int variant, int *blocks_per_cu) {
 #define FE_SEG_OCC(V, W, DEP, XB) \

@@ -318,8 +318,6 @@ fe_status fe_set_graph_mode(fe_drafter *h, int32_t on) {
 fe_status fe_set_pass_mode(fe_drafter *h, int32_t mode) {
   if (!h) return fail(FE_E_INVALID, "handle is NULL");
   if (mode != 0 && mode != 1) return fail(FE_E_INVALID, "pass mode %d is not 0 or 1", mode);
-  // The persistent launches faulted the device on their first run and the
-  // access at fault has not been found; until it is, they are not launched.
   if (mode == 0 && !kSegEnabled)
     return fail(FE_E_UNSUPPORTED, "the persistent batch-1 pass (mode 0) is switched off");
   h->pass_mode = mode;

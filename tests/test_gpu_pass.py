@@ -1,10 +1,7 @@
 """Batch-1 pass shapes (widths multiples of 512, up to eight cascade layers)
 through the one-launch-per-stage pass against the oracle, and the persistent
 batch-1 pass (stages between attention launches as one launch that hands
-results on through tagged words).  The persistent pass faulted the device on
-its first run and the faulting access is not found: it is switched off
-(fe_set_pass_mode(0) is refused) and its tests below are skipped until the
-cause is shown.  Rules in tests/parity.py."""
+results on through tagged words).  Rules in tests/parity.py."""
 import os
 
 import numpy as np
@@ -16,11 +13,6 @@ from fe_synth import make_inputs, make_weights
 pytestmark = pytest.mark.gpu
 
 PASS_SMALL = [C.SMALL_PASS_GQA, C.SMALL_PASS_GQA8, C.SMALL_PASS_MHA_N8]
-
-PERSISTENT_OFF = pytest.mark.skip(
-    reason="persistent batch-1 pass switched off: its first GPU run faulted the device and "
-           "the faulting access is not found")
-
 
 @pytest.fixture(scope="module", autouse=True)
 def _gpu():
@@ -46,20 +38,20 @@ def test_batch1_pass_shapes(cfg, ctx, graph):
     assert not rep["persistent"]
 
 
-def test_persistent_mode_is_refused():
+def test_pass_mode_values():
     from paper_2509_20416_amd import Drafter
     from paper_2509_20416_amd.fe import FeError
     cfg = C.SMALL_PASS_GQA
     dr = Drafter(cfg, make_weights(cfg, 1), max_batch=1, max_prefix=cfg.prefix)
     try:
-        with pytest.raises(FeError, match="switched off"):
-            dr.set_pass_mode(0)
+        with pytest.raises(FeError):
+            dr.set_pass_mode(2)
+        dr.set_pass_mode(0)
         dr.set_pass_mode(1)
     finally:
         dr.close()
 
 
-@PERSISTENT_OFF
 @pytest.mark.parametrize("graph", [False, True])
 @pytest.mark.parametrize("ctx", ["cascade", "self", "parallel"])
 @pytest.mark.parametrize("cfg", PASS_SMALL, ids=lambda c: c.name)
@@ -68,7 +60,6 @@ def test_persistent_pass_parity(cfg, ctx, graph):
     assert rep["persistent"], "the persistent pass did not run"
 
 
-@PERSISTENT_OFF
 @pytest.mark.parametrize("P", [0, 1, 64, 65])
 def test_persistent_pass_short_prefixes(P):
     """Empty and one-chunk prefixes (the attention's cascade keys alone, one key)."""
@@ -77,7 +68,6 @@ def test_persistent_pass_short_prefixes(P):
     assert rep["persistent"]
 
 
-@PERSISTENT_OFF
 def test_persistent_matches_per_stage_launches():
     """Same inputs through both pass modes: results agree to the storage tolerance,
     top-k ids wherever the logits are well separated, the tree structure exactly."""
@@ -100,7 +90,6 @@ def test_persistent_matches_per_stage_launches():
     assert_rows_close("logits", res[0]["logits"], res[1]["logits"], TOL["bf16"])
 
 
-@PERSISTENT_OFF
 def test_persistent_pass_inputs_change_between_passes():
     """Three passes with different features and next tokens on one handle (graph
     replay of the same buffers, refilled between passes), each equal bit for bit
@@ -132,6 +121,7 @@ def test_persistent_pass_inputs_change_between_passes():
         assert dr.pass_status() & 1 == 0
         got = {n: t.cpu().numpy() for n, t in out.items()}
         fresh = Drafter(cfg, w, max_batch=1, max_prefix=cfg.prefix)
+        fresh.set_pass_mode(0)
         want = {n: t.cpu().numpy()
                 for n, t in fresh.forward(fresh.upload_inputs(inp), logits=True, hidden=True).items()}
         fresh.close()
@@ -140,7 +130,6 @@ def test_persistent_pass_inputs_change_between_passes():
     dr.close()
 
 
-@PERSISTENT_OFF
 def test_persistent_pass_graph_replays_bitwise():
     import torch
     from paper_2509_20416_amd import Drafter
