@@ -640,7 +640,7 @@ int seg_variant(int xbytes) {
 
 // (waves, bank depth, activation bytes) per variant
 #ifndef FE_SEG_VARIANTS
-#define FE_SEG_VARIANTS(X) X(0, 12, 8, 40960) X(1, 12, 8, 65536) X(2, 12, 8, 81920)
+#define FE_SEG_VARIANTS(X) X(0, 16, 4, 40960) X(1, 16, 4, 65536) X(2, 16, 4, 81920)
 #endif
 
 hipError_t seg_occupancy(int variant, int *blocks_per_cu) {

@@ -156,3 +156,18 @@ def test_persistent_pass_graph_replays_bitwise():
             assert torch.equal(tree[n], t2[n]), (rep, n)
     assert dr.pass_status() == (1 << 16)
     dr.close()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cfg", [C.LLAMA8B_BF16_B1, C.LLAMA70B_BF16_B1], ids=lambda c: c.name)
+def test_persistent_pass_full_size(cfg):
+    """The persistent pass at the paper's 8B and 70B batch-1 shapes (one
+    workgroup per compute unit handing every stage's rows on through tagged
+    words; the 70B activations take the largest workgroup variant), graph
+    mode as the bench times it: element-wise cascade states and logits
+    against the oracle, the top-k rule, the tree."""
+    from tests.parity import DRIFT
+    rep, _, _ = _run(cfg, seed=0, graph=True, pass_mode=0)
+    assert rep["persistent"], "the persistent pass did not run"
+    for n in ("hidden_err", "logit_err"):
+        assert rep[n] <= DRIFT[cfg.dtype], (n, rep[n])
