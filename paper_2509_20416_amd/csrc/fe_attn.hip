@@ -394,7 +394,10 @@ __global__ __launch_bounds__(64) void k_attn_mma(const bf16_t *__restrict__ Kc,
     }
     int col, ch0, n, slot, np;
     eq.piece(x, xe, first, cnt, ncols, col, ch0, n, slot, np);
-    unit(b, col, ch0, n, slot, false, np, ch0 == 0);
+    // items [ch0, ch0 + n) of the segment: prefix chunks below its last item,
+    // which stands for the cascade keys
+    const int items = cnt / ncols, pre = min(ch0 + n, items - 1) - ch0;
+    unit(b, col, ch0, pre > 0 ? pre : 0, slot, false, np, ch0 + n == items);
     x += n;
   }
 }

@@ -227,10 +227,12 @@ __host__ __device__ inline int attn_prefix(Seqs cu, int b, int pmax, bool &bad) 
   return bad ? 0 : P;
 }
 
-// Equal-chunk split of the persistent attention.  The 64-key chunks of all
-// (sequence, column) segments, numbered sequence by sequence and column by
-// column (total of them), are cut into W contiguous ranges, range w starting at
-// chunk floor(total * w / W).  A range crossing segments does one piece per
+// Equal-chunk split of the persistent attention.  The work items of all
+// (sequence, column) segments -- each segment's 64-key prefix chunks and, as
+// its last item, its cascade keys (about a chunk's work, so that the waves
+// that take them do not finish last) -- numbered sequence by sequence and
+// column by column (total of them), are cut into W contiguous ranges, range w
+// starting at item floor(total * w / W).  A range crossing segments does one piece per
 // segment.  The pieces of the segment at [S, S + n) are numbered by the range
 // starts they contain: the piece at chunk x takes partial slot
 // starts(x) - starts(S), where starts(y) counts the w >= 1 whose range begins
@@ -258,11 +260,12 @@ struct AttnSplit {
     npieces = ch0 == 0 ? (int)(starts(S + nch_b - 1) - starts(S)) + 1 : 0;
   }
 };
-// Chunks of one (sequence, column) segment: at least one (the cascade keys of
-// an empty prefix), at most nch_ld.
+// Work items of one (sequence, column) segment in that split: its prefix
+// chunks (at most nch_ld - 1, nch_ld being the partial slots per segment)
+// followed by one item for its cascade keys, so between 1 and nch_ld.
 __host__ __device__ inline int attn_seg_chunks(int P, int nch_ld) {
   const int n = (P + kAttnChunk - 1) / kAttnChunk;
-  return n < 1 ? 1 : (n > nch_ld ? nch_ld : n);
+  return (n < 0 ? 0 : (n > nch_ld - 1 ? nch_ld - 1 : n)) + 1;
 }
 
 // Row m of a GEMM's A operand is row (m / per) * outer + j0 + m % per of its buffer.

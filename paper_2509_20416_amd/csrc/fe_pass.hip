@@ -27,6 +27,10 @@
 //    fixed order (deterministic, no atomics on data).
 // Every wait is bounded: a poll that gives up sets a status bit and the
 // kernel runs on to its normal end.
+// On the 8B-, 13B- and 70B-shaped drafters these launches are slower than one
+// launch per stage (their one-workgroup-per-CU streaming loop reads the
+// weights at about 4 TB/s, the per-stage GEMVs at up to 5.7), so a pass takes
+// this path only when the caller selects it (fe_set_pass_mode(h, 0)).
 #include <type_traits>
 
 #include "fe_internal.h"

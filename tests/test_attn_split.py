@@ -1,9 +1,10 @@
 """The persistent bf16 attention's equal-chunk split, checked on the host through
 the library's own split arithmetic (fe_test_attn_split runs the helper the
-kernel runs): for ragged batches every chunk of every (sequence, column)
-segment is taken exactly once, partial slots stay below the slots the
-workspace holds, the slots of a segment are 0..np-1 in chunk order, and the
-count its first piece stores equals its number of pieces."""
+kernel runs): for ragged batches every work item of every (sequence, column)
+segment -- its prefix chunks, then one item for its cascade keys -- is taken
+exactly once, partial slots stay below the slots the workspace holds, the
+slots of a segment are 0..np-1 in item order, and the count its first piece
+stores equals its number of pieces."""
 import numpy as np
 import pytest
 
@@ -18,7 +19,8 @@ def fe():
 def _check(fe, plens, ncols, nch_ld, pmax, waves):
     pieces = fe.fe_test_attn_split(plens, ncols, nch_ld, pmax, waves)
     B = len(plens)
-    chunks = [max(1, min(-(-int(p) // 64), nch_ld)) if 0 <= p <= pmax else 1 for p in plens]
+    # prefix chunks (at most nch_ld - 1) plus the cascade-key item
+    chunks = [min(-(-int(p) // 64), nch_ld - 1) + 1 if 0 <= p <= pmax else 1 for p in plens]
     seen = {}
     for w, b, col, ch0, n, slot, np_ in pieces:
         assert 0 <= b < B and 0 <= col < ncols and n >= 1
@@ -69,7 +71,7 @@ def test_split_batch32_workload(fe):
 
 
 def test_split_edge_cases(fe):
-    _check(fe, [0], 1, 1, 0, 1024)                      # empty prefix: one chunk (cascade keys)
+    _check(fe, [0], 1, 1, 0, 1024)                      # empty prefix: the cascade-key item alone
     _check(fe, [0] * 256, 8, 2, 64, 1024)
     _check(fe, [8192] * 256, 8, 129, 8192, 1024)        # the largest batch
     _check(fe, [1, 64, 65, 128, 129], 3, 4, 129, 2)
