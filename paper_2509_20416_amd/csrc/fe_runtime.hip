@@ -236,7 +236,7 @@ struct fe_drafter {
   bool graph_mode = false;
   int attn_split = 0;  // 64-key chunks per attention work unit (0 = automatic)
   bool table_ready = false;  // rotary table built (first pass on the handle)
-  int pass_mode = 1;          // 1: one launch per stage (0, persistent launches, is switched off)
+  int pass_mode = 1;          // 1: one launch per stage; 0: persistent launches where the shape allows
   bool seg_ready = false;     // tagged words zeroed (first persistent pass on the handle)
   int seg_nwg = 0, seg_var = -2;  // workgroups (compute units) and variant of the persistent pass
   bool last_seg = false;      // the most recent pass ran as persistent launches
