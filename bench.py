@@ -651,7 +651,8 @@ def main():
                    "cascade_layers": cfg.n_layers, "draft_vocab": cfg.draft_vocab,
                    "target_vocab": cfg.target_vocab, "prefix": cfg.prefix, "topk": cfg.topk,
                    "tree_nodes": cfg.tree_nodes, "cascade_ctx": cfg.cascade_ctx,
-                   "graph": not args.eager},
+                   "graph": not args.eager,
+                   "pass_launches": "persistent" if args.pass_mode == 0 else "one per stage"},
         # the whole pass as the unit: every weight and each layer's prefix K/V
         # once, over the time of one graph replay (all of its launches)
         "roofline": {"kernel": "whole drafting pass (one graph replay)",
